@@ -1,0 +1,62 @@
+"""Analytic flops F and algorithmic HBM bytes B of each kernel (oracle side).
+
+The paper counts FLOP instructions and memory loads per kernel to place each
+kernel on its multi-level roofline (Sec. III-C, Sec. IV-G).  Here the counts
+are the algorithmic ones, written per op from its shape: every operand element
+is read or written once, a read-modify-write counts twice, and a GEMM costs
+2*M*N*K flops.  Integer arithmetic only.
+"""
+from workloads.format import (DT_SIZE, MODE_RW, OP_ARGMAX, OP_ATTN_CACHE,
+                              OP_ATTN_QKV, OP_EMBED, OP_LAYERNORM, OP_LINEAR,
+                              OP_LINEAR_GELU, OP_LINEAR_RESID,
+                              OP_LINEAR_SWIGLU, OP_RMSNORM, OP_ROPE_KV,
+                              OP_TOUCH)
+
+
+def kernel_cost(op, shape, operands, dtypes, nbytes):
+    """operands: list of (tid, mode) in positional order; dtypes/nbytes by tid.
+
+    Returns (F, B) as Python ints.
+    """
+    es = [DT_SIZE[dtypes[t]] for t, _ in operands]
+    sh = list(shape) + [0] * (8 - len(shape))
+    if op == OP_TOUCH:
+        seen = {}
+        for t, m in operands:
+            seen[t] = seen.get(t, 0) | m
+        return 0, sum(nbytes[t] * (2 if m == MODE_RW else 1) for t, m in seen.items())
+    if op == OP_EMBED:
+        T, H = sh[0], sh[1]
+        return 0, 4 * T + T * H * es[1] + T * H * es[2]
+    if op == OP_LAYERNORM:
+        T, H = sh[0], sh[1]
+        return 8 * T * H, T * H * es[0] + H * es[1] + H * es[2] + T * H * es[3]
+    if op == OP_RMSNORM:
+        T, H = sh[0], sh[1]
+        return 4 * T * H, T * H * es[0] + H * es[1] + T * H * es[2]
+    if op in (OP_LINEAR, OP_LINEAR_GELU, OP_LINEAR_RESID):
+        M, N, K = sh[0], sh[1], sh[2]
+        F = 2 * M * N * K + {OP_LINEAR: 0, OP_LINEAR_GELU: 8 * M * N, OP_LINEAR_RESID: M * N}[op]
+        out = M * N * es[2] * (2 if op == OP_LINEAR_RESID else 1)
+        return F, M * K * es[0] + N * K * es[1] + out
+    if op == OP_LINEAR_SWIGLU:
+        M, N, K = sh[0], sh[1], sh[2]
+        return 4 * M * N * K + 4 * M * N, M * K * es[0] + N * K * (es[1] + es[2]) + M * N * es[3]
+    if op == OP_ATTN_QKV:
+        Bt, S, nH, d = sh[0], sh[1], sh[2], sh[3]
+        pairs = S * (S + 1) // 2
+        return Bt * nH * pairs * (4 * d + 4), Bt * S * nH * d * (3 * es[0] + es[1])
+    if op == OP_ROPE_KV:
+        Bt, S, nH, d = sh[0], sh[1], sh[2], sh[3]
+        n = Bt * S * nH * d
+        return 6 * n, n * (2 * es[0] + es[1] + es[2] + es[3] + es[4])
+    if op == OP_ATTN_CACHE:
+        Bt, S, nH, d, pos0 = sh[0], sh[1], sh[2], sh[3], sh[5]
+        pairs = S * pos0 + S * (S + 1) // 2
+        F = Bt * nH * pairs * (4 * d + 4)
+        B = Bt * S * nH * d * (es[0] + es[3]) + Bt * nH * (pos0 + S) * d * (es[1] + es[2])
+        return F, B
+    if op == OP_ARGMAX:
+        Bt, V = sh[0], sh[1]
+        return Bt * V, Bt * V * es[0] + 4 * Bt + (4 * Bt if len(operands) > 2 else 0)
+    raise ValueError(f"unknown op {op}")

@@ -1,0 +1,56 @@
+"""Trace helpers shared by the planner tests (oracle pins and C-ABI parity)."""
+import json
+import os
+import random
+
+from workloads.format import DT_U8, KIND_ACT, KIND_PARAM, OP_TOUCH
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "planner_cases.json")
+
+
+def load_golden():
+    with open(GOLDEN) as f:
+        return json.load(f)
+
+
+def golden_inputs(case):
+    tensors = [dict(nbytes=b, dtype=DT_U8, kind=KIND_PARAM if k == "param" else KIND_ACT,
+                    host_init=(k == "param")) for b, k in case["tensors"]]
+    kernels = [dict(op=OP_TOUCH, shape=(0,), operands=[tuple(o) for o in ops],
+                    flops=1, hbm_bytes=1) for ops in case["kernels"]]
+    return tensors, kernels
+
+
+def random_trace(seed, n_tensors=None, n_kernels=None, max_ops=4, equal=False,
+                 read_only=False, unit=256):
+    """Random trace of touch kernels with explicit or analytic costs."""
+    r = random.Random(seed)
+    nT = n_tensors or r.randint(1, 40)
+    nK = n_kernels or r.randint(1, 200)
+    tensors = []
+    for t in range(nT):
+        kind = KIND_PARAM if (read_only or r.random() < 0.6) else KIND_ACT
+        nbytes = unit if equal else r.choice([1, 200, 256, 300, 512, 1000, 2048, 4096, 777])
+        tensors.append(dict(nbytes=nbytes, dtype=DT_U8, kind=kind,
+                            host_init=(kind == KIND_PARAM or r.random() < 0.3)))
+    written = set(t for t in range(nT) if tensors[t]["host_init"])
+    kernels = []
+    for k in range(nK):
+        n = r.randint(1, max_ops)
+        ops = []
+        for _ in range(n):
+            t = r.randrange(nT)
+            if read_only:
+                m = 1
+            elif t in written:
+                m = r.choice([1, 1, 1, 2, 3])
+            else:
+                m = 2
+            ops.append((t, m))
+        written.update(t for t, m in ops if m & 2)
+        if r.random() < 0.5:
+            fl, hb = r.choice([(1, 1), (10**12, 10**6), (10**6, 10**9), (0, 0)])
+        else:
+            fl, hb = 0, 0
+        kernels.append(dict(op=OP_TOUCH, shape=(0,), operands=ops, flops=fl, hbm_bytes=hb))
+    return tensors, kernels

@@ -1,0 +1,69 @@
+"""Synthetic decoder configurations (random-init stand-ins for the paper's LLMs).
+
+The paper evaluates ten Hugging Face decoders of 12-32 layers, sequence length
+1.9k-4.0k and 1.4-11.4 GB footprint (Sec. V, Table II).  Those checkpoints are
+not used; seeded random-init decoders of the shapes below stand in for them.
+The oversubscription factor is allocated bytes over device capacity
+(Sec. II-A); a config's device budget is footprint * den / num.
+"""
+from dataclasses import dataclass, replace
+from typing import Tuple
+
+from .format import DT_F32, DT_BF16
+
+
+@dataclass(frozen=True)
+class DecoderConfig:
+    name: str
+    style: str              # "gpt": LayerNorm + GELU FFN + fused qkv, tied head
+                            # "llama": RMSNorm + SwiGLU + RoPE + KV cache, untied head
+    n_layers: int
+    hidden: int
+    n_heads: int
+    ffn: int
+    vocab: int
+    dtype: int              # storage type of weights and activations (DT_F32 / DT_BF16)
+    batch: int
+    prompt_len: int
+    decode_steps: int = 0   # greedy steps after the prompt (llama style only)
+    factor: Tuple[int, int] = (3, 2)   # oversubscription factor num/den
+    logits_all: bool = False           # gpt style: logits at every position (else last only)
+    seed: int = 0
+
+    @property
+    def head_dim(self) -> int:
+        return self.hidden // self.n_heads
+
+    @property
+    def tokens(self) -> int:
+        return self.batch * self.prompt_len
+
+    @property
+    def kv_len(self) -> int:
+        return self.prompt_len + self.decode_steps
+
+    def with_factor(self, num: int, den: int) -> "DecoderConfig":
+        return replace(self, factor=(num, den))
+
+
+# Tiny parity decoder: 2 layers, hidden 128, 4 heads of 32, GELU FFN 512,
+# LayerNorm, vocab 1000, fp32; prefill 1 x 32; budget 50% of the footprint.
+TINY = DecoderConfig("tiny", "gpt", 2, 128, 4, 512, 1000, DT_F32, 1, 32,
+                     factor=(2, 1), logits_all=True)
+
+# 1.3B-shape GPT-style decoder, prefill 4 x 2048, bf16, 1.25x oversubscription.
+GPT_1P3B = DecoderConfig("gpt-1.3b", "gpt", 24, 2048, 16, 8192, 50000, DT_BF16,
+                         4, 2048, factor=(5, 4))
+
+# 7B-shape LLaMA-style decoder: 1024-token prompt then 256 greedy steps at batch
+# 16 with a growing KV cache, bf16, 1.5x oversubscription.
+LLAMA_7B = DecoderConfig("llama-7b", "llama", 32, 4096, 32, 11008, 32000, DT_BF16,
+                         16, 1024, decode_steps=256, factor=(3, 2))
+
+# Small variants used by parity tests (same structure, seconds on the CPU).
+LLAMA_SMALL = DecoderConfig("llama-small", "llama", 2, 256, 2, 512, 1000, DT_BF16,
+                            2, 40, decode_steps=6, factor=(3, 2))
+GPT_SMALL = DecoderConfig("gpt-small", "gpt", 2, 256, 2, 640, 1000, DT_BF16,
+                          2, 160, factor=(5, 4))
+
+CONFIGS = {c.name: c for c in (TINY, GPT_1P3B, LLAMA_7B, LLAMA_SMALL, GPT_SMALL)}
