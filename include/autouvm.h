@@ -1,0 +1,236 @@
+/*
+ * autouvm.h — C interface of the tensor-granular, roofline-gated prefetch
+ * runtime for decoder inference under device-memory oversubscription.
+ *
+ * The paper's problem statement (Sec. I, goals (1)-(3); Sec. IV-A) asks for
+ * three things, which this interface exposes directly:
+ *   1. tensor-level access information: tensors are registered as
+ *      sub-allocations of one pooled arena (Sec. II-B, the pooling allocator
+ *      hides them from the driver), and each kernel is registered with the
+ *      list of tensors it touches (Sec. IV-D, kernel--tensor access tracing);
+ *   2. which migrations are performance-critical: a multi-level roofline
+ *      (GPU compute, HBM, CPU--GPU interconnect) classifies kernels and only
+ *      interconnect-bound kernels get their tensors fetched ahead
+ *      (Sec. III-C, Sec. IV-D "UVM Analyzer", Sec. IV-E "Prefetch Engine");
+ *   3. adaptation to memory pressure: the device budget caps a pooled device
+ *      arena, and classes are re-evaluated on the residency the plan itself
+ *      produces (Sec. IV-E "Runtime Monitor").
+ * The oversubscription factor is registered bytes over the device budget
+ * (Sec. II-A).
+ *
+ * Lifecycle: create -> arena_init -> register_tensor* -> (write initial host
+ * contents through tensor_host_ptr) -> add_kernel* -> set_budget ->
+ * [set_roofs] [set_policy] -> plan -> [bind_streams] -> run* -> read_tensor /
+ * get_* -> destroy.  run may be called in contiguous, increasing segments.
+ *
+ * Threading: a context is not thread-safe; use one context per thread.
+ * Errors: every call returns an auvm_status; on failure auvm_last_error()
+ * describes it (valid until the next call on the same context).  No call
+ * aborts the process.
+ */
+#ifndef AUTOUVM_H
+#define AUTOUVM_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct auvm_ctx auvm_ctx;
+typedef int32_t auvm_status;
+
+enum {
+  AUVM_OK = 0,
+  AUVM_E_INVAL = -1,   /* bad argument, unknown id/op, read of a never-written tensor */
+  AUVM_E_STATE = -2,   /* call out of lifecycle order */
+  AUVM_E_BUDGET = -3,  /* some kernel's operands exceed the device budget */
+  AUVM_E_FRAG = -4,    /* no contiguous pool window although bytes would fit */
+  AUVM_E_HIP = -5,     /* a HIP runtime call failed (message in last_error) */
+  AUVM_E_NOMEM = -6,   /* host or device allocation failed */
+  AUVM_E_RANGE = -7    /* caller buffer too small */
+};
+
+/* tensor element types */
+enum { AUVM_F32 = 0, AUVM_BF16 = 1, AUVM_I32 = 2, AUVM_U8 = 3 };
+/* tensor kinds: parameters start valid on the host */
+enum { AUVM_PARAM = 0, AUVM_ACT = 1, AUVM_KV = 2 };
+/* registration flags: HOST_INIT marks a non-parameter with valid host contents */
+enum { AUVM_HOST_INIT = 1 };
+/* operand access modes */
+enum { AUVM_R = 1, AUVM_W = 2, AUVM_RW = 3 };
+
+/* kernel ops; shape[] integers and positional operands per op:
+ *  TOUCH         (log_slot)          log RW (>= 64*(log_slot+1) B), then 1..7 data
+ *                                    operands (bytes % 4 == 0): for each data
+ *                                    operand i the min and max u32 word read
+ *                                    are logged at log[16*slot + 2i], writes
+ *                                    fill the operand with slot+1.
+ *  EMBED         (T,H,V)             ids R i32[T], E R [V,H], x W f32[T,H]
+ *  LAYERNORM     (T,H,stride,offset) x R f32, g R [H], b R [H], h W [T,H];
+ *                                    output row i normalises input row i*stride+offset
+ *  RMSNORM       (T,H,stride,offset) x R f32, g R [H], h W [T,H]
+ *  LINEAR        (M,N,K)             a R [M,K], W R [N,K], c W [M,N]: c = a W^T
+ *  LINEAR_GELU   (M,N,K)             as LINEAR, c = gelu_erf(a W^T)
+ *  LINEAR_RESID  (M,N,K)             a R, W R, x RW f32[M,N]: x += a W^T
+ *  LINEAR_SWIGLU (M,N,K)             a R, Wg R, Wu R, c W: c = silu(a Wg^T) * (a Wu^T)
+ *  ATTN_QKV      (B,S,nH,d)          qkv R [B*S, 3*nH*d] (q|k|v column blocks),
+ *                                    o W [B*S, nH*d]; causal within each sequence
+ *  ROPE_KV       (B,S,nH,d,Lmax,pos0) q RW, k R, v R [B*S, nH*d], Kc, Vc [B,nH,Lmax,d]:
+ *                                    rotate-half RoPE (base 1e4) on q and k at
+ *                                    positions pos0.., k and v stored at pos0..
+ *  ATTN_CACHE    (B,S,nH,d,Lmax,pos0) q R, Kc R, Vc R, o W: query i attends to
+ *                                    cache positions 0..pos0+i
+ *  ARGMAX        (B,V,row)           logits R f32[B,V], tok W i32[B], [gen RW i32[.,B]]:
+ *                                    lowest index of the row maximum; also gen[row]
+ * Activations between kernels use the tensors' own dtypes (f32 or bf16);
+ * arithmetic accumulates in fp32. */
+enum {
+  AUVM_OP_TOUCH = 0, AUVM_OP_EMBED = 1, AUVM_OP_LAYERNORM = 2, AUVM_OP_RMSNORM = 3,
+  AUVM_OP_LINEAR = 4, AUVM_OP_LINEAR_GELU = 5, AUVM_OP_LINEAR_RESID = 6,
+  AUVM_OP_LINEAR_SWIGLU = 7, AUVM_OP_ATTN_QKV = 8, AUVM_OP_ROPE_KV = 9,
+  AUVM_OP_ATTN_CACHE = 10, AUVM_OP_ARGMAX = 11, AUVM_OP_COUNT = 12
+};
+
+/* policy variants: the paper's ablation ladder (T, T+A, T+A+P; Sec. V-E)
+ * and the two demand-migration baselines (Sec. V-A "Baseline") */
+enum { AUVM_DEMAND_LRU = 0, AUVM_DEMAND_BELADY = 1, AUVM_T = 2, AUVM_T_A = 3, AUVM_T_A_P = 4 };
+enum { AUVM_PLACE_POOL = 0, AUVM_PLACE_IDEAL = 1 };
+/* schedule entry ops */
+enum { AUVM_H2D_PREFETCH = 0, AUVM_H2D_DEMAND = 1, AUVM_D2H_WRITEBACK = 2,
+       AUVM_DROP = 3, AUVM_ALLOC = 4, AUVM_LAUNCH = 5 };
+/* roofline classes (Sec. IV-D "UVM Analyzer") */
+enum { AUVM_CLS_COMPUTE = 0, AUVM_CLS_MEMORY = 1, AUVM_CLS_CGI = 2 };
+
+typedef struct {
+  uint32_t op;            /* AUVM_OP_* */
+  int64_t shape[8];       /* op-specific integers, unused trailing entries 0 */
+  uint32_t n;             /* operand count */
+  const int32_t* ids;     /* n tensor ids in the op's positional order */
+  const uint8_t* modes;   /* n access modes (AUVM_R/W/RW) */
+  uint64_t flops;         /* 0: analytic count for the op */
+  uint64_t hbm_bytes;     /* 0: analytic algorithmic bytes for the op */
+  uint32_t layer;         /* reporting only */
+} auvm_kernel_desc;
+
+typedef struct {
+  uint32_t variant;       /* AUVM_DEMAND_LRU .. AUVM_T_A_P (default T_A_P) */
+  uint32_t lookahead;     /* max kernels a fetch runs ahead; 0 = T/T+A: 1, T+A+P: unlimited */
+  uint32_t affinity_w;    /* pin operands reused within this many kernels (default 1) */
+  uint32_t placement;     /* AUVM_PLACE_POOL (default) or AUVM_PLACE_IDEAL (plan-only) */
+  uint32_t validate;      /* 1: fill every dropped or written-back window with NaN bytes */
+  uint32_t timing;        /* 1: record per-kernel start/end events during run */
+} auvm_policy;
+
+typedef struct {
+  int32_t op;             /* AUVM_H2D_PREFETCH .. AUVM_LAUNCH */
+  int32_t tensor;         /* -1 for LAUNCH */
+  uint64_t dev_off;       /* pool offset of the tensor's window */
+  uint64_t bytes;         /* 256-aligned tensor size (0 for LAUNCH) */
+  int32_t issue_k;        /* boundary: before launch k (demand/alloc/evict) or after it (prefetch) */
+  int32_t need_k;         /* kernel the fetch serves; -1 for evictions */
+} auvm_sched_entry;
+
+typedef struct {
+  int32_t k;
+  int32_t n_resident;
+  uint64_t resident_bytes; /* resident bytes when kernel k launches */
+} auvm_residency;
+
+typedef struct {
+  uint8_t static_cls;     /* class with every read operand host-resident */
+  uint8_t dyn_cls;        /* class on the planned residency at the kernel's boundary */
+  uint8_t pad[6];
+  uint64_t flops;
+  uint64_t hbm_bytes;
+} auvm_kernel_class;
+
+typedef struct {
+  uint64_t h2d_prefetch_n, h2d_prefetch_B;
+  uint64_t h2d_demand_n, h2d_demand_B;    /* demand fetches ("faults") */
+  uint64_t d2h_wb_n, d2h_wb_B;
+  uint64_t drop_n, alloc_n;
+  uint64_t useless_prefetch_n, useless_prefetch_B;
+  uint64_t class_n[3];                    /* kernels per dynamic class */
+  uint64_t plan_ns;                       /* host time of the last auvm_plan */
+  uint64_t run_ns;                        /* host wall time inside auvm_run calls */
+  uint64_t kernels_run;                   /* launches executed since plan/reset */
+} auvm_counters;
+
+/* Create a context bound to HIP device `hip_device`; a negative device gives a
+ * plan-only context (no HIP call is ever made; run/read_tensor fail with
+ * AUVM_E_STATE).  *out receives the context; caller destroys it. */
+auvm_status auvm_create(int hip_device, auvm_ctx** out);
+/* Free everything the context allocated; borrowed memory and streams are left alone. */
+void auvm_destroy(auvm_ctx* ctx);
+const char* auvm_last_error(const auvm_ctx* ctx);
+
+/* Host backing store of all tensors.  host_pinned == NULL: the context
+ * allocates arena_bytes of pinned host memory (plan-only contexts allocate
+ * nothing).  Otherwise the caller lends memory that must be pinned, at least
+ * arena_bytes long, and outlive the context.  Once per context. */
+auvm_status auvm_arena_init(auvm_ctx* ctx, uint64_t arena_bytes, void* host_pinned);
+
+/* Register a tensor as the sub-allocation [arena_off, arena_off+bytes) of the
+ * arena; ids are dense in registration order.  arena_off must be 256-aligned;
+ * windows must not overlap and must lie inside the arena.  PARAM and
+ * HOST_INIT tensors start valid on the host; others start with no value. */
+auvm_status auvm_register_tensor(auvm_ctx* ctx, uint64_t arena_off, uint64_t bytes,
+                                 uint32_t dtype, uint32_t kind, uint32_t flags,
+                                 int32_t* out_id);
+/* Host address of a tensor's arena window (for writing initial contents). */
+auvm_status auvm_tensor_host_ptr(auvm_ctx* ctx, int32_t id, void** out);
+
+/* Append a kernel to the trace.  The op's operand count, dtypes and byte
+ * sizes are checked against its shape here (AUVM_E_INVAL on mismatch), so no
+ * launch can address outside its operands.  Repeated ids in one kernel are
+ * merged for planning with the union of their modes.  *out_k = kernel index. */
+auvm_status auvm_add_kernel(auvm_ctx* ctx, const auvm_kernel_desc* desc, int32_t* out_k);
+
+/* Device budget M (rounded down to 256) and the pool it is carved from.
+ * device_pool == NULL: the context allocates M bytes (never in plan-only
+ * contexts).  Otherwise the caller lends a device buffer of >= M bytes. */
+auvm_status auvm_set_budget(auvm_ctx* ctx, uint64_t device_bytes, void* device_pool);
+/* Roofs in flop/s and byte/s (integers).  Default: 2.5e15, 8e12, 64e9. */
+auvm_status auvm_set_roofs(auvm_ctx* ctx, uint64_t peak_flops, uint64_t hbm_Bps, uint64_t link_Bps);
+auvm_status auvm_set_policy(auvm_ctx* ctx, const auvm_policy* policy);
+
+/* Build the transfer schedule for the whole trace (host only, deterministic).
+ * AUVM_E_BUDGET / AUVM_E_FRAG / AUVM_E_INVAL as described above. */
+auvm_status auvm_plan(auvm_ctx* ctx);
+
+/* Lend the compute, host-to-device and device-to-host streams (hipStream_t
+ * values passed as pointers); NULL entries are created by the context. */
+auvm_status auvm_bind_streams(auvm_ctx* ctx, void* compute, void* h2d, void* d2h);
+
+/* Execute boundaries first_k .. first_k+n_k-1 of the plan (their transfers
+ * and launches, plus fetches issued after the last launch), then wait for
+ * all three streams.  Segments must be contiguous and increasing from 0. */
+auvm_status auvm_run(auvm_ctx* ctx, uint32_t first_k, uint32_t n_k);
+/* Forget all device residency and rewind to kernel 0.  The caller must
+ * restore host contents of tensors the trace reads before writing. */
+auvm_status auvm_reset(auvm_ctx* ctx);
+
+/* Copy the current value of a tensor into dst (host memory, >= its bytes):
+ * from the device when the newest copy is there, else from the host arena.
+ * Does not change residency or the schedule. */
+auvm_status auvm_read_tensor(auvm_ctx* ctx, int32_t id, void* dst, uint64_t dst_bytes);
+
+auvm_status auvm_get_counters(const auvm_ctx* ctx, auvm_counters* out);
+/* Two-call pattern: buf == NULL stores the count in *n; cap < count gives
+ * AUVM_E_RANGE.  get_schedule returns the plan, get_executed the entries
+ * executed so far (identical to the plan's prefix). */
+auvm_status auvm_get_schedule(const auvm_ctx* ctx, auvm_sched_entry* buf, uint64_t cap, uint64_t* n);
+auvm_status auvm_get_executed(const auvm_ctx* ctx, auvm_sched_entry* buf, uint64_t cap, uint64_t* n);
+auvm_status auvm_get_residency(const auvm_ctx* ctx, auvm_residency* buf, uint64_t cap, uint64_t* n);
+auvm_status auvm_get_classes(const auvm_ctx* ctx, auvm_kernel_class* buf, uint64_t cap, uint64_t* n);
+/* Per executed kernel (timing policy): duration and the compute-stream gap
+ * before it (time from the previous kernel's end to this kernel's start), in
+ * milliseconds, for kernels 0 .. n-1 of the last run segments since reset. */
+auvm_status auvm_get_kernel_times(const auvm_ctx* ctx, float* dur_ms, float* gap_ms,
+                                  uint64_t cap, uint64_t* n);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* AUTOUVM_H */

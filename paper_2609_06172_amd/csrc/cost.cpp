@@ -1,0 +1,276 @@
+// Kernel cost model and operand validation.
+//
+// The roofline placement of a kernel (Sec. III-C, Sec. IV-D "UVM Analyzer")
+// needs its floating-point work F and its memory traffic B.  The paper counts
+// them with binary instrumentation; here they are the algorithmic counts of
+// each op from its shape: 2*M*N*K per GEMM, every operand element read or
+// written once, read-modify-write counted twice.
+#include <sstream>
+
+#include "core.h"
+
+namespace auvm {
+
+namespace {
+
+uint64_t es(const std::vector<Tensor>& T, const Kernel& k, int i) {
+  return dtype_size(T[k.ids[i]].dtype);
+}
+
+}  // namespace
+
+void kernel_cost(const Kernel& k, const std::vector<Tensor>& T, uint64_t* Fo, uint64_t* Bo) {
+  const int64_t* s = k.shape;
+  uint64_t F = 0, B = 0;
+  switch (k.op) {
+    case AUVM_OP_TOUCH:
+      for (auto& a : k.acc) B += T[a.first].bytes * (a.second == AUVM_RW ? 2 : 1);
+      break;
+    case AUVM_OP_EMBED: {
+      uint64_t Tn = s[0], H = s[1];
+      B = 4 * Tn + Tn * H * es(T, k, 1) + Tn * H * es(T, k, 2);
+      break;
+    }
+    case AUVM_OP_LAYERNORM: {
+      uint64_t Tn = s[0], H = s[1];
+      F = 8 * Tn * H;
+      B = Tn * H * es(T, k, 0) + H * es(T, k, 1) + H * es(T, k, 2) + Tn * H * es(T, k, 3);
+      break;
+    }
+    case AUVM_OP_RMSNORM: {
+      uint64_t Tn = s[0], H = s[1];
+      F = 4 * Tn * H;
+      B = Tn * H * es(T, k, 0) + H * es(T, k, 1) + Tn * H * es(T, k, 2);
+      break;
+    }
+    case AUVM_OP_LINEAR:
+    case AUVM_OP_LINEAR_GELU:
+    case AUVM_OP_LINEAR_RESID: {
+      uint64_t M = s[0], N = s[1], K = s[2];
+      F = 2 * M * N * K;
+      if (k.op == AUVM_OP_LINEAR_GELU) F += 8 * M * N;
+      if (k.op == AUVM_OP_LINEAR_RESID) F += M * N;
+      uint64_t out = M * N * es(T, k, 2) * (k.op == AUVM_OP_LINEAR_RESID ? 2 : 1);
+      B = M * K * es(T, k, 0) + N * K * es(T, k, 1) + out;
+      break;
+    }
+    case AUVM_OP_LINEAR_SWIGLU: {
+      uint64_t M = s[0], N = s[1], K = s[2];
+      F = 4 * M * N * K + 4 * M * N;
+      B = M * K * es(T, k, 0) + N * K * (es(T, k, 1) + es(T, k, 2)) + M * N * es(T, k, 3);
+      break;
+    }
+    case AUVM_OP_ATTN_QKV: {
+      uint64_t Bt = s[0], S = s[1], nH = s[2], d = s[3];
+      uint64_t pairs = S * (S + 1) / 2;
+      F = Bt * nH * pairs * (4 * d + 4);
+      B = Bt * S * nH * d * (3 * es(T, k, 0) + es(T, k, 1));
+      break;
+    }
+    case AUVM_OP_ROPE_KV: {
+      uint64_t n = uint64_t(s[0]) * s[1] * s[2] * s[3];
+      F = 6 * n;
+      B = n * (2 * es(T, k, 0) + es(T, k, 1) + es(T, k, 2) + es(T, k, 3) + es(T, k, 4));
+      break;
+    }
+    case AUVM_OP_ATTN_CACHE: {
+      uint64_t Bt = s[0], S = s[1], nH = s[2], d = s[3], pos0 = s[5];
+      uint64_t pairs = S * pos0 + S * (S + 1) / 2;
+      F = Bt * nH * pairs * (4 * d + 4);
+      B = Bt * S * nH * d * (es(T, k, 0) + es(T, k, 3)) +
+          Bt * nH * (pos0 + S) * d * (es(T, k, 1) + es(T, k, 2));
+      break;
+    }
+    case AUVM_OP_ARGMAX: {
+      uint64_t Bt = s[0], V = s[1];
+      F = Bt * V;
+      B = Bt * V * es(T, k, 0) + 4 * Bt + (k.ids.size() > 2 ? 4 * Bt : 0);
+      break;
+    }
+  }
+  *Fo = F;
+  *Bo = B;
+}
+
+uint8_t classify(uint64_t F, uint64_t B, uint64_t X, const Roofs& r) {
+  using u128 = unsigned __int128;
+  if (X > 0 && u128(X) * r.P > u128(F) * r.Bl && u128(X) * r.Bh > u128(B) * r.Bl)
+    return AUVM_CLS_CGI;
+  return u128(F) * r.Bh >= u128(B) * r.P ? AUVM_CLS_COMPUTE : AUVM_CLS_MEMORY;
+}
+
+namespace {
+
+struct V {
+  const Kernel& k;
+  const std::vector<Tensor>& T;
+  std::ostringstream err;
+  bool ok = true;
+
+  void fail(const std::string& m) {
+    if (ok) err << m;
+    ok = false;
+  }
+  const Tensor& t(int i) { return T[k.ids[i]]; }
+  // operand i: allowed dtype mask (bit per dtype), minimum elements, mode mask
+  void need(int i, unsigned dtmask, uint64_t elems, const char* what) {
+    if (!ok) return;
+    const Tensor& x = t(i);
+    if (!(dtmask & (1u << x.dtype))) {
+      fail(std::string("operand ") + what + " has an unsupported dtype");
+      return;
+    }
+    if (x.bytes < elems * dtype_size(x.dtype)) {
+      std::ostringstream m;
+      m << "operand " << what << " holds " << x.bytes << " B, shape needs "
+        << elems * dtype_size(x.dtype);
+      fail(m.str());
+    }
+  }
+  void mode(int i, unsigned allowed_mask, const char* what) {
+    if (!ok) return;
+    if (!(allowed_mask & (1u << k.modes[i]))) fail(std::string("operand ") + what + " has the wrong mode");
+  }
+  void count(size_t lo, size_t hi) {
+    if (k.ids.size() < lo || k.ids.size() > hi) fail("wrong operand count for the op");
+  }
+  void pos(int i, const char* what) {
+    if (k.shape[i] <= 0) fail(std::string("shape ") + what + " must be positive");
+  }
+};
+
+constexpr unsigned F32 = 1u << AUVM_F32, BF16 = 1u << AUVM_BF16, I32 = 1u << AUVM_I32,
+                   U8 = 1u << AUVM_U8, FP = F32 | BF16;
+constexpr unsigned MR = 1u << AUVM_R, MW = 1u << AUVM_W, MRW = 1u << AUVM_RW;
+
+}  // namespace
+
+std::string validate_kernel(const Kernel& k, const std::vector<Tensor>& T) {
+  V v{k, T, {}};
+  const int64_t* s = k.shape;
+  for (size_t i = 0; i < k.modes.size(); ++i)
+    if (k.modes[i] < 1 || k.modes[i] > 3) v.fail("bad access mode");
+  switch (k.op) {
+    case AUVM_OP_TOUCH: {
+      v.count(2, 8);
+      if (!v.ok) break;
+      if (s[0] < 0) v.fail("negative log slot");
+      v.need(0, F32 | I32 | U8, 0, "log");
+      v.mode(0, MRW, "log");
+      if (v.ok && T[k.ids[0]].bytes < 64 * uint64_t(s[0] + 1)) v.fail("log too small for slot");
+      for (size_t i = 1; i < k.ids.size(); ++i) {
+        if (T[k.ids[i]].bytes % 4 || T[k.ids[i]].bytes == 0) v.fail("touch operand bytes % 4 != 0");
+        if (k.ids[i] == k.ids[0]) v.fail("touch data operand aliases the log");
+        for (size_t j = 1; j < i; ++j)
+          if (k.ids[j] == k.ids[i]) v.fail("touch data operands repeat");
+      }
+      break;
+    }
+    case AUVM_OP_EMBED:
+      v.count(3, 3);
+      v.pos(0, "T"); v.pos(1, "H"); v.pos(2, "V");
+      if (!v.ok) break;
+      v.need(0, I32, s[0], "ids"); v.mode(0, MR, "ids");
+      v.need(1, FP, uint64_t(s[2]) * s[1], "E"); v.mode(1, MR, "E");
+      v.need(2, F32, uint64_t(s[0]) * s[1], "x"); v.mode(2, MW | MRW, "x");
+      break;
+    case AUVM_OP_LAYERNORM:
+    case AUVM_OP_RMSNORM: {
+      bool ln = k.op == AUVM_OP_LAYERNORM;
+      v.count(ln ? 4 : 3, ln ? 4 : 3);
+      v.pos(0, "T"); v.pos(1, "H"); v.pos(2, "stride");
+      if (!v.ok) break;
+      if (s[3] < 0) v.fail("negative row offset");
+      uint64_t rows = uint64_t(s[0] - 1) * s[2] + s[3] + 1;
+      v.need(0, F32, rows * s[1], "x"); v.mode(0, MR, "x");
+      v.need(1, FP, s[1], "g"); v.mode(1, MR, "g");
+      if (ln) { v.need(2, FP, s[1], "b"); v.mode(2, MR, "b"); }
+      int o = ln ? 3 : 2;
+      v.need(o, FP, uint64_t(s[0]) * s[1], "h"); v.mode(o, MW | MRW, "h");
+      if (v.ok && T[k.ids[1]].dtype != T[k.ids[o]].dtype) v.fail("gain and output dtypes differ");
+      break;
+    }
+    case AUVM_OP_LINEAR:
+    case AUVM_OP_LINEAR_GELU:
+    case AUVM_OP_LINEAR_RESID:
+    case AUVM_OP_LINEAR_SWIGLU: {
+      bool sw = k.op == AUVM_OP_LINEAR_SWIGLU;
+      v.count(sw ? 4 : 3, sw ? 4 : 3);
+      v.pos(0, "M"); v.pos(1, "N"); v.pos(2, "K");
+      if (!v.ok) break;
+      uint64_t M = s[0], N = s[1], K = s[2];
+      v.need(0, FP, M * K, "a"); v.mode(0, MR, "a");
+      v.need(1, FP, N * K, "W"); v.mode(1, MR, "W");
+      if (sw) { v.need(2, FP, N * K, "Wu"); v.mode(2, MR, "Wu"); }
+      int o = sw ? 3 : 2;
+      if (k.op == AUVM_OP_LINEAR_RESID) {
+        v.need(o, F32, M * N, "x"); v.mode(o, MRW, "x");
+      } else {
+        v.need(o, FP, M * N, "c"); v.mode(o, MW | MRW, "c");
+      }
+      if (!v.ok) break;
+      uint32_t da = T[k.ids[0]].dtype, dw = T[k.ids[1]].dtype;
+      if (da != dw || (sw && T[k.ids[2]].dtype != dw)) v.fail("activation and weight dtypes differ");
+      if (da == AUVM_BF16 && K % 32) v.fail("bf16 GEMM needs K % 32 == 0");
+      if (da == AUVM_F32 && T[k.ids[o]].dtype != AUVM_F32) v.fail("fp32 GEMM writes fp32");
+      break;
+    }
+    case AUVM_OP_ATTN_QKV: {
+      v.count(2, 2);
+      v.pos(0, "B"); v.pos(1, "S"); v.pos(2, "nH"); v.pos(3, "d");
+      if (!v.ok) break;
+      uint64_t rows = uint64_t(s[0]) * s[1], hd = uint64_t(s[2]) * s[3];
+      v.need(0, FP, rows * 3 * hd, "qkv"); v.mode(0, MR, "qkv");
+      v.need(1, FP, rows * hd, "o"); v.mode(1, MW | MRW, "o");
+      if (!v.ok) break;
+      if (T[k.ids[0]].dtype != T[k.ids[1]].dtype) v.fail("qkv and o dtypes differ");
+      if (s[3] != 32 && s[3] != 64 && s[3] != 128) v.fail("head dim must be 32, 64 or 128");
+      break;
+    }
+    case AUVM_OP_ROPE_KV:
+    case AUVM_OP_ATTN_CACHE: {
+      bool rope = k.op == AUVM_OP_ROPE_KV;
+      v.count(rope ? 5 : 4, rope ? 5 : 4);
+      v.pos(0, "B"); v.pos(1, "S"); v.pos(2, "nH"); v.pos(3, "d"); v.pos(4, "Lmax");
+      if (!v.ok) break;
+      if (s[5] < 0 || s[5] + s[1] > s[4]) v.fail("positions exceed the cache length");
+      uint64_t rows = uint64_t(s[0]) * s[1], hd = uint64_t(s[2]) * s[3];
+      uint64_t cache = uint64_t(s[0]) * s[2] * s[4] * s[3];
+      if (rope) {
+        v.need(0, FP, rows * hd, "q"); v.mode(0, MRW, "q");
+        v.need(1, FP, rows * hd, "k"); v.mode(1, MR, "k");
+        v.need(2, FP, rows * hd, "v"); v.mode(2, MR, "v");
+        v.need(3, FP, cache, "Kc"); v.mode(3, MW | MRW, "Kc");
+        v.need(4, FP, cache, "Vc"); v.mode(4, MW | MRW, "Vc");
+      } else {
+        v.need(0, FP, rows * hd, "q"); v.mode(0, MR, "q");
+        v.need(1, FP, cache, "Kc"); v.mode(1, MR, "Kc");
+        v.need(2, FP, cache, "Vc"); v.mode(2, MR, "Vc");
+        v.need(3, FP, rows * hd, "o"); v.mode(3, MW | MRW, "o");
+      }
+      if (!v.ok) break;
+      uint32_t dt = T[k.ids[0]].dtype;
+      for (size_t i = 1; i < k.ids.size(); ++i)
+        if (T[k.ids[i]].dtype != dt) v.fail("attention operand dtypes differ");
+      if (s[3] != 32 && s[3] != 64 && s[3] != 128) v.fail("head dim must be 32, 64 or 128");
+      break;
+    }
+    case AUVM_OP_ARGMAX: {
+      v.count(2, 3);
+      v.pos(0, "B"); v.pos(1, "V");
+      if (!v.ok) break;
+      v.need(0, F32, uint64_t(s[0]) * s[1], "logits"); v.mode(0, MR, "logits");
+      v.need(1, I32, s[0], "tok"); v.mode(1, MW | MRW, "tok");
+      if (k.ids.size() > 2) {
+        if (s[2] < 0) v.fail("negative gen row");
+        v.need(2, I32, uint64_t(s[2] + 1) * s[0], "gen"); v.mode(2, MRW, "gen");
+      }
+      break;
+    }
+    default:
+      v.fail("unknown op");
+  }
+  return v.ok ? std::string() : v.err.str();
+}
+
+}  // namespace auvm

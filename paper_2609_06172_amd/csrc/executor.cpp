@@ -1,0 +1,453 @@
+// Transfer engine and executor on the HIP runtime.
+//
+// Replays a plan on three streams: compute (kernels), h2d (pinned host arena
+// -> device pool copies) and d2h (write-backs).  Ordering is event based and
+// never blocks the host inside a run segment:
+//  * a copy into a pool window waits for the kernels that last used the
+//    tensors previously in that window and for write-backs out of it;
+//  * a demand fetch for kernel k additionally waits for kernel k-1, so it
+//    starts when execution reaches k (the fault-driven baseline of the paper,
+//    Sec. II-A and V-A); prefetches wait only for their victims;
+//  * a refetch of a tensor waits for its own pending write-back;
+//  * a kernel waits for the copies that brought its operands and, for
+//    first-write allocations, for transfers still touching the window.
+// Streams are in-order, so each stream keeps the highest kernel/copy index it
+// already waits on and skips older waits.
+#include <hip/hip_runtime_api.h>
+
+#include <algorithm>
+#include <cstring>
+#include <map>
+
+#include "ctx.h"
+#include "kernels.h"
+
+namespace auvm {
+
+namespace {
+constexpr int64_t kRing = 8192;    // events per ring
+constexpr int64_t kTimeRing = 4096;
+}  // namespace
+
+class Executor {
+ public:
+  explicit Executor(Ctx& c) : c_(c) {}
+  ~Executor() { destroy(); }
+
+  auvm_status init() {
+    if (!ok(hipSetDevice(c_.device), "hipSetDevice")) return AUVM_E_HIP;
+    hipStream_t* ss[3] = {&comp_, &h2d_, &d2h_};
+    for (int i = 0; i < 3; ++i) {
+      if (!ok(hipStreamCreateWithFlags(ss[i], hipStreamNonBlocking), "hipStreamCreate")) return AUVM_E_HIP;
+      own_[i] = true;
+    }
+    for (auto* ring : {&kev_, &hev_, &dev_}) {
+      ring->assign(kRing, nullptr);
+      for (auto& e : *ring)
+        if (!ok(hipEventCreateWithFlags(&e, hipEventDisableTiming), "hipEventCreate")) return AUVM_E_HIP;
+    }
+    kown_.assign(kRing, -1);
+    hown_.assign(kRing, -1);
+    down_.assign(kRing, -1);
+    return AUVM_OK;
+  }
+
+  void destroy() {
+    if (c_.device < 0) return;
+    (void)hipSetDevice(c_.device);
+    hipStream_t ss[3] = {comp_, h2d_, d2h_};
+    for (int i = 0; i < 3; ++i)
+      if (ss[i]) (void)hipStreamSynchronize(ss[i]);
+    for (auto* ring : {&kev_, &hev_, &dev_, &tstart_, &tend_})
+      for (auto& e : *ring)
+        if (e) (void)hipEventDestroy(e);
+    for (int i = 0; i < 3; ++i)
+      if (own_[i] && ss[i]) (void)hipStreamDestroy(ss[i]);
+    comp_ = h2d_ = d2h_ = nullptr;
+  }
+
+  auvm_status bind(void* comp, void* h2d, void* d2h) {
+    hipStream_t* ss[3] = {&comp_, &h2d_, &d2h_};
+    void* in[3] = {comp, h2d, d2h};
+    for (int i = 0; i < 3; ++i) {
+      if (!in[i]) continue;
+      if (*ss[i]) (void)hipStreamSynchronize(*ss[i]);
+      if (own_[i] && *ss[i]) (void)hipStreamDestroy(*ss[i]);
+      *ss[i] = static_cast<hipStream_t>(in[i]);
+      own_[i] = false;
+    }
+    return AUVM_OK;
+  }
+
+  auvm_status reset() {
+    if (!ok(hipSetDevice(c_.device), "hipSetDevice")) return AUVM_E_HIP;
+    if (!sync_all()) return AUVM_E_HIP;
+    const size_t nT = c_.tensors.size(), K = c_.kernels.size();
+    cursor_ = 0;
+    next_k_ = 0;
+    where_.assign(nT, -1);
+    last_use_.assign(nT, -1);
+    copy_seq_.assign(nT, 0);
+    wb_seq_.assign(nT, 0);
+    h2d_seq_ = d2h_seq_ = 0;
+    h2d_waited_k_ = d2h_waited_k_ = -1;
+    h2d_waited_d2h_ = comp_waited_h2d_ = comp_waited_d2h_ = 0;
+    pend_h2d_ = pend_d2h_ = 0;
+    std::fill(kown_.begin(), kown_.end(), -1);
+    std::fill(hown_.begin(), hown_.end(), -1);
+    std::fill(down_.begin(), down_.end(), -1);
+    hazards_.clear();
+    log_.clear();
+    kernels_run_ = 0;
+    dur_.assign(K, 0.f);
+    gap_.assign(K, 0.f);
+    seg_start_.assign(K, 0);
+    times_n_ = 0;
+    harvested_ = 0;
+    // kernels whose completion some transfer waits on
+    need_ev_.assign(K, 0);
+    std::vector<int64_t> last(nT, -1);
+    for (const auto& e : c_.plan.schedule) {
+      if (e.op == AUVM_LAUNCH) {
+        for (auto& a : c_.kernels[e.issue_k].acc) last[a.first] = e.issue_k;
+      } else if (e.op == AUVM_D2H_WRITEBACK || e.op == AUVM_DROP) {
+        if (last[e.tensor] >= 0) need_ev_[last[e.tensor]] = 1;
+      } else if (e.op == AUVM_H2D_DEMAND && e.issue_k > 0) {
+        need_ev_[e.issue_k - 1] = 1;
+      }
+    }
+    return AUVM_OK;
+  }
+
+  auvm_status run(uint32_t first_k, uint32_t n_k) {
+    if (int64_t(first_k) != next_k_) {
+      c_.err = "run segments must be contiguous: next kernel is " + std::to_string(next_k_);
+      return AUVM_E_STATE;
+    }
+    if (!ok(hipSetDevice(c_.device), "hipSetDevice")) return AUVM_E_HIP;
+    if (c_.pol.timing) ensure_time_events();
+    if (first_k < seg_start_.size()) seg_start_[first_k] = 1;
+    const int64_t end_k = int64_t(first_k) + n_k;
+    const auto& S = c_.plan.schedule;
+    while (cursor_ < S.size() && S[cursor_].issue_k < end_k) {
+      auvm_status s = step(S[cursor_]);
+      if (s != AUVM_OK) return s;
+      log_.push_back(S[cursor_]);
+      ++cursor_;
+    }
+    if (!sync_all()) return AUVM_E_HIP;
+    if (c_.pol.timing) harvest_all();
+    return AUVM_OK;
+  }
+
+  auvm_status read(int32_t id, void* dst) {
+    if (!ok(hipSetDevice(c_.device), "hipSetDevice")) return AUVM_E_HIP;
+    if (!sync_all()) return AUVM_E_HIP;
+    const Tensor& t = c_.tensors[id];
+    if (where_.size() == c_.tensors.size() && where_[id] >= 0) {
+      if (!ok(hipMemcpy(dst, c_.pool + where_[id], t.bytes, hipMemcpyDeviceToHost), "hipMemcpy D2H"))
+        return AUVM_E_HIP;
+    } else {
+      std::memcpy(dst, c_.host + t.arena_off, t.bytes);
+    }
+    return AUVM_OK;
+  }
+
+  const std::vector<auvm_sched_entry>& log() const { return log_; }
+  uint64_t kernels_run() const { return kernels_run_; }
+
+  auvm_status times(float* dur, float* gap, uint64_t cap, uint64_t* n) const {
+    *n = times_n_;
+    if (!dur && !gap) return AUVM_OK;
+    if (cap < times_n_) return AUVM_E_RANGE;
+    if (dur) std::memcpy(dur, dur_.data(), times_n_ * sizeof(float));
+    if (gap) std::memcpy(gap, gap_.data(), times_n_ * sizeof(float));
+    return AUVM_OK;
+  }
+
+ private:
+  struct Hazard {
+    uint64_t end;
+    int64_t last_k, d2h, h2d;
+  };
+
+  bool ok(hipError_t e, const char* what) {
+    if (e == hipSuccess) return true;
+    c_.err = std::string(what) + ": " + hipGetErrorString(e);
+    return false;
+  }
+
+  bool sync_all() {
+    hipStream_t ss[3] = {comp_, h2d_, d2h_};
+    for (auto s : ss)
+      if (s && !ok(hipStreamSynchronize(s), "hipStreamSynchronize")) return false;
+    return true;
+  }
+
+  // -- event rings ------------------------------------------------------------
+  bool record(std::vector<hipEvent_t>& ring, std::vector<int64_t>& own, int64_t idx, hipStream_t s) {
+    int64_t slot = idx % kRing;
+    if (!ok(hipEventRecord(ring[slot], s), "hipEventRecord")) return false;
+    own[slot] = idx;
+    return true;
+  }
+  // Make stream s wait until item idx of a ring is complete.  A slot reused by
+  // a later item of the same in-order stream implies idx is complete too.
+  bool wait(hipStream_t s, std::vector<hipEvent_t>& ring, std::vector<int64_t>& own, int64_t idx,
+            int64_t& waited) {
+    if (idx <= waited) return true;
+    int64_t slot = idx % kRing;
+    if (own[slot] < idx) {
+      c_.err = "internal: wait on an event that was never recorded";
+      return false;
+    }
+    if (!ok(hipStreamWaitEvent(s, ring[slot], 0), "hipStreamWaitEvent")) return false;
+    waited = own[slot];
+    return true;
+  }
+
+  // -- pool-window hazards left behind by evicted tensors ----------------------
+  void add_hazard(uint64_t off, uint64_t end, int64_t last_k, int64_t d2h, int64_t h2d) {
+    hazards_[off] = Hazard{end, last_k, d2h, h2d};
+  }
+  // Collect and remove the hazards overlapping [a, b), keeping uncovered parts.
+  void take_hazards(uint64_t a, uint64_t b, int64_t* last_k, int64_t* d2h, int64_t* h2d) {
+    *last_k = -1;
+    *d2h = *h2d = 0;
+    auto it = hazards_.lower_bound(a);
+    if (it != hazards_.begin()) {
+      auto p = std::prev(it);
+      if (p->second.end > a) it = p;
+    }
+    std::vector<std::pair<uint64_t, Hazard>> keep;
+    while (it != hazards_.end() && it->first < b) {
+      const Hazard& h = it->second;
+      *last_k = std::max(*last_k, h.last_k);
+      *d2h = std::max(*d2h, h.d2h);
+      *h2d = std::max(*h2d, h.h2d);
+      if (it->first < a) keep.push_back({it->first, Hazard{a, h.last_k, h.d2h, h.h2d}});
+      if (h.end > b) keep.push_back({b, Hazard{h.end, h.last_k, h.d2h, h.h2d}});
+      it = hazards_.erase(it);
+    }
+    for (auto& kv : keep) hazards_[kv.first] = kv.second;
+  }
+
+  // -- one schedule entry -------------------------------------------------------
+  auvm_status step(const auvm_sched_entry& e) {
+    const int32_t t = e.tensor;
+    switch (e.op) {
+      case AUVM_D2H_WRITEBACK:
+      case AUVM_DROP: {
+        if (where_[t] != int64_t(e.dev_off)) return internal("eviction of a tensor not at its window");
+        int64_t wb = 0;
+        if (e.op == AUVM_D2H_WRITEBACK) {
+          if (last_use_[t] >= 0 && !wait(d2h_, kev_, kown_, last_use_[t], d2h_waited_k_)) return AUVM_E_HIP;
+          const Tensor& x = c_.tensors[t];
+          if (!ok(hipMemcpyAsync(c_.host + x.arena_off, c_.pool + e.dev_off, x.bytes,
+                                 hipMemcpyDeviceToHost, d2h_), "hipMemcpyAsync D2H"))
+            return AUVM_E_HIP;
+          wb = ++d2h_seq_;
+          if (!record(dev_, down_, wb, d2h_)) return AUVM_E_HIP;
+          wb_seq_[t] = wb;
+        }
+        int64_t h2d = copy_seq_[t];
+        if (c_.pol.validate) {
+          // poison the vacated window once its readers and write-back are done
+          if (last_use_[t] >= 0 && !wait(h2d_, kev_, kown_, last_use_[t], h2d_waited_k_)) return AUVM_E_HIP;
+          if (wb && !wait(h2d_, dev_, down_, wb, h2d_waited_d2h_)) return AUVM_E_HIP;
+          if (!ok(launch_poison(c_.pool + e.dev_off, e.bytes, h2d_), "poison")) return AUVM_E_HIP;
+          h2d = ++h2d_seq_;
+          if (!record(hev_, hown_, h2d, h2d_)) return AUVM_E_HIP;
+        }
+        add_hazard(e.dev_off, e.dev_off + e.bytes, last_use_[t], wb, h2d);
+        where_[t] = -1;
+        return AUVM_OK;
+      }
+      case AUVM_H2D_DEMAND:
+      case AUVM_H2D_PREFETCH: {
+        if (where_[t] >= 0) return internal("fetch of a resident tensor");
+        int64_t lk, d2h, h2d;
+        take_hazards(e.dev_off, e.dev_off + e.bytes, &lk, &d2h, &h2d);
+        if (lk >= 0 && !wait(h2d_, kev_, kown_, lk, h2d_waited_k_)) return AUVM_E_HIP;
+        if (e.op == AUVM_H2D_DEMAND && e.issue_k > 0 &&
+            !wait(h2d_, kev_, kown_, e.issue_k - 1, h2d_waited_k_))
+          return AUVM_E_HIP;
+        int64_t dw = std::max(d2h, wb_seq_[t]);
+        if (dw && !wait(h2d_, dev_, down_, dw, h2d_waited_d2h_)) return AUVM_E_HIP;
+        const Tensor& x = c_.tensors[t];
+        if (!ok(hipMemcpyAsync(c_.pool + e.dev_off, c_.host + x.arena_off, x.bytes,
+                               hipMemcpyHostToDevice, h2d_), "hipMemcpyAsync H2D"))
+          return AUVM_E_HIP;
+        int64_t seq = ++h2d_seq_;
+        if (!record(hev_, hown_, seq, h2d_)) return AUVM_E_HIP;
+        copy_seq_[t] = seq;
+        where_[t] = int64_t(e.dev_off);
+        return AUVM_OK;
+      }
+      case AUVM_ALLOC: {
+        if (where_[t] >= 0) return internal("allocation of a resident tensor");
+        int64_t lk, d2h, h2d;
+        take_hazards(e.dev_off, e.dev_off + e.bytes, &lk, &d2h, &h2d);
+        // previous readers ran earlier on the compute stream; transfers did not
+        pend_d2h_ = std::max(pend_d2h_, d2h);
+        pend_h2d_ = std::max(pend_h2d_, h2d);
+        copy_seq_[t] = 0;
+        where_[t] = int64_t(e.dev_off);
+        return AUVM_OK;
+      }
+      case AUVM_LAUNCH:
+        return launch(e.issue_k);
+    }
+    return internal("unknown schedule op");
+  }
+
+  auvm_status launch(int64_t k) {
+    const Kernel& kd = c_.kernels[k];
+    int64_t need_h2d = pend_h2d_;
+    for (auto& a : kd.acc) {
+      if (where_[a.first] < 0) return internal("operand not resident at launch");
+      need_h2d = std::max(need_h2d, copy_seq_[a.first]);
+    }
+    if (need_h2d && !wait(comp_, hev_, hown_, need_h2d, comp_waited_h2d_)) return AUVM_E_HIP;
+    if (pend_d2h_ && !wait(comp_, dev_, down_, pend_d2h_, comp_waited_d2h_)) return AUVM_E_HIP;
+    pend_h2d_ = pend_d2h_ = 0;
+    uint8_t* ptrs[16];
+    for (size_t i = 0; i < kd.ids.size(); ++i) ptrs[i] = c_.pool + where_[kd.ids[i]];
+    bool timing = c_.pol.timing != 0;
+    if (timing) {
+      if (!make_room(k)) return AUVM_E_HIP;
+      if (!ok(hipEventRecord(tstart_[k % kTimeRing], comp_), "hipEventRecord")) return AUVM_E_HIP;
+    }
+    if (!ok(launch_op(kd, c_.tensors, ptrs, comp_), "kernel launch")) return AUVM_E_HIP;
+    if (timing) {
+      if (!ok(hipEventRecord(tend_[k % kTimeRing], comp_), "hipEventRecord")) return AUVM_E_HIP;
+      times_n_ = size_t(k) + 1;
+    }
+    if (need_ev_[k] && !record(kev_, kown_, k, comp_)) return AUVM_E_HIP;
+    for (auto& a : kd.acc) last_use_[a.first] = k;
+    next_k_ = k + 1;
+    ++kernels_run_;
+    return AUVM_OK;
+  }
+
+  auvm_status internal(const char* m) {
+    c_.err = std::string("internal: ") + m;
+    return AUVM_E_STATE;
+  }
+
+  // -- per-kernel timing ----------------------------------------------------------
+  void ensure_time_events() {
+    if (!tstart_.empty()) return;
+    tstart_.assign(kTimeRing, nullptr);
+    tend_.assign(kTimeRing, nullptr);
+    for (auto& e : tstart_) (void)hipEventCreate(&e);
+    for (auto& e : tend_) (void)hipEventCreate(&e);
+  }
+  // Before recording kernel k, read out the kernel whose events occupy k's slot.
+  bool make_room(int64_t k) {
+    while (harvested_ + kTimeRing <= k) {
+      if (!harvest(harvested_)) return false;
+      ++harvested_;
+    }
+    return true;
+  }
+  bool harvest(int64_t j) {
+    float ms = 0;
+    hipEvent_t s = tstart_[j % kTimeRing], e = tend_[j % kTimeRing];
+    if (!ok(hipEventSynchronize(e), "hipEventSynchronize")) return false;
+    if (!ok(hipEventElapsedTime(&ms, s, e), "hipEventElapsedTime")) return false;
+    dur_[j] = ms;
+    // the gap before the first kernel of a run segment includes host time: not reported
+    if (j + 1 < int64_t(times_n_) && !seg_start_[j + 1]) {
+      hipEvent_t s2 = tstart_[(j + 1) % kTimeRing];
+      if (!ok(hipEventSynchronize(s2), "hipEventSynchronize")) return false;
+      float g = 0;
+      if (!ok(hipEventElapsedTime(&g, e, s2), "hipEventElapsedTime")) return false;
+      gap_[j + 1] = g;
+    }
+    return true;
+  }
+  void harvest_all() {
+    while (harvested_ < int64_t(times_n_)) {
+      if (!harvest(harvested_)) return;
+      ++harvested_;
+    }
+  }
+
+  Ctx& c_;
+  hipStream_t comp_ = nullptr, h2d_ = nullptr, d2h_ = nullptr;
+  bool own_[3] = {false, false, false};
+  std::vector<hipEvent_t> kev_, hev_, dev_, tstart_, tend_;
+  std::vector<int64_t> kown_, hown_, down_;
+  size_t cursor_ = 0;
+  int64_t next_k_ = 0;
+  std::vector<uint8_t> seg_start_;
+  std::vector<int64_t> where_, last_use_, copy_seq_, wb_seq_;
+  int64_t h2d_seq_ = 0, d2h_seq_ = 0;
+  int64_t h2d_waited_k_ = -1, d2h_waited_k_ = -1, h2d_waited_d2h_ = 0;
+  int64_t comp_waited_h2d_ = 0, comp_waited_d2h_ = 0;
+  int64_t pend_h2d_ = 0, pend_d2h_ = 0;
+  std::map<uint64_t, Hazard> hazards_;
+  std::vector<uint8_t> need_ev_;
+  std::vector<auvm_sched_entry> log_;
+  uint64_t kernels_run_ = 0;
+  std::vector<float> dur_, gap_;
+  size_t times_n_ = 0;
+  int64_t harvested_ = 0;
+};
+
+Ctx::~Ctx() {
+  exec.reset();
+  free_owned(*this);
+}
+
+void ExecDeleter::operator()(Executor* e) const { delete e; }
+
+ExecPtr make_executor(Ctx& c) {
+  ExecPtr x(new Executor(c));
+  if (x->init() != AUVM_OK) return nullptr;
+  return x;
+}
+
+auvm_status exec_bind_streams(Ctx& c, void* a, void* b, void* d) { return c.exec->bind(a, b, d); }
+auvm_status exec_run(Ctx& c, uint32_t f, uint32_t n) { return c.exec->run(f, n); }
+auvm_status exec_reset(Ctx& c) { return c.exec->reset(); }
+auvm_status exec_read(Ctx& c, int32_t id, void* dst, uint64_t) { return c.exec->read(id, dst); }
+const std::vector<auvm_sched_entry>& exec_log(const Ctx& c) { return c.exec->log(); }
+uint64_t exec_kernels_run(const Ctx& c) { return c.exec->kernels_run(); }
+auvm_status exec_kernel_times(const Ctx& c, float* d, float* g, uint64_t cap, uint64_t* n) {
+  return c.exec->times(d, g, cap, n);
+}
+
+auvm_status host_alloc_pinned(Ctx& c, uint64_t bytes) {
+  void* p = nullptr;
+  if (hipHostMalloc(&p, bytes, hipHostMallocDefault) != hipSuccess || !p) {
+    c.err = "hipHostMalloc of the host arena failed";
+    return AUVM_E_NOMEM;
+  }
+  c.host = static_cast<uint8_t*>(p);
+  c.host_owned = true;
+  return AUVM_OK;
+}
+
+auvm_status device_alloc_pool(Ctx& c, uint64_t bytes) {
+  void* p = nullptr;
+  if (hipSetDevice(c.device) != hipSuccess || hipMalloc(&p, bytes) != hipSuccess || !p) {
+    c.err = "hipMalloc of the device pool failed";
+    return AUVM_E_NOMEM;
+  }
+  c.pool = static_cast<uint8_t*>(p);
+  c.pool_owned = true;
+  return AUVM_OK;
+}
+
+void free_owned(Ctx& c) {
+  if (c.device >= 0) (void)hipSetDevice(c.device);
+  if (c.pool_owned && c.pool) (void)hipFree(c.pool);
+  if (c.host_owned && c.host) (void)hipHostFree(c.host);
+  c.pool = nullptr;
+  c.host = nullptr;
+  c.pool_owned = c.host_owned = false;
+}
+
+}  // namespace auvm

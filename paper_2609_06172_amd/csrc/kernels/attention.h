@@ -1,0 +1,25 @@
+// Causal softmax attention over strided q / k / v views.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace auvm {
+
+// Query i of sequence b, head h sits at position pos0+i and attends to keys
+// 0..pos0+i.  Element addresses (in elements of the dtype):
+//   q(b,h,i) = q + (b*S + i)*q_rs + h*d
+//   k(b,h,j) = k + b*kv_bstride + h*kv_hstride + j*kv_rs   (same for v)
+//   o(b,h,i) = o + (b*S + i)*o_rs + h*d
+struct AttnArgs {
+  const uint8_t *q, *k, *v;
+  uint8_t* o;
+  int64_t B, S, nH, d, pos0;
+  int64_t q_rs, o_rs, kv_rs, kv_bstride, kv_hstride;
+  bool bf16;
+};
+
+hipError_t launch_attention(const AttnArgs& a, hipStream_t s);
+
+}  // namespace auvm

@@ -1,0 +1,22 @@
+// GEMM entry: C[M,N] (epilogue) = A[M,K] * W[N,K]^T, fp32 accumulation.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace auvm {
+
+struct GemmArgs {
+  int64_t M, N, K;
+  const uint8_t* a;   // [M,K] f32 or bf16
+  const uint8_t* w;   // [N,K] same dtype as a
+  const uint8_t* w2;  // second weight for the SwiGLU epilogue (else null)
+  uint8_t* c;         // [M,N]: f32 or bf16 output, f32 residual for EPI_RESID
+  int epi;            // dev::Epi
+  bool in_bf16, out_bf16;
+};
+
+hipError_t launch_gemm(const GemmArgs& g, hipStream_t s);
+
+}  // namespace auvm

@@ -1,0 +1,88 @@
+"""Load a workload (tensor list + kernel trace) into a runtime context.
+
+Marshalling only: registers the workload's tensors and kernels through the C
+interface, writes the seeded initial host contents into the context's arena,
+lends the device pool and streams (allocated with PyTorch) and plans.  All
+scheduling and every kernel run inside the library.
+"""
+import ctypes as C
+
+import numpy as np
+
+from workloads import init as winit
+from workloads.format import DT_BF16, DT_F32, DT_I32, DT_U8
+
+from .capi import Context
+
+NP_DTYPE = {DT_F32: np.float32, DT_I32: np.int32, DT_U8: np.uint8, DT_BF16: np.uint16}
+
+
+class Session:
+    def __init__(self, w, device=-1, M=None, variant=4, lookahead=0, affinity_w=1, placement=0,
+                 validate=0, timing=0, roofs=None, fill=True, threads=16):
+        self.w = w
+        self.device = device
+        self.ctx = Context(device)
+        ctx = self.ctx
+        ctx.arena_init(w.arena_bytes)
+        for t in w.tensors:
+            tid = ctx.register_tensor(t.off, t.nbytes, t.dtype, t.kind, t.flags)
+            assert tid == t.tid
+        if device >= 0 and fill:
+            winit.fill_host(w, self.host_view, threads=threads)
+        for k in w.kernels:
+            ctx.add_kernel(k.op, k.shape, k.operands, layer=k.layer)
+        self.M = w.budget() if M is None else M
+        self._torch_refs = []
+        if device >= 0:
+            import torch
+            pool = torch.empty(self.M, dtype=torch.uint8, device=f"cuda:{device}")
+            self._torch_refs.append(pool)
+            ctx.set_budget(self.M, pool.data_ptr())
+        else:
+            ctx.set_budget(self.M)
+        if roofs is not None:
+            ctx.set_roofs(*roofs)
+        self.set_policy(variant, lookahead, affinity_w, placement, validate, timing)
+        if device >= 0:
+            import torch
+            with torch.cuda.device(device):
+                ss = [torch.cuda.Stream(device=device) for _ in range(3)]
+            self._torch_refs += ss
+            ctx.bind_streams(*[s.cuda_stream for s in ss])
+
+    def set_policy(self, variant=4, lookahead=0, affinity_w=1, placement=0, validate=0, timing=0):
+        self.ctx.set_policy(variant, lookahead, affinity_w, placement, validate, timing)
+        self.ctx.plan()
+
+    # -- host arena access ----------------------------------------------------
+    def host_view(self, t):
+        """uint8 numpy view of tensor t's host arena window."""
+        addr = self.ctx.tensor_host_ptr(t.tid)
+        return np.ctypeslib.as_array((C.c_uint8 * t.nbytes).from_address(addr))
+
+    def write(self, name, value):
+        t = self.w.tensors[self.w.id(name)]
+        src = np.ascontiguousarray(value, NP_DTYPE[t.dtype]).view(np.uint8).reshape(-1)
+        self.host_view(t)[:] = src
+
+    def read(self, name):
+        """Current value of a tensor (fp32 for bf16 tensors), shaped."""
+        t = self.w.tensors[self.w.id(name)]
+        buf = np.empty(t.nbytes, np.uint8)
+        self.ctx.read_tensor(t.tid, buf.ctypes.data, t.nbytes)
+        v = buf.view(NP_DTYPE[t.dtype])
+        if t.dtype == DT_BF16:
+            v = winit.bf16_to_f32(v)
+        return v.reshape(t.shape)
+
+    # -- execution --------------------------------------------------------------
+    def run(self, first_k, n_k):
+        self.ctx.run(first_k, n_k)
+
+    def run_all(self):
+        self.ctx.run(0, len(self.w.kernels))
+
+    def close(self):
+        self.ctx.destroy()
+        self._torch_refs.clear()

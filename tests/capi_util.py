@@ -1,0 +1,41 @@
+"""Helpers to load traces into a plan-only C-ABI context and compare with the oracle."""
+from paper_2609_06172_amd.capi import Context
+from workloads.format import ALIGN, FLAG_HOST_INIT, KIND_PARAM
+
+
+def plan_ctx(tensors, kernels, M, variant=4, lookahead=0, affinity_w=1, placement=0, roofs=None):
+    """Register a trace (oracle-style dicts) in a plan-only context and plan it."""
+    ctx = Context(-1)
+    off = 0
+    offs = []
+    for t in tensors:
+        offs.append(off)
+        off += (t["nbytes"] + ALIGN - 1) // ALIGN * ALIGN
+    ctx.arena_init(max(off, ALIGN))
+    for t, o in zip(tensors, offs):
+        flags = FLAG_HOST_INIT if (t["host_init"] and t["kind"] != KIND_PARAM) else 0
+        ctx.register_tensor(o, t["nbytes"], t["dtype"], t["kind"], flags)
+    for k in kernels:
+        ctx.add_kernel(k["op"], k["shape"], k["operands"], k.get("flops", 0), k.get("hbm_bytes", 0))
+    ctx.set_budget(M)
+    if roofs is not None:
+        ctx.set_roofs(*roofs)
+    ctx.set_policy(variant, lookahead, affinity_w, placement)
+    ctx.plan()
+    return ctx
+
+
+def assert_same_plan(ctx, r):
+    """C++ plan in ctx equals oracle Result r field by field."""
+    sched = ctx.get_schedule()
+    assert len(sched) == len(r.schedule)
+    for i, (a, b) in enumerate(zip(sched, r.schedule)):
+        assert tuple(a) == tuple(b), f"schedule entry {i}: lib {a} oracle {b}"
+    assert [tuple(x) for x in ctx.get_residency()] == [tuple(x) for x in r.residency]
+    cls = ctx.get_classes()
+    assert [c[0] for c in cls] == list(r.static_cls)
+    assert [c[1] for c in cls] == list(r.dyn_cls)
+    assert [(c[2], c[3]) for c in cls] == [tuple(x) for x in r.costs]
+    c = ctx.get_counters()
+    for k, v in r.counters.items():
+        assert c[k] == v, (k, c[k], v)

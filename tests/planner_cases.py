@@ -22,24 +22,36 @@ def golden_inputs(case):
 
 
 def random_trace(seed, n_tensors=None, n_kernels=None, max_ops=4, equal=False,
-                 read_only=False, unit=256):
-    """Random trace of touch kernels with explicit or analytic costs."""
+                 read_only=False, unit=256, touch=False):
+    """Random trace of touch kernels with explicit or analytic costs.
+
+    touch=True makes every kernel a well-formed touch op: tensor 0 is a log
+    (read-write operand 0 of every kernel, one 64-byte slot per kernel), data
+    operands are distinct and their sizes are multiples of 4 bytes.
+    """
     r = random.Random(seed)
     nT = n_tensors or r.randint(1, 40)
     nK = n_kernels or r.randint(1, 200)
     tensors = []
+    sizes = [4, 200, 256, 300, 512, 1000, 2048, 4096, 776] if touch else \
+        [1, 200, 256, 300, 512, 1000, 2048, 4096, 777]
     for t in range(nT):
         kind = KIND_PARAM if (read_only or r.random() < 0.6) else KIND_ACT
-        nbytes = unit if equal else r.choice([1, 200, 256, 300, 512, 1000, 2048, 4096, 777])
+        nbytes = unit if equal else r.choice(sizes)
         tensors.append(dict(nbytes=nbytes, dtype=DT_U8, kind=kind,
                             host_init=(kind == KIND_PARAM or r.random() < 0.3)))
-    written = set(t for t in range(nT) if tensors[t]["host_init"])
+    if touch:
+        tensors.insert(0, dict(nbytes=64 * nK, dtype=DT_U8, kind=KIND_ACT, host_init=True))
+    first = 1 if touch else 0
+    written = set(t for t in range(len(tensors)) if tensors[t]["host_init"])
     kernels = []
     for k in range(nK):
         n = r.randint(1, max_ops)
         ops = []
         for _ in range(n):
-            t = r.randrange(nT)
+            t = r.randrange(first, len(tensors))
+            if touch and any(t == u for u, _ in ops):
+                continue
             if read_only:
                 m = 1
             elif t in written:
@@ -52,5 +64,8 @@ def random_trace(seed, n_tensors=None, n_kernels=None, max_ops=4, equal=False,
             fl, hb = r.choice([(1, 1), (10**12, 10**6), (10**6, 10**9), (0, 0)])
         else:
             fl, hb = 0, 0
-        kernels.append(dict(op=OP_TOUCH, shape=(0,), operands=ops, flops=fl, hbm_bytes=hb))
+        if touch:
+            ops = [(0, 3)] + ops
+        kernels.append(dict(op=OP_TOUCH, shape=(k if touch else 0,), operands=ops,
+                            flops=fl, hbm_bytes=hb))
     return tensors, kernels

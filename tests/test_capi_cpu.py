@@ -1,0 +1,167 @@
+"""CPU tests of the C-ABI library: exported symbols, argument checking, and
+bit-exact agreement of the library's planner with the oracle replay."""
+import os
+import random
+import re
+
+import pytest
+
+import paper_2609_06172_amd as pkg
+from paper_2609_06172_amd.capi import AuvmError, Context
+from oracle import planner as op
+from workloads import configs, trace
+from workloads.format import (DT_BF16, DT_F32, DT_I32, DT_U8, KIND_ACT,
+                              KIND_PARAM, MODE_R, MODE_RW, MODE_W, OP_LINEAR,
+                              OP_TOUCH, PLACE_IDEAL, PLACE_POOL,
+                              VAR_DEMAND_BELADY, VAR_DEMAND_LRU, VAR_T,
+                              VAR_T_A, VAR_T_A_P)
+
+from capi_util import assert_same_plan, plan_ctx
+from planner_cases import golden_inputs, load_golden, random_trace
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "autouvm.h")
+
+
+def test_library_exports_every_declared_symbol():
+    text = open(HEADER).read()
+    declared = set(re.findall(r"\b(auvm_[a-z_]+)\s*\(", text))
+    assert declared == set(pkg.SYMBOLS)
+    L = pkg.lib()
+    for name in declared:
+        assert hasattr(L, name), name
+
+
+def _tiny_ctx():
+    ctx = Context(-1)
+    ctx.arena_init(4096)
+    a = ctx.register_tensor(0, 256, DT_U8, KIND_PARAM)
+    b = ctx.register_tensor(256, 256, DT_U8, KIND_ACT)
+    return ctx, a, b
+
+
+def test_argument_errors():
+    ctx, a, b = _tiny_ctx()
+    with pytest.raises(AuvmError) as e:
+        ctx.register_tensor(128, 256, DT_U8, KIND_PARAM)          # overlap
+    assert e.value.code == -1
+    with pytest.raises(AuvmError):
+        ctx.register_tensor(3, 256, DT_U8, KIND_PARAM)            # unaligned
+    with pytest.raises(AuvmError):
+        ctx.register_tensor(3840, 512, DT_U8, KIND_PARAM)         # beyond the arena
+    with pytest.raises(AuvmError) as e:
+        ctx.add_kernel(OP_TOUCH, (0,), [(a, MODE_RW), (99, MODE_R)])  # unknown id
+    assert e.value.code == -1
+    with pytest.raises(AuvmError):
+        ctx.add_kernel(77, (0,), [(a, MODE_RW)])                  # unknown op
+    with pytest.raises(AuvmError):
+        ctx.add_kernel(OP_TOUCH, (9,), [(a, MODE_RW), (b, MODE_R)])  # log slot too large
+    with pytest.raises(AuvmError) as e:
+        ctx.run(0, 1)                                             # plan-only context
+    assert e.value.code == -2
+
+
+def test_shape_validation_rejects_out_of_bounds_operands():
+    ctx = Context(-1)
+    ctx.arena_init(1 << 20)
+    x = ctx.register_tensor(0, 16 * 64 * 2, DT_BF16, KIND_ACT, 1)
+    W = ctx.register_tensor(4096, 32 * 64 * 2, DT_BF16, KIND_PARAM)
+    c = ctx.register_tensor(12288, 16 * 32 * 2, DT_BF16, KIND_ACT)
+    ctx.add_kernel(OP_LINEAR, (16, 32, 64), [(x, MODE_R), (W, MODE_R), (c, MODE_W)])
+    with pytest.raises(AuvmError):       # N larger than the weight holds
+        ctx.add_kernel(OP_LINEAR, (16, 64, 64), [(x, MODE_R), (W, MODE_R), (c, MODE_W)])
+    with pytest.raises(AuvmError):       # K not a multiple of 32 for bf16
+        ctx.add_kernel(OP_LINEAR, (16, 32, 48), [(x, MODE_R), (W, MODE_R), (c, MODE_W)])
+    with pytest.raises(AuvmError):       # weight written
+        ctx.add_kernel(OP_LINEAR, (16, 32, 64), [(x, MODE_R), (W, MODE_W), (c, MODE_W)])
+
+
+def test_every_config_trace_is_accepted():
+    for cfg in configs.CONFIGS.values():
+        if cfg.name == "llama-7b":
+            continue          # covered (truncated) below
+        w = trace.build(cfg)
+        from paper_2609_06172_amd.session import Session
+        s = Session(w, device=-1)
+        assert len(s.ctx.get_classes()) == len(w.kernels)
+        s.close()
+
+
+@pytest.mark.parametrize("case", load_golden()["cases"], ids=lambda c: c["name"])
+def test_golden_schedules_through_the_library(case):
+    tensors, kernels = golden_inputs(case)
+    # golden traces use plain touch ops without a log: give them one
+    tensors = [dict(nbytes=64, dtype=DT_U8, kind=KIND_ACT, host_init=True)] + tensors
+    ks = []
+    for i, k in enumerate(kernels):
+        ops = [(t + 1, m) for t, m in k["operands"]]
+        ks.append(dict(op=OP_TOUCH, shape=(0,), operands=[(0, MODE_RW)] + ops, flops=1, hbm_bytes=1))
+    M = case["M"] + 256
+    ctx = plan_ctx(tensors, ks, M, variant=case["variant"], affinity_w=case["affinity_w"],
+                   placement=case["placement"])
+    r = op.plan(tensors, ks, M, variant=case["variant"], affinity_w=case["affinity_w"],
+                placement=case["placement"])
+    assert_same_plan(ctx, r)
+
+
+@pytest.mark.parametrize("case", load_golden()["errors"], ids=lambda c: c["name"])
+def test_golden_errors_through_the_library(case):
+    tensors, kernels = golden_inputs(case)
+    tensors = [dict(nbytes=64, dtype=DT_U8, kind=KIND_ACT, host_init=True)] + tensors
+    ks = [dict(op=OP_TOUCH, shape=(0,), operands=[(0, MODE_RW)] + [(t + 1, m) for t, m in k["operands"]],
+               flops=1, hbm_bytes=1) for k in kernels]
+    with pytest.raises(AuvmError) as e:
+        plan_ctx(tensors, ks, case["M"] + 256, variant=case["variant"])
+    assert e.value.code == case["code"]
+
+
+VARIANTS = [VAR_DEMAND_LRU, VAR_DEMAND_BELADY, VAR_T, VAR_T_A, VAR_T_A_P]
+
+
+@pytest.mark.parametrize("seed", range(60))
+def test_random_traces_bit_exact(seed):
+    tensors, kernels = random_trace(seed, touch=True)
+    fp = sum(op.aligned(t["nbytes"]) for t in tensors)
+    rnd = random.Random(seed)
+    for variant in VARIANTS:
+        for placement in (PLACE_POOL, PLACE_IDEAL):
+            M = max(1024, (fp * rnd.choice([1, 2, 3, 4]) // rnd.choice([2, 3, 4, 5])) // 256 * 256)
+            kw = dict(variant=variant, placement=placement, affinity_w=rnd.choice([0, 1, 2, 3]),
+                      lookahead=rnd.choice([0, 0, 1, 2, 5]))
+            roofs = rnd.choice([None, (10**15, 10**13, 10**10), (10**9, 10**9, 10**9)])
+            try:
+                r = op.plan(tensors, kernels, M, roofs=roofs or op.DEFAULT_ROOFS, **kw)
+            except op.PlanError as e:
+                with pytest.raises(AuvmError) as ee:
+                    plan_ctx(tensors, kernels, M, roofs=roofs, **kw)
+                assert ee.value.code == e.code
+                continue
+            assert_same_plan(plan_ctx(tensors, kernels, M, roofs=roofs, **kw), r)
+
+
+@pytest.mark.parametrize("name", ["tiny", "gpt-small", "llama-small", "gpt-1.3b"])
+@pytest.mark.parametrize("variant", VARIANTS)
+def test_config_traces_bit_exact(name, variant):
+    from paper_2609_06172_amd.session import Session
+    cfg = configs.CONFIGS[name]
+    w = trace.build(cfg)
+    s = Session(w, device=-1, variant=variant)
+    r = op.plan_workload(w, s.M, variant=variant)
+    assert_same_plan(s.ctx, r)
+    s.close()
+
+
+@pytest.mark.parametrize("factor", [(5, 4), (3, 2), (2, 1)])
+def test_llama7b_prefill_and_decode_bit_exact(factor):
+    """The 7B-shape trace (prefill + 6 decode steps) at its full tensor sizes."""
+    import dataclasses
+    from paper_2609_06172_amd.session import Session
+    cfg = dataclasses.replace(configs.LLAMA_7B, factor=factor)
+    full = trace.build(cfg)
+    M = full.budget()                    # budget from the whole 256-step job
+    w = trace.build(dataclasses.replace(cfg, decode_steps=6))
+    w_kernels = w.kernels
+    # same tensors (gen rows differ): compare on the shorter trace with the full budget
+    s = Session(w, device=-1, M=M)
+    r = op.plan_workload(w, M)
+    assert_same_plan(s.ctx, r)
+    s.close()
