@@ -24,11 +24,14 @@ notes) are:
   X*P > F*Bl and X*Bh > B*Bl (link time exceeds both device roof times);
   exact integer cross-products, ties not CGI;
 * victims for the full method are chosen by farthest next use (Belady/MIN,
-  possible because the profile gives the future), dead values first; LRU for
-  the demand baseline and the T / T+A ablation steps;
+  possible because the profile gives the future), dead values first, and a
+  window that needs no write-back is preferred over one that does (the host
+  link is shared by both directions); LRU for the demand baseline and the
+  T / T+A ablation steps;
 * placement picks a window of the pool whose resident tensors may all be
-  evicted, maximising (worst victim priority, -writeback bytes, -victim bytes,
-  -offset);
+  evicted, maximising (-writeback bytes, worst victim priority, -victim
+  bytes, -offset) under farthest-next-use and (worst victim priority,
+  -writeback bytes, -victim bytes, -offset) under LRU;
 * after each launch, the prefetch scan walks upcoming kernels in order and
   fetches the missing read operands of each CGI kernel whose host value is
   still live, stopping at the first operand that cannot be placed
@@ -195,9 +198,11 @@ def _replay(tensors, kernels, M, roofs, variant, lookahead, affinity_w, placemen
         if placement == PLACE_IDEAL:
             if M - used_bytes[0] >= s:
                 return 0, []
-            cands = sorted((u for u in off if eligible(u)),
-                           key=lambda u: (-prio(u, kp), size[u] if writes_back(u, kp) else 0,
-                                          -size[u], u))
+            if belady:
+                order = lambda u: (size[u] if writes_back(u, kp) else 0, -prio(u, kp), -size[u], u)
+            else:
+                order = lambda u: (-prio(u, kp), size[u] if writes_back(u, kp) else 0, -size[u], u)
+            cands = sorted((u for u in off if eligible(u)), key=order)
             freed, chosen = M - used_bytes[0], []
             for u in cands:
                 if freed >= s:
@@ -223,7 +228,7 @@ def _replay(tensors, kernels, M, roofs, variant, lookahead, affinity_w, placemen
             minpr = min((prio(u, kp) for u in over), default=INF)
             wb = sum(size[u] for u in over if writes_back(u, kp))
             vb = sum(size[u] for u in over)
-            key = (minpr, -wb, -vb, -a)
+            key = (-wb, minpr, -vb, -a) if belady else (minpr, -wb, -vb, -a)
             if best_key is None or key > best_key:
                 best, best_key = (a, over), key
         return best

@@ -69,6 +69,20 @@ class AuvmError(RuntimeError):
 _lib = None
 
 
+def _hip_runtimes():
+    """Distinct HIP runtime files mapped into this process."""
+    paths = set()
+    try:
+        with open("/proc/self/maps") as f:
+            for line in f:
+                p = line.split()[-1] if line.strip() else ""
+                if os.path.basename(p).startswith("libamdhip64.so"):
+                    paths.add(os.path.realpath(p))
+    except OSError:
+        pass
+    return paths
+
+
 def lib():
     global _lib
     if _lib is not None:
@@ -76,7 +90,18 @@ def lib():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is missing: build it with "
                           "`python -m paper_2609_06172_amd.build`")
+    # PyTorch ships its own HIP runtime with the same soname as the system
+    # one.  Loading torch first makes the library bind to that runtime, so the
+    # process has a single HIP runtime and torch's device buffers and streams
+    # are valid handles for the library.
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
     L = C.CDLL(LIB_PATH)
+    if len(_hip_runtimes()) > 1:
+        raise ImportError(f"two HIP runtimes are loaded ({sorted(_hip_runtimes())}); "
+                          "import torch before any other HIP library")
     P = C.c_void_p
     st = C.c_int32
     sig = {

@@ -235,6 +235,11 @@ class Executor {
   // -- one schedule entry -------------------------------------------------------
   auvm_status step(const auvm_sched_entry& e) {
     const int32_t t = e.tensor;
+    if (e.op != AUVM_LAUNCH) {
+      if (t < 0 || size_t(t) >= c_.tensors.size()) return internal("schedule names an unknown tensor");
+      if (e.dev_off > c_.M || c_.M - e.dev_off < e.bytes || e.bytes < c_.tensors[t].bytes)
+        return internal("schedule window outside the device pool");
+    }
     switch (e.op) {
       case AUVM_D2H_WRITEBACK:
       case AUVM_DROP: {

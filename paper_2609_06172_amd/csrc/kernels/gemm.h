@@ -17,6 +17,10 @@ struct GemmArgs {
   bool in_bf16, out_bf16;
 };
 
+// Dispatch: bf16 with M <= 16 -> matrix-core GEMV (gemv.hip); other bf16 ->
+// matrix-core tiled GEMM (gemm_mfma.hip); fp32 -> LDS-tiled FMA GEMM.
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s);
+hipError_t launch_gemv_bf16(const GemmArgs& g, hipStream_t s);
+hipError_t launch_gemm_mfma_bf16(const GemmArgs& g, hipStream_t s);
 
 }  // namespace auvm

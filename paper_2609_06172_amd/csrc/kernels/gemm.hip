@@ -1,8 +1,10 @@
-// Tiled GEMM with fused epilogues (store, exact GELU, residual add, SwiGLU).
+// fp32 GEMM with fused epilogues (store, exact GELU, residual add, SwiGLU),
+// and the GEMM dispatch.
 //
 // C[m,n] = sum_k A[m,k] W[n,k]: both operands are K-contiguous ("[out,in]"
 // weights).  Tiles of A and W are staged through LDS as fp32 and each thread
-// accumulates a TM x TN block in registers.
+// accumulates a TM x TN block in registers.  Used for fp32 decoders; bf16
+// work goes to the matrix-core kernels.
 #include <hip/hip_runtime.h>
 
 #include "common.h"
@@ -128,7 +130,7 @@ hipError_t by_epi(const GemmArgs& g, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s) {
-  if (g.in_bf16) return g.out_bf16 ? by_epi<bf16_t, bf16_t>(g, s) : by_epi<bf16_t, float>(g, s);
+  if (g.in_bf16) return g.M <= 16 ? launch_gemv_bf16(g, s) : launch_gemm_mfma_bf16(g, s);
   return by_epi<float, float>(g, s);
 }
 

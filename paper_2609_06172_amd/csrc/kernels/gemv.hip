@@ -1,0 +1,120 @@
+// Decode-shaped GEMM (M <= 16 token rows) on bf16 matrix cores.
+//
+// Y[m, n] = sum_k A[m, k] W[n, k] is HBM-bound on W (16 flop per weight
+// byte).  The 16 token rows fill the M side of v_mfma_f32_16x16x32_bf16 and
+// 16 weight rows its N side, so every weight byte is read once from HBM and
+// fed straight from registers to the matrix core; no LDS staging.
+//
+// Work split: one 256-thread workgroup per 16 output features; its four
+// waves take interleaved 32-wide K chunks (adjacent waves read adjacent 64 B
+// of every weight row), keep fp32 partial tiles in registers and reduce them
+// through LDS in a fixed order (deterministic).  Lane (r, g) = (l % 16, l / 16)
+// holds A[r, 32c + 8g .. +8] and W[n0 + r, 32c + 8g .. +8] for chunk c, so
+// each weight row contributes one full 64-byte segment per load instruction.
+#include <hip/hip_runtime.h>
+
+#include "common.h"
+#include "gemm.h"
+
+namespace auvm {
+
+using namespace dev;
+
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kUnroll = 8;  // K chunks in flight per wave
+
+template <int EPI, class TC>
+__global__ void __launch_bounds__(256) gemv_mfma(const bf16_t* __restrict__ A, const bf16_t* __restrict__ W,
+                                                 const bf16_t* __restrict__ W2, TC* __restrict__ C,
+                                                 int M, int64_t N, int64_t K) {
+  constexpr bool DUAL = EPI == EPI_SWIGLU;
+  __shared__ f32x4 part[4][DUAL ? 2 : 1][64];
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int r = lane & 15, g = lane >> 4;
+  const int64_t n0 = int64_t(blockIdx.x) * 16;
+  const int64_t n = n0 + r;
+  const bool a_ok = r < M, w_ok = n < N;
+  const bf16_t* arow = A + int64_t(a_ok ? r : 0) * K + 8 * g;
+  const bf16_t* wrow = W + (w_ok ? n : 0) * K + 8 * g;
+  const bf16_t* w2row = DUAL ? W2 + (w_ok ? n : 0) * K + 8 * g : nullptr;
+  const int64_t nch = K / 32;
+  const bf16x8 zero = {};
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f}, acc2 = {0.f, 0.f, 0.f, 0.f};
+  for (int64_t c0 = wv; c0 < nch; c0 += 4 * kUnroll) {
+    bf16x8 av[kUnroll], wvv[kUnroll], w2v[DUAL ? kUnroll : 1];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int64_t c = c0 + 4 * u;
+      const bool in = c < nch;
+      av[u] = (in && a_ok) ? *reinterpret_cast<const bf16x8*>(arow + 32 * c) : zero;
+      wvv[u] = (in && w_ok) ? *reinterpret_cast<const bf16x8*>(wrow + 32 * c) : zero;
+      if constexpr (DUAL) w2v[u] = (in && w_ok) ? *reinterpret_cast<const bf16x8*>(w2row + 32 * c) : zero;
+    }
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[u], wvv[u], acc, 0, 0, 0);
+      if constexpr (DUAL) acc2 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[u], w2v[u], acc2, 0, 0, 0);
+    }
+  }
+  part[wv][0][lane] = acc;
+  if constexpr (DUAL) part[wv][1][lane] = acc2;
+  __syncthreads();
+  if (wv != 0) return;
+  f32x4 s = part[0][0][lane], s2 = {0.f, 0.f, 0.f, 0.f};
+  if constexpr (DUAL) s2 = part[0][1][lane];
+#pragma unroll
+  for (int w = 1; w < 4; ++w) {
+    s += part[w][0][lane];
+    if constexpr (DUAL) s2 += part[w][1][lane];
+  }
+  // accumulator layout: element i of lane l is row 4*(l/16)+i, column l%16
+  const int64_t col = n0 + (lane & 15);
+  if (col >= N) return;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row = 4 * (lane >> 4) + i;
+    if (row >= M) continue;
+    float v = s[i];
+    if constexpr (EPI == EPI_GELU) v = gelu_erf(v);
+    if constexpr (EPI == EPI_SWIGLU) v = silu(v) * s2[i];
+    if constexpr (EPI == EPI_RESID) {
+      float* x = reinterpret_cast<float*>(C);
+      x[int64_t(row) * N + col] += v;
+    } else {
+      st(C, int64_t(row) * N + col, v);
+    }
+  }
+}
+
+template <int EPI, class TC>
+hipError_t go(const GemmArgs& g, hipStream_t s) {
+  dim3 grid(unsigned((g.N + 15) / 16));
+  hipLaunchKernelGGL((gemv_mfma<EPI, TC>), grid, dim3(256), 0, s, reinterpret_cast<const bf16_t*>(g.a),
+                     reinterpret_cast<const bf16_t*>(g.w), reinterpret_cast<const bf16_t*>(g.w2),
+                     reinterpret_cast<TC*>(g.c), int(g.M), g.N, g.K);
+  return hipGetLastError();
+}
+
+template <class TC>
+hipError_t by_epi(const GemmArgs& g, hipStream_t s) {
+  switch (g.epi) {
+    case EPI_STORE: return go<EPI_STORE, TC>(g, s);
+    case EPI_GELU: return go<EPI_GELU, TC>(g, s);
+    case EPI_RESID: return go<EPI_RESID, float>(g, s);
+    case EPI_SWIGLU: return go<EPI_SWIGLU, TC>(g, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+// bf16 operands, M <= 16, K % 32 == 0 (checked when the kernel was added).
+hipError_t launch_gemv_bf16(const GemmArgs& g, hipStream_t s) {
+  return g.out_bf16 ? by_epi<bf16_t>(g, s) : by_epi<float>(g, s);
+}
+
+}  // namespace auvm

@@ -19,9 +19,11 @@
 //    CGI kernel to the earliest boundary at which its pool window can be
 //    vacated, in demand order (integrated prefetching with optimal
 //    replacements, issued early);
-//  * pool windows are chosen by (worst victim priority, -writeback bytes,
-//    -victim bytes, -offset); dead values are the best victims and are
-//    dropped, not written back.
+//  * pool windows are chosen by (-writeback bytes, worst victim priority,
+//    -victim bytes, -offset) under farthest-next-use victims (the host link
+//    carries both directions, so a clean victim is cheaper) and by (worst
+//    victim priority, -writeback bytes, -victim bytes, -offset) under LRU;
+//    dead values are the best victims and are dropped, not written back.
 // Integer arithmetic only, so the schedule is reproducible bit for bit.
 #include <algorithm>
 #include <cstring>
@@ -207,7 +209,9 @@ class Replay {
       std::vector<C> c;
       for (auto& sp : spans_)
         if (elig(sp.t)) c.push_back({prio(sp.t, kp), writes_back(sp.t, kp) ? size_[sp.t] : 0, size_[sp.t], sp.t});
-      std::sort(c.begin(), c.end(), [](const C& x, const C& y) {
+      const bool wb_first = belady_;
+      std::sort(c.begin(), c.end(), [wb_first](const C& x, const C& y) {
+        if (wb_first && x.wb != y.wb) return x.wb < y.wb;
         if (x.pr != y.pr) return x.pr > y.pr;
         if (x.wb != y.wb) return x.wb < y.wb;
         if (x.sz != y.sz) return x.sz > y.sz;
@@ -250,7 +254,13 @@ class Replay {
         vb += size_[u];
       }
       if (!ok) continue;
-      bool better = !found || pr > b_pr || (pr == b_pr && (wb < b_wb || (wb == b_wb && vb < b_vb)));
+      bool better;
+      if (!found)
+        better = true;
+      else if (belady_)  // (-writeback bytes, worst priority, -victim bytes)
+        better = wb < b_wb || (wb == b_wb && (pr > b_pr || (pr == b_pr && vb < b_vb)));
+      else               // (worst priority, -writeback bytes, -victim bytes)
+        better = pr > b_pr || (pr == b_pr && (wb < b_wb || (wb == b_wb && vb < b_vb)));
       if (better) {
         found = true;
         b_pr = pr;

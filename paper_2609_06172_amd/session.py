@@ -10,7 +10,7 @@ import ctypes as C
 import numpy as np
 
 from workloads import init as winit
-from workloads.format import DT_BF16, DT_F32, DT_I32, DT_U8
+from workloads.format import DT_BF16, DT_F32, DT_I32, DT_U8, KIND_PARAM
 
 from .capi import Context
 
@@ -60,6 +60,13 @@ class Session:
         """uint8 numpy view of tensor t's host arena window."""
         addr = self.ctx.tensor_host_ptr(t.tid)
         return np.ctypeslib.as_array((C.c_uint8 * t.nbytes).from_address(addr))
+
+    def restore_inputs(self, threads=16):
+        """Rewrite the initial host contents of non-parameter inputs (a rerun
+        after reset must start from them; write-backs may have changed them)."""
+        todo = [t for t in self.w.tensors if t.host_init and t.kind != KIND_PARAM]
+        for t in todo:
+            self.host_view(t)[: t.nbytes] = winit.tensor_bytes(self.w, t)
 
     def write(self, name, value):
         t = self.w.tensors[self.w.id(name)]

@@ -1,0 +1,99 @@
+"""End-to-end parity of whole decoders run through the C-ABI under their
+device budgets: per-layer outputs and logits against the fp64 oracle (fp32:
+rel-L2 1e-4, bf16: 2e-2), greedy tokens under teacher forcing, and outputs
+that do not depend on the transfer policy."""
+import dataclasses
+
+import numpy as np
+import pytest
+
+from oracle import forward as of
+from workloads import configs, init, trace
+
+from gpu_util import rel_l2
+
+pytestmark = pytest.mark.gpu
+
+
+def _session(cfg, **kw):
+    from paper_2609_06172_amd.session import Session
+    w = trace.build(cfg)
+    return Session(w, device=0, **kw), w
+
+
+def test_tiny_fp32_layers_and_logits():
+    cfg = configs.TINY
+    print("tiny fp32 forward at 50% budget", flush=True)
+    s, w = _session(cfg, validate=1)
+    Wt = init.weights_f64(w)
+    ids = init.token_ids(cfg.seed, cfg.batch, cfg.prompt_len, cfg.vocab)
+    outs, logits = of.gpt_forward(cfg, Wt, ids)
+    segs = w.segments["forward"]
+    s.run(*segs[0])
+    for l in range(cfg.n_layers):
+        s.run(*segs[1 + l])
+        assert rel_l2(s.read("x"), outs[l]) < 1e-4, l
+    s.run(*segs[-1])
+    assert rel_l2(s.read("logits"), logits) < 1e-4
+    assert s.ctx.get_executed() == s.ctx.get_schedule()
+    c = s.ctx.get_counters()
+    assert c["d2h_wb_n"] + c["drop_n"] > 0          # the budget forced evictions
+    s.close()
+
+
+def test_gpt_small_bf16_logits():
+    cfg = configs.GPT_SMALL
+    print("gpt-small bf16 prefill", flush=True)
+    s, w = _session(cfg)
+    s.run_all()
+    Wt = init.weights_f64(w)
+    ids = init.token_ids(cfg.seed, cfg.batch, cfg.prompt_len, cfg.vocab)
+    outs, logits = of.gpt_forward(cfg, Wt, ids)
+    assert rel_l2(s.read("logits"), logits) < 2e-2
+    assert rel_l2(s.read("x"), outs[-1]) < 2e-2
+    s.close()
+
+
+def _llama_run(cfg, **kw):
+    s, w = _session(cfg, **kw)
+    logits = []
+    k0, n = w.segments["prefill"][0]
+    s.run(k0, n)
+    logits.append(s.read("logits"))
+    for k0, n in w.segments["decode"]:
+        s.run(k0, n)
+        logits.append(s.read("logits"))
+    gen = s.read("gen")
+    counters = s.ctx.get_counters()
+    executed_ok = s.ctx.get_executed() == s.ctx.get_schedule()
+    s.close()
+    return w, logits, gen, counters, executed_ok
+
+
+def test_llama_small_prefill_decode_teacher_forced():
+    cfg = configs.LLAMA_SMALL
+    print("llama-small bf16 prefill + decode at 1.5x", flush=True)
+    w, logits, gen, c, ex_ok = _llama_run(cfg, validate=1)
+    assert ex_ok
+    Wt = init.weights_f64(w)
+    ids = init.token_ids(cfg.seed, cfg.batch, cfg.prompt_len, cfg.vocab)
+    ref = of.llama_generate(cfg, Wt, ids, forced=gen[:cfg.decode_steps])
+    for s_, (a, b) in enumerate(zip(logits, ref["logits"])):
+        assert rel_l2(a, b) < 2e-2, s_
+        err = np.abs(a - b).max()
+        srt = np.sort(b, axis=-1)
+        margin = srt[:, -1] - srt[:, -2]
+        sure = margin > 4 * err
+        assert np.array_equal(gen[s_][sure], ref["tokens"][s_][sure]), s_
+    assert c["h2d_prefetch_n"] > 0
+
+
+def test_outputs_do_not_depend_on_the_policy():
+    cfg = configs.LLAMA_SMALL
+    print("llama-small under three policies", flush=True)
+    runs = [_llama_run(cfg, variant=v) for v in (4, 0, 2)]
+    for w, logits, gen, c, ex_ok in runs[1:]:
+        assert ex_ok
+        assert np.array_equal(gen, runs[0][2])
+        for a, b in zip(logits, runs[0][1]):
+            assert np.array_equal(a, b)

@@ -1,0 +1,167 @@
+"""Per-op parity of the HIP kernels with the fp64 oracle, each op run as a
+one-kernel trace through the C-ABI (budget = footprint).  Shapes cover several
+tiles and ragged tails; bf16 results are compared at bf16 output precision."""
+import numpy as np
+import pytest
+
+from oracle import forward as of
+from workloads.format import (DT_BF16, DT_F32, DT_I32, MODE_R, MODE_RW, MODE_W,
+                              OP_ARGMAX, OP_ATTN_CACHE, OP_ATTN_QKV, OP_EMBED,
+                              OP_LAYERNORM, OP_LINEAR, OP_LINEAR_GELU,
+                              OP_LINEAR_RESID, OP_LINEAR_SWIGLU, OP_RMSNORM,
+                              OP_ROPE_KV)
+
+from gpu_util import rel_l2, single_kernel, write_inputs
+
+pytestmark = pytest.mark.gpu
+
+# fp32 kernels differ from fp64 only by accumulation order; bf16 outputs are
+# rounded once to 8 mantissa bits (relative error <= 2^-9 per element)
+TOL = {DT_F32: 1e-5, DT_BF16: 4e-3}
+
+
+def _run(op_, shape, operands, out):
+    from paper_2609_06172_amd.session import Session
+    w, vals = single_kernel(op_, shape, operands)
+    print(f"op={op_} shape={shape}", flush=True)
+    s = Session(w, device=0, M=w.footprint, fill=False)
+    write_inputs(s, w, vals)
+    s.run_all()
+    res = {n: s.read(n) for n in out}
+    s.close()
+    return vals, res
+
+
+RNG = np.random.default_rng(1234)
+
+
+def rnd(*shape, scale=1.0):
+    return RNG.standard_normal(shape).astype(np.float32) * scale
+
+
+LIN_SHAPES = [(1, 64, 32), (5, 100, 64), (16, 4096 + 16, 256), (17, 96, 96), (100, 130, 160),
+              (257, 300, 512)]
+
+
+@pytest.mark.parametrize("dt", [DT_F32, DT_BF16])
+@pytest.mark.parametrize("M,N,K", LIN_SHAPES)
+@pytest.mark.parametrize("op_", [OP_LINEAR, OP_LINEAR_GELU, OP_LINEAR_RESID, OP_LINEAR_SWIGLU])
+def test_linear_family(op_, M, N, K, dt):
+    a, W, W2 = rnd(M, K), rnd(N, K, scale=K ** -0.5), rnd(N, K, scale=K ** -0.5)
+    out_dt = DT_F32 if op_ == OP_LINEAR_RESID else dt
+    x0 = rnd(M, N)
+    ops = [("a", (M, K), dt, MODE_R, a), ("W", (N, K), dt, MODE_R, W)]
+    if op_ == OP_LINEAR_SWIGLU:
+        ops.append(("W2", (N, K), dt, MODE_R, W2))
+    if op_ == OP_LINEAR_RESID:
+        ops.append(("c", (M, N), DT_F32, MODE_RW, x0))
+    else:
+        ops.append(("c", (M, N), out_dt, MODE_W, None))
+    vals, res = _run(op_, (M, N, K), ops, ["c"])
+    y = of.linear(vals["a"], vals["W"])
+    if op_ == OP_LINEAR_GELU:
+        y = of.gelu(y)
+    elif op_ == OP_LINEAR_RESID:
+        y = vals["c"] + y
+    elif op_ == OP_LINEAR_SWIGLU:
+        y = of.silu(y) * of.linear(vals["a"], vals["W2"])
+    assert rel_l2(res["c"], y) < TOL[out_dt]
+
+
+@pytest.mark.parametrize("dt", [DT_F32, DT_BF16])
+@pytest.mark.parametrize("T,H,stride,offset", [(7, 128, 1, 0), (3, 4096, 5, 4), (33, 2048, 1, 0)])
+def test_norms(T, H, stride, offset, dt):
+    rows = (T - 1) * stride + offset + 1
+    x = rnd(rows, H) * 3 + 0.5
+    g, b = rnd(H) * 0.5 + 1, rnd(H) * 0.1
+    vals, res = _run(OP_LAYERNORM, (T, H, stride, offset),
+                     [("x", (rows, H), DT_F32, MODE_R, x), ("g", (H,), dt, MODE_R, g),
+                      ("b", (H,), dt, MODE_R, b), ("h", (T, H), dt, MODE_W, None)], ["h"])
+    sel = vals["x"][np.arange(T) * stride + offset]
+    assert rel_l2(res["h"], of.layernorm(sel, vals["g"], vals["b"])) < TOL[dt] * 2
+    vals, res = _run(OP_RMSNORM, (T, H, stride, offset),
+                     [("x", (rows, H), DT_F32, MODE_R, x), ("g", (H,), dt, MODE_R, g),
+                      ("h", (T, H), dt, MODE_W, None)], ["h"])
+    assert rel_l2(res["h"], of.rmsnorm(sel, vals["g"])) < TOL[dt] * 2
+
+
+@pytest.mark.parametrize("dt", [DT_F32, DT_BF16])
+def test_embed(dt):
+    V, H, T = 1000, 256, 37
+    E = rnd(V, H)
+    ids = RNG.integers(0, V, T).astype(np.int32)
+    vals, res = _run(OP_EMBED, (T, H, V), [("ids", (T,), DT_I32, MODE_R, ids),
+                                           ("E", (V, H), dt, MODE_R, E),
+                                           ("x", (T, H), DT_F32, MODE_W, None)], ["x"])
+    assert np.array_equal(res["x"], vals["E"][ids].astype(np.float32))
+
+
+@pytest.mark.parametrize("dt", [DT_F32, DT_BF16])
+@pytest.mark.parametrize("B,S,nH,d", [(1, 32, 4, 32), (2, 75, 3, 64), (1, 130, 2, 128)])
+def test_attention_fused_qkv(B, S, nH, d, dt):
+    Hd = nH * d
+    qkv = rnd(B * S, 3 * Hd)
+    vals, res = _run(OP_ATTN_QKV, (B, S, nH, d), [("qkv", (B * S, 3 * Hd), dt, MODE_R, qkv),
+                                                  ("o", (B * S, Hd), dt, MODE_W, None)], ["o"])
+    q = vals["qkv"]
+    ref = np.empty((B * S, Hd))
+    for b in range(B):
+        r = slice(b * S, (b + 1) * S)
+        for h in range(nH):
+            c = slice(h * d, (h + 1) * d)
+            ref[r, c] = of.causal_attention(q[r, c], q[r, Hd + h * d:Hd + (h + 1) * d],
+                                            q[r, 2 * Hd + h * d:2 * Hd + (h + 1) * d])
+    assert rel_l2(res["o"], ref) < TOL[dt] * 2
+
+
+@pytest.mark.parametrize("B,S,nH,d,Lmax,pos0", [(2, 1, 2, 128, 300, 257), (3, 40, 2, 128, 64, 0),
+                                                (1, 5, 4, 64, 20, 9), (16, 1, 2, 128, 1280, 1100)])
+def test_rope_kv_and_cached_attention(B, S, nH, d, Lmax, pos0):
+    dt = DT_BF16
+    Hd = nH * d
+    q, k, v = rnd(B * S, Hd), rnd(B * S, Hd), rnd(B * S, Hd)
+    Kc, Vc = rnd(B, nH, Lmax, d), rnd(B, nH, Lmax, d)
+    shape = (B, S, nH, d, Lmax, pos0)
+    vals, res = _run(OP_ROPE_KV, shape,
+                     [("q", (B * S, Hd), dt, MODE_RW, q), ("k", (B * S, Hd), dt, MODE_R, k),
+                      ("v", (B * S, Hd), dt, MODE_R, v), ("Kc", (B, nH, Lmax, d), dt, MODE_RW, Kc),
+                      ("Vc", (B, nH, Lmax, d), dt, MODE_RW, Vc)], ["q", "Kc", "Vc"])
+    pos = pos0 + np.arange(S)
+    qr = of.rope(vals["q"].reshape(B, S, nH, d), pos[None, :, None])
+    kr = of.rope(vals["k"].reshape(B, S, nH, d), pos[None, :, None])
+    Kref, Vref = vals["Kc"].copy(), vals["Vc"].copy()
+    Kref[:, :, pos0:pos0 + S] = kr.transpose(0, 2, 1, 3)
+    Vref[:, :, pos0:pos0 + S] = vals["v"].reshape(B, S, nH, d).transpose(0, 2, 1, 3)
+    assert rel_l2(res["q"], qr.reshape(B * S, Hd)) < TOL[dt] * 2
+    assert rel_l2(res["Kc"][:, :, pos0:pos0 + S], Kref[:, :, pos0:pos0 + S]) < TOL[dt] * 2
+    assert np.array_equal(res["Vc"], Vref.astype(np.float32))
+    untouched = np.ones(Lmax, bool)
+    untouched[pos0:pos0 + S] = False
+    assert np.array_equal(res["Kc"][:, :, untouched], Kref[:, :, untouched].astype(np.float32))
+    # attention of the roped queries over the updated cache
+    vals2, res2 = _run(OP_ATTN_CACHE, shape,
+                       [("q", (B * S, Hd), dt, MODE_R, res["q"]), ("Kc", (B, nH, Lmax, d), dt, MODE_R, res["Kc"]),
+                        ("Vc", (B, nH, Lmax, d), dt, MODE_R, res["Vc"]), ("o", (B * S, Hd), dt, MODE_W, None)], ["o"])
+    qq = vals2["q"].reshape(B, S, nH, d)
+    ref = np.empty((B, S, nH, d))
+    for b in range(B):
+        for h in range(nH):
+            L = pos0 + S
+            ref[b, :, h] = of.causal_attention(qq[b, :, h], vals2["Kc"][b, h, :L], vals2["Vc"][b, h, :L], pos0)
+    assert rel_l2(res2["o"], ref.reshape(B * S, Hd)) < TOL[dt] * 2
+
+
+@pytest.mark.parametrize("B,V", [(1, 1000), (16, 32000), (3, 50000)])
+def test_argmax_lowest_index(B, V):
+    logits = rnd(B, V)
+    logits[0, 5] = logits[0, 900] = 50.0          # tie: lowest index wins
+    row = 2
+    vals, res = _run(OP_ARGMAX, (B, V, row), [("logits", (B, V), DT_F32, MODE_R, logits),
+                                             ("tok", (B,), DT_I32, MODE_W, None),
+                                             ("gen", (row + 1, B), DT_I32, MODE_RW,
+                                              np.zeros((row + 1, B), np.int32))], ["tok", "gen"])
+    ref = of.argmax_lowest(vals["logits"])
+    assert ref[0] == 5
+    assert np.array_equal(res["tok"], ref)
+    assert np.array_equal(res["gen"][row], ref)
+    assert np.array_equal(res["gen"][:row], np.zeros((row, B), np.int32))
