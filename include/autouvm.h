@@ -114,12 +114,15 @@ typedef struct {
 } auvm_kernel_desc;
 
 typedef struct {
-  uint32_t variant;       /* AUVM_DEMAND_LRU .. AUVM_T_A_P (default T_A_P) */
+  uint32_t variant;       /* AUVM_DEMAND_LRU .. AUVM_T_A_P (default T_A_P, guard 4) */
   uint32_t lookahead;     /* max kernels a fetch runs ahead; 0 = T/T+A: 1, T+A+P: unlimited */
   uint32_t affinity_w;    /* pin operands reused within this many kernels (default 1) */
   uint32_t placement;     /* AUVM_PLACE_POOL (default) or AUVM_PLACE_IDEAL (plan-only) */
   uint32_t validate;      /* 1: fill every dropped or written-back window with NaN bytes */
   uint32_t timing;        /* 1: record per-kernel start/end events during run */
+  uint32_t guard;         /* T+A+P only: a demand at kernel j prefers victims not used by
+                             kernels j-guard..j-1, so their replacement fetch can start
+                             that many kernels earlier (0 = plain farthest-next-use) */
 } auvm_policy;
 
 typedef struct {

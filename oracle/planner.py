@@ -100,7 +100,7 @@ class Result:
 
 
 def plan(tensors, kernels, M, roofs=DEFAULT_ROOFS, variant=VAR_T_A_P, lookahead=0,
-         affinity_w=1, placement=PLACE_POOL):
+         affinity_w=1, placement=PLACE_POOL, guard=None):
     """Replay the policy.
 
     tensors: list of dicts with keys nbytes, dtype, kind, host_init.
@@ -111,15 +111,20 @@ def plan(tensors, kernels, M, roofs=DEFAULT_ROOFS, variant=VAR_T_A_P, lookahead=
     The full method (T+A+P) is two passes: the demand timeline with
     farthest-next-use victims and affinity pins, then every fetch of a CGI
     kernel is moved to the earliest boundary at which its window can be
-    vacated (``_retime``).  The other variants are one pass.
+    vacated (``_retime``).  In its demand pass a victim must, if any window
+    allows it, not have been used by the ``guard`` kernels before the demand
+    point, so that the moved fetch overlaps those kernels (default 4; 0 gives
+    plain farthest-next-use).  The other variants are one pass.
     """
     if variant == VAR_T_A_P and placement == PLACE_IDEAL:
         raise PlanError(E_INVAL, "the full method retimes fetches into physical pool windows")
+    if guard is None:
+        guard = 4 if variant == VAR_T_A_P else 0
     if variant != VAR_T_A_P:
         return _replay(tensors, kernels, M, roofs, variant, lookahead, affinity_w,
-                       placement, scan=variant in (VAR_T, VAR_T_A))
+                       placement, scan=variant in (VAR_T, VAR_T_A), guard=0)
     base = _replay(tensors, kernels, M, roofs, variant, lookahead, affinity_w,
-                   placement, scan=False)
+                   placement, scan=False, guard=guard)
     return _retime(tensors, kernels, M, roofs, lookahead, base)
 
 
@@ -135,7 +140,7 @@ def _access(tensors, kernels):
     return A, uses, use_mode
 
 
-def _replay(tensors, kernels, M, roofs, variant, lookahead, affinity_w, placement, scan):
+def _replay(tensors, kernels, M, roofs, variant, lookahead, affinity_w, placement, scan, guard):
     nT, K = len(tensors), len(kernels)
     size = [aligned(t["nbytes"]) for t in tensors]
     dtypes = [t["dtype"] for t in tensors]
@@ -269,7 +274,12 @@ def _replay(tensors, kernels, M, roofs, variant, lookahead, affinity_w, placemen
 
             def elig(u, k=k):
                 return u not in Aset[k] and pin[u] < k
-            r = place(t, elig, k)
+
+            def elig_guarded(u, k=k):
+                return elig(u) and last[u] < k - guard
+            r = place(t, elig_guarded, k) if guard else None
+            if r is None:
+                r = place(t, elig, k)
             if r is None:
                 for u in range(nT):
                     pin[u] = -1

@@ -30,7 +30,8 @@ class KernelDesc(C.Structure):
 
 class Policy(C.Structure):
     _fields_ = [("variant", C.c_uint32), ("lookahead", C.c_uint32), ("affinity_w", C.c_uint32),
-                ("placement", C.c_uint32), ("validate", C.c_uint32), ("timing", C.c_uint32)]
+                ("placement", C.c_uint32), ("validate", C.c_uint32), ("timing", C.c_uint32),
+                ("guard", C.c_uint32)]
 
 
 class SchedEntry(C.Structure):
@@ -198,8 +199,11 @@ class Context:
     def set_roofs(self, peak_flops, hbm_Bps, link_Bps):
         self._check(self._L.auvm_set_roofs(self._h, int(peak_flops), int(hbm_Bps), int(link_Bps)))
 
-    def set_policy(self, variant=4, lookahead=0, affinity_w=1, placement=0, validate=0, timing=0):
-        p = Policy(variant, lookahead, affinity_w, placement, validate, timing)
+    def set_policy(self, variant=4, lookahead=0, affinity_w=1, placement=0, validate=0, timing=0,
+                   guard=None):
+        if guard is None:
+            guard = 4 if variant == 4 else 0
+        p = Policy(variant, lookahead, affinity_w, placement, validate, timing, guard)
         self._check(self._L.auvm_set_policy(self._h, C.byref(p)))
 
     def plan(self):

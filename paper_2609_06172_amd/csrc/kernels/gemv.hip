@@ -5,9 +5,9 @@
 // 16 weight rows its N side, so every weight byte is read once from HBM and
 // fed straight from registers to the matrix core; no LDS staging.
 //
-// Work split: one 256-thread workgroup per 16 output features; its four
+// Work split: one 512-thread workgroup per 16 output features; its eight
 // waves take interleaved 32-wide K chunks (adjacent waves read adjacent 64 B
-// of every weight row), keep fp32 partial tiles in registers and reduce them
+// of every weight row), eight chunks in flight per wave, keep fp32 partial tiles in registers and reduce them
 // through LDS in a fixed order (deterministic).  Lane (r, g) = (l % 16, l / 16)
 // holds A[r, 32c + 8g .. +8] and W[n0 + r, 32c + 8g .. +8] for chunk c, so
 // each weight row contributes one full 64-byte segment per load instruction.
@@ -26,13 +26,14 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kUnroll = 8;  // K chunks in flight per wave
+constexpr int kWaves = 8;   // waves per workgroup, splitting K
 
 template <int EPI, class TC>
-__global__ void __launch_bounds__(256) gemv_mfma(const bf16_t* __restrict__ A, const bf16_t* __restrict__ W,
+__global__ void __launch_bounds__(64 * kWaves) gemv_mfma(const bf16_t* __restrict__ A, const bf16_t* __restrict__ W,
                                                  const bf16_t* __restrict__ W2, TC* __restrict__ C,
                                                  int M, int64_t N, int64_t K) {
   constexpr bool DUAL = EPI == EPI_SWIGLU;
-  __shared__ f32x4 part[4][DUAL ? 2 : 1][64];
+  __shared__ f32x4 part[kWaves][DUAL ? 2 : 1][64];
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int r = lane & 15, g = lane >> 4;
   const int64_t n0 = int64_t(blockIdx.x) * 16;
@@ -44,11 +45,11 @@ __global__ void __launch_bounds__(256) gemv_mfma(const bf16_t* __restrict__ A, c
   const int64_t nch = K / 32;
   const bf16x8 zero = {};
   f32x4 acc = {0.f, 0.f, 0.f, 0.f}, acc2 = {0.f, 0.f, 0.f, 0.f};
-  for (int64_t c0 = wv; c0 < nch; c0 += 4 * kUnroll) {
+  for (int64_t c0 = wv; c0 < nch; c0 += kWaves * kUnroll) {
     bf16x8 av[kUnroll], wvv[kUnroll], w2v[DUAL ? kUnroll : 1];
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
-      const int64_t c = c0 + 4 * u;
+      const int64_t c = c0 + kWaves * u;
       const bool in = c < nch;
       av[u] = (in && a_ok) ? *reinterpret_cast<const bf16x8*>(arow + 32 * c) : zero;
       wvv[u] = (in && w_ok) ? *reinterpret_cast<const bf16x8*>(wrow + 32 * c) : zero;
@@ -67,7 +68,7 @@ __global__ void __launch_bounds__(256) gemv_mfma(const bf16_t* __restrict__ A, c
   f32x4 s = part[0][0][lane], s2 = {0.f, 0.f, 0.f, 0.f};
   if constexpr (DUAL) s2 = part[0][1][lane];
 #pragma unroll
-  for (int w = 1; w < 4; ++w) {
+  for (int w = 1; w < kWaves; ++w) {
     s += part[w][0][lane];
     if constexpr (DUAL) s2 += part[w][1][lane];
   }
@@ -93,7 +94,7 @@ __global__ void __launch_bounds__(256) gemv_mfma(const bf16_t* __restrict__ A, c
 template <int EPI, class TC>
 hipError_t go(const GemmArgs& g, hipStream_t s) {
   dim3 grid(unsigned((g.N + 15) / 16));
-  hipLaunchKernelGGL((gemv_mfma<EPI, TC>), grid, dim3(256), 0, s, reinterpret_cast<const bf16_t*>(g.a),
+  hipLaunchKernelGGL((gemv_mfma<EPI, TC>), grid, dim3(64 * kWaves), 0, s, reinterpret_cast<const bf16_t*>(g.a),
                      reinterpret_cast<const bf16_t*>(g.w), reinterpret_cast<const bf16_t*>(g.w2),
                      reinterpret_cast<TC*>(g.c), int(g.M), g.N, g.K);
   return hipGetLastError();

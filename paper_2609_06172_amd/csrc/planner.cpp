@@ -18,7 +18,8 @@
 //    demand paging (the profile knows the future) and moves each fetch of a
 //    CGI kernel to the earliest boundary at which its pool window can be
 //    vacated, in demand order (integrated prefetching with optimal
-//    replacements, issued early);
+//    replacements, issued early); its demand pass prefers victims not used
+//    by the previous `guard` kernels, which lets each fetch overlap them;
 //  * pool windows are chosen by (-writeback bytes, worst victim priority,
 //    -victim bytes, -offset) under farthest-next-use victims (the host link
 //    carries both directions, so a clean victim is cheaper) and by (worst
@@ -109,6 +110,8 @@ class Replay {
     pin_.assign(nT_, -1);
     pf_need_.assign(nT_, -1);
     mark_.assign(nT_, -1);
+    last_.assign(nT_, -1);
+    guard_ = (p.variant == AUVM_T_A_P && !scan) ? int64_t(p.guard) : 0;
   }
 
   PlanResult run() {
@@ -130,9 +133,11 @@ class Replay {
           throw PlanError{AUVM_E_INVAL, "kernel " + std::to_string(k) + " reads tensor " +
                                             std::to_string(t) + " before any write"};
         auto elig = [&](int32_t u) { return mark_[u] != k && pin_[u] < k; };
+        auto guarded = [&](int32_t u) { return elig(u) && last_[u] < k - guard_; };
         uint64_t a_off;
         std::vector<int32_t> victims;
-        if (!place(t, elig, k, &a_off, &victims)) {
+        bool placed = guard_ > 0 && place(t, guarded, k, &a_off, &victims);
+        if (!placed && !place(t, elig, k, &a_off, &victims)) {
           std::fill(pin_.begin(), pin_.end(), -1);
           if (!place(t, elig, k, &a_off, &victims)) {
             uint64_t need = 0;
@@ -169,6 +174,7 @@ class Replay {
       for (auto& a : kd.acc) {
         if (a.second & AUVM_W) val_[a.first] = DEV_DIRTY;
         lru_[a.first] = k;
+        last_[a.first] = k;
         pf_need_[a.first] = -1;
       }
       // (v) look-ahead affinity pins
@@ -373,7 +379,8 @@ class Replay {
   uint32_t D_ = 1;
   std::vector<uint8_t> val_, resident_;
   std::vector<uint64_t> off_;
-  std::vector<int64_t> lru_, pin_, pf_need_, mark_, prot_;
+  std::vector<int64_t> lru_, pin_, pf_need_, mark_, prot_, last_;
+  int64_t guard_ = 0;
   int64_t scan_id_ = 0;
   std::vector<Span> spans_;  // resident windows sorted by offset (insertion order for IDEAL)
   uint64_t used_ = 0;

@@ -97,7 +97,7 @@ def test_embed(dt):
 
 
 @pytest.mark.parametrize("dt", [DT_F32, DT_BF16])
-@pytest.mark.parametrize("B,S,nH,d", [(1, 32, 4, 32), (2, 75, 3, 64), (1, 130, 2, 128)])
+@pytest.mark.parametrize("B,S,nH,d", [(1, 32, 4, 32), (2, 75, 3, 64), (1, 130, 2, 128), (2, 12, 2, 128)])
 def test_attention_fused_qkv(B, S, nH, d, dt):
     Hd = nH * d
     qkv = rnd(B * S, 3 * Hd)
@@ -115,7 +115,9 @@ def test_attention_fused_qkv(B, S, nH, d, dt):
 
 
 @pytest.mark.parametrize("B,S,nH,d,Lmax,pos0", [(2, 1, 2, 128, 300, 257), (3, 40, 2, 128, 64, 0),
-                                                (1, 5, 4, 64, 20, 9), (16, 1, 2, 128, 1280, 1100)])
+                                                (1, 5, 4, 64, 20, 9), (16, 1, 2, 128, 1280, 1100),
+                                                (2, 7, 2, 128, 64, 20), (1, 1, 1, 128, 8, 0),
+                                                (4, 16, 2, 128, 300, 131)])
 def test_rope_kv_and_cached_attention(B, S, nH, d, Lmax, pos0):
     dt = DT_BF16
     Hd = nH * d
