@@ -114,7 +114,7 @@ typedef struct {
 } auvm_kernel_desc;
 
 typedef struct {
-  uint32_t variant;       /* AUVM_DEMAND_LRU .. AUVM_T_A_P (default T_A_P, guard 4) */
+  uint32_t variant;       /* AUVM_DEMAND_LRU .. AUVM_T_A_P (default T_A_P, guard 4, bucket 32) */
   uint32_t lookahead;     /* max kernels a fetch runs ahead; 0 = T/T+A: 1, T+A+P: unlimited */
   uint32_t affinity_w;    /* pin operands reused within this many kernels (default 1) */
   uint32_t placement;     /* AUVM_PLACE_POOL (default) or AUVM_PLACE_IDEAL (plan-only) */
@@ -123,6 +123,10 @@ typedef struct {
   uint32_t guard;         /* T+A+P only: a demand at kernel j prefers victims not used by
                              kernels j-guard..j-1, so their replacement fetch can start
                              that many kernels earlier (0 = plain farthest-next-use) */
+  uint32_t bucket;        /* T+A+P and DEMAND_BELADY: victims' next uses are compared in
+                             buckets of this many kernels, and within a bucket the pool
+                             window that evicts fewer bytes wins (1 = exact
+                             farthest-next-use; 0 is read as 1; default 32 for T+A+P) */
 } auvm_policy;
 
 typedef struct {

@@ -29,8 +29,11 @@ notes) are:
   link is shared by both directions); LRU for the demand baseline and the
   T / T+A ablation steps;
 * placement picks a window of the pool whose resident tensors may all be
-  evicted, maximising (-writeback bytes, worst victim priority, -victim
-  bytes, -offset) under farthest-next-use and (worst victim priority,
+  evicted, maximising (-writeback bytes, bucket of the worst victim's
+  next-use distance, -victim bytes, worst victim's next use, -offset) under
+  farthest-next-use, where uses within the same ``bucket`` kernels count as
+  equally far so that, among them, the window evicting fewer bytes wins
+  (bucket 1 is exact farthest-next-use), and (worst victim priority,
   -writeback bytes, -victim bytes, -offset) under LRU;
 * after each launch, the prefetch scan walks upcoming kernels in order and
   fetches the missing read operands of each CGI kernel whose host value is
@@ -100,7 +103,7 @@ class Result:
 
 
 def plan(tensors, kernels, M, roofs=DEFAULT_ROOFS, variant=VAR_T_A_P, lookahead=0,
-         affinity_w=1, placement=PLACE_POOL, guard=None):
+         affinity_w=1, placement=PLACE_POOL, guard=None, bucket=None):
     """Replay the policy.
 
     tensors: list of dicts with keys nbytes, dtype, kind, host_init.
@@ -120,11 +123,14 @@ def plan(tensors, kernels, M, roofs=DEFAULT_ROOFS, variant=VAR_T_A_P, lookahead=
         raise PlanError(E_INVAL, "the full method retimes fetches into physical pool windows")
     if guard is None:
         guard = 4 if variant == VAR_T_A_P else 0
+    if bucket is None:
+        bucket = 32 if variant == VAR_T_A_P else 1
     if variant != VAR_T_A_P:
         return _replay(tensors, kernels, M, roofs, variant, lookahead, affinity_w,
-                       placement, scan=variant in (VAR_T, VAR_T_A), guard=0)
+                       placement, scan=variant in (VAR_T, VAR_T_A), guard=0,
+                       bucket=bucket if variant == VAR_DEMAND_BELADY else 1)
     base = _replay(tensors, kernels, M, roofs, variant, lookahead, affinity_w,
-                   placement, scan=False, guard=guard)
+                   placement, scan=False, guard=guard, bucket=bucket)
     return _retime(tensors, kernels, M, roofs, lookahead, base)
 
 
@@ -140,7 +146,8 @@ def _access(tensors, kernels):
     return A, uses, use_mode
 
 
-def _replay(tensors, kernels, M, roofs, variant, lookahead, affinity_w, placement, scan, guard):
+def _replay(tensors, kernels, M, roofs, variant, lookahead, affinity_w, placement, scan, guard,
+            bucket):
     nT, K = len(tensors), len(kernels)
     size = [aligned(t["nbytes"]) for t in tensors]
     dtypes = [t["dtype"] for t in tensors]
@@ -194,6 +201,10 @@ def _replay(tensors, kernels, M, roofs, variant, lookahead, affinity_w, placemen
             return nu(u, kp) if live(u, kp) else INF
         return -lru[u]
 
+    def near(p, kp):
+        """Next-use distance class: uses within the same bucket count as equally far."""
+        return INF if p == INF else (p - kp) // bucket
+
     def writes_back(u, kp):
         return val[u] == DEV_DIRTY and (variant == VAR_DEMAND_LRU or live(u, kp))
 
@@ -204,7 +215,8 @@ def _replay(tensors, kernels, M, roofs, variant, lookahead, affinity_w, placemen
             if M - used_bytes[0] >= s:
                 return 0, []
             if belady:
-                order = lambda u: (size[u] if writes_back(u, kp) else 0, -prio(u, kp), -size[u], u)
+                order = lambda u: (size[u] if writes_back(u, kp) else 0, -near(prio(u, kp), kp),
+                                   -size[u], -prio(u, kp), u)
             else:
                 order = lambda u: (-prio(u, kp), size[u] if writes_back(u, kp) else 0, -size[u], u)
             cands = sorted((u for u in off if eligible(u)), key=order)
@@ -233,7 +245,10 @@ def _replay(tensors, kernels, M, roofs, variant, lookahead, affinity_w, placemen
             minpr = min((prio(u, kp) for u in over), default=INF)
             wb = sum(size[u] for u in over if writes_back(u, kp))
             vb = sum(size[u] for u in over)
-            key = (-wb, minpr, -vb, -a) if belady else (minpr, -wb, -vb, -a)
+            if belady:
+                key = (-wb, near(minpr, kp), -vb, minpr, -a)
+            else:
+                key = (minpr, -wb, -vb, -a)
             if best_key is None or key > best_key:
                 best, best_key = (a, over), key
         return best

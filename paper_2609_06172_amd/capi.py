@@ -31,7 +31,7 @@ class KernelDesc(C.Structure):
 class Policy(C.Structure):
     _fields_ = [("variant", C.c_uint32), ("lookahead", C.c_uint32), ("affinity_w", C.c_uint32),
                 ("placement", C.c_uint32), ("validate", C.c_uint32), ("timing", C.c_uint32),
-                ("guard", C.c_uint32)]
+                ("guard", C.c_uint32), ("bucket", C.c_uint32)]
 
 
 class SchedEntry(C.Structure):
@@ -200,10 +200,12 @@ class Context:
         self._check(self._L.auvm_set_roofs(self._h, int(peak_flops), int(hbm_Bps), int(link_Bps)))
 
     def set_policy(self, variant=4, lookahead=0, affinity_w=1, placement=0, validate=0, timing=0,
-                   guard=None):
+                   guard=None, bucket=None):
         if guard is None:
             guard = 4 if variant == 4 else 0
-        p = Policy(variant, lookahead, affinity_w, placement, validate, timing, guard)
+        if bucket is None:
+            bucket = 32 if variant == 4 else 1
+        p = Policy(variant, lookahead, affinity_w, placement, validate, timing, guard, bucket)
         self._check(self._L.auvm_set_policy(self._h, C.byref(p)))
 
     def plan(self):

@@ -31,7 +31,7 @@ struct Ctx {
   bool pool_owned = false;
   bool budget_set = false;
   Roofs roofs;
-  auvm_policy pol{AUVM_T_A_P, 0, 1, AUVM_PLACE_POOL, 0, 0, 4};
+  auvm_policy pol{AUVM_T_A_P, 0, 1, AUVM_PLACE_POOL, 0, 0, 4, 32};
   // plan and execution
   bool planned = false;
   PlanResult plan;

@@ -20,11 +20,13 @@
 //    vacated, in demand order (integrated prefetching with optimal
 //    replacements, issued early); its demand pass prefers victims not used
 //    by the previous `guard` kernels, which lets each fetch overlap them;
-//  * pool windows are chosen by (-writeback bytes, worst victim priority,
-//    -victim bytes, -offset) under farthest-next-use victims (the host link
-//    carries both directions, so a clean victim is cheaper) and by (worst
-//    victim priority, -writeback bytes, -victim bytes, -offset) under LRU;
-//    dead values are the best victims and are dropped, not written back.
+//  * pool windows are chosen by (-writeback bytes, bucket of the worst
+//    victim's next-use distance, -victim bytes, worst next use, -offset)
+//    under farthest-next-use victims (the host link carries both directions,
+//    so a clean victim is cheaper; next uses within one bucket of kernels
+//    count as equally far, so fewer evicted bytes decide among them) and by
+//    (worst victim priority, -writeback bytes, -victim bytes, -offset) under
+//    LRU; dead values are the best victims and are dropped, not written back.
 // Integer arithmetic only, so the schedule is reproducible bit for bit.
 #include <algorithm>
 #include <cstring>
@@ -112,6 +114,7 @@ class Replay {
     mark_.assign(nT_, -1);
     last_.assign(nT_, -1);
     guard_ = (p.variant == AUVM_T_A_P && !scan) ? int64_t(p.guard) : 0;
+    bucket_ = belady_ ? std::max<int64_t>(1, p.bucket) : 1;
   }
 
   PlanResult run() {
@@ -194,6 +197,8 @@ class Replay {
     if (belady_) return uses_.live(u, kp) ? uses_.nu(u, kp) : kInf;
     return -lru_[u];
   }
+  // next-use distance class: uses within the same bucket count as equally far
+  int64_t near(int64_t p, int64_t kp) const { return p == kInf ? kInf : (p - kp) / bucket_; }
   bool writes_back(int32_t u, int64_t kp) const {
     return val_[u] == DEV_DIRTY && (pol_.variant == AUVM_DEMAND_LRU || uses_.live(u, kp));
   }
@@ -208,16 +213,25 @@ class Replay {
         return true;
       }
       struct C {
-        int64_t pr;
+        int64_t pr, nb;
         uint64_t wb, sz;
         int32_t u;
       };
       std::vector<C> c;
       for (auto& sp : spans_)
-        if (elig(sp.t)) c.push_back({prio(sp.t, kp), writes_back(sp.t, kp) ? size_[sp.t] : 0, size_[sp.t], sp.t});
-      const bool wb_first = belady_;
-      std::sort(c.begin(), c.end(), [wb_first](const C& x, const C& y) {
-        if (wb_first && x.wb != y.wb) return x.wb < y.wb;
+        if (elig(sp.t)) {
+          int64_t pr = prio(sp.t, kp);
+          c.push_back({pr, near(pr, kp), writes_back(sp.t, kp) ? size_[sp.t] : 0, size_[sp.t], sp.t});
+        }
+      const bool belady = belady_;
+      std::sort(c.begin(), c.end(), [belady](const C& x, const C& y) {
+        if (belady) {  // (write-back asc, bucket desc, size desc, next use desc, id)
+          if (x.wb != y.wb) return x.wb < y.wb;
+          if (x.nb != y.nb) return x.nb > y.nb;
+          if (x.sz != y.sz) return x.sz > y.sz;
+          if (x.pr != y.pr) return x.pr > y.pr;
+          return x.u < y.u;
+        }
         if (x.pr != y.pr) return x.pr > y.pr;
         if (x.wb != y.wb) return x.wb < y.wb;
         if (x.sz != y.sz) return x.sz > y.sz;
@@ -261,12 +275,15 @@ class Replay {
       }
       if (!ok) continue;
       bool better;
-      if (!found)
+      if (!found) {
         better = true;
-      else if (belady_)  // (-writeback bytes, worst priority, -victim bytes)
-        better = wb < b_wb || (wb == b_wb && (pr > b_pr || (pr == b_pr && vb < b_vb)));
-      else               // (worst priority, -writeback bytes, -victim bytes)
+      } else if (belady_) {  // (-writeback bytes, bucket of worst next use, -victim bytes, worst next use)
+        const int64_t nb = near(pr, kp), bnb = near(b_pr, kp);
+        better = wb < b_wb ||
+                 (wb == b_wb && (nb > bnb || (nb == bnb && (vb < b_vb || (vb == b_vb && pr > b_pr)))));
+      } else {               // (worst priority, -writeback bytes, -victim bytes)
         better = pr > b_pr || (pr == b_pr && (wb < b_wb || (wb == b_wb && vb < b_vb)));
+      }
       if (better) {
         found = true;
         b_pr = pr;
@@ -380,7 +397,7 @@ class Replay {
   std::vector<uint8_t> val_, resident_;
   std::vector<uint64_t> off_;
   std::vector<int64_t> lru_, pin_, pf_need_, mark_, prot_, last_;
-  int64_t guard_ = 0;
+  int64_t guard_ = 0, bucket_ = 1;
   int64_t scan_id_ = 0;
   std::vector<Span> spans_;  // resident windows sorted by offset (insertion order for IDEAL)
   uint64_t used_ = 0;

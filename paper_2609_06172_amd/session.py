@@ -19,7 +19,7 @@ NP_DTYPE = {DT_F32: np.float32, DT_I32: np.int32, DT_U8: np.uint8, DT_BF16: np.u
 
 class Session:
     def __init__(self, w, device=-1, M=None, variant=4, lookahead=0, affinity_w=1, placement=0,
-                 validate=0, timing=0, roofs=None, fill=True, threads=16, guard=None):
+                 validate=0, timing=0, roofs=None, fill=True, threads=16, guard=None, bucket=None):
         self.w = w
         self.device = device
         self.ctx = Context(device)
@@ -43,7 +43,7 @@ class Session:
             ctx.set_budget(self.M)
         if roofs is not None:
             ctx.set_roofs(*roofs)
-        self.set_policy(variant, lookahead, affinity_w, placement, validate, timing, guard)
+        self.set_policy(variant, lookahead, affinity_w, placement, validate, timing, guard, bucket)
         if device >= 0:
             import torch
             with torch.cuda.device(device):
@@ -52,8 +52,8 @@ class Session:
             ctx.bind_streams(*[s.cuda_stream for s in ss])
 
     def set_policy(self, variant=4, lookahead=0, affinity_w=1, placement=0, validate=0, timing=0,
-                   guard=None):
-        self.ctx.set_policy(variant, lookahead, affinity_w, placement, validate, timing, guard)
+                   guard=None, bucket=None):
+        self.ctx.set_policy(variant, lookahead, affinity_w, placement, validate, timing, guard, bucket)
         self.ctx.plan()
 
     # -- host arena access ----------------------------------------------------

@@ -4,7 +4,7 @@ from workloads.format import ALIGN, FLAG_HOST_INIT, KIND_PARAM
 
 
 def plan_ctx(tensors, kernels, M, variant=4, lookahead=0, affinity_w=1, placement=0, roofs=None,
-             guard=None):
+             guard=None, bucket=None):
     """Register a trace (oracle-style dicts) in a plan-only context and plan it."""
     ctx = Context(-1)
     off = 0
@@ -21,7 +21,7 @@ def plan_ctx(tensors, kernels, M, variant=4, lookahead=0, affinity_w=1, placemen
     ctx.set_budget(M)
     if roofs is not None:
         ctx.set_roofs(*roofs)
-    ctx.set_policy(variant, lookahead, affinity_w, placement, guard=guard)
+    ctx.set_policy(variant, lookahead, affinity_w, placement, guard=guard, bucket=bucket)
     ctx.plan()
     return ctx
 

@@ -97,9 +97,9 @@ def test_golden_schedules_through_the_library(case):
         ks.append(dict(op=OP_TOUCH, shape=(0,), operands=[(0, MODE_RW)] + ops, flops=1, hbm_bytes=1))
     M = case["M"] + 256
     ctx = plan_ctx(tensors, ks, M, variant=case["variant"], affinity_w=case["affinity_w"],
-                   placement=case["placement"], guard=case.get("guard"))
+                   placement=case["placement"], guard=case.get("guard"), bucket=case.get("bucket"))
     r = op.plan(tensors, ks, M, variant=case["variant"], affinity_w=case["affinity_w"],
-                placement=case["placement"], guard=case.get("guard"))
+                placement=case["placement"], guard=case.get("guard"), bucket=case.get("bucket"))
     assert_same_plan(ctx, r)
 
 
@@ -126,7 +126,8 @@ def test_random_traces_bit_exact(seed):
         for placement in (PLACE_POOL, PLACE_IDEAL):
             M = max(1024, (fp * rnd.choice([1, 2, 3, 4]) // rnd.choice([2, 3, 4, 5])) // 256 * 256)
             kw = dict(variant=variant, placement=placement, affinity_w=rnd.choice([0, 1, 2, 3]),
-                      lookahead=rnd.choice([0, 0, 1, 2, 5]), guard=rnd.choice([None, 0, 1, 3, 8]))
+                      lookahead=rnd.choice([0, 0, 1, 2, 5]), guard=rnd.choice([None, 0, 1, 3, 8]),
+                      bucket=rnd.choice([None, 1, 2, 5, 40]))
             roofs = rnd.choice([None, (10**15, 10**13, 10**10), (10**9, 10**9, 10**9)])
             try:
                 r = op.plan(tensors, kernels, M, roofs=roofs or op.DEFAULT_ROOFS, **kw)

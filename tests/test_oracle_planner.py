@@ -24,7 +24,8 @@ VARIANTS = [VAR_DEMAND_LRU, VAR_DEMAND_BELADY, VAR_T, VAR_T_A, VAR_T_A_P]
 def test_golden_schedules(case):
     tensors, kernels = golden_inputs(case)
     r = op.plan(tensors, kernels, case["M"], variant=case["variant"],
-                affinity_w=case["affinity_w"], placement=case["placement"], guard=case.get("guard"))
+                affinity_w=case["affinity_w"], placement=case["placement"], guard=case.get("guard"),
+                bucket=case.get("bucket"))
     assert [list(e) for e in r.schedule] == case["schedule"]
     if "residency" in case:
         assert [list(e) for e in r.residency] == case["residency"]
@@ -186,7 +187,8 @@ def test_gate_limits(seed):
     M = max(256, fp // 2 // 256 * 256)
     fast_link = (op.DEFAULT_ROOFS[0], op.DEFAULT_ROOFS[1], 10 ** 18)
     try:
-        a = op.plan(tensors, kernels, M, roofs=fast_link, variant=VAR_T_A_P, affinity_w=0, guard=0)
+        a = op.plan(tensors, kernels, M, roofs=fast_link, variant=VAR_T_A_P, affinity_w=0, guard=0,
+                    bucket=1)
         b = op.plan(tensors, kernels, M, roofs=fast_link, variant=VAR_DEMAND_BELADY, affinity_w=0)
     except op.PlanError:
         return
