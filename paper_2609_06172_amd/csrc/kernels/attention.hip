@@ -4,7 +4,8 @@
 // row with an online softmax over 64-key tiles: each lane scores one key of
 // the tile, the wave takes the tile maximum, and every lane accumulates two
 // output dimensions of P*V.
-// attn_decode_d128 (bf16, head dim 128, short query blocks): see below.
+// attn_decode_d128 (bf16, head dim 128, short query blocks) and
+// attn_prefill_d128 (bf16, head dim 128, matrix cores): see below.
 #include <hip/hip_runtime.h>
 
 #include "attention.h"
@@ -176,12 +177,172 @@ __global__ void __launch_bounds__(256) attn_decode_d128(AttnArgs a) {
   }
 }
 
+// Prefill attention, head dim 128, bf16, on matrix cores (flash-style).
+// One workgroup per (b, h, block of 64 queries); wave w owns queries
+// 16w..16w+15 with its Q fragments in registers.  For each block of 64 keys:
+//   K is staged in LDS row-major and V transposed (dims x keys), so every
+//   MFMA operand is one 16-byte LDS read;
+//   S = Q K^T: 4 key tiles x 4 dim steps of v_mfma_f32_16x16x32_bf16;
+//   online softmax on the accumulators (a lane holds 4 query rows);
+//   P goes through a per-wave LDS tile to become the A operand of
+//   O += P V: 2 key steps x 8 dim tiles of the same MFMA.
+// Blocks past the diagonal are skipped; only diagonal blocks are masked.
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2v __attribute__((ext_vector_type(2)));
+
+constexpr int FQ = 64, FK = 64, FD = 128;
+constexpr int KP = FD + 8;   // K tile pitch (elements)
+constexpr int VP = FK + 8;   // transposed V tile pitch
+constexpr int PP = FK + 8;   // P tile pitch
+
+__global__ void __launch_bounds__(256) attn_prefill_d128(AttnArgs a, int64_t nqb) {
+  __shared__ __align__(16) bf16_t Ks[FK * KP];
+  __shared__ __align__(16) bf16_t Vt[FD * VP];
+  __shared__ __align__(16) bf16_t Ps[4][16 * PP];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int lr = lane & 15, lg = lane >> 4;
+  // heaviest query blocks first
+  const int64_t wg = blockIdx.x;
+  const int64_t qb = nqb - 1 - wg % nqb, bh = wg / nqb;
+  const int64_t h = bh % a.nH, b = bh / a.nH;
+  const int64_t q0 = qb * FQ;
+  const bf16_t* Q = reinterpret_cast<const bf16_t*>(a.q) + (b * a.S) * a.q_rs + h * FD;
+  const bf16_t* Kg = reinterpret_cast<const bf16_t*>(a.k) + b * a.kv_bstride + h * a.kv_hstride;
+  const bf16_t* Vg = reinterpret_cast<const bf16_t*>(a.v) + b * a.kv_bstride + h * a.kv_hstride;
+  bf16_t* O = reinterpret_cast<bf16_t*>(a.o) + (b * a.S) * a.o_rs + h * FD;
+
+  // this wave's query rows: q0 + 16*wv + r; Q fragment for dim step c: dims 32c + 8g .. +8
+  const int64_t qr = q0 + 16 * wv + lr;
+  bf16x8 qf[4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    if (qr < a.S)
+      qf[c] = *reinterpret_cast<const bf16x8*>(Q + qr * a.q_rs + 32 * c + 8 * lg);
+    else
+      qf[c] = bf16x8{};
+  }
+  const float scale = 0.08838834764831845f;  // 1/sqrt(128)
+  f32x4 o[8];
+#pragma unroll
+  for (int t = 0; t < 8; ++t) o[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m[4], l[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    m[i] = -INFINITY;
+    l[i] = 0.f;
+  }
+  // queries of this workgroup see keys 0 .. pos0 + min(q0 + 63, S - 1)
+  const int64_t qlast = (q0 + FQ - 1 < a.S ? q0 + FQ - 1 : a.S - 1);
+  const int64_t klast = a.pos0 + qlast;
+  // staging assignment: thread t moves keys 4*(t%16)..+3, dims 8*(t/16)..+7
+  const int sk = 4 * (tid & 15), sd = 8 * (tid >> 4);
+  for (int64_t k0 = 0; k0 <= klast; k0 += FK) {
+    __syncthreads();  // previous block's tiles are no longer read
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int64_t key = k0 + sk + j;
+      u32x4v kv = u32x4v{0u, 0u, 0u, 0u}, vv = u32x4v{0u, 0u, 0u, 0u};
+      if (key <= klast) {
+        kv = *reinterpret_cast<const u32x4v*>(Kg + key * a.kv_rs + sd);
+        vv = *reinterpret_cast<const u32x4v*>(Vg + key * a.kv_rs + sd);
+      }
+      *reinterpret_cast<u32x4v*>(Ks + (sk + j) * KP + sd) = kv;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        Vt[(sd + 2 * e) * VP + sk + j] = bf16_t(vv[e] & 0xffffu);
+        Vt[(sd + 2 * e + 1) * VP + sk + j] = bf16_t(vv[e] >> 16);
+      }
+    }
+    __syncthreads();
+    // S = Q K^T for this wave's 16 queries x 64 keys
+    f32x4 sacc[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      sacc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const bf16x8 kb = *reinterpret_cast<const bf16x8*>(Ks + (16 * t + lr) * KP + 32 * c + 8 * lg);
+        sacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[c], kb, sacc[t], 0, 0, 0);
+      }
+    }
+    // element i of a lane: query row 16*wv + 4*lg + i, key k0 + 16*t + lr
+    const bool diag = k0 + FK - 1 > a.pos0 + q0 + 16 * wv;
+    float rmax[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int64_t qpos = a.pos0 + q0 + 16 * wv + 4 * lg + i;
+      float mx = -INFINITY;
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        float v = sacc[t][i] * scale;
+        if (diag && k0 + 16 * t + lr > qpos) v = -INFINITY;
+        sacc[t][i] = v;
+        mx = fmaxf(mx, v);
+      }
+      mx = fmaxf(mx, __shfl_xor(mx, 1, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, 2, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, 4, 64));
+      mx = fmaxf(mx, __shfl_xor(mx, 8, 64));
+      rmax[i] = mx;
+    }
+    bf16_t* ps = Ps[wv];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float mn = fmaxf(m[i], rmax[i]);
+      // rows with no visible key yet keep m = -inf and contribute nothing
+      const float corr = mn == -INFINITY ? 1.f : __expf(m[i] - mn);
+      float sum = 0.f;
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        const float p = mn == -INFINITY ? 0.f : __expf(sacc[t][i] - mn);
+        sum += p;
+        ps[(4 * lg + i) * PP + 16 * t + lr] = f2bf(p);
+      }
+      sum += __shfl_xor(sum, 1, 64);
+      sum += __shfl_xor(sum, 2, 64);
+      sum += __shfl_xor(sum, 4, 64);
+      sum += __shfl_xor(sum, 8, 64);
+      l[i] = l[i] * corr + sum;
+      m[i] = mn;
+#pragma unroll
+      for (int t = 0; t < 8; ++t) o[t][i] *= corr;
+    }
+    // the P tile is private to this wave; its writes precede these reads
+    __builtin_amdgcn_wave_barrier();
+#pragma unroll
+    for (int c = 0; c < 2; ++c) {
+      const bf16x8 pa = *reinterpret_cast<const bf16x8*>(ps + lr * PP + 32 * c + 8 * lg);
+#pragma unroll
+      for (int t = 0; t < 8; ++t) {
+        const bf16x8 vb = *reinterpret_cast<const bf16x8*>(Vt + (16 * t + lr) * VP + 32 * c + 8 * lg);
+        o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, vb, o[t], 0, 0, 0);
+      }
+    }
+    __builtin_amdgcn_wave_barrier();
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int64_t q = q0 + 16 * wv + 4 * lg + i;
+    if (q >= a.S) continue;
+    const float inv = 1.f / l[i];
+#pragma unroll
+    for (int t = 0; t < 8; ++t) O[q * a.o_rs + 16 * t + lr] = f2bf(o[t][i] * inv);
+  }
+}
+
 }  // namespace
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
   const int64_t rows = a.B * a.nH * a.S;
   if (a.bf16 && a.d == 128 && a.S <= 16) {
     hipLaunchKernelGGL(attn_decode_d128, dim3(unsigned(rows)), dim3(256), 0, s, a);
+    return hipGetLastError();
+  }
+  if (a.bf16 && a.d == 128) {
+    const int64_t nqb = (a.S + FQ - 1) / FQ;
+    hipLaunchKernelGGL(attn_prefill_d128, dim3(unsigned(a.B * a.nH * nqb)), dim3(256), 0, s, a, nqb);
     return hipGetLastError();
   }
   dim3 grid(unsigned((rows + 3) / 4));

@@ -5,8 +5,8 @@
 // staged through LDS (rows padded by 16 bytes so the 32 row reads of one
 // ds_read_b128 spread over the banks) with two buffers: the next K step is
 // loaded into registers while the current one feeds the matrix cores.
-// Tiles are numbered so that consecutive workgroups on one XCD (dispatch is
-// round-robin over the 8 XCDs) share A rows and hit the same L2.
+// Tiles are ordered so that the workgroups resident on one XCD (dispatch is
+// round-robin over the 8 XCDs) share A row-blocks and W column-blocks in L2.
 #include <hip/hip_runtime.h>
 
 #include "common.h"
@@ -24,6 +24,7 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int BM = 128, BN = 128, BK = 64, LDK = BK + 8;  // LDS row pitch in elements
 constexpr int kXcd = 8;
+constexpr int kGroupM = 8;
 
 struct Frag {
   u32x4 v[4];  // 4 x 16 B per thread per 128 x 64 tile
@@ -60,11 +61,19 @@ __global__ void __launch_bounds__(256) gemm_mfma(const bf16_t* __restrict__ A, c
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int wm = wv >> 1, wn = wv & 1;
 
-  // XCD-aware tile order
+  // Tile order.  Dispatch sends workgroup i to XCD i % 8, so the remap gives
+  // each XCD a contiguous run of the tile sequence; the sequence walks groups
+  // of kGroupM row-blocks column by column, so the ~64 tiles resident on one
+  // XCD span about 8 row-blocks x 8 column-blocks and share both A and W in
+  // that XCD's L2.
   const int nwg = gridDim.x, per = nwg / kXcd;
   int id = blockIdx.x;
   if (per > 0 && id < per * kXcd) id = (id % kXcd) * per + id / kXcd;
-  const int64_t m0 = int64_t(id / tilesN) * BM, n0 = int64_t(id % tilesN) * BN;
+  const int tilesM = nwg / tilesN;
+  const int gsize = kGroupM * tilesN, grp = id / gsize, first = grp * kGroupM;
+  const int gm = (tilesM - first) < kGroupM ? (tilesM - first) : kGroupM;
+  const int in = id - grp * gsize;
+  const int64_t m0 = int64_t(first + in % gm) * BM, n0 = int64_t(in / gm) * BN;
 
   f32x16 acc[2][2], acc2[DUAL ? 2 : 1][DUAL ? 2 : 1];
 #pragma unroll

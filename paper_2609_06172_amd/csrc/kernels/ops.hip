@@ -102,6 +102,74 @@ __global__ void __launch_bounds__(256) norm_kernel(const float* x, const TO* g, 
   }
 }
 
+// Row in registers: H % 4 == 0 and H <= 4 * 256 * NV; float4 loads, one read.
+template <class TO, bool LN, int NV>
+__global__ void __launch_bounds__(256) norm_vec_kernel(const float* x, const TO* g, const TO* b, TO* h,
+                                                       int64_t H, int64_t stride, int64_t offset,
+                                                       float eps) {
+  __shared__ float red[16];
+  const int64_t r = blockIdx.x;
+  const float4* xr = reinterpret_cast<const float4*>(x + (r * stride + offset) * H);
+  const int n4 = int(H / 4);
+  float4 v[NV];
+  float s = 0.f;
+#pragma unroll
+  for (int u = 0; u < NV; ++u) {
+    const int j = threadIdx.x + 256 * u;
+    v[u] = j < n4 ? xr[j] : float4{0.f, 0.f, 0.f, 0.f};
+    s += LN ? (v[u].x + v[u].y + v[u].z + v[u].w)
+            : (v[u].x * v[u].x + v[u].y * v[u].y + v[u].z * v[u].z + v[u].w * v[u].w);
+  }
+  s = block_sum(s, red);
+  float mean = 0.f, var;
+  if (LN) {
+    mean = s / float(H);
+    float q = 0.f;
+#pragma unroll
+    for (int u = 0; u < NV; ++u) {
+      if (threadIdx.x + 256 * u < n4) {
+        const float a0 = v[u].x - mean, a1 = v[u].y - mean, a2 = v[u].z - mean, a3 = v[u].w - mean;
+        q += a0 * a0 + a1 * a1 + a2 * a2 + a3 * a3;
+      }
+    }
+    var = block_sum(q, red) / float(H);
+  } else {
+    var = s / float(H);
+  }
+  const float rs = rsqrtf(var + eps);
+#pragma unroll
+  for (int u = 0; u < NV; ++u) {
+    const int j = threadIdx.x + 256 * u;
+    if (j >= n4) continue;
+    const float e[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int64_t col = 4 * int64_t(j) + c;
+      float y = (e[c] - mean) * rs * ld(g, col);
+      if (LN) y += ld(b, col);
+      st(h, r * H + col, y);
+    }
+  }
+}
+
+template <class TO, bool LN>
+void launch_norm(const uint8_t* x, const uint8_t* g, const uint8_t* b, uint8_t* h, const int64_t* sh,
+                 float eps, hipStream_t s) {
+  const int64_t T = sh[0], H = sh[1];
+  const float* xf = reinterpret_cast<const float*>(x);
+  const TO *gp = reinterpret_cast<const TO*>(g), *bp = reinterpret_cast<const TO*>(b);
+  TO* hp = reinterpret_cast<TO*>(h);
+  if (H % 4 == 0 && H <= 4 * 256 * 2)
+    hipLaunchKernelGGL((norm_vec_kernel<TO, LN, 2>), dim3(unsigned(T)), dim3(256), 0, s, xf, gp, bp, hp, H,
+                       sh[2], sh[3], eps);
+  else if (H % 4 == 0 && H <= 4 * 256 * 8)
+    hipLaunchKernelGGL((norm_vec_kernel<TO, LN, 8>), dim3(unsigned(T)), dim3(256), 0, s, xf, gp, bp, hp, H,
+                       sh[2], sh[3], eps);
+  else
+    hipLaunchKernelGGL((norm_kernel<TO, LN>), dim3(unsigned(T)), dim3(256), 0, s, xf, gp, bp, hp, H, sh[2],
+                       sh[3], eps);
+}
+
 // ---------------------------------------------------------------- RoPE + KV append
 // One block per (token row, head): rotate pairs (i, i+d/2) of q and k by
 // pos * 10000^(-2i/d); write rotated k and v into the caches at pos.
@@ -113,9 +181,13 @@ __global__ void rope_kv_kernel(T* q, const T* k, const T* v, T* Kc, T* Vc, int64
   const int64_t half = d / 2;
   const int64_t base = row * nH * d + h * d;
   const int64_t cbase = ((b * nH + h) * Lmax + pos) * d;
+  // inverse frequency 10000^(-2i/d) = 2^(-(2i/d) log2 10000); fp32 angle error
+  // at position 1280 is ~1e-4 rad, far below the bf16 storage step
+  const float lg = 13.287712379549449f;  // log2(10000)
   for (int64_t i = threadIdx.x; i < half; i += blockDim.x) {
-    double ang = double(pos) * pow(10000.0, -2.0 * double(i) / double(d));
-    float c = float(cos(ang)), sn = float(sin(ang));
+    const float ang = float(pos) * exp2f(-2.f * float(i) / float(d) * lg);
+    float sn, c;
+    sincosf(ang, &sn, &c);
     float q1 = ld(q, base + i), q2 = ld(q, base + i + half);
     st(q, base + i, q1 * c - q2 * sn);
     st(q, base + i + half, q2 * c + q1 * sn);
@@ -206,23 +278,15 @@ hipError_t launch_op(const Kernel& k, const std::vector<Tensor>& T, uint8_t* con
       return hipGetLastError();
     case AUVM_OP_LAYERNORM:
       if (dt(3) == AUVM_BF16)
-        hipLaunchKernelGGL((norm_kernel<bf16_t, true>), dim3(unsigned(sh[0])), dim3(256), 0, s,
-                           (const float*)p[0], (const bf16_t*)p[1], (const bf16_t*)p[2], (bf16_t*)p[3],
-                           sh[1], sh[2], sh[3], 1e-5f);
+        launch_norm<bf16_t, true>(p[0], p[1], p[2], p[3], sh, 1e-5f, s);
       else
-        hipLaunchKernelGGL((norm_kernel<float, true>), dim3(unsigned(sh[0])), dim3(256), 0, s,
-                           (const float*)p[0], (const float*)p[1], (const float*)p[2], (float*)p[3],
-                           sh[1], sh[2], sh[3], 1e-5f);
+        launch_norm<float, true>(p[0], p[1], p[2], p[3], sh, 1e-5f, s);
       return hipGetLastError();
     case AUVM_OP_RMSNORM:
       if (dt(2) == AUVM_BF16)
-        hipLaunchKernelGGL((norm_kernel<bf16_t, false>), dim3(unsigned(sh[0])), dim3(256), 0, s,
-                           (const float*)p[0], (const bf16_t*)p[1], (const bf16_t*)nullptr,
-                           (bf16_t*)p[2], sh[1], sh[2], sh[3], 1e-6f);
+        launch_norm<bf16_t, false>(p[0], p[1], nullptr, p[2], sh, 1e-6f, s);
       else
-        hipLaunchKernelGGL((norm_kernel<float, false>), dim3(unsigned(sh[0])), dim3(256), 0, s,
-                           (const float*)p[0], (const float*)p[1], (const float*)nullptr, (float*)p[2],
-                           sh[1], sh[2], sh[3], 1e-6f);
+        launch_norm<float, false>(p[0], p[1], nullptr, p[2], sh, 1e-6f, s);
       return hipGetLastError();
     case AUVM_OP_LINEAR:
     case AUVM_OP_LINEAR_GELU:

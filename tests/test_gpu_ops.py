@@ -69,7 +69,9 @@ def test_linear_family(op_, M, N, K, dt):
 
 
 @pytest.mark.parametrize("dt", [DT_F32, DT_BF16])
-@pytest.mark.parametrize("T,H,stride,offset", [(7, 128, 1, 0), (3, 4096, 5, 4), (33, 2048, 1, 0)])
+@pytest.mark.parametrize("T,H,stride,offset", [(7, 128, 1, 0), (3, 4096, 5, 4), (33, 2048, 1, 0),
+                                              (5, 8192, 2, 1), (4, 130, 1, 0), (2, 8196, 1, 0),
+                                              (9, 12, 3, 2), (16, 2052, 1, 0)])
 def test_norms(T, H, stride, offset, dt):
     rows = (T - 1) * stride + offset + 1
     x = rnd(rows, H) * 3 + 0.5
@@ -97,7 +99,8 @@ def test_embed(dt):
 
 
 @pytest.mark.parametrize("dt", [DT_F32, DT_BF16])
-@pytest.mark.parametrize("B,S,nH,d", [(1, 32, 4, 32), (2, 75, 3, 64), (1, 130, 2, 128), (2, 12, 2, 128)])
+@pytest.mark.parametrize("B,S,nH,d", [(1, 32, 4, 32), (2, 75, 3, 64), (1, 130, 2, 128), (2, 12, 2, 128),
+                                     (2, 75, 3, 128), (1, 257, 2, 128)])
 def test_attention_fused_qkv(B, S, nH, d, dt):
     Hd = nH * d
     qkv = rnd(B * S, 3 * Hd)
@@ -117,7 +120,8 @@ def test_attention_fused_qkv(B, S, nH, d, dt):
 @pytest.mark.parametrize("B,S,nH,d,Lmax,pos0", [(2, 1, 2, 128, 300, 257), (3, 40, 2, 128, 64, 0),
                                                 (1, 5, 4, 64, 20, 9), (16, 1, 2, 128, 1280, 1100),
                                                 (2, 7, 2, 128, 64, 20), (1, 1, 1, 128, 8, 0),
-                                                (4, 16, 2, 128, 300, 131)])
+                                                (4, 16, 2, 128, 300, 131), (2, 33, 2, 128, 100, 50),
+                                                (1, 200, 1, 128, 256, 0), (2, 64, 2, 128, 192, 64)])
 def test_rope_kv_and_cached_attention(B, S, nH, d, Lmax, pos0):
     dt = DT_BF16
     Hd = nH * d
