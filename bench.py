@@ -130,6 +130,27 @@ def run_decode(s, w, W, K):
     return prefill_s, time.perf_counter() - t0, first, first + nk
 
 
+def link_timeline(tl, K):
+    """Host-to-device link over the timed run segment (the last one): busy and
+    idle time, and the part of each idle gap during which the host had not yet
+    issued the next copy (host and device clocks share the segment's start)."""
+    from paper_2609_06172_amd.capi import TL_H2D
+    seg = max(e[1] for e in tl)
+    cur = [e for e in tl if e[1] == seg]
+    h = sorted((e for e in cur if e[0] == TL_H2D), key=lambda e: e[5])
+    span = max(e[6] for e in cur)
+    busy = sum(e[6] - e[5] for e in h)
+    late, prev = 0.0, 0.0
+    for e in h:
+        late += max(0.0, min(e[5], e[4]) - prev)
+        prev = e[6]
+    nbytes = sum(e[3] for e in h)
+    return {"h2d_busy_ms_per_step": round(busy / K, 3), "h2d_idle_ms_per_step": round((span - busy) / K, 3),
+            "idle_before_host_issue_ms_per_step": round(late / K, 3),
+            "h2d_GBps_while_busy": round(nbytes / (busy * 1e-3) / 1e9, 2) if busy > 0 else None,
+            "copies_per_step": round(len(h) / K, 2)}
+
+
 def cpu_baseline(cfg, w, seconds, pos):
     """fp64 oracle decode of a few layers at the timed position, scaled to the model."""
     import numpy as np
@@ -225,6 +246,7 @@ def main():
     sched = s.ctx.get_schedule()
     classes = s.ctx.get_classes()
     dur, gap = s.ctx.get_kernel_times()
+    link_tl = link_timeline(s.ctx.get_timeline(), K)
     gen_tap = s.read("gen")[: W + K + 1].copy()
     st = step_stats(w, sched, classes, M, k0, k1)
 
@@ -280,7 +302,8 @@ def main():
                       "demand_fetches": st["demand_fetches"],
                       "achieved_h2d_GBps": round(st["h2d_bytes"] / decode_s / 1e9, 2),
                       "compute_busy_ms_per_step": round(busy_ms / K, 3),
-                      "compute_stall_ms_per_step": round(stall_ms / K, 3)},
+                      "compute_stall_ms_per_step": round(stall_ms / K, 3),
+                      "link_timeline": link_tl},
         "prefill": {"seconds": round(prefill_s, 3), "tokens": cfg.batch * cfg.prompt_len},
         "per_kernel_ms_per_step": {k: round(v[1] / K, 4) for k, v in sorted(per_op.items())},
     }

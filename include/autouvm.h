@@ -207,7 +207,12 @@ auvm_status auvm_set_policy(auvm_ctx* ctx, const auvm_policy* policy);
 auvm_status auvm_plan(auvm_ctx* ctx);
 
 /* Lend the compute, host-to-device and device-to-host streams (hipStream_t
- * values passed as pointers); NULL entries are created by the context. */
+ * values passed as pointers); NULL entries keep the context's own.  The
+ * context creates its streams each on a hardware queue of its own, so copies
+ * overlap kernels.  Lent streams must not share a hardware queue with each
+ * other (HIP maps ordinary streams onto a few shared queues): on a shared
+ * queue a kernel waits for every copy enqueued before it, which serializes
+ * transfers with compute. */
 auvm_status auvm_bind_streams(auvm_ctx* ctx, void* compute, void* h2d, void* d2h);
 
 /* Execute boundaries first_k .. first_k+n_k-1 of the plan (their transfers
@@ -236,6 +241,29 @@ auvm_status auvm_get_classes(const auvm_ctx* ctx, auvm_kernel_class* buf, uint64
  * milliseconds, for kernels 0 .. n-1 of the last run segments since reset. */
 auvm_status auvm_get_kernel_times(const auvm_ctx* ctx, float* dur_ms, float* gap_ms,
                                   uint64_t cap, uint64_t* n);
+
+/* One executed kernel or copy on the device timeline (timing policy).  Times
+ * are milliseconds from the start of the run segment that issued it: host_ms
+ * when the host thread issued it, start_ms/end_ms when its stream began and
+ * finished it (from an event recorded on the idle streams at the segment's
+ * start).  This extends the runtime monitor's kernel timestamps (Sec. IV,
+ * Online Executor, Runtime Monitor) to the copies, so that link busy time,
+ * compute busy time and the stalls of each on the other can be measured. */
+enum { AUVM_TL_KERNEL = 0, AUVM_TL_H2D = 1, AUVM_TL_D2H = 2 };
+typedef struct auvm_timeline_entry {
+  int32_t kind;     /* AUVM_TL_* */
+  int32_t segment;  /* run call ordinal since the last reset, from 0 */
+  int64_t index;    /* kernel index, or index of the copy's schedule entry */
+  uint64_t bytes;   /* bytes moved (copies), 0 for kernels */
+  double host_ms;
+  double start_ms;
+  double end_ms;
+} auvm_timeline_entry;
+
+/* Entries of the run segments since reset in issue order (kernels and copies
+ * interleaved).  Two-call pattern as get_schedule; empty unless the policy's
+ * timing flag was set while they ran. */
+auvm_status auvm_get_timeline(const auvm_ctx* ctx, auvm_timeline_entry* buf, uint64_t cap, uint64_t* n);
 
 #ifdef __cplusplus
 }

@@ -19,6 +19,7 @@ SYMBOLS = [
     "auvm_set_roofs", "auvm_set_policy", "auvm_plan", "auvm_bind_streams", "auvm_run",
     "auvm_reset", "auvm_read_tensor", "auvm_get_counters", "auvm_get_schedule",
     "auvm_get_executed", "auvm_get_residency", "auvm_get_classes", "auvm_get_kernel_times",
+    "auvm_get_timeline",
 ]
 
 
@@ -46,6 +47,14 @@ class Residency(C.Structure):
 class KernelClass(C.Structure):
     _fields_ = [("static_cls", C.c_uint8), ("dyn_cls", C.c_uint8), ("pad", C.c_uint8 * 6),
                 ("flops", C.c_uint64), ("hbm_bytes", C.c_uint64)]
+
+
+class TimelineEntry(C.Structure):
+    _fields_ = [("kind", C.c_int32), ("segment", C.c_int32), ("index", C.c_int64), ("bytes", C.c_uint64),
+                ("host_ms", C.c_double), ("start_ms", C.c_double), ("end_ms", C.c_double)]
+
+
+TL_KERNEL, TL_H2D, TL_D2H = 0, 1, 2
 
 
 class Counters(C.Structure):
@@ -129,6 +138,7 @@ def lib():
         "auvm_get_classes": (st, [P, C.POINTER(KernelClass), C.c_uint64, C.POINTER(C.c_uint64)]),
         "auvm_get_kernel_times": (st, [P, C.POINTER(C.c_float), C.POINTER(C.c_float), C.c_uint64,
                                        C.POINTER(C.c_uint64)]),
+        "auvm_get_timeline": (st, [P, C.POINTER(TimelineEntry), C.c_uint64, C.POINTER(C.c_uint64)]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -258,3 +268,8 @@ class Context:
         gap = (C.c_float * max(1, n.value))()
         self._check(self._L.auvm_get_kernel_times(self._h, dur, gap, n.value, C.byref(n)))
         return list(dur[:n.value]), list(gap[:n.value])
+
+    def get_timeline(self):
+        """(kind, segment, index, bytes, host_ms, start_ms, end_ms) per kernel or copy, in issue order."""
+        buf, n = self._array(self._L.auvm_get_timeline, TimelineEntry)
+        return [(e.kind, e.segment, e.index, e.bytes, e.host_ms, e.start_ms, e.end_ms) for e in buf[:n]]

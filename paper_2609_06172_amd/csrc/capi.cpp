@@ -302,4 +302,13 @@ auvm_status auvm_get_kernel_times(const auvm_ctx* x, float* dur, float* gap, uin
   return exec_kernel_times(x->c, dur, gap, cap, n);
 }
 
+auvm_status auvm_get_timeline(const auvm_ctx* x, auvm_timeline_entry* buf, uint64_t cap, uint64_t* n) {
+  if (!x || !n) return AUVM_E_INVAL;
+  if (!x->c.exec) {
+    *n = 0;
+    return AUVM_OK;
+  }
+  return copy_out(exec_timeline(x->c), buf, cap, n, x);
+}
+
 }  // extern "C"

@@ -13,9 +13,16 @@
 //    first-write allocations, for transfers still touching the window.
 // Streams are in-order, so each stream keeps the highest kernel/copy index it
 // already waits on and skips older waits.
+//
+// Timing policy: kernels, host-to-device and device-to-host copies each get a
+// track of start/end events; times are chained from one base event per run
+// segment through the short gaps between consecutive items of a track, so
+// they keep float precision over long runs.
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
+#include <chrono>
+#include <vector>
 #include <cstring>
 #include <map>
 
@@ -36,9 +43,19 @@ class Executor {
 
   auvm_status init() {
     if (!ok(hipSetDevice(c_.device), "hipSetDevice")) return AUVM_E_HIP;
+    // HIP spreads streams over a few hardware queues; two streams that share
+    // one are serialized (a kernel queued behind a copy's completion marker
+    // waits for the copy).  A stream created with a CU mask gets a hardware
+    // queue of its own; the mask enables every CU.
+    int ncu = 0;
+    if (!ok(hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, c_.device), "hipDeviceGetAttribute"))
+      return AUVM_E_HIP;
+    std::vector<uint32_t> mask(size_t((ncu + 31) / 32), 0xffffffffu);
+    if (ncu % 32) mask.back() = (1u << (ncu % 32)) - 1u;
     hipStream_t* ss[3] = {&comp_, &h2d_, &d2h_};
     for (int i = 0; i < 3; ++i) {
-      if (!ok(hipStreamCreateWithFlags(ss[i], hipStreamNonBlocking), "hipStreamCreate")) return AUVM_E_HIP;
+      if (!ok(hipExtStreamCreateWithCUMask(ss[i], uint32_t(mask.size()), mask.data()), "hipExtStreamCreateWithCUMask"))
+        return AUVM_E_HIP;
       own_[i] = true;
     }
     for (auto* ring : {&kev_, &hev_, &dev_}) {
@@ -58,9 +75,13 @@ class Executor {
     hipStream_t ss[3] = {comp_, h2d_, d2h_};
     for (int i = 0; i < 3; ++i)
       if (ss[i]) (void)hipStreamSynchronize(ss[i]);
-    for (auto* ring : {&kev_, &hev_, &dev_, &tstart_, &tend_})
+    for (auto* ring : {&kev_, &hev_, &dev_, &bases_})
       for (auto& e : *ring)
         if (e) (void)hipEventDestroy(e);
+    for (Track* tr : {&ktr_, &htr_, &dtr_})
+      for (auto* ring : {&tr->s, &tr->e})
+        for (auto& e : *ring)
+          if (e) (void)hipEventDestroy(e);
     for (int i = 0; i < 3; ++i)
       if (own_[i] && ss[i]) (void)hipStreamDestroy(ss[i]);
     comp_ = h2d_ = d2h_ = nullptr;
@@ -101,9 +122,9 @@ class Executor {
     kernels_run_ = 0;
     dur_.assign(K, 0.f);
     gap_.assign(K, 0.f);
-    seg_start_.assign(K, 0);
-    times_n_ = 0;
-    harvested_ = 0;
+    for (Track* tr : {&ktr_, &htr_, &dtr_}) tr->restart();
+    tl_.clear();
+    seg_ = -1;
     // kernels whose completion some transfer waits on
     need_ev_.assign(K, 0);
     std::vector<int64_t> last(nT, -1);
@@ -125,8 +146,7 @@ class Executor {
       return AUVM_E_STATE;
     }
     if (!ok(hipSetDevice(c_.device), "hipSetDevice")) return AUVM_E_HIP;
-    if (c_.pol.timing) ensure_time_events();
-    if (first_k < seg_start_.size()) seg_start_[first_k] = 1;
+    if (c_.pol.timing && !begin_segment()) return AUVM_E_HIP;
     const int64_t end_k = int64_t(first_k) + n_k;
     const auto& S = c_.plan.schedule;
     while (cursor_ < S.size() && S[cursor_].issue_k < end_k) {
@@ -157,13 +177,15 @@ class Executor {
   uint64_t kernels_run() const { return kernels_run_; }
 
   auvm_status times(float* dur, float* gap, uint64_t cap, uint64_t* n) const {
-    *n = times_n_;
+    const uint64_t m = uint64_t(ktr_.n);
+    *n = m;
     if (!dur && !gap) return AUVM_OK;
-    if (cap < times_n_) return AUVM_E_RANGE;
-    if (dur) std::memcpy(dur, dur_.data(), times_n_ * sizeof(float));
-    if (gap) std::memcpy(gap, gap_.data(), times_n_ * sizeof(float));
+    if (cap < m) return AUVM_E_RANGE;
+    if (dur) std::memcpy(dur, dur_.data(), m * sizeof(float));
+    if (gap) std::memcpy(gap, gap_.data(), m * sizeof(float));
     return AUVM_OK;
   }
+  const std::vector<auvm_timeline_entry>& timeline() const { return tl_; }
 
  private:
   struct Hazard {
@@ -248,9 +270,12 @@ class Executor {
         if (e.op == AUVM_D2H_WRITEBACK) {
           if (last_use_[t] >= 0 && !wait(d2h_, kev_, kown_, last_use_[t], d2h_waited_k_)) return AUVM_E_HIP;
           const Tensor& x = c_.tensors[t];
+          if (c_.pol.timing && !begin_item(dtr_, d2h_, AUVM_TL_D2H, int64_t(cursor_), x.bytes))
+            return AUVM_E_HIP;
           if (!ok(hipMemcpyAsync(c_.host + x.arena_off, c_.pool + e.dev_off, x.bytes,
                                  hipMemcpyDeviceToHost, d2h_), "hipMemcpyAsync D2H"))
             return AUVM_E_HIP;
+          if (c_.pol.timing && !end_item(dtr_, d2h_)) return AUVM_E_HIP;
           wb = ++d2h_seq_;
           if (!record(dev_, down_, wb, d2h_)) return AUVM_E_HIP;
           wb_seq_[t] = wb;
@@ -280,9 +305,12 @@ class Executor {
         int64_t dw = std::max(d2h, wb_seq_[t]);
         if (dw && !wait(h2d_, dev_, down_, dw, h2d_waited_d2h_)) return AUVM_E_HIP;
         const Tensor& x = c_.tensors[t];
+        if (c_.pol.timing && !begin_item(htr_, h2d_, AUVM_TL_H2D, int64_t(cursor_), x.bytes))
+          return AUVM_E_HIP;
         if (!ok(hipMemcpyAsync(c_.pool + e.dev_off, c_.host + x.arena_off, x.bytes,
                                hipMemcpyHostToDevice, h2d_), "hipMemcpyAsync H2D"))
           return AUVM_E_HIP;
+        if (c_.pol.timing && !end_item(htr_, h2d_)) return AUVM_E_HIP;
         int64_t seq = ++h2d_seq_;
         if (!record(hev_, hown_, seq, h2d_)) return AUVM_E_HIP;
         copy_seq_[t] = seq;
@@ -318,16 +346,13 @@ class Executor {
     pend_h2d_ = pend_d2h_ = 0;
     uint8_t* ptrs[16];
     for (size_t i = 0; i < kd.ids.size(); ++i) ptrs[i] = c_.pool + where_[kd.ids[i]];
-    bool timing = c_.pol.timing != 0;
+    const bool timing = c_.pol.timing != 0;
     if (timing) {
-      if (!make_room(k)) return AUVM_E_HIP;
-      if (!ok(hipEventRecord(tstart_[k % kTimeRing], comp_), "hipEventRecord")) return AUVM_E_HIP;
+      if (ktr_.n != k) return internal("timed kernels must run from kernel 0 in order");
+      if (!begin_item(ktr_, comp_, AUVM_TL_KERNEL, k, 0)) return AUVM_E_HIP;
     }
     if (!ok(launch_op(kd, c_.tensors, ptrs, comp_), "kernel launch")) return AUVM_E_HIP;
-    if (timing) {
-      if (!ok(hipEventRecord(tend_[k % kTimeRing], comp_), "hipEventRecord")) return AUVM_E_HIP;
-      times_n_ = size_t(k) + 1;
-    }
+    if (timing && !end_item(ktr_, comp_)) return AUVM_E_HIP;
     if (need_ev_[k] && !record(kev_, kown_, k, comp_)) return AUVM_E_HIP;
     for (auto& a : kd.acc) last_use_[a.first] = k;
     next_k_ = k + 1;
@@ -340,53 +365,104 @@ class Executor {
     return AUVM_E_STATE;
   }
 
-  // -- per-kernel timing ----------------------------------------------------------
-  void ensure_time_events() {
-    if (!tstart_.empty()) return;
-    tstart_.assign(kTimeRing, nullptr);
-    tend_.assign(kTimeRing, nullptr);
-    for (auto& e : tstart_) (void)hipEventCreate(&e);
-    for (auto& e : tend_) (void)hipEventCreate(&e);
-  }
-  // Before recording kernel k, read out the kernel whose events occupy k's slot.
-  bool make_room(int64_t k) {
-    while (harvested_ + kTimeRing <= k) {
-      if (!harvest(harvested_)) return false;
-      ++harvested_;
+  // -- timing tracks ---------------------------------------------------------------
+  struct Track {
+    std::vector<hipEvent_t> s, e;  // start/end events, ring of kTimeRing
+    std::vector<int64_t> tl;       // timeline entry of each item
+    int64_t n = 0, harvested = 0;
+    double next = 0;               // chained start time of item `harvested`
+    void restart() {
+      tl.clear();
+      n = harvested = 0;
+      next = 0;
     }
+  };
+
+  bool begin_segment() {
+    for (Track* tr : {&ktr_, &htr_, &dtr_}) {
+      if (!tr->s.empty()) continue;
+      tr->s.assign(kTimeRing, nullptr);
+      tr->e.assign(kTimeRing, nullptr);
+      for (auto* ring : {&tr->s, &tr->e})
+        for (auto& e : *ring)
+          if (!ok(hipEventCreate(&e), "hipEventCreate")) return false;
+    }
+    ++seg_;
+    if (size_t(seg_) >= bases_.size()) {
+      hipEvent_t b = nullptr;
+      if (!ok(hipEventCreate(&b), "hipEventCreate")) return false;
+      bases_.push_back(b);
+    }
+    // the streams are idle here (every segment ends with a full wait)
+    if (!ok(hipEventRecord(bases_[seg_], comp_), "hipEventRecord")) return false;
+    host0_ = std::chrono::steady_clock::now();
     return true;
   }
-  bool harvest(int64_t j) {
+
+  bool begin_item(Track& tr, hipStream_t st, int32_t kind, int64_t index, uint64_t bytes) {
+    while (tr.harvested + kTimeRing <= tr.n)   // free the slot this item reuses
+      if (!harvest(tr, tr.harvested++)) return false;
+    auvm_timeline_entry x{};
+    x.kind = kind;
+    x.segment = seg_;
+    x.index = index;
+    x.bytes = bytes;
+    x.host_ms = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - host0_).count();
+    tr.tl.push_back(int64_t(tl_.size()));
+    tl_.push_back(x);
+    return ok(hipEventRecord(tr.s[tr.n % kTimeRing], st), "hipEventRecord");
+  }
+  bool end_item(Track& tr, hipStream_t st) {
+    if (!ok(hipEventRecord(tr.e[tr.n % kTimeRing], st), "hipEventRecord")) return false;
+    ++tr.n;
+    return true;
+  }
+
+  // Item j's duration; its start is the segment base's elapsed time for the
+  // first item of a segment, else the chained value; the gap to item j+1 of
+  // the same segment sets the next chained start.
+  bool harvest(Track& tr, int64_t j) {
+    hipEvent_t s = tr.s[j % kTimeRing], e = tr.e[j % kTimeRing];
     float ms = 0;
-    hipEvent_t s = tstart_[j % kTimeRing], e = tend_[j % kTimeRing];
     if (!ok(hipEventSynchronize(e), "hipEventSynchronize")) return false;
     if (!ok(hipEventElapsedTime(&ms, s, e), "hipEventElapsedTime")) return false;
-    dur_[j] = ms;
-    // the gap before the first kernel of a run segment includes host time: not reported
-    if (j + 1 < int64_t(times_n_) && !seg_start_[j + 1]) {
-      hipEvent_t s2 = tstart_[(j + 1) % kTimeRing];
+    auvm_timeline_entry& x = tl_[tr.tl[j]];
+    const bool first = j == 0 || tl_[tr.tl[j - 1]].segment != x.segment;
+    if (first) {
+      float b = 0;
+      if (!ok(hipEventElapsedTime(&b, bases_[x.segment], s), "hipEventElapsedTime")) return false;
+      tr.next = b;
+    }
+    x.start_ms = tr.next;
+    x.end_ms = tr.next + ms;
+    float g = 0;
+    const bool chained = j + 1 < tr.n && tl_[tr.tl[j + 1]].segment == x.segment;
+    if (chained) {
+      hipEvent_t s2 = tr.s[(j + 1) % kTimeRing];
       if (!ok(hipEventSynchronize(s2), "hipEventSynchronize")) return false;
-      float g = 0;
       if (!ok(hipEventElapsedTime(&g, e, s2), "hipEventElapsedTime")) return false;
-      gap_[j + 1] = g;
+      tr.next = x.end_ms + g;
+    }
+    if (&tr == &ktr_) {
+      dur_[j] = ms;
+      // the gap before the first kernel of a run segment includes host time: not reported
+      if (chained) gap_[j + 1] = g;
     }
     return true;
   }
   void harvest_all() {
-    while (harvested_ < int64_t(times_n_)) {
-      if (!harvest(harvested_)) return;
-      ++harvested_;
-    }
+    for (Track* tr : {&ktr_, &htr_, &dtr_})
+      while (tr->harvested < tr->n)
+        if (!harvest(*tr, tr->harvested++)) return;
   }
 
   Ctx& c_;
   hipStream_t comp_ = nullptr, h2d_ = nullptr, d2h_ = nullptr;
   bool own_[3] = {false, false, false};
-  std::vector<hipEvent_t> kev_, hev_, dev_, tstart_, tend_;
+  std::vector<hipEvent_t> kev_, hev_, dev_, bases_;
   std::vector<int64_t> kown_, hown_, down_;
   size_t cursor_ = 0;
   int64_t next_k_ = 0;
-  std::vector<uint8_t> seg_start_;
   std::vector<int64_t> where_, last_use_, copy_seq_, wb_seq_;
   int64_t h2d_seq_ = 0, d2h_seq_ = 0;
   int64_t h2d_waited_k_ = -1, d2h_waited_k_ = -1, h2d_waited_d2h_ = 0;
@@ -397,8 +473,10 @@ class Executor {
   std::vector<auvm_sched_entry> log_;
   uint64_t kernels_run_ = 0;
   std::vector<float> dur_, gap_;
-  size_t times_n_ = 0;
-  int64_t harvested_ = 0;
+  Track ktr_, htr_, dtr_;
+  std::vector<auvm_timeline_entry> tl_;
+  int32_t seg_ = -1;
+  std::chrono::steady_clock::time_point host0_;
 };
 
 Ctx::~Ctx() {
@@ -423,6 +501,7 @@ uint64_t exec_kernels_run(const Ctx& c) { return c.exec->kernels_run(); }
 auvm_status exec_kernel_times(const Ctx& c, float* d, float* g, uint64_t cap, uint64_t* n) {
   return c.exec->times(d, g, cap, n);
 }
+const std::vector<auvm_timeline_entry>& exec_timeline(const Ctx& c) { return c.exec->timeline(); }
 
 auvm_status host_alloc_pinned(Ctx& c, uint64_t bytes) {
   void* p = nullptr;

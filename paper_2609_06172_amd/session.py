@@ -2,8 +2,9 @@
 
 Marshalling only: registers the workload's tensors and kernels through the C
 interface, writes the seeded initial host contents into the context's arena,
-lends the device pool and streams (allocated with PyTorch) and plans.  All
-scheduling and every kernel run inside the library.
+lends the device pool (allocated with PyTorch) and plans.  The library runs
+on streams of its own (one hardware queue each); all scheduling and every
+kernel run inside it.
 """
 import ctypes as C
 
@@ -44,12 +45,6 @@ class Session:
         if roofs is not None:
             ctx.set_roofs(*roofs)
         self.set_policy(variant, lookahead, affinity_w, placement, validate, timing, guard, bucket)
-        if device >= 0:
-            import torch
-            with torch.cuda.device(device):
-                ss = [torch.cuda.Stream(device=device) for _ in range(3)]
-            self._torch_refs += ss
-            ctx.bind_streams(*[s.cuda_stream for s in ss])
 
     def set_policy(self, variant=4, lookahead=0, affinity_w=1, placement=0, validate=0, timing=0,
                    guard=None, bucket=None):

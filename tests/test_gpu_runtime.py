@@ -86,3 +86,86 @@ def test_reset_and_rerun_gives_the_same_reads():
     s.run_all()
     assert np.array_equal(first, s.read("t0"))
     s.close()
+
+
+@pytest.mark.parametrize("seed,variant", [(5, 0), (5, 4), (9, 1), (9, 4)])
+def test_timeline_is_complete_ordered_and_causal(seed, variant):
+    """Timing policy: one timeline entry per kernel and per executed copy, each
+    stream's items in order without overlap, every kernel starting after the
+    copies that brought its operands, and demand fetches after the kernel
+    before their need."""
+    from paper_2609_06172_amd.capi import TL_D2H, TL_H2D, TL_KERNEL
+    from workloads.format import S_ALLOC, S_D2H_WRITEBACK, S_H2D_DEMAND, S_H2D_PREFETCH, S_LAUNCH
+    tensors, kernels = random_trace(seed, touch=True, n_kernels=90)
+    M = feasible_budget(tensors, kernels, variant)
+    print(f"timeline seed={seed} variant={variant} M={M}", flush=True)
+    s, w = _session_from_trace(tensors, kernels, M, variant=variant, timing=1)
+    _init_words(s, w, tensors)
+    K = len(kernels)
+    cuts = [0, K // 2, K]
+    for a, b in zip(cuts, cuts[1:]):
+        s.run(a, b - a)
+    tl = s.ctx.get_timeline()
+    sched = s.ctx.get_schedule()
+    s.close()
+    tol = 0.02   # ms
+    kern = [e for e in tl if e[0] == TL_KERNEL]
+    assert [e[2] for e in kern] == list(range(K))
+    assert [e[1] for e in kern] == [0 if k < K // 2 else 1 for k in range(K)]
+    for kind, ops in ((TL_H2D, (S_H2D_PREFETCH, S_H2D_DEMAND)), (TL_D2H, (S_D2H_WRITEBACK,))):
+        got = [(e[2], e[3]) for e in tl if e[0] == kind]
+        want = [(i, tensors[x[1]]["nbytes"]) for i, x in enumerate(sched) if x[0] in ops]
+        assert got == want
+    for kind in (TL_KERNEL, TL_H2D, TL_D2H):
+        items = [e for e in tl if e[0] == kind]
+        for a, b in zip(items, items[1:]):
+            assert b[5] <= b[6] + 1e-6 and a[5] >= -tol
+            if a[1] == b[1]:
+                assert b[5] >= a[6] - tol and b[4] >= a[4]
+    # causality through the schedule
+    start = {e[2]: e[5] for e in kern}
+    end = {e[2]: e[6] for e in kern}
+    seg = {e[2]: e[1] for e in kern}
+    copy = {e[2]: e for e in tl if e[0] == TL_H2D}
+    latest = {}
+    for i, x in enumerate(sched):
+        if x[0] in (S_H2D_PREFETCH, S_H2D_DEMAND):
+            latest[x[1]] = i
+            if x[0] == S_H2D_DEMAND and x[4] > 0 and seg[x[4] - 1] == copy[i][1]:
+                assert copy[i][5] >= end[x[4] - 1] - tol
+        elif x[0] == S_LAUNCH:
+            k = x[4]
+            for t, _ in kernels[k]["operands"]:
+                j = latest.get(t)
+                if j is not None and copy[j][1] == seg[k]:
+                    assert copy[j][6] <= start[k] + tol, (k, t)
+        elif x[0] == S_ALLOC:
+            latest.pop(x[1], None)
+
+
+def test_kernels_overlap_an_unrelated_prefetch():
+    """Kernels that do not read a tensor being prefetched run while its copy is
+    on the link: the compute and copy streams must not be serialized (as they
+    are when two streams share a hardware queue)."""
+    from paper_2609_06172_amd.capi import TL_H2D, TL_KERNEL
+    from workloads.format import DT_U8, MODE_RW, OP_TOUCH
+    tensors = [dict(nbytes=4096, dtype=DT_U8, kind=KIND_ACT, host_init=True),    # log: 64 slots
+               dict(nbytes=128 << 20, dtype=DT_U8, kind=KIND_PARAM, host_init=False),
+               dict(nbytes=4096, dtype=DT_U8, kind=KIND_ACT, host_init=True)]
+    kernels = [dict(op=OP_TOUCH, shape=(k,), operands=[(0, MODE_RW), (2, MODE_RW)], flops=1, hbm_bytes=1)
+               for k in range(31)]
+    kernels.append(dict(op=OP_TOUCH, shape=(31,), operands=[(0, MODE_RW), (1, MODE_R)], flops=1, hbm_bytes=1))
+    M = sum(op.aligned(t["nbytes"]) for t in tensors)
+    s, w = _session_from_trace(tensors, kernels, M, variant=4, timing=1)
+    _init_words(s, w, tensors)
+    s.run_all()
+    tl = s.ctx.get_timeline()
+    sched = s.ctx.get_schedule()
+    s.close()
+    big = [e for e in tl if e[0] == TL_H2D and sched[e[2]][1] == 1]
+    assert len(big) == 1
+    kern = {e[2]: e for e in tl if e[0] == TL_KERNEL}
+    assert big[0][5] < kern[1][5], "the prefetch is issued before the small kernels"
+    # every kernel that does not read the big tensor ends before its copy does
+    assert max(kern[k][6] for k in range(1, 31)) < big[0][6] - 0.5
+    assert kern[31][5] >= big[0][6] - 0.02
