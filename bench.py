@@ -1,22 +1,34 @@
 #!/usr/bin/env python3
-"""Decode throughput of a 7B-shape decoder whose tensors oversubscribe the
-device budget 1.5x, with tensor-granular roofline-gated prefetching.
+"""Throughput of decoders whose tensors oversubscribe the device budget, with
+tensor-granular roofline-gated prefetching.
 
-One step = one greedy decode step of the whole model at batch 16 (every layer's
-transfers and kernels, scheduled by the planner).  The job is a 1024-token
-prompt (prefill, untimed, reported) followed by up to 256 decode steps; W steps
-are run untimed, then K steps are timed between two device synchronisations.
+Default (llama-7b config): one step = one greedy decode step of the whole
+model at batch 16 (every layer's transfers and kernels, scheduled by the
+planner).  The job is a 1024-token prompt (prefill, untimed, reported)
+followed by up to 256 decode steps; W steps run untimed, then K steps are
+timed between two device synchronisations.  --factor sets the
+oversubscription (default 3/2); --sweep runs several factors in one job.
+
+GPT-style configs (gpt-1.3b): one step = one prefill forward pass over the
+same ids; one cold pass is reported separately, then --iterations passes are
+timed back to back.
 
 Reported next to the value (one JSON line on stdout):
   * path_roofline: max(F/P, B/Bh, L/Bl) for the timed steps, with L the
     tensor-granular lower bound on host-to-device bytes (bytes the steps read
     before writing minus the budget), at nominal MI355X roofs and at the host
     link measured in the same run;
-  * roofline: the decode projection GEMV kernels (the dominant compute
-    kernels), algorithmic bytes over their average duration from HIP events;
-  * no_prefetch_baseline: the same engine with fault-driven demand fetches and
-    LRU eviction;
-  * cpu_baseline: the CPU oracle on a bounded sample of the same decode.
+  * roofline: the dominant compute kernels (decode: the projection GEMVs;
+    prefill: the projection GEMMs), algorithmic bytes or flops over their
+    average duration from HIP events on the compute stream;
+  * transfers: host-to-device bytes against L, link busy and idle time from
+    the executor's timeline, compute-stream stall time;
+  * per_layer: wall and kernel time per layer and step;
+  * no_prefetch_baseline and ablation: the same engine with fault-driven
+    demand fetches (LRU, then Belady eviction) and with the paper's T and
+    T+A policies;
+  * cpu_baseline: the CPU oracle on a bounded sample of the same work, and
+    the oracle's planner replay timed against the library's planner.
 """
 import argparse
 import json
@@ -27,8 +39,8 @@ import time
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-METRIC = "tokens/sec at 1.5x oversubscription; fraction of max(compute,HBM,link) roofline"
 NOMINAL = dict(P=2.5e15, Bh=8.0e12, Bl=64.0e9)
+POLICY_NAMES = {0: "DEMAND_LRU", 1: "DEMAND_BELADY", 2: "T", 3: "T+A", 4: "T+A+P"}
 
 
 def log(*a):
@@ -38,18 +50,32 @@ def log(*a):
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=256, help="timed decode steps")
+    ap.add_argument("--steps", type=int, default=None,
+                    help="timed decode steps (default 256; 32 per factor with --sweep)")
     ap.add_argument("--warmup", type=int, default=0, help="untimed decode steps before")
     ap.add_argument("--config", default="llama-7b")
-    ap.add_argument("--factor", default="3/2", help="oversubscription factor num/den")
+    ap.add_argument("--factor", default=None, help="oversubscription factor num/den (default: the "
+                                                    "config's own, 3/2 for llama-7b)")
+    ap.add_argument("--sweep", default=None, help="comma-separated factors, e.g. 5/4,3/2,7/4,2/1")
+    ap.add_argument("--iterations", type=int, default=4, help="timed passes (gpt-style configs)")
     ap.add_argument("--baseline-steps", type=int, default=8)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-baseline", action="store_true")
+    ap.add_argument("--no-ablation", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="first run one 256 MiB device-to-device copy kernel (a known-size "
                          "reference for hardware byte counters)")
     return ap.parse_args()
+
+
+def factor_of(s):
+    num, den = (int(x) for x in s.split("/"))
+    return num, den
+
+
+def metric(kind, num, den):
+    return f"{kind}tokens/sec at {num / den:g}x oversubscription; fraction of max(compute,HBM,link) roofline"
 
 
 def link_bandwidth():
@@ -79,20 +105,20 @@ def counted_traffic():
         meta = json.load(open(prof))
         if hashlib.sha256(open(src, "rb").read()).hexdigest() != meta["kernel_source_sha256"]:
             return None
-        return int(meta["traffic_bytes_per_launch"])
-    except (OSError, ValueError, KeyError):
+        return meta["hbm_bytes_per_launch"]
+    except (OSError, KeyError, ValueError):
         return None
 
 
-def step_stats(w, sched, classes, M, k0, k1):
-    """Work and transfers of kernels k0..k1-1 (whole decode steps)."""
+def seg_stats(w, sched, classes, M, segs):
+    """Work and transfers of whole units (decode steps or forward passes) segs."""
     from workloads.format import MODE_R
+    k0 = segs[0][0]
+    k1 = segs[-1][0] + segs[-1][1]
     F = sum(c[2] for c in classes[k0:k1])
     B = sum(c[3] for c in classes[k0:k1])
     lmin = 0
-    for a, n in w.segments["decode"]:
-        if a < k0 or a + n > k1:
-            continue
+    for a, n in segs:
         first = {}
         for kd in w.kernels[a:a + n]:
             merged = {}
@@ -107,27 +133,6 @@ def step_stats(w, sched, classes, M, k0, k1):
     demand = sum(1 for e in sched if e[0] == 1 and k0 <= e[4] < k1)
     return dict(flops=F, hbm_bytes=B, lmin_bytes=lmin, h2d_bytes=h2d, d2h_bytes=d2h,
                 demand_fetches=demand)
-
-
-def run_decode(s, w, W, K):
-    import torch
-    steps = w.segments["decode"]
-    k0, n = w.segments["prefill"][0]
-    torch.cuda.synchronize()
-    t = time.perf_counter()
-    s.run(k0, n)
-    torch.cuda.synchronize()
-    prefill_s = time.perf_counter() - t
-    for i in range(W):
-        s.run(*steps[i])
-    first = steps[W][0]
-    last = steps[W + K - 1]
-    nk = last[0] + last[1] - first
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    s.run(first, nk)
-    torch.cuda.synchronize()
-    return prefill_s, time.perf_counter() - t0, first, first + nk
 
 
 def link_timeline(tl, K):
@@ -151,11 +156,103 @@ def link_timeline(tl, K):
             "copies_per_step": round(len(h) / K, 2)}
 
 
-def cpu_baseline(cfg, w, seconds, pos):
-    """fp64 oracle decode of a few layers at the timed position, scaled to the model."""
-    import numpy as np
-    from oracle import forward as of
-    from workloads import init as winit
+def per_layer(w, tl, segs, n_layers):
+    """Mean wall time per layer (first kernel of the layer to the first kernel
+    after it) and mean kernel time per layer, over the units segs."""
+    from paper_2609_06172_amd.capi import TL_KERNEL
+    seg = max(e[1] for e in tl)
+    start = {e[2]: e[5] for e in tl if e[0] == TL_KERNEL and e[1] == seg}
+    end = {e[2]: e[6] for e in tl if e[0] == TL_KERNEL and e[1] == seg}
+    wall = [0.0] * n_layers
+    kern = [0.0] * n_layers
+    for a, n in segs:
+        first = {}
+        for k in range(a, a + n):
+            kd = w.kernels[k]
+            if kd.tag == "embed":
+                continue
+            first.setdefault(kd.layer, k)
+            if kd.layer < n_layers:
+                kern[kd.layer] += end[k] - start[k]
+        for l in range(n_layers):
+            nxt = first.get(l + 1)
+            if l in first and nxt is not None:
+                wall[l] += start[nxt] - start[first[l]]
+    u = len(segs)
+    return {"wall_ms": [round(x / u, 3) for x in wall], "kernel_ms": [round(x / u, 3) for x in kern]}
+
+
+def step_series(tl, segs, block=32):
+    """Mean wall time per unit over consecutive blocks of units (start of a
+    unit's first kernel to the start of the next unit's first kernel)."""
+    from paper_2609_06172_amd.capi import TL_KERNEL
+    seg = max(e[1] for e in tl)
+    start = {e[2]: e[5] for e in tl if e[0] == TL_KERNEL and e[1] == seg}
+    end = max(e[6] for e in tl if e[1] == seg)
+    t = [start[a] for a, _ in segs] + [end]
+    d = [t[i + 1] - t[i] for i in range(len(segs))]
+    return [round(sum(d[i:i + block]) / len(d[i:i + block]), 2) for i in range(0, len(d), block)]
+
+
+def run_decode(s, w, W, K):
+    import torch
+    steps = w.segments["decode"]
+    k0, n = w.segments["prefill"][0]
+    torch.cuda.synchronize()
+    t = time.perf_counter()
+    s.run(k0, n)
+    torch.cuda.synchronize()
+    prefill_s = time.perf_counter() - t
+    for i in range(W):
+        s.run(*steps[i])
+    first = steps[W][0]
+    last = steps[W + K - 1]
+    nk = last[0] + last[1] - first
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    s.run(first, nk)
+    torch.cuda.synchronize()
+    return prefill_s, time.perf_counter() - t0, first, first + nk
+
+
+def decode_policy(s, w, M, variant, W, K, ref_gen):
+    """Rerun the decode under another policy (timing off) and summarise it."""
+    s.set_policy(variant=variant, timing=0)
+    s.ctx.reset()
+    s.restore_inputs()
+    pb, db, _, _ = run_decode(s, w, W, K)
+    gen = s.read("gen")[: W + K + 1]
+    st = seg_stats(w, s.ctx.get_schedule(), s.ctx.get_classes(), M, w.segments["decode"][W:W + K])
+    b = w.cfg.batch
+    return {"policy": POLICY_NAMES[variant], "steps": K, "value": round(b * K / db, 3), "unit": "tokens/s",
+            "ms_per_step": round(db / K * 1e3, 3), "prefill_seconds": round(pb, 3),
+            "h2d_bytes_per_step": st["h2d_bytes"] // K, "d2h_bytes_per_step": st["d2h_bytes"] // K,
+            "demand_fetches_per_step": round(st["demand_fetches"] / K, 2),
+            "tokens_identical": bool((gen == ref_gen[: W + K + 1]).all())}
+
+
+def planner_replay(cfg, M, steps):
+    """The oracle's planner and the library's on the prefill + `steps` decode
+    steps of the same trace (same budget): wall times and schedule identity."""
+    import dataclasses
+    from oracle import planner as op
+    from paper_2609_06172_amd.session import Session
+    from workloads import trace
+    w = trace.build(dataclasses.replace(cfg, decode_steps=steps))
+    s = Session(w, device=-1, M=M)
+    cxx_s = s.ctx.get_counters()["plan_ns"] / 1e9
+    sched = s.ctx.get_schedule()
+    s.close()
+    t = time.perf_counter()
+    r = op.plan_workload(w, M)
+    oracle_s = time.perf_counter() - t
+    same = [tuple(e) for e in sched] == [tuple(e) for e in r.schedule]
+    return {"trace": f"prefill + {steps} decode steps ({len(w.kernels)} kernels)",
+            "library_plan_s": round(cxx_s, 4), "oracle_plan_s": round(oracle_s, 3),
+            "schedules_identical": bool(same)}
+
+
+def blas_info():
     try:
         from threadpoolctl import threadpool_info
         info = threadpool_info()
@@ -163,6 +260,15 @@ def cpu_baseline(cfg, w, seconds, pos):
         vendor = ",".join(sorted(set(i.get("internal_api", "?") for i in info)))
     except Exception:
         threads, vendor = len(os.sched_getaffinity(0)), "unknown"
+    return threads, vendor
+
+
+def cpu_baseline_decode(cfg, w, seconds, pos, M):
+    """fp64 oracle decode of a few layers at the timed position, scaled to the model."""
+    import numpy as np
+    from oracle import forward as of
+    from workloads import init as winit
+    threads, vendor = blas_info()
     from concurrent.futures import ThreadPoolExecutor
     L = 2
     B, nH, d, Lmax = cfg.batch, cfg.n_heads, cfg.head_dim, cfg.kv_len
@@ -200,28 +306,65 @@ def cpu_baseline(cfg, w, seconds, pos):
             "blas": vendor,
             "sample": f"fp64 numpy oracle decode step at position {pos}, batch {B}: {L} of "
                       f"{cfg.n_layers} layers timed over {reps} repetitions plus the LM head, "
-                      f"scaled to {cfg.n_layers} layers ({step_s:.2f} s per step)"}
+                      f"scaled to {cfg.n_layers} layers ({step_s:.2f} s per step)",
+            "planner": planner_replay(cfg, M, 16)}
 
 
-def main():
-    args = parse()
-    world = int(os.environ.get("WORLD_SIZE", "1"))
-    if args.gpus != 1 or world != 1:
-        print("bench.py runs on one GPU: this build has no multi-GPU path "
-              "(the per-GPU hot path is what it measures)", file=sys.stderr)
-        sys.exit(2)
-    import dataclasses
+def cpu_baseline_prefill(cfg, w, seconds):
+    """fp64 oracle forward of one layer over the whole prompt, scaled to the model."""
+    import numpy as np
+    from oracle import forward as of
+    from workloads import init as winit
+    threads, vendor = blas_info()
+    names = [n for n in ("L0.ln1.g", "L0.ln1.b", "L0.wqkv", "L0.wo", "L0.ln2.g", "L0.ln2.b", "L0.w1", "L0.w2")]
+    Wt = {nm: winit.tensor_value(w, w.tensors[w.id(nm)]).astype(np.float64) for nm in names}
+    x0 = np.random.default_rng(8).standard_normal((cfg.tokens, cfg.hidden)) * 0.02
+    reps, t_layer = 0, 0.0
+    t_start = time.perf_counter()
+    while reps == 0 or time.perf_counter() - t_start < seconds:
+        t = time.perf_counter()
+        of.gpt_layer(cfg, Wt, 0, x0)
+        t_layer += time.perf_counter() - t
+        reps += 1
+    pass_s = t_layer / reps * cfg.n_layers
+    return {"value": cfg.tokens / pass_s, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "blas": vendor,
+            "sample": f"fp64 numpy oracle: 1 of {cfg.n_layers} layers over {cfg.batch} x {cfg.prompt_len} "
+                      f"tokens timed over {reps} repetitions, scaled to {cfg.n_layers} layers (LM head "
+                      f"not included; {pass_s:.1f} s per pass)"}
 
+
+def roofline_fields(st, seconds, bl_meas, units):
+    import numpy as np
+    t_comp = st["flops"] / NOMINAL["P"]
+    t_hbm = st["hbm_bytes"] / NOMINAL["Bh"]
+    t_link = st["lmin_bytes"] / NOMINAL["Bl"]
+    roof_s = max(t_comp, t_hbm, t_link)
+    roof_meas = max(t_comp, t_hbm, st["lmin_bytes"] / bl_meas)
+    return {"bound": ["mfma", "hbm", "link"][int(np.argmax([t_comp, t_hbm, t_link]))],
+            "roofline_units_per_s": round(units / roof_s, 3),
+            "frac": round(roof_s / seconds, 4),
+            "frac_measured_link": round(roof_meas / seconds, 4),
+            "link_GBps_nominal": NOMINAL["Bl"] / 1e9, "link_GBps_measured": round(bl_meas / 1e9, 2),
+            "t_mfma_ms": round(t_comp * 1e3, 3), "t_hbm_ms": round(t_hbm * 1e3, 3),
+            "t_link_ms": round(t_link * 1e3, 3), "t_measured_ms": round(seconds * 1e3, 3)}
+
+
+def linear_kernels(w, k0, k1):
+    from workloads.format import OP_LINEAR, OP_LINEAR_GELU, OP_LINEAR_RESID, OP_LINEAR_SWIGLU
+    return [k for k in range(k0, k1)
+            if w.kernels[k].op in (OP_LINEAR, OP_LINEAR_GELU, OP_LINEAR_RESID, OP_LINEAR_SWIGLU)]
+
+
+def decode_main(args, cfg):
     import numpy as np
     import torch
 
     from paper_2609_06172_amd.session import Session
-    from workloads import configs, trace
-    from workloads.format import OP_LINEAR, OP_LINEAR_GELU, OP_LINEAR_RESID, OP_LINEAR_SWIGLU
+    from workloads import trace
 
-    num, den = (int(x) for x in args.factor.split("/"))
-    cfg = dataclasses.replace(configs.CONFIGS[args.config], factor=(num, den))
-    W, K = args.warmup, args.steps
+    num, den = cfg.factor
+    W, K = args.warmup, (256 if args.steps is None else args.steps)
     if W + K > cfg.decode_steps or K < 1:
         sys.exit(f"warmup + steps must be within 1..{cfg.decode_steps}")
     w = trace.build(cfg)
@@ -246,34 +389,29 @@ def main():
     sched = s.ctx.get_schedule()
     classes = s.ctx.get_classes()
     dur, gap = s.ctx.get_kernel_times()
-    link_tl = link_timeline(s.ctx.get_timeline(), K)
+    tl = s.ctx.get_timeline()
     gen_tap = s.read("gen")[: W + K + 1].copy()
-    st = step_stats(w, sched, classes, M, k0, k1)
+    segs = w.segments["decode"][W:W + K]
+    st = seg_stats(w, sched, classes, M, segs)
 
     # dominant kernels: decode projections (M <= 16 rows) on the matrix cores
-    lin = [k for k in range(k0, k1)
-           if w.kernels[k].op in (OP_LINEAR, OP_LINEAR_GELU, OP_LINEAR_RESID, OP_LINEAR_SWIGLU)]
+    lin = linear_kernels(w, k0, k1)
     g_bytes = sum(classes[k][3] for k in lin)
     g_time = sum(dur[k] for k in lin) * 1e-3
     g_achieved = g_bytes / g_time / 1e9
     per_op = {}
     for k in range(k0, k1):
-        tag = w.kernels[k].tag
-        e = per_op.setdefault(tag, [0, 0.0, 0])
+        e = per_op.setdefault(w.kernels[k].tag, [0, 0.0])
         e[0] += 1
         e[1] += dur[k]
-        e[2] += classes[k][3]
     stall_ms = sum(gap[k] for k in range(k0 + 1, k1))
     busy_ms = sum(dur[k] for k in range(k0, k1))
 
     tok_s = cfg.batch * K / decode_s
-    t_comp = st["flops"] / NOMINAL["P"]
-    t_hbm = st["hbm_bytes"] / NOMINAL["Bh"]
-    t_link = st["lmin_bytes"] / NOMINAL["Bl"]
-    roof_s = max(t_comp, t_hbm, t_link)
-    roof_meas = max(t_comp, t_hbm, st["lmin_bytes"] / bl_meas)
+    pr = roofline_fields(st, decode_s, bl_meas, cfg.batch * K)
+    pr["roofline_tok_s"] = pr.pop("roofline_units_per_s")
     result = {
-        "metric": METRIC, "value": round(tok_s, 3), "unit": "tokens/s", "n_gpus": 1,
+        "metric": metric("", num, den), "value": round(tok_s, 3), "unit": "tokens/s", "n_gpus": 1,
         "steps": K, "warmup": W, "ms_per_step": round(decode_s / K * 1e3, 3),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic",
@@ -283,14 +421,7 @@ def main():
                                f"budget = footprint*{den}/{num}",
                    "batch": cfg.batch, "prompt_len": cfg.prompt_len, "factor": f"{num}/{den}",
                    "footprint_bytes": w.footprint, "budget_bytes": M, "policy": "T+A+P"},
-        "path_roofline": {
-            "bound": ["mfma", "hbm", "link"][int(np.argmax([t_comp, t_hbm, t_link]))],
-            "roofline_tok_s": round(cfg.batch * K / roof_s, 3),
-            "frac": round(roof_s / decode_s, 4),
-            "frac_measured_link": round(roof_meas / decode_s, 4),
-            "link_GBps_nominal": NOMINAL["Bl"] / 1e9, "link_GBps_measured": round(bl_meas / 1e9, 2),
-            "t_mfma_ms": round(t_comp * 1e3, 3), "t_hbm_ms": round(t_hbm * 1e3, 3),
-            "t_link_ms": round(t_link * 1e3, 3), "t_measured_ms": round(decode_s * 1e3, 3)},
+        "path_roofline": pr,
         "roofline": {"kernel": "decode projection GEMV (M=16, bf16 matrix cores)", "bound": "hbm",
                      "achieved": round(g_achieved, 1), "peak": 8000.0, "unit": "GB/s",
                      "frac": round(g_achieved / 8000.0, 4), "traffic": counted_traffic(),
@@ -303,32 +434,194 @@ def main():
                       "achieved_h2d_GBps": round(st["h2d_bytes"] / decode_s / 1e9, 2),
                       "compute_busy_ms_per_step": round(busy_ms / K, 3),
                       "compute_stall_ms_per_step": round(stall_ms / K, 3),
-                      "link_timeline": link_tl},
+                      "link_timeline": link_timeline(tl, K)},
         "prefill": {"seconds": round(prefill_s, 3), "tokens": cfg.batch * cfg.prompt_len},
         "per_kernel_ms_per_step": {k: round(v[1] / K, 4) for k, v in sorted(per_op.items())},
+        "per_layer": per_layer(w, tl, segs, cfg.n_layers),
+        "step_ms_per_32_steps": step_series(tl, segs),
     }
 
     if not args.no_baseline:
         Bk = min(args.baseline_steps, K)
-        s.set_policy(variant=0, timing=0)
-        s.ctx.reset()
-        s.restore_inputs()
-        pb, db, _, _ = run_decode(s, w, W, Bk)
-        gen_lru = s.read("gen")[: W + Bk + 1]
-        result["no_prefetch_baseline"] = {
-            "policy": "demand fetch at launch, LRU eviction", "steps": Bk,
-            "value": round(cfg.batch * Bk / db, 3), "unit": "tokens/s",
-            "ms_per_step": round(db / Bk * 1e3, 3), "prefill_seconds": round(pb, 3),
-            "speedup_of_T+A+P": round(tok_s / (cfg.batch * Bk / db), 3),
-            "tokens_identical": bool(np.array_equal(gen_lru, gen_tap[: W + Bk + 1]))}
-        log(f"baseline {Bk} steps {db:.3f} s")
+        b = decode_policy(s, w, M, 0, W, Bk, gen_tap)
+        b["policy"] = "demand fetch at launch, LRU eviction"
+        b["speedup_of_T+A+P"] = round(tok_s / b["value"], 3)
+        result["no_prefetch_baseline"] = b
+        log(f"baseline {Bk} steps {Bk / b['value'] * cfg.batch:.3f} s")
+        if not args.no_ablation:
+            result["ablation"] = [decode_policy(s, w, M, v, W, Bk, gen_tap) for v in (1, 2, 3)]
+            log("ablation: " + ", ".join(f"{a['policy']} {a['value']}" for a in result["ablation"]))
     s.close()
     del s
     torch.cuda.empty_cache()
 
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(cfg, w, args.cpu_seconds, cfg.prompt_len + W)
+        result["cpu_baseline"] = cpu_baseline_decode(cfg, w, args.cpu_seconds, cfg.prompt_len + W, M)
     print(json.dumps(result), flush=True)
+
+
+def sweep_main(args, cfg):
+    """The decode at several oversubscription factors, one session each."""
+    import dataclasses
+
+    import torch
+
+    from paper_2609_06172_amd.session import Session
+    from workloads import trace
+
+    W, K = args.warmup, (32 if args.steps is None else args.steps)
+    bl_meas = link_bandwidth()
+    rows = []
+    for f in args.sweep.split(","):
+        num, den = factor_of(f)
+        c = dataclasses.replace(cfg, factor=(num, den))
+        w = trace.build(c)
+        M = w.budget()
+        s = Session(w, device=0, M=M, variant=4, timing=1)
+        _, decode_s, k0, k1 = run_decode(s, w, W, K)
+        segs = w.segments["decode"][W:W + K]
+        st = seg_stats(w, s.ctx.get_schedule(), s.ctx.get_classes(), M, segs)
+        gen = s.read("gen")[: W + K + 1].copy()
+        pr = roofline_fields(st, decode_s, bl_meas, c.batch * K)
+        row = {"factor": f"{num}/{den}", "budget_bytes": M, "value": round(c.batch * K / decode_s, 3),
+               "ms_per_step": round(decode_s / K * 1e3, 3), "roofline_tok_s": pr["roofline_units_per_s"],
+               "bound": pr["bound"], "frac": pr["frac"], "frac_measured_link": pr["frac_measured_link"],
+               "h2d_bytes_per_step": st["h2d_bytes"] // K, "lmin_bytes_per_step": st["lmin_bytes"] // K,
+               "h2d_over_lmin": round(st["h2d_bytes"] / max(1, st["lmin_bytes"]), 4),
+               "link_timeline": link_timeline(s.ctx.get_timeline(), K)}
+        if not args.no_baseline:
+            Bk = min(args.baseline_steps, K)
+            b = decode_policy(s, w, M, 0, W, Bk, gen)
+            row["demand_lru_value"] = b["value"]
+            row["speedup_over_demand_lru"] = round(row["value"] / b["value"], 3)
+            row["tokens_identical"] = b["tokens_identical"]
+        log(f"factor {num}/{den}: {row['value']} tok/s, frac {row['frac']}")
+        rows.append(row)
+        s.close()
+        del s
+        torch.cuda.empty_cache()
+    out = {"metric": "tokens/sec per oversubscription factor; fraction of max(compute,HBM,link) roofline",
+           "unit": "tokens/s", "n_gpus": 1, "steps": K, "warmup": W, "higher_is_better": True,
+           "dtype": "bf16", "data": "synthetic", "link_GBps_measured": round(bl_meas / 1e9, 2),
+           "config": {"workload": f"{cfg.name}-shape decode, batch {cfg.batch}, {cfg.prompt_len}-token prompt",
+                      "policy": "T+A+P"},
+           "sweep": rows}
+    print(json.dumps(out), flush=True)
+
+
+def prefill_main(args, cfg):
+    """GPT-style prefill: one cold pass, then timed passes over the same ids."""
+    import dataclasses
+
+    import torch
+
+    from paper_2609_06172_amd.session import Session
+    from workloads import trace
+
+    num, den = cfg.factor
+    I = args.iterations
+    cfg = dataclasses.replace(cfg, iterations=1 + I)
+    w = trace.build(cfg)
+    M = w.budget()
+    its = w.segments["iterations"]
+    log(f"workload {cfg.name}: {len(w.tensors)} tensors, {len(w.kernels)} kernels, "
+        f"footprint {w.footprint} B, budget {M} B")
+    bl_meas = link_bandwidth()
+    s = Session(w, device=0, M=M, variant=4, timing=1)
+
+    def passes(sess):
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        sess.run(*its[0])
+        torch.cuda.synchronize()
+        cold = time.perf_counter() - t
+        k0 = its[1][0]
+        k1 = its[-1][0] + its[-1][1]
+        t = time.perf_counter()
+        sess.run(k0, k1 - k0)
+        torch.cuda.synchronize()
+        return cold, time.perf_counter() - t, k0, k1
+
+    cold_s, hot_s, k0, k1 = passes(s)
+    sched, classes = s.ctx.get_schedule(), s.ctx.get_classes()
+    dur, gap = s.ctx.get_kernel_times()
+    tl = s.ctx.get_timeline()
+    st = seg_stats(w, sched, classes, M, its[1:])
+    st0 = seg_stats(w, sched, classes, M, its[:1])
+    logits = s.read("logits").copy()
+    lin = linear_kernels(w, k0, k1)
+    g_flops = sum(classes[k][2] for k in lin)
+    g_time = sum(dur[k] for k in lin) * 1e-3
+    attn = [k for k in range(k0, k1) if w.kernels[k].tag == "attn"]
+    a_flops = sum(classes[k][2] for k in attn)
+    a_time = sum(dur[k] for k in attn) * 1e-3
+    tok_s = cfg.tokens * I / hot_s
+    pr = roofline_fields(st, hot_s, bl_meas, cfg.tokens * I)
+    pr["roofline_tok_s"] = pr.pop("roofline_units_per_s")
+    result = {
+        "metric": metric("prefill ", num, den), "value": round(tok_s, 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": I, "warmup": 1, "ms_per_step": round(hot_s / I * 1e3, 3), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"{cfg.name}-shape prefill: {cfg.n_layers} layers, hidden {cfg.hidden}, "
+                               f"GELU {cfg.ffn}, vocab {cfg.vocab}, {cfg.batch} x {cfg.prompt_len} tokens, "
+                               f"budget = footprint*{den}/{num}",
+                   "tokens_per_pass": cfg.tokens, "factor": f"{num}/{den}", "footprint_bytes": w.footprint,
+                   "budget_bytes": M, "policy": "T+A+P"},
+        "path_roofline": pr,
+        "roofline": {"kernel": "prefill projection GEMM (bf16 matrix cores)", "bound": "mfma",
+                     "achieved": round(g_flops / g_time / 1e12, 1), "peak": 2500.0, "unit": "TFLOP/s",
+                     "frac": round(g_flops / g_time / 2.5e15, 4), "traffic": None, "launches": len(lin),
+                     "avg_us": round(g_time / max(1, len(lin)) * 1e6, 2),
+                     "avg_flops": int(g_flops / max(1, len(lin)))},
+        "attention": {"launches": len(attn), "avg_us": round(a_time / max(1, len(attn)) * 1e6, 2),
+                      "TFLOPs": round(a_flops / a_time / 1e12, 1) if a_time > 0 else None},
+        "transfers": {"h2d_bytes_per_pass": st["h2d_bytes"] // I, "lmin_bytes_per_pass": st["lmin_bytes"] // I,
+                      "h2d_over_lmin": round(st["h2d_bytes"] / max(1, st["lmin_bytes"]), 4),
+                      "d2h_bytes_per_pass": st["d2h_bytes"] // I,
+                      "compute_busy_ms_per_pass": round(sum(dur[k] for k in range(k0, k1)) / I, 3),
+                      "compute_stall_ms_per_pass": round(sum(gap[k] for k in range(k0 + 1, k1)) / I, 3),
+                      "link_timeline": link_timeline(tl, I)},
+        "cold_pass": {"seconds": round(cold_s, 4), "h2d_bytes": st0["h2d_bytes"]},
+        "per_layer": per_layer(w, tl, [w.segments["iterations"][1]], cfg.n_layers),
+    }
+    if not args.no_baseline:
+        s.set_policy(variant=0, timing=0)
+        s.ctx.reset()
+        s.restore_inputs()
+        _, hot_b, _, _ = passes(s)
+        result["no_prefetch_baseline"] = {
+            "policy": "demand fetch at launch, LRU eviction", "value": round(cfg.tokens * I / hot_b, 1),
+            "unit": "tokens/s", "ms_per_pass": round(hot_b / I * 1e3, 3),
+            "speedup_of_T+A+P": round(hot_b / hot_s, 3),
+            "logits_identical": bool((s.read("logits") == logits).all())}
+    s.close()
+    del s
+    torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline_prefill(cfg, w, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py runs on one GPU: this build has no multi-GPU path "
+              "(the per-GPU hot path is what it measures)", file=sys.stderr)
+        sys.exit(2)
+    import dataclasses
+
+    from workloads import configs
+
+    cfg = configs.CONFIGS[args.config]
+    if args.factor:
+        cfg = dataclasses.replace(cfg, factor=factor_of(args.factor))
+    if cfg.style == "gpt":
+        prefill_main(args, cfg)
+    elif args.sweep:
+        sweep_main(args, cfg)
+    else:
+        decode_main(args, cfg)
 
 
 if __name__ == "__main__":

@@ -29,6 +29,7 @@ class DecoderConfig:
     factor: Tuple[int, int] = (3, 2)   # oversubscription factor num/den
     logits_all: bool = False           # gpt style: logits at every position (else last only)
     seed: int = 0
+    iterations: int = 1                # gpt style: forward passes over the same ids
 
     @property
     def head_dim(self) -> int:

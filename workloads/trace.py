@@ -139,6 +139,20 @@ def _build_gpt(c: DecoderConfig) -> Workload:
         logits = w.tensor("logits", (B, V), DT_F32, KIND_ACT)
 
     R, W_, RW = MODE_R, MODE_W, MODE_RW
+    w.segments["iterations"] = []
+    for it in range(c.iterations):
+        i0 = len(w.kernels)
+        segs = _gpt_forward(w, c, layers, E, gf, bf, ids, x, h, qkv, attn, ffn, logits,
+                            None if c.logits_all else hl)
+        if it == 0:
+            w.segments["forward"] = segs       # embed, one entry per layer, head (first pass)
+        w.segments["iterations"].append((i0, len(w.kernels) - i0))
+    return w
+
+
+def _gpt_forward(w, c, layers, E, gf, bf, ids, x, h, qkv, attn, ffn, logits, hl):
+    H, F, V, T, B, S = c.hidden, c.ffn, c.vocab, c.tokens, c.batch, c.prompt_len
+    R, W_, RW = MODE_R, MODE_W, MODE_RW
     segs = []
     k0 = w.kernel(OP_EMBED, (T, H, V), [(ids, R), (E, R), (x, W_)], tag="embed")
     segs.append((k0, 1))
@@ -160,8 +174,7 @@ def _build_gpt(c: DecoderConfig) -> Workload:
         w.kernel(OP_LAYERNORM, (B, H, S, S - 1), [(x, R), (gf, R), (bf, R), (hl, W_)], c.n_layers, "lnf")
         w.kernel(OP_LINEAR, (B, V, H), [(hl, R), (E, R), (logits, W_)], c.n_layers, "head")
     segs.append((k0, len(w.kernels) - k0))
-    w.segments["forward"] = segs       # embed, one entry per layer, head
-    return w
+    return segs
 
 
 def _build_llama(c: DecoderConfig) -> Workload:
