@@ -17,10 +17,13 @@ struct GemmArgs {
   bool in_bf16, out_bf16;
 };
 
-// Dispatch: bf16 with M <= 16 -> matrix-core GEMV (gemv.hip); other bf16 ->
-// matrix-core tiled GEMM (gemm_mfma.hip); fp32 -> LDS-tiled FMA GEMM.
+// Dispatch: bf16 with M <= 16 -> matrix-core GEMV (gemv.hip); bf16 with
+// M >= 512 and K % 64 == 0 -> 256 x 256 matrix-core GEMM fed by direct LDS
+// loads (gemm_big.hip); other bf16 -> 128 x 128 matrix-core GEMM
+// (gemm_mfma.hip); fp32 -> LDS-tiled FMA GEMM.
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s);
 hipError_t launch_gemv_bf16(const GemmArgs& g, hipStream_t s);
 hipError_t launch_gemm_mfma_bf16(const GemmArgs& g, hipStream_t s);
+hipError_t launch_gemm_big_bf16(const GemmArgs& g, hipStream_t s);
 
 }  // namespace auvm

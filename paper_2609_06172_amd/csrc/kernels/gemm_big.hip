@@ -1,0 +1,203 @@
+// Large prefill GEMM on bf16 matrix cores: C[M,N] (epilogue) = A[M,K] W[N,K]^T.
+//
+// Workgroup tile 256 x 256 (256 x 128 per weight for the two-weight SwiGLU
+// epilogue), K step 64, four waves in a 2 x 2 grid; each wave owns 4 x 4
+// (4 x 2 per weight) tiles of v_mfma_f32_32x32x16_bf16, so one fragment read
+// from LDS feeds four matrix-core instructions.
+//
+// Operand tiles go from global memory straight into LDS (16-byte
+// global_load_lds, no register staging), two stages deep: the next K step
+// streams in while the current one feeds the matrix cores.  One wave
+// instruction fills 8 rows x 128 bytes of a stage; within a row the eight
+// 16-byte chunks are stored at slot chunk ^ (row & 7), which spreads a
+// fragment read (32 rows, one chunk) over the LDS banks.  Rows past M or N are
+// clamped to the last row (every load stays in bounds) and their results are
+// dropped by the epilogue; K must be a multiple of 64.
+#include <hip/hip_runtime.h>
+
+#include "common.h"
+#include "gemm.h"
+
+namespace auvm {
+
+using namespace dev;
+
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int kBK = 64;      // K elements per stage row (128 bytes)
+constexpr int kXcd = 8;
+constexpr int kGroupM = 8;
+
+template <int EPI>
+struct Shape {
+  static constexpr bool kDual = EPI == EPI_SWIGLU;
+  static constexpr int kTM = 4, kTN = kDual ? 2 : 4;          // 32x32 tiles per wave (per weight)
+  static constexpr int kBM = 2 * 32 * kTM, kBN = 2 * 32 * kTN;
+  static constexpr int kRows = kBM + (kDual ? 2 : 1) * kBN;   // rows staged per K step
+  static constexpr int kStage = kRows * kBK;                   // bf16 elements per stage
+};
+
+// One K step of operand rows into LDS stage buf.  Wave wv fills the 8-row
+// blocks wv, wv + 4, ...; lane l fills row 8 * block + l / 8 at slot l % 8
+// with the row's chunk (l % 8) ^ (row & 7).  A device function, not a lambda:
+// the LDS-load builtin exists only in the device pass.
+template <int EPI>
+__device__ __forceinline__ void load_stage(bf16_t* smem, const bf16_t* __restrict__ A, const bf16_t* __restrict__ W,
+                                           const bf16_t* __restrict__ W2, int64_t M, int64_t N, int64_t K,
+                                           int64_t m0, int64_t n0, int wv, int lane, int buf, int64_t k0) {
+  using S = Shape<EPI>;
+  constexpr bool DUAL = S::kDual;
+  constexpr int BM = S::kBM, BN = S::kBN;
+  static_assert(S::kRows % 32 == 0, "stage rows split evenly over four waves");
+  bf16_t* base = smem + buf * S::kStage;
+  const int rin = lane >> 3, slot = lane & 7;
+#pragma unroll
+  for (int t = 0; t < S::kRows / 32; ++t) {
+    const int b = wv + 4 * t;
+    const int row = 8 * b + rin;
+    const bf16_t* src;
+    if (row < BM) {
+      const int64_t r = m0 + row;
+      src = A + (r < M ? r : M - 1) * K;
+    } else {
+      const int wrow = row - BM;
+      const bool second = DUAL && wrow >= BN;
+      const int64_t r = n0 + (second ? wrow - BN : wrow);
+      src = (second ? W2 : W) + (r < N ? r : N - 1) * K;
+    }
+    const int chunk = slot ^ (row & 7);
+    __builtin_amdgcn_global_load_lds(src + k0 + 8 * chunk, base + 8 * b * kBK, 16, 0, 0);
+  }
+}
+
+template <int EPI, class TC>
+__global__ void __launch_bounds__(256) gemm_big(const bf16_t* __restrict__ A, const bf16_t* __restrict__ W,
+                                                const bf16_t* __restrict__ W2, TC* __restrict__ C,
+                                                int64_t M, int64_t N, int64_t K, int tilesN) {
+  using S = Shape<EPI>;
+  constexpr bool DUAL = S::kDual;
+  constexpr int TM = S::kTM, TN = S::kTN, BM = S::kBM, BN = S::kBN;
+  extern __shared__ __align__(16) bf16_t smem[];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int wm = wv >> 1, wn = wv & 1;
+
+  // tile order: XCD round-robin remap, then groups of kGroupM row-blocks
+  const int nwg = gridDim.x, per = nwg / kXcd;
+  int id = blockIdx.x;
+  if (per > 0 && id < per * kXcd) id = (id % kXcd) * per + id / kXcd;
+  const int tilesM = nwg / tilesN;
+  const int gsize = kGroupM * tilesN, grp = id / gsize, first = grp * kGroupM;
+  const int gm = (tilesM - first) < kGroupM ? (tilesM - first) : kGroupM;
+  const int in = id - grp * gsize;
+  const int64_t m0 = int64_t(first + in % gm) * BM, n0 = int64_t(in / gm) * BN;
+
+  f32x16 acc[TM][TN], acc2[DUAL ? TM : 1][DUAL ? TN : 1];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = f32x16{};
+  if constexpr (DUAL) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j) acc2[i][j] = f32x16{};
+  }
+
+  const int lr = lane & 31, lc = lane >> 5;     // fragment row, chunk half
+  const int64_t nk = K / kBK;
+  load_stage<EPI>(smem, A, W, W2, M, N, K, m0, n0, wv, lane, 0, 0);
+  for (int64_t kt = 0; kt < nk; ++kt) {
+    __builtin_amdgcn_s_waitcnt(0);   // this wave's loads of stage kt have landed
+    __syncthreads();                 // ... and every other wave's; stage kt-1 is free
+    asm volatile("" ::: "memory");   // LDS now holds data written outside the compiler's view
+    if (kt + 1 < nk) load_stage<EPI>(smem, A, W, W2, M, N, K, m0, n0, wv, lane, int((kt + 1) & 1), (kt + 1) * kBK);
+    const bf16_t* stg = smem + int(kt & 1) * S::kStage;
+#pragma unroll
+    for (int ks = 0; ks < kBK / 16; ++ks) {
+      const int c = 2 * ks + lc;
+      bf16x8 a[TM], b[TN], b2[DUAL ? TN : 1];
+#pragma unroll
+      for (int i = 0; i < TM; ++i) {
+        const int row = wm * 32 * TM + 32 * i + lr;
+        a[i] = *reinterpret_cast<const bf16x8*>(stg + row * kBK + 8 * (c ^ (row & 7)));
+      }
+#pragma unroll
+      for (int j = 0; j < TN; ++j) {
+        const int row = BM + wn * 32 * TN + 32 * j + lr;
+        b[j] = *reinterpret_cast<const bf16x8*>(stg + row * kBK + 8 * (c ^ (row & 7)));
+        if constexpr (DUAL) {
+          const int row2 = row + BN;
+          b2[j] = *reinterpret_cast<const bf16x8*>(stg + row2 * kBK + 8 * (c ^ (row2 & 7)));
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+          if constexpr (DUAL) acc2[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b2[j], acc2[i][j], 0, 0, 0);
+        }
+    }
+  }
+
+  // accumulator layout: element e of lane l is row 8*(e/4) + 4*(l/32) + e%4, column l%32.
+  // Unrolled in full whatever the epilogue's size: a loop left rolled would
+  // index the accumulators at run time and move them to scratch memory.
+#pragma clang loop unroll(full)
+  for (int i = 0; i < TM; ++i)
+#pragma clang loop unroll(full)
+    for (int j = 0; j < TN; ++j) {
+      const int64_t col = n0 + wn * 32 * TN + 32 * j + lr;
+      if (col >= N) continue;
+#pragma clang loop unroll(full)
+      for (int e = 0; e < 16; ++e) {
+        const int64_t row = m0 + wm * 32 * TM + 32 * i + 8 * (e >> 2) + 4 * lc + (e & 3);
+        if (row >= M) continue;
+        float v = acc[i][j][e];
+        if constexpr (EPI == EPI_GELU) v = gelu_erf(v);
+        if constexpr (EPI == EPI_SWIGLU) v = silu(v) * acc2[i][j][e];
+        if constexpr (EPI == EPI_RESID) {
+          float* x = reinterpret_cast<float*>(C);
+          x[row * N + col] += v;
+        } else {
+          st(C, row * N + col, v);
+        }
+      }
+    }
+}
+
+template <int EPI, class TC>
+hipError_t go(const GemmArgs& g, hipStream_t s) {
+  using S = Shape<EPI>;
+  const int tilesM = int((g.M + S::kBM - 1) / S::kBM), tilesN = int((g.N + S::kBN - 1) / S::kBN);
+  const size_t lds = size_t(2) * S::kStage * sizeof(bf16_t);
+  hipLaunchKernelGGL((gemm_big<EPI, TC>), dim3(unsigned(tilesM * tilesN)), dim3(256), lds, s,
+                     reinterpret_cast<const bf16_t*>(g.a), reinterpret_cast<const bf16_t*>(g.w),
+                     reinterpret_cast<const bf16_t*>(g.w2), reinterpret_cast<TC*>(g.c), g.M, g.N, g.K,
+                     tilesN);
+  return hipGetLastError();
+}
+
+template <class TC>
+hipError_t by_epi(const GemmArgs& g, hipStream_t s) {
+  switch (g.epi) {
+    case EPI_STORE: return go<EPI_STORE, TC>(g, s);
+    case EPI_GELU: return go<EPI_GELU, TC>(g, s);
+    case EPI_RESID: return go<EPI_RESID, float>(g, s);
+    case EPI_SWIGLU: return go<EPI_SWIGLU, TC>(g, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+// bf16 operands, K % 64 == 0, M, N >= 1.
+hipError_t launch_gemm_big_bf16(const GemmArgs& g, hipStream_t s) {
+  if (g.K % kBK != 0 || g.M < 1 || g.N < 1) return hipErrorInvalidValue;
+  return g.out_bf16 ? by_epi<bf16_t>(g, s) : by_epi<float>(g, s);
+}
+
+}  // namespace auvm

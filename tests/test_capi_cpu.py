@@ -166,3 +166,18 @@ def test_llama7b_prefill_and_decode_bit_exact(factor):
     r = op.plan_workload(w, M)
     assert_same_plan(s.ctx, r)
     s.close()
+
+
+def test_library_defines_every_kernel_launch_stub():
+    """A kernel template whose host pass fails (a device-only builtin reachable
+    from host-compiled code) loses its launch stub without a compile error; the
+    library then fails to load on a GPU machine."""
+    import shutil
+    import subprocess
+    nm = shutil.which("nm")
+    if nm is None:
+        pytest.skip("nm not available")
+    path = pkg.lib()._name
+    out = subprocess.run([nm, "-D", "--undefined-only", path], capture_output=True, text=True, check=True).stdout
+    missing = [l.split()[-1] for l in out.splitlines() if "__device_stub__" in l]
+    assert not missing, missing
