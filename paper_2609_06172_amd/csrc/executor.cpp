@@ -383,14 +383,16 @@ class Executor {
       if (!tr->s.empty()) continue;
       tr->s.assign(kTimeRing, nullptr);
       tr->e.assign(kTimeRing, nullptr);
+      // timestamps only (ordering uses the sync events and every segment ends
+      // with a full wait), so no system-scope fence per event
       for (auto* ring : {&tr->s, &tr->e})
         for (auto& e : *ring)
-          if (!ok(hipEventCreate(&e), "hipEventCreate")) return false;
+          if (!ok(hipEventCreateWithFlags(&e, hipEventDisableSystemFence), "hipEventCreate")) return false;
     }
     ++seg_;
     if (size_t(seg_) >= bases_.size()) {
       hipEvent_t b = nullptr;
-      if (!ok(hipEventCreate(&b), "hipEventCreate")) return false;
+      if (!ok(hipEventCreateWithFlags(&b, hipEventDisableSystemFence), "hipEventCreate")) return false;
       bases_.push_back(b);
     }
     // the streams are idle here (every segment ends with a full wait)
