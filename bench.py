@@ -95,19 +95,31 @@ def link_bandwidth():
     return best
 
 
-def counted_traffic():
-    """HBM bytes per GEMV launch from the committed counter runs, if the kernel
-    source is unchanged since they were taken (else None)."""
+def counted_traffic(profile, source):
+    """HBM bytes per launch of a kernel from its committed counter runs, if the
+    kernel source is unchanged since they were taken (else None)."""
     import hashlib
-    prof = os.path.join(ROOT, "profiles", "gemv_mfma_traffic_llama7b_decode.json")
-    src = os.path.join(ROOT, "paper_2609_06172_amd", "csrc", "kernels", "gemv.hip")
+    prof = os.path.join(ROOT, "profiles", profile)
+    src = os.path.join(ROOT, "paper_2609_06172_amd", "csrc", "kernels", source)
     try:
         meta = json.load(open(prof))
         if hashlib.sha256(open(src, "rb").read()).hexdigest() != meta["kernel_source_sha256"]:
             return None
-        return meta["hbm_bytes_per_launch"]
+        return meta["traffic_bytes_per_launch"]
     except (OSError, KeyError, ValueError):
         return None
+
+
+def calibrate_copy():
+    """One 256 MiB device-to-device copy kernel: a known-size reference for
+    hardware byte counters taken over the same command."""
+    import torch
+    n = 256 << 20
+    src = torch.empty(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty(n, dtype=torch.uint8, device="cuda")
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    del src, dst
 
 
 def seg_stats(w, sched, classes, M, segs):
@@ -372,12 +384,7 @@ def decode_main(args, cfg):
     log(f"workload {cfg.name}: {len(w.tensors)} tensors, {len(w.kernels)} kernels, "
         f"footprint {w.footprint} B, budget {M} B")
     if args.calibrate_copy:
-        n = 256 << 20
-        src = torch.empty(n, dtype=torch.uint8, device="cuda")
-        dst = torch.empty(n, dtype=torch.uint8, device="cuda")
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        del src, dst
+        calibrate_copy()
     bl_meas = link_bandwidth()
     log(f"measured pinned H2D: {bl_meas / 1e9:.1f} GB/s")
 
@@ -424,7 +431,8 @@ def decode_main(args, cfg):
         "path_roofline": pr,
         "roofline": {"kernel": "decode projection GEMV (M=16, bf16 matrix cores)", "bound": "hbm",
                      "achieved": round(g_achieved, 1), "peak": 8000.0, "unit": "GB/s",
-                     "frac": round(g_achieved / 8000.0, 4), "traffic": counted_traffic(),
+                     "frac": round(g_achieved / 8000.0, 4),
+                     "traffic": counted_traffic("gemv_mfma_traffic_llama7b_decode.json", "gemv.hip"),
                      "launches": len(lin), "avg_us": round(g_time / max(1, len(lin)) * 1e6, 2),
                      "avg_bytes": int(g_bytes / max(1, len(lin)))},
         "transfers": {"h2d_bytes_per_step": st["h2d_bytes"] // K, "d2h_bytes_per_step": st["d2h_bytes"] // K,
@@ -526,6 +534,8 @@ def prefill_main(args, cfg):
     its = w.segments["iterations"]
     log(f"workload {cfg.name}: {len(w.tensors)} tensors, {len(w.kernels)} kernels, "
         f"footprint {w.footprint} B, budget {M} B")
+    if args.calibrate_copy:
+        calibrate_copy()
     bl_meas = link_bandwidth()
     s = Session(w, device=0, M=M, variant=4, timing=1)
 
@@ -549,7 +559,7 @@ def prefill_main(args, cfg):
     st = seg_stats(w, sched, classes, M, its[1:])
     st0 = seg_stats(w, sched, classes, M, its[:1])
     logits = s.read("logits").copy()
-    lin = linear_kernels(w, k0, k1)
+    lin = [k for k in linear_kernels(w, k0, k1) if w.kernels[k].shape[0] >= 512]   # the projection GEMMs
     g_flops = sum(classes[k][2] for k in lin)
     g_time = sum(dur[k] for k in lin) * 1e-3
     attn = [k for k in range(k0, k1) if w.kernels[k].tag == "attn"]
@@ -570,7 +580,9 @@ def prefill_main(args, cfg):
         "path_roofline": pr,
         "roofline": {"kernel": "prefill projection GEMM (bf16 matrix cores)", "bound": "mfma",
                      "achieved": round(g_flops / g_time / 1e12, 1), "peak": 2500.0, "unit": "TFLOP/s",
-                     "frac": round(g_flops / g_time / 2.5e15, 4), "traffic": None, "launches": len(lin),
+                     "frac": round(g_flops / g_time / 2.5e15, 4),
+                     "traffic": counted_traffic("gemm_big_traffic_gpt1p3b_prefill.json", "gemm_big.hip"),
+                     "launches": len(lin),
                      "avg_us": round(g_time / max(1, len(lin)) * 1e6, 2),
                      "avg_flops": int(g_flops / max(1, len(lin)))},
         "attention": {"launches": len(attn), "avg_us": round(a_time / max(1, len(attn)) * 1e6, 2),
