@@ -178,157 +178,199 @@ __global__ void __launch_bounds__(256) attn_decode_d128(AttnArgs a) {
 }
 
 // Prefill attention, head dim 128, bf16, on matrix cores (flash-style).
-// One workgroup per (b, h, block of 64 queries); wave w owns queries
-// 16w..16w+15 with its Q fragments in registers.  For each block of 64 keys:
-//   K is staged in LDS row-major and V transposed (dims x keys), so every
-//   MFMA operand is one 16-byte LDS read;
-//   S = Q K^T: 4 key tiles x 4 dim steps of v_mfma_f32_16x16x32_bf16;
-//   online softmax on the accumulators (a lane holds 4 query rows);
-//   P goes through a per-wave LDS tile to become the A operand of
-//   O += P V: 2 key steps x 8 dim tiles of the same MFMA.
-// Blocks past the diagonal are skipped; only diagonal blocks are masked.
+// One workgroup of 4 waves per (b, h, block of 128 queries); wave w owns
+// queries 32w..32w+31.  Everything is computed transposed, so that a lane owns
+// one query: lane l holds query l % 32 and half of the keys or dims.
+//   S^T = K Q^T: A = a 32-key x 16-dim K fragment (LDS), B = Q^T (registers),
+//     2 key tiles x 8 dim steps of v_mfma_f32_32x32x16_bf16 per 64-key block;
+//   online softmax: a query's 64 scores sit in lanes l and l+32 (32 each), so
+//     its max and sum are one exchange between the two;
+//   O^T += V^T P^T: A = a 32-dim x 16-key fragment of V transposed (LDS),
+//     B = P^T assembled in registers (each lane trades four values with its
+//     partner lane), 4 dim tiles x 4 key steps per block.
+// Each 1 KB fragment read from LDS feeds a 32x32x16 MFMA (32k flop).  Keys go
+// in blocks of 64 through two LDS buffers: the next block loads into
+// registers while this one is consumed and is written to the other buffer
+// afterwards (one barrier per block).  A wave skips blocks wholly past its
+// queries; only blocks crossing its diagonal are masked.  Heaviest query
+// blocks are dispatched first.
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2v __attribute__((ext_vector_type(2)));
 
-constexpr int FQ = 64, FK = 64, FD = 128;
-constexpr int KP = FD + 8;   // K tile pitch (elements)
-constexpr int VP = FK + 8;   // transposed V tile pitch
-constexpr int PP = FK + 8;   // P tile pitch
+constexpr int FW = 4;          // waves per workgroup
+constexpr int FQ = 32 * FW;    // queries per workgroup
+constexpr int FK = 64, FD = 128;
+constexpr int KP = FD + 8;     // K tile pitch (elements): rows 272 B apart
+constexpr int VP = FK + 8;     // transposed V tile pitch: rows 144 B apart
+constexpr int KS = FK * KP, VS = FD * VP;   // elements per tile
+constexpr size_t kFlashLds = size_t(2 * KS + 2 * VS) * sizeof(bf16_t);
 
-__global__ void __launch_bounds__(256) attn_prefill_d128(AttnArgs a, int64_t nqb) {
-  __shared__ __align__(16) bf16_t Ks[FK * KP];
-  __shared__ __align__(16) bf16_t Vt[FD * VP];
-  __shared__ __align__(16) bf16_t Ps[4][16 * PP];
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// two floats to bf16 (round to nearest even, one conversion instruction)
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
+  const bf16x2 v = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(uint32_t, v);
+}
+
+__global__ void __launch_bounds__(64 * FW, 2) attn_prefill_d128(AttnArgs a, int64_t nqb) {
+  extern __shared__ __align__(16) bf16_t fsm[];
+  bf16_t* Ks = fsm;                 // [2][FK][KP]
+  bf16_t* Vt = fsm + 2 * KS;        // [2][FD][VP]
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  const int lr = lane & 15, lg = lane >> 4;
-  // heaviest query blocks first
+  const int lq = lane & 31, lh = lane >> 5;
   const int64_t wg = blockIdx.x;
   const int64_t qb = nqb - 1 - wg % nqb, bh = wg / nqb;
   const int64_t h = bh % a.nH, b = bh / a.nH;
-  const int64_t q0 = qb * FQ;
+  const int64_t q0 = qb * FQ, qw = q0 + 32 * wv;
   const bf16_t* Q = reinterpret_cast<const bf16_t*>(a.q) + (b * a.S) * a.q_rs + h * FD;
   const bf16_t* Kg = reinterpret_cast<const bf16_t*>(a.k) + b * a.kv_bstride + h * a.kv_hstride;
   const bf16_t* Vg = reinterpret_cast<const bf16_t*>(a.v) + b * a.kv_bstride + h * a.kv_hstride;
   bf16_t* O = reinterpret_cast<bf16_t*>(a.o) + (b * a.S) * a.o_rs + h * FD;
 
-  // this wave's query rows: q0 + 16*wv + r; Q fragment for dim step c: dims 32c + 8g .. +8
-  const int64_t qr = q0 + 16 * wv + lr;
-  bf16x8 qf[4];
+  // Q^T fragment for dim step c: dims 16c + 8*lh .. +8 of this lane's query
+  const int64_t qr = qw + lq, qpos = a.pos0 + qr;
+  bf16x8 qf[8];
 #pragma unroll
-  for (int c = 0; c < 4; ++c) {
+  for (int c = 0; c < 8; ++c) {
     if (qr < a.S)
-      qf[c] = *reinterpret_cast<const bf16x8*>(Q + qr * a.q_rs + 32 * c + 8 * lg);
+      qf[c] = *reinterpret_cast<const bf16x8*>(Q + qr * a.q_rs + 16 * c + 8 * lh);
     else
       qf[c] = bf16x8{};
   }
-  const float scale = 0.08838834764831845f;  // 1/sqrt(128)
-  f32x4 o[8];
+  // softmax in base 2 on raw scores: p = 2^(c*s - c*max) with c = log2(e)/sqrt(128)
+  const float c2 = 0.12751743074565512f;
+  // O^T tile dt: element e is dim 32*dt + 8*(e/4) + 4*lh + e%4 of this lane's query
+  f32x16 ot[4];
 #pragma unroll
-  for (int t = 0; t < 8; ++t) o[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m[4], l[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    m[i] = -INFINITY;
-    l[i] = 0.f;
-  }
-  // queries of this workgroup see keys 0 .. pos0 + min(q0 + 63, S - 1)
+  for (int t = 0; t < 4; ++t) ot[t] = f32x16{};
+  float m = -INFINITY, l = 0.f;
+  // the workgroup's queries see keys 0 .. klast; this wave's, 0 .. wlast
   const int64_t qlast = (q0 + FQ - 1 < a.S ? q0 + FQ - 1 : a.S - 1);
   const int64_t klast = a.pos0 + qlast;
-  // staging assignment: thread t moves keys 4*(t%16)..+3, dims 8*(t/16)..+7
-  const int sk = 4 * (tid & 15), sd = 8 * (tid >> 4);
-  for (int64_t k0 = 0; k0 <= klast; k0 += FK) {
-    __syncthreads();  // previous block's tiles are no longer read
+  const int64_t wlast = a.pos0 + qw + 31;
+
+  // staging: thread t moves dims 8*(t%16)..+7 of keys 4*(t/16)..+3
+  const int sc = 8 * (tid & 15), sk = 4 * (tid >> 4);
+  u32x4v kr[4], vr[4];
+  auto fetch = [&](int64_t k0) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const int64_t key = k0 + sk + j;
-      u32x4v kv = u32x4v{0u, 0u, 0u, 0u}, vv = u32x4v{0u, 0u, 0u, 0u};
+      kr[j] = u32x4v{0u, 0u, 0u, 0u};
+      vr[j] = u32x4v{0u, 0u, 0u, 0u};
       if (key <= klast) {
-        kv = *reinterpret_cast<const u32x4v*>(Kg + key * a.kv_rs + sd);
-        vv = *reinterpret_cast<const u32x4v*>(Vg + key * a.kv_rs + sd);
-      }
-      *reinterpret_cast<u32x4v*>(Ks + (sk + j) * KP + sd) = kv;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        Vt[(sd + 2 * e) * VP + sk + j] = bf16_t(vv[e] & 0xffffu);
-        Vt[(sd + 2 * e + 1) * VP + sk + j] = bf16_t(vv[e] >> 16);
+        kr[j] = *reinterpret_cast<const u32x4v*>(Kg + key * a.kv_rs + sc);
+        vr[j] = *reinterpret_cast<const u32x4v*>(Vg + key * a.kv_rs + sc);
       }
     }
-    __syncthreads();
-    // S = Q K^T for this wave's 16 queries x 64 keys
-    f32x4 sacc[4];
+  };
+  auto stage = [&](int buf) {
+    bf16_t* ks = Ks + buf * KS;
+    bf16_t* vt = Vt + buf * VS;
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      sacc[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < 4; ++j) *reinterpret_cast<u32x4v*>(ks + (sk + j) * KP + sc) = kr[j];
+    // V transposed: dim sc + i of keys sk..sk+3 is one 8-byte row piece
 #pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        const bf16x8 kb = *reinterpret_cast<const bf16x8*>(Ks + (16 * t + lr) * KP + 32 * c + 8 * lg);
-        sacc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(qf[c], kb, sacc[t], 0, 0, 0);
-      }
+    for (int e = 0; e < 4; ++e) {
+      const u32x2v lo = {(vr[0][e] & 0xffffu) | (vr[1][e] << 16), (vr[2][e] & 0xffffu) | (vr[3][e] << 16)};
+      const u32x2v hi = {(vr[0][e] >> 16) | (vr[1][e] & 0xffff0000u), (vr[2][e] >> 16) | (vr[3][e] & 0xffff0000u)};
+      *reinterpret_cast<u32x2v*>(vt + (sc + 2 * e) * VP + sk) = lo;
+      *reinterpret_cast<u32x2v*>(vt + (sc + 2 * e + 1) * VP + sk) = hi;
     }
-    // element i of a lane: query row 16*wv + 4*lg + i, key k0 + 16*t + lr
-    const bool diag = k0 + FK - 1 > a.pos0 + q0 + 16 * wv;
-    float rmax[4];
+  };
+
+  fetch(0);
+  stage(0);
+  __syncthreads();
+  int buf = 0;
+  for (int64_t k0 = 0; k0 <= klast; k0 += FK, buf ^= 1) {
+    const bool more = k0 + FK <= klast;
+    if (more) fetch(k0 + FK);   // in flight while this block is consumed
+    if (k0 <= wlast) {
+      const bf16_t* ks = Ks + buf * KS;
+      const bf16_t* vt = Vt + buf * VS;
+      // S^T tile kt: element e is key k0 + 32*kt + 8*(e/4) + 4*lh + e%4 of this lane's query
+      f32x16 st[2];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int64_t qpos = a.pos0 + q0 + 16 * wv + 4 * lg + i;
+      for (int kt = 0; kt < 2; ++kt) {
+        st[kt] = f32x16{};
+#pragma unroll
+        for (int c = 0; c < 8; ++c) {
+          const bf16x8 kf = *reinterpret_cast<const bf16x8*>(ks + (32 * kt + lq) * KP + 16 * c + 8 * lh);
+          st[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[c], st[kt], 0, 0, 0);
+        }
+      }
+      const bool diag = k0 + FK - 1 > a.pos0 + qw;
+      if (diag) {
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+          for (int e = 0; e < 16; ++e)
+            if (k0 + 32 * kt + 8 * (e >> 2) + 4 * lh + (e & 3) > qpos) st[kt][e] = -INFINITY;
+      }
       float mx = -INFINITY;
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        float v = sacc[t][i] * scale;
-        if (diag && k0 + 16 * t + lr > qpos) v = -INFINITY;
-        sacc[t][i] = v;
-        mx = fmaxf(mx, v);
-      }
-      mx = fmaxf(mx, __shfl_xor(mx, 1, 64));
-      mx = fmaxf(mx, __shfl_xor(mx, 2, 64));
-      mx = fmaxf(mx, __shfl_xor(mx, 4, 64));
-      mx = fmaxf(mx, __shfl_xor(mx, 8, 64));
-      rmax[i] = mx;
-    }
-    bf16_t* ps = Ps[wv];
+      for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const float mn = fmaxf(m[i], rmax[i]);
-      // rows with no visible key yet keep m = -inf and contribute nothing
-      const float corr = mn == -INFINITY ? 1.f : __expf(m[i] - mn);
+        for (int e = 0; e < 16; ++e) mx = fmaxf(mx, st[kt][e]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+      const float mn = fmaxf(m, mx);
+      // a query with no visible key yet keeps m = -inf and contributes nothing
+      const bool none = mn == -INFINITY;
+      const float corr = none ? 1.f : __builtin_amdgcn_exp2f((m - mn) * c2);
+      const float off = none ? 0.f : mn * c2;
       float sum = 0.f;
 #pragma unroll
-      for (int t = 0; t < 4; ++t) {
-        const float p = mn == -INFINITY ? 0.f : __expf(sacc[t][i] - mn);
-        sum += p;
-        ps[(4 * lg + i) * PP + 16 * t + lr] = f2bf(p);
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const float p = __builtin_amdgcn_exp2f(fmaf(st[kt][e], c2, -off));
+          st[kt][e] = p;
+          sum += p;
+        }
+      sum += __shfl_xor(sum, 32, 64);
+      l = l * corr + sum;
+      m = mn;
+      if (__any(corr != 1.f)) {   // the running max moved for some query of this wave
+#pragma unroll
+        for (int t = 0; t < 4; ++t) ot[t] *= corr;
       }
-      sum += __shfl_xor(sum, 1, 64);
-      sum += __shfl_xor(sum, 2, 64);
-      sum += __shfl_xor(sum, 4, 64);
-      sum += __shfl_xor(sum, 8, 64);
-      l[i] = l[i] * corr + sum;
-      m[i] = mn;
+      // key step s covers keys 16s..16s+15 of the block: lane lh = 0 needs
+      // 16s..+7, lh = 1 needs 16s+8..+15.  In tile kt = s/2 a lane holds
+      // groups g of 4 keys (8g + 4*lh ..); group g0 = 2*(s%2) and g0+1 are
+      // split between the two lanes, which trade one group each.
 #pragma unroll
-      for (int t = 0; t < 8; ++t) o[t][i] *= corr;
-    }
-    // the P tile is private to this wave; its writes precede these reads
-    __builtin_amdgcn_wave_barrier();
+      for (int s = 0; s < 4; ++s) {
+        const int kt = s >> 1, g0 = 2 * (s & 1);
+        const uint32_t a0 = pack_bf16(st[kt][4 * g0 + 0], st[kt][4 * g0 + 1]);
+        const uint32_t a1 = pack_bf16(st[kt][4 * g0 + 2], st[kt][4 * g0 + 3]);
+        const uint32_t b0 = pack_bf16(st[kt][4 * g0 + 4], st[kt][4 * g0 + 5]);
+        const uint32_t b1 = pack_bf16(st[kt][4 * g0 + 6], st[kt][4 * g0 + 7]);
+        const uint32_t s0 = lh ? a0 : b0, s1 = lh ? a1 : b1;
+        const uint32_t r0 = uint32_t(__shfl_xor(int(s0), 32, 64)), r1 = uint32_t(__shfl_xor(int(s1), 32, 64));
+        const u32x4v pf = lh ? u32x4v{r0, r1, b0, b1} : u32x4v{a0, a1, r0, r1};
+        const bf16x8 pb = __builtin_bit_cast(bf16x8, pf);
 #pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      const bf16x8 pa = *reinterpret_cast<const bf16x8*>(ps + lr * PP + 32 * c + 8 * lg);
-#pragma unroll
-      for (int t = 0; t < 8; ++t) {
-        const bf16x8 vb = *reinterpret_cast<const bf16x8*>(Vt + (16 * t + lr) * VP + 32 * c + 8 * lg);
-        o[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(pa, vb, o[t], 0, 0, 0);
+        for (int dt = 0; dt < 4; ++dt) {
+          const bf16x8 vf = *reinterpret_cast<const bf16x8*>(vt + (32 * dt + lq) * VP + 16 * s + 8 * lh);
+          ot[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb, ot[dt], 0, 0, 0);
+        }
       }
     }
-    __builtin_amdgcn_wave_barrier();
+    // the other buffer was last read before the previous barrier
+    if (more) stage(buf ^ 1);
+    __syncthreads();
   }
+  if (qr < a.S) {
+    const float inv = 1.f / l;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int64_t q = q0 + 16 * wv + 4 * lg + i;
-    if (q >= a.S) continue;
-    const float inv = 1.f / l[i];
+    for (int dt = 0; dt < 4; ++dt)
 #pragma unroll
-    for (int t = 0; t < 8; ++t) O[q * a.o_rs + 16 * t + lr] = f2bf(o[t][i] * inv);
+      for (int e = 0; e < 16; ++e)
+        O[qr * a.o_rs + 32 * dt + 8 * (e >> 2) + 4 * lh + (e & 3)] = f2bf(ot[dt][e] * inv);
   }
 }
 
@@ -342,7 +384,7 @@ hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
   }
   if (a.bf16 && a.d == 128) {
     const int64_t nqb = (a.S + FQ - 1) / FQ;
-    hipLaunchKernelGGL(attn_prefill_d128, dim3(unsigned(a.B * a.nH * nqb)), dim3(256), 0, s, a, nqb);
+    hipLaunchKernelGGL(attn_prefill_d128, dim3(unsigned(a.B * a.nH * nqb)), dim3(64 * FW), kFlashLds, s, a, nqb);
     return hipGetLastError();
   }
   dim3 grid(unsigned((rows + 3) / 4));
