@@ -185,29 +185,31 @@ __global__ void __launch_bounds__(256) attn_decode_d128(AttnArgs a) {
 //     2 key tiles x 8 dim steps of v_mfma_f32_32x32x16_bf16 per 64-key block;
 //   online softmax: a query's 64 scores sit in lanes l and l+32 (32 each), so
 //     its max and sum are one exchange between the two;
-//   O^T += V^T P^T: A = a 32-dim x 16-key fragment of V transposed (LDS),
-//     B = P^T assembled in registers (each lane trades four values with its
-//     partner lane), 4 dim tiles x 4 key steps per block.
-// Each 1 KB fragment read from LDS feeds a 32x32x16 MFMA (32k flop).  Keys go
-// in blocks of 64 through two LDS buffers: the next block loads into
-// registers while this one is consumed and is written to the other buffer
-// afterwards (one barrier per block).  A wave skips blocks wholly past its
-// queries; only blocks crossing its diagonal are masked.  Heaviest query
-// blocks are dispatched first.
+//   O^T += V^T P^T: A = a 32-dim x 16-key fragment of V^T, read from the
+//     row-major V tile with the LDS transpose read (ds_read_b64_tr_b16: within
+//     each 16-lane group, lane 4a+b receives element b of the 8-byte rows that
+//     lanes a, a+4, a+8, a+12 address), B = P^T assembled in registers (each
+//     lane trades four values with its partner lane); 4 dim tiles x 4 key
+//     steps per block.
+// K and V blocks of 64 keys go from global memory straight into one of two
+// LDS buffers (16-byte global_load_lds; a 256-byte row's chunks are permuted
+// by a row-dependent XOR that keeps fragment and transpose reads free of bank
+// conflicts); the next block streams in while this one is consumed, one
+// barrier per block.  Rows past the last visible key are clamped to it: those
+// keys are masked, so they contribute exactly zero.  A wave skips blocks
+// wholly past its queries; only blocks crossing its diagonal are masked.
+// Heaviest query blocks are dispatched first.
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2v __attribute__((ext_vector_type(2)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
 
 constexpr int FW = 4;          // waves per workgroup
 constexpr int FQ = 32 * FW;    // queries per workgroup
 constexpr int FK = 64, FD = 128;
-constexpr int KP = FD + 8;     // K tile pitch (elements): rows 272 B apart
-constexpr int VP = FK + 8;     // transposed V tile pitch: rows 144 B apart
-constexpr int KS = FK * KP, VS = FD * VP;   // elements per tile
-constexpr size_t kFlashLds = size_t(2 * KS + 2 * VS) * sizeof(bf16_t);
-
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+constexpr int TS = FK * FD;    // elements per K or V tile (rows of 256 bytes)
+constexpr size_t kFlashLds = size_t(4 * TS) * sizeof(bf16_t);   // K and V, two buffers each
 
 // two floats to bf16 (round to nearest even, one conversion instruction)
 __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
@@ -215,10 +217,37 @@ __device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, v);
 }
 
+// Slot of a 16-byte chunk in a 256-byte tile row: chunk ^ kv_swz(row).  A K
+// fragment read takes one chunk of 16 aligned consecutive rows per pass; a V
+// transpose read takes 4 chunks of 4 consecutive rows.  Rotating the row's
+// low nibble by two bits gives both patterns 16 distinct slots (no LDS bank
+// conflicts; rows 256 bytes apart all start on the same bank).
+__device__ __forceinline__ int kv_swz(int row) { return ((row & 3) << 2) | ((row >> 2) & 3); }
+
+// element offset of (row, dim) in a swizzled 64 x 128 tile
+__device__ __forceinline__ int tile_at(int row, int dim) {
+  return row * FD + (((dim >> 3) ^ kv_swz(row)) << 3) + (dim & 7);
+}
+
+// One 64-key block of K or V rows k0.. into an LDS tile: wave wv fills rows
+// 16*i + 4*wv .. +3 for i = 0..3 (1 KB per instruction); lane l fills row
+// +l/16, slot l % 16 with the row's chunk (l % 16) ^ kv_swz(row).
+__device__ __forceinline__ void load_kv(bf16_t* tile, const bf16_t* __restrict__ G, int64_t rs, int64_t k0,
+                                        int64_t klast, int wv, int lane) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int r0 = 16 * i + 4 * wv;
+    const int row = r0 + (lane >> 4);
+    const int64_t key = k0 + row <= klast ? k0 + row : klast;
+    const int chunk = (lane & 15) ^ kv_swz(row);
+    __builtin_amdgcn_global_load_lds(G + key * rs + 8 * chunk, tile + r0 * FD, 16, 0, 0);
+  }
+}
+
 __global__ void __launch_bounds__(64 * FW, 2) attn_prefill_d128(AttnArgs a, int64_t nqb) {
   extern __shared__ __align__(16) bf16_t fsm[];
-  bf16_t* Ks = fsm;                 // [2][FK][KP]
-  bf16_t* Vt = fsm + 2 * KS;        // [2][FD][VP]
+  bf16_t* Ks = fsm;                 // [2][FK][FD]
+  bf16_t* Vs = fsm + 2 * TS;        // [2][FK][FD]
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int lq = lane & 31, lh = lane >> 5;
   const int64_t wg = blockIdx.x;
@@ -252,117 +281,96 @@ __global__ void __launch_bounds__(64 * FW, 2) attn_prefill_d128(AttnArgs a, int6
   const int64_t klast = a.pos0 + qlast;
   const int64_t wlast = a.pos0 + qw + 31;
 
-  // staging: thread t moves dims 8*(t%16)..+7 of keys 4*(t/16)..+3
-  const int sc = 8 * (tid & 15), sk = 4 * (tid >> 4);
-  u32x4v kr[4], vr[4];
-  auto fetch = [&](int64_t k0) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int64_t key = k0 + sk + j;
-      kr[j] = u32x4v{0u, 0u, 0u, 0u};
-      vr[j] = u32x4v{0u, 0u, 0u, 0u};
-      if (key <= klast) {
-        kr[j] = *reinterpret_cast<const u32x4v*>(Kg + key * a.kv_rs + sc);
-        vr[j] = *reinterpret_cast<const u32x4v*>(Vg + key * a.kv_rs + sc);
-      }
-    }
-  };
-  auto stage = [&](int buf) {
-    bf16_t* ks = Ks + buf * KS;
-    bf16_t* vt = Vt + buf * VS;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) *reinterpret_cast<u32x4v*>(ks + (sk + j) * KP + sc) = kr[j];
-    // V transposed: dim sc + i of keys sk..sk+3 is one 8-byte row piece
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const u32x2v lo = {(vr[0][e] & 0xffffu) | (vr[1][e] << 16), (vr[2][e] & 0xffffu) | (vr[3][e] << 16)};
-      const u32x2v hi = {(vr[0][e] >> 16) | (vr[1][e] & 0xffff0000u), (vr[2][e] >> 16) | (vr[3][e] & 0xffff0000u)};
-      *reinterpret_cast<u32x2v*>(vt + (sc + 2 * e) * VP + sk) = lo;
-      *reinterpret_cast<u32x2v*>(vt + (sc + 2 * e + 1) * VP + sk) = hi;
-    }
-  };
-
-  fetch(0);
-  stage(0);
-  __syncthreads();
+  // transpose-read address of this lane as a source: row +(j/4), dims +4*(j%4)
+  const int tg = lane >> 4, tj = lane & 15;
+  load_kv(Ks, Kg, a.kv_rs, 0, klast, wv, lane);
+  load_kv(Vs, Vg, a.kv_rs, 0, klast, wv, lane);
   int buf = 0;
   for (int64_t k0 = 0; k0 <= klast; k0 += FK, buf ^= 1) {
-    const bool more = k0 + FK <= klast;
-    if (more) fetch(k0 + FK);   // in flight while this block is consumed
-    if (k0 <= wlast) {
-      const bf16_t* ks = Ks + buf * KS;
-      const bf16_t* vt = Vt + buf * VS;
-      // S^T tile kt: element e is key k0 + 32*kt + 8*(e/4) + 4*lh + e%4 of this lane's query
-      f32x16 st[2];
+    __builtin_amdgcn_s_waitcnt(0);   // this wave's loads of the block have landed
+    __syncthreads();                 // ... and every other wave's; the other buffer is free
+    asm volatile("" ::: "memory");   // LDS now holds data written outside the compiler's view
+    if (k0 + FK <= klast) {
+      load_kv(Ks + (buf ^ 1) * TS, Kg, a.kv_rs, k0 + FK, klast, wv, lane);
+      load_kv(Vs + (buf ^ 1) * TS, Vg, a.kv_rs, k0 + FK, klast, wv, lane);
+    }
+    if (k0 > wlast) continue;
+    const bf16_t* ks = Ks + buf * TS;
+    const bf16_t* vs = Vs + buf * TS;
+    // S^T tile kt: element e is key k0 + 32*kt + 8*(e/4) + 4*lh + e%4 of this lane's query
+    f32x16 st[2];
 #pragma unroll
-      for (int kt = 0; kt < 2; ++kt) {
-        st[kt] = f32x16{};
+    for (int kt = 0; kt < 2; ++kt) {
+      st[kt] = f32x16{};
 #pragma unroll
-        for (int c = 0; c < 8; ++c) {
-          const bf16x8 kf = *reinterpret_cast<const bf16x8*>(ks + (32 * kt + lq) * KP + 16 * c + 8 * lh);
-          st[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[c], st[kt], 0, 0, 0);
-        }
-      }
-      const bool diag = k0 + FK - 1 > a.pos0 + qw;
-      if (diag) {
-#pragma unroll
-        for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-          for (int e = 0; e < 16; ++e)
-            if (k0 + 32 * kt + 8 * (e >> 2) + 4 * lh + (e & 3) > qpos) st[kt][e] = -INFINITY;
-      }
-      float mx = -INFINITY;
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) mx = fmaxf(mx, st[kt][e]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-      const float mn = fmaxf(m, mx);
-      // a query with no visible key yet keeps m = -inf and contributes nothing
-      const bool none = mn == -INFINITY;
-      const float corr = none ? 1.f : __builtin_amdgcn_exp2f((m - mn) * c2);
-      const float off = none ? 0.f : mn * c2;
-      float sum = 0.f;
-#pragma unroll
-      for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const float p = __builtin_amdgcn_exp2f(fmaf(st[kt][e], c2, -off));
-          st[kt][e] = p;
-          sum += p;
-        }
-      sum += __shfl_xor(sum, 32, 64);
-      l = l * corr + sum;
-      m = mn;
-      if (__any(corr != 1.f)) {   // the running max moved for some query of this wave
-#pragma unroll
-        for (int t = 0; t < 4; ++t) ot[t] *= corr;
-      }
-      // key step s covers keys 16s..16s+15 of the block: lane lh = 0 needs
-      // 16s..+7, lh = 1 needs 16s+8..+15.  In tile kt = s/2 a lane holds
-      // groups g of 4 keys (8g + 4*lh ..); group g0 = 2*(s%2) and g0+1 are
-      // split between the two lanes, which trade one group each.
-#pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        const int kt = s >> 1, g0 = 2 * (s & 1);
-        const uint32_t a0 = pack_bf16(st[kt][4 * g0 + 0], st[kt][4 * g0 + 1]);
-        const uint32_t a1 = pack_bf16(st[kt][4 * g0 + 2], st[kt][4 * g0 + 3]);
-        const uint32_t b0 = pack_bf16(st[kt][4 * g0 + 4], st[kt][4 * g0 + 5]);
-        const uint32_t b1 = pack_bf16(st[kt][4 * g0 + 6], st[kt][4 * g0 + 7]);
-        const uint32_t s0 = lh ? a0 : b0, s1 = lh ? a1 : b1;
-        const uint32_t r0 = uint32_t(__shfl_xor(int(s0), 32, 64)), r1 = uint32_t(__shfl_xor(int(s1), 32, 64));
-        const u32x4v pf = lh ? u32x4v{r0, r1, b0, b1} : u32x4v{a0, a1, r0, r1};
-        const bf16x8 pb = __builtin_bit_cast(bf16x8, pf);
-#pragma unroll
-        for (int dt = 0; dt < 4; ++dt) {
-          const bf16x8 vf = *reinterpret_cast<const bf16x8*>(vt + (32 * dt + lq) * VP + 16 * s + 8 * lh);
-          ot[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb, ot[dt], 0, 0, 0);
-        }
+      for (int c = 0; c < 8; ++c) {
+        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(ks + tile_at(32 * kt + lq, 16 * c + 8 * lh));
+        st[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[c], st[kt], 0, 0, 0);
       }
     }
-    // the other buffer was last read before the previous barrier
-    if (more) stage(buf ^ 1);
-    __syncthreads();
+    if (k0 + FK - 1 > a.pos0 + qw) {   // the block crosses this wave's diagonal
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int e = 0; e < 16; ++e)
+          if (k0 + 32 * kt + 8 * (e >> 2) + 4 * lh + (e & 3) > qpos) st[kt][e] = -INFINITY;
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, st[kt][e]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float mn = fmaxf(m, mx);
+    // a query with no visible key yet keeps m = -inf and contributes nothing
+    const bool none = mn == -INFINITY;
+    const float corr = none ? 1.f : __builtin_amdgcn_exp2f((m - mn) * c2);
+    const float off = none ? 0.f : mn * c2;
+    float sum = 0.f;
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const float p = __builtin_amdgcn_exp2f(fmaf(st[kt][e], c2, -off));
+        st[kt][e] = p;
+        sum += p;
+      }
+    sum += __shfl_xor(sum, 32, 64);
+    l = l * corr + sum;
+    m = mn;
+    if (__any(corr != 1.f)) {   // the running max moved for some query of this wave
+#pragma unroll
+      for (int t = 0; t < 4; ++t) ot[t] *= corr;
+    }
+    // key step s covers keys 16s..16s+15 of the block: lane lh = 0 needs
+    // 16s..+7, lh = 1 needs 16s+8..+15.  In tile kt = s/2 a lane holds
+    // groups g of 4 keys (8g + 4*lh ..); group g0 = 2*(s%2) and g0+1 are
+    // split between the two lanes, which trade one group each.
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const int kt = s >> 1, g0 = 2 * (s & 1);
+      const uint32_t a0 = pack_bf16(st[kt][4 * g0 + 0], st[kt][4 * g0 + 1]);
+      const uint32_t a1 = pack_bf16(st[kt][4 * g0 + 2], st[kt][4 * g0 + 3]);
+      const uint32_t b0 = pack_bf16(st[kt][4 * g0 + 4], st[kt][4 * g0 + 5]);
+      const uint32_t b1 = pack_bf16(st[kt][4 * g0 + 6], st[kt][4 * g0 + 7]);
+      const uint32_t s0 = lh ? a0 : b0, s1 = lh ? a1 : b1;
+      const uint32_t r0 = uint32_t(__shfl_xor(int(s0), 32, 64)), r1 = uint32_t(__shfl_xor(int(s1), 32, 64));
+      const u32x4v pf = lh ? u32x4v{r0, r1, b0, b1} : u32x4v{a0, a1, r0, r1};
+      const bf16x8 pb = __builtin_bit_cast(bf16x8, pf);
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) {
+        // V^T fragment: dim 32*dt + lq, keys 16s + 8*lh + 0..7, as two transpose reads
+        const int row = 16 * s + 8 * (tg >> 1) + (tj >> 2);
+        const int dim = 32 * dt + 16 * (tg & 1) + 4 * (tj & 3);
+        typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+        const i16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vs + tile_at(row, dim)));
+        const i16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vs + tile_at(row + 4, dim)));
+        typedef short i16x8 __attribute__((ext_vector_type(8)));
+        const i16x8 vv = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
+        const bf16x8 vf = __builtin_bit_cast(bf16x8, vv);
+        ot[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb, ot[dt], 0, 0, 0);
+      }
+    }
   }
   if (qr < a.S) {
     const float inv = 1.f / l;

@@ -9,8 +9,8 @@
 // global_load_lds, no register staging), two stages deep: the next K step
 // streams in while the current one feeds the matrix cores.  One wave
 // instruction fills 8 rows x 128 bytes of a stage; within a row the eight
-// 16-byte chunks are stored at slot chunk ^ (row & 7), which spreads a
-// fragment read (32 rows, one chunk) over the LDS banks.  Rows past M or N are
+// 16-byte chunks are stored at slot chunk ^ ((row >> 1) & 7), which keeps a
+// fragment read (32 rows, one chunk) free of LDS bank conflicts.  Rows past M or N are
 // clamped to the last row (every load stays in bounds) and their results are
 // dropped by the epilogue; K must be a multiple of 64.
 #include <hip/hip_runtime.h>
@@ -31,6 +31,12 @@ constexpr int kBK = 64;      // K elements per stage row (128 bytes)
 constexpr int kXcd = 8;
 constexpr int kGroupM = 8;
 
+// LDS slot of a 16-byte chunk: chunk ^ swz(row).  A fragment read takes one
+// chunk of 32 consecutive rows, served 16 rows at a time over 256 bytes of
+// banks (two 128-byte rows); (row >> 1) & 7 gives 16 consecutive rows 16
+// distinct (row parity, slot) pairs, so the read is free of bank conflicts.
+__device__ __forceinline__ int swz(int row) { return (row >> 1) & 7; }
+
 template <int EPI>
 struct Shape {
   static constexpr bool kDual = EPI == EPI_SWIGLU;
@@ -42,7 +48,7 @@ struct Shape {
 
 // One K step of operand rows into LDS stage buf.  Wave wv fills the 8-row
 // blocks wv, wv + 4, ...; lane l fills row 8 * block + l / 8 at slot l % 8
-// with the row's chunk (l % 8) ^ (row & 7).  A device function, not a lambda:
+// with the row's chunk (l % 8) ^ swz(row).  A device function, not a lambda:
 // the LDS-load builtin exists only in the device pass.
 template <int EPI>
 __device__ __forceinline__ void load_stage(bf16_t* smem, const bf16_t* __restrict__ A, const bf16_t* __restrict__ W,
@@ -68,7 +74,7 @@ __device__ __forceinline__ void load_stage(bf16_t* smem, const bf16_t* __restric
       const int64_t r = n0 + (second ? wrow - BN : wrow);
       src = (second ? W2 : W) + (r < N ? r : N - 1) * K;
     }
-    const int chunk = slot ^ (row & 7);
+    const int chunk = slot ^ swz(row);
     __builtin_amdgcn_global_load_lds(src + k0 + 8 * chunk, base + 8 * b * kBK, 16, 0, 0);
   }
 }
@@ -122,15 +128,15 @@ __global__ void __launch_bounds__(256) gemm_big(const bf16_t* __restrict__ A, co
 #pragma unroll
       for (int i = 0; i < TM; ++i) {
         const int row = wm * 32 * TM + 32 * i + lr;
-        a[i] = *reinterpret_cast<const bf16x8*>(stg + row * kBK + 8 * (c ^ (row & 7)));
+        a[i] = *reinterpret_cast<const bf16x8*>(stg + row * kBK + 8 * (c ^ swz(row)));
       }
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
         const int row = BM + wn * 32 * TN + 32 * j + lr;
-        b[j] = *reinterpret_cast<const bf16x8*>(stg + row * kBK + 8 * (c ^ (row & 7)));
+        b[j] = *reinterpret_cast<const bf16x8*>(stg + row * kBK + 8 * (c ^ swz(row)));
         if constexpr (DUAL) {
           const int row2 = row + BN;
-          b2[j] = *reinterpret_cast<const bf16x8*>(stg + row2 * kBK + 8 * (c ^ (row2 & 7)));
+          b2[j] = *reinterpret_cast<const bf16x8*>(stg + row2 * kBK + 8 * (c ^ swz(row2)));
         }
       }
 #pragma unroll
