@@ -1,9 +1,11 @@
 // Large prefill GEMM on bf16 matrix cores: C[M,N] (epilogue) = A[M,K] W[N,K]^T.
 //
 // Workgroup tile 256 x 256 (256 x 128 per weight for the two-weight SwiGLU
-// epilogue), K step 64, four waves in a 2 x 2 grid; each wave owns 4 x 4
-// (4 x 2 per weight) tiles of v_mfma_f32_32x32x16_bf16, so one fragment read
-// from LDS feeds four matrix-core instructions.
+// epilogue), K step 64, eight waves in a 2 x 4 grid (two per SIMD, which hide
+// each other's LDS and barrier waits); each wave owns 4 x 2 (4 x 1 per weight)
+// tiles of v_mfma_f32_32x32x16_bf16.  Within a K step the fragments of the
+// next 16-wide sub-step are read from LDS while the current sub-step's MFMAs
+// run, interleaved by scheduling barriers.
 //
 // Operand tiles go from global memory straight into LDS (16-byte
 // global_load_lds, no register staging), two stages deep: the next K step
@@ -37,17 +39,19 @@ constexpr int kGroupM = 8;
 // distinct (row parity, slot) pairs, so the read is free of bank conflicts.
 __device__ __forceinline__ int swz(int row) { return (row >> 1) & 7; }
 
+constexpr int kWaves = 8, kWN = 4;   // 2 x 4 waves
+
 template <int EPI>
 struct Shape {
   static constexpr bool kDual = EPI == EPI_SWIGLU;
-  static constexpr int kTM = 4, kTN = kDual ? 2 : 4;          // 32x32 tiles per wave (per weight)
-  static constexpr int kBM = 2 * 32 * kTM, kBN = 2 * 32 * kTN;
+  static constexpr int kTM = 4, kTN = kDual ? 1 : 2;          // 32x32 tiles per wave (per weight)
+  static constexpr int kBM = 2 * 32 * kTM, kBN = kWN * 32 * kTN;
   static constexpr int kRows = kBM + (kDual ? 2 : 1) * kBN;   // rows staged per K step
   static constexpr int kStage = kRows * kBK;                   // bf16 elements per stage
 };
 
 // One K step of operand rows into LDS stage buf.  Wave wv fills the 8-row
-// blocks wv, wv + 4, ...; lane l fills row 8 * block + l / 8 at slot l % 8
+// blocks wv, wv + 8, ...; lane l fills row 8 * block + l / 8 at slot l % 8
 // with the row's chunk (l % 8) ^ swz(row).  A device function, not a lambda:
 // the LDS-load builtin exists only in the device pass.
 template <int EPI>
@@ -57,12 +61,12 @@ __device__ __forceinline__ void load_stage(bf16_t* smem, const bf16_t* __restric
   using S = Shape<EPI>;
   constexpr bool DUAL = S::kDual;
   constexpr int BM = S::kBM, BN = S::kBN;
-  static_assert(S::kRows % 32 == 0, "stage rows split evenly over four waves");
+  static_assert(S::kRows % (8 * kWaves) == 0, "stage rows split evenly over the waves");
   bf16_t* base = smem + buf * S::kStage;
   const int rin = lane >> 3, slot = lane & 7;
 #pragma unroll
-  for (int t = 0; t < S::kRows / 32; ++t) {
-    const int b = wv + 4 * t;
+  for (int t = 0; t < S::kRows / (8 * kWaves); ++t) {
+    const int b = wv + kWaves * t;
     const int row = 8 * b + rin;
     const bf16_t* src;
     if (row < BM) {
@@ -80,7 +84,7 @@ __device__ __forceinline__ void load_stage(bf16_t* smem, const bf16_t* __restric
 }
 
 template <int EPI, class TC>
-__global__ void __launch_bounds__(256) gemm_big(const bf16_t* __restrict__ A, const bf16_t* __restrict__ W,
+__global__ void __launch_bounds__(64 * kWaves) gemm_big(const bf16_t* __restrict__ A, const bf16_t* __restrict__ W,
                                                 const bf16_t* __restrict__ W2, TC* __restrict__ C,
                                                 int64_t M, int64_t N, int64_t K, int tilesN) {
   using S = Shape<EPI>;
@@ -88,7 +92,7 @@ __global__ void __launch_bounds__(256) gemm_big(const bf16_t* __restrict__ A, co
   constexpr int TM = S::kTM, TN = S::kTN, BM = S::kBM, BN = S::kBN;
   extern __shared__ __align__(16) bf16_t smem[];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  const int wm = wv >> 1, wn = wv & 1;
+  const int wm = wv / kWN, wn = wv % kWN;
 
   // tile order: XCD round-robin remap, then groups of kGroupM row-blocks
   const int nwg = gridDim.x, per = nwg / kXcd;
@@ -121,31 +125,47 @@ __global__ void __launch_bounds__(256) gemm_big(const bf16_t* __restrict__ A, co
     asm volatile("" ::: "memory");   // LDS now holds data written outside the compiler's view
     if (kt + 1 < nk) load_stage<EPI>(smem, A, W, W2, M, N, K, m0, n0, wv, lane, int((kt + 1) & 1), (kt + 1) * kBK);
     const bf16_t* stg = smem + int(kt & 1) * S::kStage;
-#pragma unroll
-    for (int ks = 0; ks < kBK / 16; ++ks) {
+    // fragments of sub-step ks into register set q
+    bf16x8 a[2][TM], b[2][TN], b2[2][DUAL ? TN : 1];
+    auto frag = [&](int ks, int q) {
       const int c = 2 * ks + lc;
-      bf16x8 a[TM], b[TN], b2[DUAL ? TN : 1];
 #pragma unroll
       for (int i = 0; i < TM; ++i) {
         const int row = wm * 32 * TM + 32 * i + lr;
-        a[i] = *reinterpret_cast<const bf16x8*>(stg + row * kBK + 8 * (c ^ swz(row)));
+        a[q][i] = *reinterpret_cast<const bf16x8*>(stg + row * kBK + 8 * (c ^ swz(row)));
       }
 #pragma unroll
       for (int j = 0; j < TN; ++j) {
         const int row = BM + wn * 32 * TN + 32 * j + lr;
-        b[j] = *reinterpret_cast<const bf16x8*>(stg + row * kBK + 8 * (c ^ swz(row)));
+        b[q][j] = *reinterpret_cast<const bf16x8*>(stg + row * kBK + 8 * (c ^ swz(row)));
         if constexpr (DUAL) {
           const int row2 = row + BN;
-          b2[j] = *reinterpret_cast<const bf16x8*>(stg + row2 * kBK + 8 * (c ^ swz(row2)));
+          b2[q][j] = *reinterpret_cast<const bf16x8*>(stg + row2 * kBK + 8 * (c ^ swz(row2)));
         }
       }
+    };
+    frag(0, 0);
+#pragma unroll
+    for (int ks = 0; ks < kBK / 16; ++ks) {
+      const int q = ks & 1;
+      if (ks + 1 < kBK / 16) frag(ks + 1, q ^ 1);
 #pragma unroll
       for (int i = 0; i < TM; ++i)
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-          if constexpr (DUAL) acc2[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b2[j], acc2[i][j], 0, 0, 0);
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[q][i], b[q][j], acc[i][j], 0, 0, 0);
+          if constexpr (DUAL) acc2[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[q][i], b2[q][j], acc2[i][j], 0, 0, 0);
         }
+      if (ks + 1 < kBK / 16) {
+        // one fragment read after every MFMA pair (or single MFMA when there are fewer)
+        constexpr int kReads = TM + TN * (DUAL ? 2 : 1), kMfma = TM * TN * (DUAL ? 2 : 1);
+        constexpr int kPer = kMfma / kReads > 0 ? kMfma / kReads : 1;
+#pragma unroll
+        for (int t = 0; t < kReads; ++t) {
+          __builtin_amdgcn_sched_group_barrier(0x008, kPer, 0);   // MFMA
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);      // LDS read
+        }
+      }
     }
   }
 
@@ -180,7 +200,7 @@ hipError_t go(const GemmArgs& g, hipStream_t s) {
   using S = Shape<EPI>;
   const int tilesM = int((g.M + S::kBM - 1) / S::kBM), tilesN = int((g.N + S::kBN - 1) / S::kBN);
   const size_t lds = size_t(2) * S::kStage * sizeof(bf16_t);
-  hipLaunchKernelGGL((gemm_big<EPI, TC>), dim3(unsigned(tilesM * tilesN)), dim3(256), lds, s,
+  hipLaunchKernelGGL((gemm_big<EPI, TC>), dim3(unsigned(tilesM * tilesN)), dim3(64 * kWaves), lds, s,
                      reinterpret_cast<const bf16_t*>(g.a), reinterpret_cast<const bf16_t*>(g.w),
                      reinterpret_cast<const bf16_t*>(g.w2), reinterpret_cast<TC*>(g.c), g.M, g.N, g.K,
                      tilesN);
