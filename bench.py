@@ -64,6 +64,8 @@ def parse():
     ap.add_argument("--no-baseline", action="store_true")
     ap.add_argument("--no-ablation", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-replan", action="store_true",
+                    help="skip the rerun planned from the measured kernel times")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="first run one 256 MiB device-to-device copy kernel (a known-size "
                          "reference for hardware byte counters)")
@@ -242,6 +244,39 @@ def decode_policy(s, w, M, variant, W, K, ref_gen):
             "h2d_bytes_per_step": st["h2d_bytes"] // K, "d2h_bytes_per_step": st["d2h_bytes"] // K,
             "demand_fetches_per_step": round(st["demand_fetches"] / K, 2),
             "tokens_identical": bool((gen == ref_gen[: W + K + 1]).all())}
+
+
+def measured_replan(s, w, dur, guard, rerun):
+    """Runtime monitor: classify again from the kernel durations of the timed
+    run (kernels it did not run keep the analytic class) and plan again.
+    rerun() (which reads the outputs it needs: planning again resets the
+    executor) runs once under the analytic plan and once under the measured
+    one, both with timing off; the analytic plan is restored after.  Returns
+    (static and dynamic class changes, schedule entries changed, analytic
+    result, measured result)."""
+    s.set_policy(variant=4, timing=0, guard=guard)
+    analytic, a_sched = s.ctx.get_classes(), s.ctx.get_schedule()
+    s.ctx.reset()
+    s.restore_inputs()
+    out_a = rerun()
+    times = [max(1, int(round(d * 1e6))) for d in dur] + [0] * (len(w.kernels) - len(dur))
+    s.ctx.set_kernel_times(times)
+    s.ctx.plan()
+    measured, sched = s.ctx.get_classes(), s.ctx.get_schedule()
+    s.ctx.reset()
+    s.restore_inputs()
+    out_m = rerun()
+    s.ctx.set_kernel_times([0] * len(w.kernels))
+    s.ctx.plan()
+    names = ("compute", "memory", "cgi")
+    flips = [{}, {}]
+    for a, m in zip(analytic[: len(dur)], measured[: len(dur)]):
+        for f, x, y in ((flips[0], a[0], m[0]), (flips[1], a[1], m[1])):
+            if x != y:
+                key = f"{names[x]}->{names[y]}"
+                f[key] = f.get(key, 0) + 1
+    moved = sum(1 for x, y in zip(a_sched, sched) if x != y) + abs(len(a_sched) - len(sched))
+    return flips, moved, out_a, out_m
 
 
 def planner_replay(cfg, M, steps):
@@ -460,6 +495,21 @@ def decode_main(args, cfg):
         if not args.no_ablation:
             result["ablation"] = [decode_policy(s, w, M, v, W, Bk, gen_tap) for v in (1, 2, 3)]
             log("ablation: " + ", ".join(f"{a['policy']} {a['value']}" for a in result["ablation"]))
+    if not args.no_replan:
+        Bk = min(args.baseline_steps, K)
+
+        def rerun():
+            r = run_decode(s, w, W, Bk)
+            return r[1], s.read("gen")[: W + Bk + 1].copy()
+        flips, moved, (da, ga), (dm, gm) = measured_replan(s, w, dur, None, rerun)
+        result["measured_replan"] = {
+            "steps": Bk, "unit": "tokens/s", "kernels_timed": len(dur),
+            "analytic_value": round(cfg.batch * Bk / da, 3), "value": round(cfg.batch * Bk / dm, 3),
+            "analytic_ms_per_step": round(da / Bk * 1e3, 3), "ms_per_step": round(dm / Bk * 1e3, 3),
+            "static_class_changes": flips[0], "dynamic_class_changes": flips[1],
+            "schedule_entries_changed": moved,
+            "tokens_identical": bool((gm == gen_tap[: W + Bk + 1]).all() and (ga == gm).all())}
+        log(f"re-planned from measured times: {result['measured_replan']}")
     s.close()
     del s
     torch.cuda.empty_cache()
@@ -611,6 +661,19 @@ def prefill_main(args, cfg):
             "unit": "tokens/s", "ms_per_pass": round(hot_b / I * 1e3, 3),
             "speedup_of_T+A+P": round(hot_b / hot_s, 3),
             "logits_identical": bool((s.read("logits") == logits).all())}
+    if not args.no_replan:
+        def rerun():
+            r = passes(s)
+            return r[1], s.read("logits").copy()
+        flips, moved, (ha, la), (hm, lm) = measured_replan(s, w, dur, PREFILL_GUARD, rerun)
+        result["measured_replan"] = {
+            "unit": "tokens/s", "kernels_timed": len(dur),
+            "analytic_value": round(cfg.tokens * I / ha, 1), "value": round(cfg.tokens * I / hm, 1),
+            "analytic_ms_per_pass": round(ha / I * 1e3, 3), "ms_per_pass": round(hm / I * 1e3, 3),
+            "static_class_changes": flips[0], "dynamic_class_changes": flips[1],
+            "schedule_entries_changed": moved,
+            "logits_identical": bool((lm == logits).all() and (la == logits).all())}
+        log(f"re-planned from measured times: {result['measured_replan']}")
     s.close()
     del s
     torch.cuda.empty_cache()

@@ -201,9 +201,20 @@ auvm_status auvm_set_budget(auvm_ctx* ctx, uint64_t device_bytes, void* device_p
 /* Roofs in flop/s and byte/s (integers).  Default: 2.5e15, 8e12, 64e9. */
 auvm_status auvm_set_roofs(auvm_ctx* ctx, uint64_t peak_flops, uint64_t hbm_Bps, uint64_t link_Bps);
 auvm_status auvm_set_policy(auvm_ctx* ctx, const auvm_policy* policy);
+/* Measured execution time of every kernel of the trace, in nanoseconds (the
+ * runtime monitor's measurements, Sec. IV, Online Executor, Runtime Monitor:
+ * kernel classifications are re-evaluated from measured kernel time).  A
+ * kernel with time t > 0 is CGI-bound iff it has host-resident read bytes X
+ * and X/Bl > t (exact integer test); t = 0 keeps the analytic roofline test.
+ * The static COMPUTE/MEMORY class stays analytic.  n must equal the number of
+ * kernels (AUVM_E_INVAL otherwise).  The current plan is dropped: call
+ * auvm_plan again (which also resets execution) before the next run. */
+auvm_status auvm_set_kernel_times(auvm_ctx* ctx, const uint64_t* t_ns, uint64_t n);
 
 /* Build the transfer schedule for the whole trace (host only, deterministic).
- * AUVM_E_BUDGET / AUVM_E_FRAG / AUVM_E_INVAL as described above. */
+ * AUVM_E_BUDGET / AUVM_E_FRAG / AUVM_E_INVAL as described above.  Then
+ * resets execution as auvm_reset does: device-resident values are forgotten,
+ * so read the outputs of a run (auvm_read_tensor) before planning again. */
 auvm_status auvm_plan(auvm_ctx* ctx);
 
 /* Lend the compute, host-to-device and device-to-host streams (hipStream_t

@@ -82,9 +82,20 @@ def merge_operands(operands):
     return [(t, modes[t]) for t in order]
 
 
-def classify(F, B, X, roofs):
+def classify(F, B, X, roofs, t_ns=0):
+    """Roofline class of a kernel with X host-resident read bytes (Sec. IV-B).
+
+    Analytic (t_ns = 0): CGI iff moving X over the link takes longer than both
+    the compute roof F/P and the HBM roof B/Bh.  With a measured kernel time
+    t_ns > 0 (the runtime monitor's re-classification, Sec. IV, Online
+    Executor): CGI iff the link time X/Bl exceeds it.  Otherwise COMPUTE iff
+    F/P >= B/Bh, else MEMORY.  Exact integer products.
+    """
     P, Bh, Bl = roofs
-    if X > 0 and X * P > F * Bl and X * Bh > B * Bl:
+    if t_ns > 0:
+        if X > 0 and X * 10**9 > t_ns * Bl:
+            return CLS_CGI
+    elif X > 0 and X * P > F * Bl and X * Bh > B * Bl:
         return CLS_CGI
     return CLS_COMPUTE if F * Bh >= B * P else CLS_MEMORY
 
@@ -108,7 +119,9 @@ def plan(tensors, kernels, M, roofs=DEFAULT_ROOFS, variant=VAR_T_A_P, lookahead=
 
     tensors: list of dicts with keys nbytes, dtype, kind, host_init.
     kernels: list of dicts with keys op, shape, operands [(tid, mode)],
-             optional flops / hbm_bytes (0 or missing: analytic cost).
+             optional flops / hbm_bytes (0 or missing: analytic cost) and
+             time_ns (a measured kernel time; 0 or missing: the analytic
+             roofline decides the CGI class, see ``classify``).
     Returns a Result; raises PlanError on E_INVAL / E_BUDGET / E_FRAG.
 
     The full method (T+A+P) is two passes: the demand timeline with
@@ -169,6 +182,7 @@ def _replay(tensors, kernels, M, roofs, variant, lookahead, affinity_w, placemen
             B = B or aB
         FB.append((F, B))
     res.costs = FB
+    tns = [kd.get("time_ns", 0) for kd in kernels]
 
     def nu(t, k):
         i = bisect_left(uses[t], k)
@@ -181,7 +195,7 @@ def _replay(tensors, kernels, M, roofs, variant, lookahead, affinity_w, placemen
     for k in range(K):
         F, B = FB[k]
         X = sum(size[t] for t, m in A[k] if m & MODE_R)
-        res.static_cls.append(classify(F, B, X, roofs))
+        res.static_cls.append(classify(F, B, X, roofs, tns[k]))
 
     # ---- state
     val = [HOST if (t["kind"] == KIND_PARAM or t["host_init"]) else NONE for t in tensors]
@@ -277,7 +291,7 @@ def _replay(tensors, kernels, M, roofs, variant, lookahead, affinity_w, placemen
 
     for k in range(K):
         F, B = FB[k]
-        cls = classify(F, B, x_missing(k), roofs)
+        cls = classify(F, B, x_missing(k), roofs, tns[k])
         res.dyn_cls.append(cls)
         C["class_n"][cls] += 1
         # (ii) demand fetch / allocation of the kernel's operands
@@ -484,7 +498,7 @@ def _retime(tensors, kernels, M, roofs, lookahead, base):
     for k in range(K):
         F, B = base.costs[k]
         X = sum(size[t] for t, m in A[k] if (m & MODE_R) and val[t] == HOST)
-        cls = classify(F, B, X, roofs)
+        cls = classify(F, B, X, roofs, kernels[k].get("time_ns", 0))
         res.dyn_cls.append(cls)
         C["class_n"][cls] += 1
         for u in units[k]:
@@ -512,5 +526,9 @@ def plan_workload(w, M=None, **kw):
     """Convenience: replay on a workloads.trace.Workload."""
     tensors = [dict(nbytes=t.nbytes, dtype=t.dtype, kind=t.kind, host_init=t.host_init)
                for t in w.tensors]
+    times = kw.pop("times", None)
     kernels = [dict(op=k.op, shape=k.shape, operands=k.operands) for k in w.kernels]
+    if times is not None:
+        for kd, t in zip(kernels, times):
+            kd["time_ns"] = int(t)
     return plan(tensors, kernels, w.budget() if M is None else M, **kw)

@@ -167,6 +167,16 @@ auvm_status auvm_set_roofs(auvm_ctx* x, uint64_t P, uint64_t Bh, uint64_t Bl) {
   return AUVM_OK;
 }
 
+auvm_status auvm_set_kernel_times(auvm_ctx* x, const uint64_t* t_ns, uint64_t n) {
+  if (!x) return AUVM_E_INVAL;
+  Ctx& c = x->c;
+  if (n != c.kernels.size()) return fail(x, AUVM_E_INVAL, "one time per kernel of the trace");
+  if (n > 0 && !t_ns) return fail(x, AUVM_E_INVAL, "null times");
+  for (uint64_t k = 0; k < n; ++k) c.kernels[k].time_ns = t_ns[k];
+  c.planned = false;
+  return AUVM_OK;
+}
+
 auvm_status auvm_set_policy(auvm_ctx* x, const auvm_policy* p) {
   if (!x || !p) return AUVM_E_INVAL;
   if (p->variant > AUVM_T_A_P || p->placement > AUVM_PLACE_IDEAL)

@@ -34,6 +34,7 @@ struct Kernel {
   std::vector<uint8_t> modes;
   std::vector<std::pair<int32_t, uint8_t>> acc;  // distinct ids, first-occurrence order, OR-ed modes
   uint64_t flops = 0, hbm = 0;                   // resolved costs
+  uint64_t time_ns = 0;                          // measured time (0: classify analytically)
   uint32_t layer = 0;
 };
 
@@ -67,8 +68,9 @@ void kernel_cost(const Kernel& k, const std::vector<Tensor>& tensors, uint64_t* 
 // Operand count / dtype / size validation of a kernel against its shape
 // (cost.cpp).  Returns an empty string when the kernel is well formed.
 std::string validate_kernel(const Kernel& k, const std::vector<Tensor>& tensors);
-// Roofline class of a kernel with X host-resident read bytes.
-uint8_t classify(uint64_t F, uint64_t B, uint64_t X, const Roofs& r);
+// Roofline class of a kernel with X host-resident read bytes; with a measured
+// kernel time t_ns > 0 the CGI test compares the link time X/Bl with it.
+uint8_t classify(uint64_t F, uint64_t B, uint64_t X, const Roofs& r, uint64_t t_ns = 0);
 
 // The policy (planner.cpp).  Throws PlanError.
 PlanResult plan(const std::vector<Tensor>& tensors, const std::vector<Kernel>& kernels,

@@ -92,10 +92,13 @@ void kernel_cost(const Kernel& k, const std::vector<Tensor>& T, uint64_t* Fo, ui
   *Bo = B;
 }
 
-uint8_t classify(uint64_t F, uint64_t B, uint64_t X, const Roofs& r) {
+uint8_t classify(uint64_t F, uint64_t B, uint64_t X, const Roofs& r, uint64_t t_ns) {
   using u128 = unsigned __int128;
-  if (X > 0 && u128(X) * r.P > u128(F) * r.Bl && u128(X) * r.Bh > u128(B) * r.Bl)
+  if (t_ns > 0) {  // runtime monitor: link time X/Bl against the measured time
+    if (X > 0 && u128(X) * 1000000000u > u128(t_ns) * r.Bl) return AUVM_CLS_CGI;
+  } else if (X > 0 && u128(X) * r.P > u128(F) * r.Bl && u128(X) * r.Bh > u128(B) * r.Bl) {
     return AUVM_CLS_CGI;
+  }
   return u128(F) * r.Bh >= u128(B) * r.P ? AUVM_CLS_COMPUTE : AUVM_CLS_MEMORY;
 }
 

@@ -12,8 +12,9 @@
 // classes as residency changes (Sec. IV-E); LRU eviction and fault-driven
 // migration for the baseline (Sec. II-A, V-A).  Where the paper gives no rule
 // (thresholds, victims, placement, look-ahead) the choices are:
-//  * class: CGI iff X>0, X*P > F*Bl and X*Bh > B*Bl, else COMPUTE iff
-//    F*Bh >= B*P, else MEMORY (exact 128-bit products, ties not CGI);
+//  * class: CGI iff X>0, X*P > F*Bl and X*Bh > B*Bl (with a measured kernel
+//    time t: iff X > 0 and X/Bl > t), else COMPUTE iff F*Bh >= B*P, else
+//    MEMORY (exact 128-bit products, ties not CGI);
 //  * the full method keeps the replacement decisions of farthest-next-use
 //    demand paging (the profile knows the future) and moves each fetch of a
 //    CGI kernel to the earliest boundary at which its pool window can be
@@ -123,7 +124,7 @@ class Replay {
     for (int64_t k = 0; k < K; ++k) {
       const Kernel& kd = K_[k];
       R.static_cls.push_back(0);  // filled by the caller
-      uint8_t cls = classify(kd.flops, kd.hbm, x_missing(kd, size_, val_), roofs_);
+      uint8_t cls = classify(kd.flops, kd.hbm, x_missing(kd, size_, val_), roofs_, kd.time_ns);
       R.dyn_cls.push_back(cls);
       R.counters.class_n[cls]++;
       for (auto& a : kd.acc) mark_[a.first] = k;  // membership in A_k
@@ -542,7 +543,7 @@ PlanResult retime(const std::vector<Tensor>& T, const std::vector<Kernel>& K, co
 
   for (int64_t k = 0; k < nK; ++k) {
     const Kernel& kd = K[k];
-    uint8_t cls = classify(kd.flops, kd.hbm, x_missing(kd, size, val), roofs);
+    uint8_t cls = classify(kd.flops, kd.hbm, x_missing(kd, size, val), roofs, kd.time_ns);
     R.dyn_cls.push_back(cls);
     R.counters.class_n[cls]++;
     for (const Unit& u : units[k]) {
@@ -591,7 +592,7 @@ PlanResult plan(const std::vector<Tensor>& T, const std::vector<Kernel>& K, uint
     uint64_t X = 0;
     for (auto& a : K[k].acc)
       if (a.second & AUVM_R) X += T[a.first].size;
-    base.static_cls[k] = classify(K[k].flops, K[k].hbm, X, roofs);
+    base.static_cls[k] = classify(K[k].flops, K[k].hbm, X, roofs, K[k].time_ns);
   }
   if (pol.variant != AUVM_T_A_P) return base;
   return retime(T, K, roofs, pol.lookahead, base);

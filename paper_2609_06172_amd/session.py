@@ -51,6 +51,23 @@ class Session:
         self.ctx.set_policy(variant, lookahead, affinity_w, placement, validate, timing, guard, bucket)
         self.ctx.plan()
 
+    def measured_kernel_times_ns(self):
+        """Duration of every kernel in the last timed run, integer ns (at least 1)."""
+        dur, _ = self.ctx.get_kernel_times()
+        if len(dur) != len(self.w.kernels):
+            raise RuntimeError(f"{len(dur)} of {len(self.w.kernels)} kernels timed: "
+                               "run every kernel with the timing policy on first")
+        return [max(1, int(round(d * 1e6))) for d in dur]
+
+    def replan_measured(self, times_ns=None):
+        """Runtime monitor (Sec. IV, Online Executor): classify the kernels
+        again from measured durations (default: the last timed run's) and
+        plan again; the executor restarts from an empty pool."""
+        t = self.measured_kernel_times_ns() if times_ns is None else times_ns
+        self.ctx.set_kernel_times(t)
+        self.ctx.plan()
+        return t
+
     # -- host arena access ----------------------------------------------------
     def host_view(self, t):
         """uint8 numpy view of tensor t's host arena window."""

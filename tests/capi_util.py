@@ -5,7 +5,11 @@ from workloads.format import ALIGN, FLAG_HOST_INIT, KIND_PARAM
 
 def plan_ctx(tensors, kernels, M, variant=4, lookahead=0, affinity_w=1, placement=0, roofs=None,
              guard=None, bucket=None):
-    """Register a trace (oracle-style dicts) in a plan-only context and plan it."""
+    """Register a trace (oracle-style dicts) in a plan-only context and plan it.
+
+    Kernels that carry a measured time (time_ns) hand the whole list to
+    set_kernel_times before planning.
+    """
     ctx = Context(-1)
     off = 0
     offs = []
@@ -22,6 +26,9 @@ def plan_ctx(tensors, kernels, M, variant=4, lookahead=0, affinity_w=1, placemen
     if roofs is not None:
         ctx.set_roofs(*roofs)
     ctx.set_policy(variant, lookahead, affinity_w, placement, guard=guard, bucket=bucket)
+    times = [k.get("time_ns", 0) for k in kernels]
+    if any(times):
+        ctx.set_kernel_times(times)
     ctx.plan()
     return ctx
 

@@ -16,18 +16,25 @@ def load_golden():
 def golden_inputs(case):
     tensors = [dict(nbytes=b, dtype=DT_U8, kind=KIND_PARAM if k == "param" else KIND_ACT,
                     host_init=(k == "param")) for b, k in case["tensors"]]
+    n = len(case["kernels"])
+    flops = case.get("flops", [1] * n)
+    times = case.get("times", [0] * n)
     kernels = [dict(op=OP_TOUCH, shape=(0,), operands=[tuple(o) for o in ops],
-                    flops=1, hbm_bytes=1) for ops in case["kernels"]]
+                    flops=f, hbm_bytes=1, time_ns=t)
+               for ops, f, t in zip(case["kernels"], flops, times)]
     return tensors, kernels
 
 
 def random_trace(seed, n_tensors=None, n_kernels=None, max_ops=4, equal=False,
-                 read_only=False, unit=256, touch=False):
+                 read_only=False, unit=256, touch=False, timed=False):
     """Random trace of touch kernels with explicit or analytic costs.
 
     touch=True makes every kernel a well-formed touch op: tensor 0 is a log
     (read-write operand 0 of every kernel, one 64-byte slot per kernel), data
     operands are distinct and their sizes are multiples of 4 bytes.
+    timed=True gives most kernels a measured time (time_ns) drawn around the
+    link time of a few hundred bytes, so both sides of the measured-time rule
+    occur.
     """
     r = random.Random(seed)
     nT = n_tensors or r.randint(1, 40)
@@ -66,6 +73,8 @@ def random_trace(seed, n_tensors=None, n_kernels=None, max_ops=4, equal=False,
             fl, hb = 0, 0
         if touch:
             ops = [(0, 3)] + ops
-        kernels.append(dict(op=OP_TOUCH, shape=(k if touch else 0,), operands=ops,
-                            flops=fl, hbm_bytes=hb))
+        kd = dict(op=OP_TOUCH, shape=(k if touch else 0,), operands=ops, flops=fl, hbm_bytes=hb)
+        if timed and r.random() < 0.8:
+            kd["time_ns"] = r.choice([1, 2, 3, 5, 8, 13, 40, 10**6])
+        kernels.append(kd)
     return tensors, kernels

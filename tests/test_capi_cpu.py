@@ -94,7 +94,8 @@ def test_golden_schedules_through_the_library(case):
     ks = []
     for i, k in enumerate(kernels):
         ops = [(t + 1, m) for t, m in k["operands"]]
-        ks.append(dict(op=OP_TOUCH, shape=(0,), operands=[(0, MODE_RW)] + ops, flops=1, hbm_bytes=1))
+        ks.append(dict(op=OP_TOUCH, shape=(0,), operands=[(0, MODE_RW)] + ops, flops=k["flops"],
+                       hbm_bytes=1, time_ns=k["time_ns"]))
     M = case["M"] + 256
     ctx = plan_ctx(tensors, ks, M, variant=case["variant"], affinity_w=case["affinity_w"],
                    placement=case["placement"], guard=case.get("guard"), bucket=case.get("bucket"))
@@ -181,3 +182,65 @@ def test_library_defines_every_kernel_launch_stub():
     out = subprocess.run([nm, "-D", "--undefined-only", path], capture_output=True, text=True, check=True).stdout
     missing = [l.split()[-1] for l in out.splitlines() if "__device_stub__" in l]
     assert not missing, missing
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_random_timed_traces_bit_exact(seed):
+    # per-kernel measured times (auvm_set_kernel_times) take the oracle's rule
+    tensors, kernels = random_trace(seed, touch=True, timed=True)
+    fp = sum(op.aligned(t["nbytes"]) for t in tensors)
+    rnd = random.Random(1000 + seed)
+    for variant in VARIANTS:
+        M = max(1024, (fp * rnd.choice([1, 2, 3]) // rnd.choice([2, 3, 4])) // 256 * 256)
+        kw = dict(variant=variant, affinity_w=rnd.choice([0, 1, 2]), guard=rnd.choice([None, 0, 3]))
+        try:
+            r = op.plan(tensors, kernels, M, **kw)
+        except op.PlanError as e:
+            with pytest.raises(AuvmError) as ee:
+                plan_ctx(tensors, kernels, M, **kw)
+            assert ee.value.code == e.code
+            continue
+        assert_same_plan(plan_ctx(tensors, kernels, M, **kw), r)
+
+
+def test_set_kernel_times_checks_its_length_and_replans():
+    tensors, kernels = random_trace(3, touch=True, timed=True)
+    fp = sum(op.aligned(t["nbytes"]) for t in tensors)
+    M = max(1024, fp * 3 // 4 // 256 * 256)
+    untimed = [dict(k, time_ns=0) for k in kernels]
+    ctx = plan_ctx(tensors, untimed, M)
+    with pytest.raises(AuvmError) as e:
+        ctx.set_kernel_times([1] * (len(kernels) - 1))
+    assert e.value.code == op.E_INVAL
+    with pytest.raises(AuvmError):
+        ctx.set_kernel_times([1] * (len(kernels) + 1))
+    ctx.set_kernel_times([k.get("time_ns", 0) for k in kernels])
+    ctx.plan()
+    assert_same_plan(ctx, op.plan(tensors, kernels, M))
+    ctx.set_kernel_times([0] * len(kernels))        # back to the analytic classes
+    ctx.plan()
+    assert_same_plan(ctx, op.plan(tensors, untimed, M))
+    ctx.destroy()
+
+
+@pytest.mark.parametrize("name", ["gpt-small", "llama-small", "gpt-1.3b"])
+def test_config_traces_with_measured_times_bit_exact(name):
+    # times scattered around the link time of each kernel's read operands, so
+    # that kernels change class both ways
+    from paper_2609_06172_amd.session import Session
+    cfg = configs.CONFIGS[name]
+    w = trace.build(cfg)
+    s = Session(w, device=-1)
+    _, _, Bl = op.DEFAULT_ROOFS
+    rnd = random.Random(7)
+    times = []
+    for k in w.kernels:
+        X = sum(op.aligned(w.tensors[t].nbytes) for t, m in k.operands if m & MODE_R)
+        times.append(max(1, int(X * 10**9 // Bl * rnd.choice([0.3, 0.9, 1.1, 3.0]))))
+    s.replan_measured(times)
+    r = op.plan_workload(w, s.M, times=times)
+    assert_same_plan(s.ctx, r)
+    base = op.plan_workload(w, s.M)
+    assert any(a != b for a, b in zip(r.static_cls, base.static_cls))
+    assert r.schedule != base.schedule
+    s.close()

@@ -97,3 +97,24 @@ def test_outputs_do_not_depend_on_the_policy():
         assert np.array_equal(gen, runs[0][2])
         for a, b in zip(logits, runs[0][1]):
             assert np.array_equal(a, b)
+
+
+def test_replanning_from_measured_kernel_times():
+    # runtime monitor: a timed run, classes again from the measured
+    # durations, a new plan (the oracle's, bit for bit), the same outputs
+    from oracle import planner as op
+    from capi_util import assert_same_plan
+    cfg = configs.LLAMA_SMALL
+    print("llama-small: timed run, re-plan from measured kernel times, rerun", flush=True)
+    s, w = _session(cfg, timing=1)
+    s.run_all()
+    gen, logits = s.read("gen"), s.read("logits")
+    t = s.replan_measured()
+    assert len(t) == len(w.kernels) and min(t) >= 1
+    assert_same_plan(s.ctx, op.plan_workload(w, s.M, times=t))
+    s.restore_inputs()
+    s.run_all()
+    assert np.array_equal(s.read("gen"), gen)
+    assert np.array_equal(s.read("logits"), logits)
+    assert s.ctx.get_executed() == s.ctx.get_schedule()
+    s.close()

@@ -237,3 +237,93 @@ def test_ablation_ladder_directions_on_cyclic_decoder():
     moved = sum(e[3] for e in r_tap.schedule
                 if e[0] in (S_H2D_DEMAND, S_H2D_PREFETCH) and k0 <= e[4] < k0 + n)
     assert moved >= lmin
+
+
+# ---- measured kernel times (the runtime monitor's re-classification, Sec. IV)
+
+def test_classify_measured_time_closed_form():
+    roofs = op.DEFAULT_ROOFS          # Bl = 6.4e10 B/s: 64 bytes per ns on the link
+    # link time of X bytes vs the measured time: a tie is not CGI
+    assert op.classify(1, 1, 64_000, roofs, 1000) != CLS_CGI
+    assert op.classify(1, 1, 64_001, roofs, 1000) == CLS_CGI
+    # nothing missing is never CGI, however short the kernel
+    assert op.classify(1, 1, 0, roofs, 1) == CLS_MEMORY
+    # a measured time overrides the analytic roofs either way: a huge GEMM
+    # (analytically COMPUTE) that ran in 1 us while 1 MB was missing ...
+    F, B = 2 * 4096 ** 3, 3 * 4096 * 4096 * 2
+    assert op.classify(F, B, 1 << 20, roofs) == CLS_COMPUTE
+    assert op.classify(F, B, 1 << 20, roofs, 1000) == CLS_CGI
+    # ... and a 1-flop kernel missing 32 MiB (analytically CGI) that took a second
+    assert op.classify(1, 1, 32 << 20, roofs) == CLS_CGI
+    assert op.classify(1, 1, 32 << 20, roofs, 10**9) == CLS_MEMORY
+    # below the link time the fallback is the plain roofline comparison
+    assert op.classify(F, B, 1 << 20, roofs, 10**9) == CLS_COMPUTE
+
+
+def _with_times(kernels, t):
+    return [dict(k, time_ns=t(i)) for i, k in enumerate(kernels)]
+
+
+@pytest.mark.parametrize("seed", range(25))
+def test_huge_times_leave_the_demand_timeline(seed):
+    # no kernel is CGI when every kernel took longer than any transfer, so the
+    # full method's second pass moves nothing: with guard 0, unit buckets and
+    # no pins its plan is plain farthest-next-use demand paging
+    tensors, kernels = random_trace(seed, touch=True)
+    kernels = _with_times(kernels, lambda i: 10**15)
+    fp = sum(op.aligned(t["nbytes"]) for t in tensors)
+    for div in (1, 2, 3):
+        M = max(1024, fp // div // 256 * 256)
+        try:
+            ref = op.plan(tensors, kernels, M, variant=VAR_DEMAND_BELADY)
+        except op.PlanError:
+            continue
+        r = op.plan(tensors, kernels, M, variant=VAR_T_A_P, affinity_w=0, guard=0, bucket=1)
+        assert r.schedule == ref.schedule
+        assert r.residency == ref.residency
+        assert r.dyn_cls == ref.dyn_cls
+        assert CLS_CGI not in r.dyn_cls and CLS_CGI not in r.static_cls
+        assert r.counters["h2d_prefetch_n"] == 0
+
+
+@pytest.mark.parametrize("seed", range(25))
+def test_one_ns_times_make_every_fetching_kernel_cgi(seed):
+    # at 1 ns even one 256-byte block takes longer on the link, so under demand
+    # paging a kernel is CGI exactly when the schedule fetches something for it
+    tensors, kernels = random_trace(seed, touch=True)
+    kernels = _with_times(kernels, lambda i: 1)
+    fp = sum(op.aligned(t["nbytes"]) for t in tensors)
+    M = max(1024, fp // 2 // 256 * 256)
+    try:
+        r = op.plan(tensors, kernels, M, variant=VAR_DEMAND_BELADY)
+    except op.PlanError:
+        return
+    fetched = set(e[5] for e in r.schedule if e[0] == S_H2D_DEMAND)
+    for k, c in enumerate(r.dyn_cls):
+        assert (c == CLS_CGI) == (k in fetched), k
+
+
+@pytest.mark.parametrize("seed", range(10))
+def test_zero_times_are_the_analytic_plan(seed):
+    tensors, kernels = random_trace(seed, touch=True)
+    fp = sum(op.aligned(t["nbytes"]) for t in tensors)
+    M = max(1024, fp // 2 // 256 * 256)
+    try:
+        ref = op.plan(tensors, kernels, M)
+    except op.PlanError:
+        return
+    r = op.plan(tensors, _with_times(kernels, lambda i: 0), M)
+    assert r.schedule == ref.schedule and r.dyn_cls == ref.dyn_cls
+
+
+@pytest.mark.parametrize("seed", range(15))
+def test_timed_plans_pass_the_checker(seed):
+    tensors, kernels = random_trace(seed, touch=True, timed=True)
+    fp = sum(op.aligned(t["nbytes"]) for t in tensors)
+    for div in (1, 2, 3):
+        M = max(1024, fp // div // 256 * 256)
+        try:
+            r = op.plan(tensors, kernels, M)
+        except op.PlanError:
+            continue
+        checker.check(tensors, kernels, M, r.schedule)
