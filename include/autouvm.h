@@ -83,13 +83,29 @@ enum { AUVM_R = 1, AUVM_W = 2, AUVM_RW = 3 };
  *                                    cache positions 0..pos0+i
  *  ARGMAX        (B,V,row)           logits R f32[B,V], tok W i32[B], [gen RW i32[.,B]]:
  *                                    lowest index of the row maximum; also gen[row]
+ * Routed-expert (MoE) FFN, top-K of E experts (K <= E <= 16), bf16 weights:
+ *  MOE_ROUTE     (M,H,E,K)           h R [M,H], Wr R [E,H], rte W i32[M,K], rtw W f32[M,K]:
+ *                                    router logits h Wr^T; the K largest (ties: lower
+ *                                    expert index) in descending order, weights the
+ *                                    softmax over the selected logits
+ *  MOE_DISPATCH  (M,E,K,row)         rte R, lists W i32[E, M+1], log RW i32[(row+1)*E]:
+ *                                    lists[e] = count, then the entries j = K*token+slot
+ *                                    with rte[j] == e in increasing j; log[row*E+e] = count
+ *  MOE_UP        (M,F,H,e,n,K)       h R [M,H], lists R, Wg R [F,H], Wu R [F,H], fe W [M,F]:
+ *                                    for i < count(e): fe[i] = silu(h[tok] Wg^T) * (h[tok] Wu^T),
+ *                                    tok = lists[e][1+i] / K; n = routed rows expected by
+ *                                    the trace (cost model only)
+ *  MOE_DOWN      (M,H,F,e,n,K)       fe R, lists R, rtw R, Wd R [H,F], x RW f32[M,H]:
+ *                                    for i < count(e): x[tok] += rtw[j] * (fe[i] Wd^T),
+ *                                    j = lists[e][1+i], tok = j / K
  * Activations between kernels use the tensors' own dtypes (f32 or bf16);
  * arithmetic accumulates in fp32. */
 enum {
   AUVM_OP_TOUCH = 0, AUVM_OP_EMBED = 1, AUVM_OP_LAYERNORM = 2, AUVM_OP_RMSNORM = 3,
   AUVM_OP_LINEAR = 4, AUVM_OP_LINEAR_GELU = 5, AUVM_OP_LINEAR_RESID = 6,
   AUVM_OP_LINEAR_SWIGLU = 7, AUVM_OP_ATTN_QKV = 8, AUVM_OP_ROPE_KV = 9,
-  AUVM_OP_ATTN_CACHE = 10, AUVM_OP_ARGMAX = 11, AUVM_OP_COUNT = 12
+  AUVM_OP_ATTN_CACHE = 10, AUVM_OP_ARGMAX = 11, AUVM_OP_MOE_ROUTE = 12,
+  AUVM_OP_MOE_DISPATCH = 13, AUVM_OP_MOE_UP = 14, AUVM_OP_MOE_DOWN = 15, AUVM_OP_COUNT = 16
 };
 
 /* policy variants: the paper's ablation ladder (T, T+A, T+A+P; Sec. V-E)
@@ -201,6 +217,15 @@ auvm_status auvm_set_budget(auvm_ctx* ctx, uint64_t device_bytes, void* device_p
 /* Roofs in flop/s and byte/s (integers).  Default: 2.5e15, 8e12, 64e9. */
 auvm_status auvm_set_roofs(auvm_ctx* ctx, uint64_t peak_flops, uint64_t hbm_Bps, uint64_t link_Bps);
 auvm_status auvm_set_policy(auvm_ctx* ctx, const auvm_policy* policy);
+/* Drop every kernel and the plan, and reset execution as auvm_reset does;
+ * tensors, host arena contents, budget, roofs and policy stay.  Lets a
+ * caller replace a profiling trace by the trace it recorded (Sec. IV-D,
+ * kernel-tensor access tracing): for routed experts the access lists depend
+ * on the router, so the profiling trace holds every expert and the recorded
+ * one only the experts that were routed rows (Sec. III-A: move only the
+ * tensors a kernel accesses).  Read outputs before calling. */
+auvm_status auvm_clear_kernels(auvm_ctx* ctx);
+
 /* Measured execution time of every kernel of the trace, in nanoseconds (the
  * runtime monitor's measurements, Sec. IV, Online Executor, Runtime Monitor:
  * kernel classifications are re-evaluated from measured kernel time).  A

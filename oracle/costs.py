@@ -9,7 +9,8 @@ is read or written once, a read-modify-write counts twice, and a GEMM costs
 from workloads.format import (DT_SIZE, MODE_RW, OP_ARGMAX, OP_ATTN_CACHE,
                               OP_ATTN_QKV, OP_EMBED, OP_LAYERNORM, OP_LINEAR,
                               OP_LINEAR_GELU, OP_LINEAR_RESID,
-                              OP_LINEAR_SWIGLU, OP_RMSNORM, OP_ROPE_KV,
+                              OP_LINEAR_SWIGLU, OP_MOE_DISPATCH, OP_MOE_DOWN,
+                              OP_MOE_ROUTE, OP_MOE_UP, OP_RMSNORM, OP_ROPE_KV,
                               OP_TOUCH)
 
 
@@ -59,4 +60,17 @@ def kernel_cost(op, shape, operands, dtypes, nbytes):
     if op == OP_ARGMAX:
         Bt, V = sh[0], sh[1]
         return Bt * V, Bt * V * es[0] + 4 * Bt + (4 * Bt if len(operands) > 2 else 0)
+    # routed experts: n is the number of rows the trace expects expert e to see
+    if op == OP_MOE_ROUTE:
+        M, H, E, K = sh[0], sh[1], sh[2], sh[3]
+        return 2 * M * H * E, M * H * es[0] + E * H * es[1] + 8 * M * K
+    if op == OP_MOE_DISPATCH:
+        M, E, K = sh[0], sh[1], sh[2]
+        return 0, 4 * M * K + 4 * (M * K + E) + 8 * E
+    if op == OP_MOE_UP:
+        M, F, H, n = sh[0], sh[1], sh[2], sh[4]
+        return 4 * n * F * H + 4 * n * F, n * H * es[0] + 4 * (n + 1) + F * H * (es[2] + es[3]) + n * F * es[4]
+    if op == OP_MOE_DOWN:
+        M, H, F, n = sh[0], sh[1], sh[2], sh[4]
+        return 2 * n * H * F + 2 * n * H, n * F * es[0] + 4 * (n + 1) + 4 * n + H * F * es[3] + 8 * n * H
     raise ValueError(f"unknown op {op}")

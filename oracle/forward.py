@@ -8,6 +8,10 @@ architecture families the workloads use:
   attention, exact-erf GELU MLP, residual adds, tied LM head.
 * LLaMA style: RMSNorm (eps 1e-6), separate q/k/v/o projections, rotate-half
   RoPE with base 10000, KV cache, SwiGLU MLP, untied LM head, greedy argmax.
+* MoE style: the LLaMA block with its MLP replaced by a routed mixture of
+  SwiGLU experts: router logits h Wr^T, the top-k experts of each token (ties
+  to the lower index), weights the softmax over the selected logits, output
+  the weighted sum of the selected experts' MLPs.
 
 Weights are stored [out, in]; a projection is ``y = x @ W.T``.  Everything is
 computed in the precision of the inputs (fp64 by default), with no blocking or
@@ -121,11 +125,61 @@ def gpt_forward(cfg, Wt, ids):
 
 
 # -------------------------------------------------------------- LLaMA style
-def llama_layer(cfg, Lw, x, K, V, pos0):
-    """One LLaMA block for S new tokens per sequence.
+def route_topk(logits, k):
+    """Top-k routing of router logits [M, E].
+
+    Returns (idx [M, k] int32, weights [M, k]): per row the k largest logits
+    in descending order, equal logits taken by increasing expert index, and
+    the softmax over the selected logits.
+    """
+    M, E = logits.shape
+    idx = np.empty((M, k), np.int32)
+    wts = np.empty((M, k), logits.dtype)
+    for m in range(M):
+        order = sorted(range(E), key=lambda e: (-logits[m, e], e))[:k]
+        sel = logits[m, order]
+        ex = np.exp(sel - sel.max())
+        idx[m] = order
+        wts[m] = ex / ex.sum()
+    return idx, wts
+
+
+def expert_mlp(h, Xw):
+    """One SwiGLU expert: (silu(h Wg^T) * (h Wu^T)) Wd^T."""
+    return linear(silu(linear(h, Xw["wg"])) * linear(h, Xw["wu"]), Xw["wd"])
+
+
+def moe_mlp(cfg, Lw, h, forced=None):
+    """Routed mixture of experts on rows h [M, H].
+
+    ``forced`` [M, k] replaces the expert choice (the weights are still the
+    softmax over this layer's logits at the forced experts).  Returns
+    (output [M, H], idx, weights, logits).
+    """
+    logits = linear(h, Lw["router"])
+    if forced is None:
+        idx, wts = route_topk(logits, cfg.top_k)
+    else:
+        idx = np.asarray(forced, np.int32)
+        sel = np.take_along_axis(logits, idx, axis=1)
+        ex = np.exp(sel - sel.max(axis=1, keepdims=True))
+        wts = ex / ex.sum(axis=1, keepdims=True)
+    y = np.zeros_like(h)
+    for e in range(cfg.n_experts):
+        rows, slots = np.nonzero(idx == e)
+        if rows.size == 0:
+            continue
+        Xw = {n: Lw[f"x{e}.{n}"] for n in ("wg", "wu", "wd")}
+        y[rows] += wts[rows, slots][:, None] * expert_mlp(h[rows], Xw)
+    return y, idx, wts, logits
+
+
+def llama_layer(cfg, Lw, x, K, V, pos0, forced_route=None, route_log=None):
+    """One LLaMA (or MoE) block for S new tokens per sequence.
 
     x [B*S, H]; K, V [B, nH, Lmax, d] caches, updated in place at positions
-    pos0..pos0+S-1.  Lw holds the layer's tensors by short name.
+    pos0..pos0+S-1.  Lw holds the layer's tensors by short name.  For MoE
+    configs the routing (idx, weights, logits) is appended to route_log.
     """
     B, nH, d = cfg.batch, cfg.n_heads, cfg.head_dim
     S = x.shape[0] // B
@@ -145,6 +199,11 @@ def llama_layer(cfg, Lw, x, K, V, pos0):
             o[b, :, i, :] = causal_attention(q[b, :, i, :], K[b, i, :L], V[b, i, :L], pos0)
     x = x + linear(o.reshape(B * S, nH * d), Lw["wo"])
     h = rmsnorm(x, Lw["ffn_norm"])
+    if cfg.style == "moe":
+        y, idx, wts, logits = moe_mlp(cfg, Lw, h, forced_route)
+        if route_log is not None:
+            route_log.append((idx, wts, logits))
+        return x + y
     return x + linear(silu(linear(h, Lw["wg"])) * linear(h, Lw["wu"]), Lw["wd"])
 
 
@@ -158,15 +217,17 @@ def new_cache(cfg, dtype=np.float64):
     return [(np.zeros(shape, dtype), np.zeros(shape, dtype)) for _ in range(cfg.n_layers)]
 
 
-def llama_step(cfg, Wt, cache, x, pos0):
+def llama_step(cfg, Wt, cache, x, pos0, forced_routes=None, route_log=None):
     """Run all layers on embedded tokens x [B*S, H] at positions pos0..; returns
-    (per-layer outputs, logits at the last position of each sequence)."""
+    (per-layer outputs, logits at the last position of each sequence).
+    forced_routes[l] forces layer l's expert choice (MoE)."""
     B = cfg.batch
     S = x.shape[0] // B
     outs = []
     for l in range(cfg.n_layers):
         K, V = cache[l]
-        x = llama_layer(cfg, layer_weights(Wt, l), x, K, V, pos0)
+        fr = None if forced_routes is None else forced_routes[l]
+        x = llama_layer(cfg, layer_weights(Wt, l), x, K, V, pos0, fr, route_log)
         outs.append(x)
     last = x[np.arange(B) * S + S - 1]
     return outs, linear(rmsnorm(last, Wt["norm_f"]), Wt["head"])
@@ -177,22 +238,30 @@ def argmax_lowest(logits):
     return np.argmax(logits, axis=-1).astype(np.int32)
 
 
-def llama_generate(cfg, Wt, ids, forced=None, dtype=np.float64):
+def llama_generate(cfg, Wt, ids, forced=None, dtype=np.float64, forced_routes=None):
     """Prefill ids [B, S] then cfg.decode_steps greedy steps.
 
     If ``forced`` [steps+1, B] is given, step s consumes forced[s] instead of
     its own argmax (teacher forcing); the chosen ids are still returned.
-    Returns dict(prefill_outs, logits=[per step], tokens=[per step]).
+    For MoE configs ``forced_routes[seg][l]`` ([M, k]; seg 0 is the prefill)
+    likewise forces the expert choice.  Returns dict(outs, logits=[per step],
+    tokens=[per step], routes=[per segment: per layer (idx, weights, logits)]).
     """
     B, S = cfg.batch, cfg.prompt_len
     cache = new_cache(cfg, dtype)
     E = Wt["E"]
-    outs, lg = llama_step(cfg, Wt, cache, E[np.asarray(ids).reshape(-1)], 0)
-    logits, tokens, step_outs = [lg], [argmax_lowest(lg)], [outs]
+
+    def fr(seg):
+        return None if forced_routes is None else forced_routes[seg]
+    log = []
+    outs, lg = llama_step(cfg, Wt, cache, E[np.asarray(ids).reshape(-1)], 0, fr(0), log)
+    logits, tokens, step_outs, routes = [lg], [argmax_lowest(lg)], [outs], [log]
     for s in range(cfg.decode_steps):
         t = tokens[-1] if forced is None else np.asarray(forced[s], np.int32)
-        outs, lg = llama_step(cfg, Wt, cache, E[t], S + s)
+        log = []
+        outs, lg = llama_step(cfg, Wt, cache, E[t], S + s, fr(s + 1), log)
         logits.append(lg)
         tokens.append(argmax_lowest(lg))
         step_outs.append(outs)
-    return dict(outs=step_outs, logits=logits, tokens=tokens, cache=cache)
+        routes.append(log)
+    return dict(outs=step_outs, logits=logits, tokens=tokens, cache=cache, routes=routes)

@@ -16,7 +16,7 @@ OK, E_INVAL, E_STATE, E_BUDGET, E_FRAG, E_HIP, E_NOMEM, E_RANGE = 0, -1, -2, -3,
 SYMBOLS = [
     "auvm_create", "auvm_destroy", "auvm_last_error", "auvm_arena_init",
     "auvm_register_tensor", "auvm_tensor_host_ptr", "auvm_add_kernel", "auvm_set_budget",
-    "auvm_set_roofs", "auvm_set_policy", "auvm_set_kernel_times", "auvm_plan", "auvm_bind_streams", "auvm_run",
+    "auvm_set_roofs", "auvm_set_policy", "auvm_set_kernel_times", "auvm_clear_kernels", "auvm_plan", "auvm_bind_streams", "auvm_run",
     "auvm_reset", "auvm_read_tensor", "auvm_get_counters", "auvm_get_schedule",
     "auvm_get_executed", "auvm_get_residency", "auvm_get_classes", "auvm_get_kernel_times",
     "auvm_get_timeline",
@@ -127,6 +127,7 @@ def lib():
         "auvm_set_roofs": (st, [P, C.c_uint64, C.c_uint64, C.c_uint64]),
         "auvm_set_policy": (st, [P, C.POINTER(Policy)]),
         "auvm_set_kernel_times": (st, [P, C.POINTER(C.c_uint64), C.c_uint64]),
+        "auvm_clear_kernels": (st, [P]),
         "auvm_plan": (st, [P]),
         "auvm_bind_streams": (st, [P, P, P, P]),
         "auvm_run": (st, [P, C.c_uint32, C.c_uint32]),
@@ -221,6 +222,10 @@ class Context:
 
     def plan(self):
         self._check(self._L.auvm_plan(self._h))
+
+    def clear_kernels(self):
+        """Drop the trace and the plan (tensors and arena stay); resets execution."""
+        self._check(self._L.auvm_clear_kernels(self._h))
 
     def set_kernel_times(self, t_ns):
         """Measured time per kernel in integer ns (0: analytic class); drops the plan."""

@@ -167,6 +167,19 @@ auvm_status auvm_set_roofs(auvm_ctx* x, uint64_t P, uint64_t Bh, uint64_t Bl) {
   return AUVM_OK;
 }
 
+auvm_status auvm_clear_kernels(auvm_ctx* x) {
+  if (!x) return AUVM_E_INVAL;
+  Ctx& c = x->c;
+  if (c.exec) {
+    auvm_status s = exec_reset(c);
+    if (s != AUVM_OK) return s;
+  }
+  c.kernels.clear();
+  c.plan = PlanResult{};
+  c.planned = false;
+  return AUVM_OK;
+}
+
 auvm_status auvm_set_kernel_times(auvm_ctx* x, const uint64_t* t_ns, uint64_t n) {
   if (!x) return AUVM_E_INVAL;
   Ctx& c = x->c;

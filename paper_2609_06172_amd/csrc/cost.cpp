@@ -87,6 +87,32 @@ void kernel_cost(const Kernel& k, const std::vector<Tensor>& T, uint64_t* Fo, ui
       B = Bt * V * es(T, k, 0) + 4 * Bt + (k.ids.size() > 2 ? 4 * Bt : 0);
       break;
     }
+    // Routed experts: n (shape[4]) is the row count the trace expects the
+    // expert to see, so a decode expert prices as a weight read and a
+    // prefill expert as its GEMM.
+    case AUVM_OP_MOE_ROUTE: {
+      uint64_t M = s[0], H = s[1], E = s[2], K = s[3];
+      F = 2 * M * H * E;
+      B = M * H * es(T, k, 0) + E * H * es(T, k, 1) + 8 * M * K;
+      break;
+    }
+    case AUVM_OP_MOE_DISPATCH: {
+      uint64_t M = s[0], E = s[1], K = s[2];
+      B = 4 * M * K + 4 * (M * K + E) + 8 * E;
+      break;
+    }
+    case AUVM_OP_MOE_UP: {
+      uint64_t Fw = s[1], H = s[2], n = s[4];
+      F = 4 * n * Fw * H + 4 * n * Fw;
+      B = n * H * es(T, k, 0) + 4 * (n + 1) + Fw * H * (es(T, k, 2) + es(T, k, 3)) + n * Fw * es(T, k, 4);
+      break;
+    }
+    case AUVM_OP_MOE_DOWN: {
+      uint64_t H = s[1], Fw = s[2], n = s[4];
+      F = 2 * n * H * Fw + 2 * n * H;
+      B = n * Fw * es(T, k, 0) + 4 * (n + 1) + 4 * n + H * Fw * es(T, k, 3) + 8 * n * H;
+      break;
+    }
   }
   *Fo = F;
   *Bo = B;
@@ -267,6 +293,58 @@ std::string validate_kernel(const Kernel& k, const std::vector<Tensor>& T) {
       if (k.ids.size() > 2) {
         if (s[2] < 0) v.fail("negative gen row");
         v.need(2, I32, uint64_t(s[2] + 1) * s[0], "gen"); v.mode(2, MRW, "gen");
+      }
+      break;
+    }
+    case AUVM_OP_MOE_ROUTE: {
+      v.count(4, 4);
+      v.pos(0, "M"); v.pos(1, "H"); v.pos(2, "E"); v.pos(3, "K");
+      if (!v.ok) break;
+      if (s[2] > 16 || s[3] > s[2]) v.fail("routing needs K <= E <= 16");
+      if (s[1] % 8) v.fail("router needs H % 8 == 0");
+      uint64_t M = s[0], H = s[1], E = s[2], K = s[3];
+      v.need(0, FP, M * H, "h"); v.mode(0, MR, "h");
+      v.need(1, FP, E * H, "Wr"); v.mode(1, MR, "Wr");
+      v.need(2, I32, M * K, "rte"); v.mode(2, MW | MRW, "rte");
+      v.need(3, F32, M * K, "rtw"); v.mode(3, MW | MRW, "rtw");
+      if (v.ok && T[k.ids[0]].dtype != T[k.ids[1]].dtype) v.fail("h and router dtypes differ");
+      break;
+    }
+    case AUVM_OP_MOE_DISPATCH: {
+      v.count(3, 3);
+      v.pos(0, "M"); v.pos(1, "E"); v.pos(2, "K");
+      if (!v.ok) break;
+      if (s[1] > 16 || s[2] > s[1]) v.fail("routing needs K <= E <= 16");
+      if (s[3] < 0) v.fail("negative log row");
+      if (s[0] * s[2] >= (int64_t(1) << 31)) v.fail("M * K must fit 31 bits");
+      uint64_t M = s[0], E = s[1], K = s[2];
+      v.need(0, I32, M * K, "rte"); v.mode(0, MR, "rte");
+      v.need(1, I32, E * (M + 1), "lists"); v.mode(1, MW | MRW, "lists");
+      v.need(2, I32, uint64_t(s[3] + 1) * E, "log"); v.mode(2, MRW, "log");
+      break;
+    }
+    case AUVM_OP_MOE_UP:
+    case AUVM_OP_MOE_DOWN: {
+      const bool up = k.op == AUVM_OP_MOE_UP;
+      v.count(5, 5);
+      v.pos(0, "M"); v.pos(1, "N"); v.pos(2, "K"); v.pos(4, "n"); v.pos(5, "topk");
+      if (!v.ok) break;
+      if (s[3] < 0) v.fail("negative expert index");
+      if (s[4] > s[0]) v.fail("routed rows exceed M");
+      if (s[1] % 64 || s[2] % 64) v.fail("expert GEMMs need N % 64 == 0 and K % 64 == 0");
+      if (s[5] > 16) v.fail("topk above 16");
+      if (!v.ok) break;
+      uint64_t M = s[0], N = s[1], Kd = s[2], e = s[3], K = s[5];
+      v.need(0, BF16, M * Kd, up ? "h" : "fe"); v.mode(0, MR, up ? "h" : "fe");
+      v.need(1, I32, (e + 1) * (M + 1), "lists"); v.mode(1, MR, "lists");
+      if (up) {
+        v.need(2, BF16, N * Kd, "Wg"); v.mode(2, MR, "Wg");
+        v.need(3, BF16, N * Kd, "Wu"); v.mode(3, MR, "Wu");
+        v.need(4, BF16, M * N, "fe"); v.mode(4, MW | MRW, "fe");
+      } else {
+        v.need(2, F32, M * K, "rtw"); v.mode(2, MR, "rtw");
+        v.need(3, BF16, N * Kd, "Wd"); v.mode(3, MR, "Wd");
+        v.need(4, F32, M * N, "x"); v.mode(4, MRW, "x");
       }
       break;
     }

@@ -50,7 +50,9 @@ __device__ __forceinline__ float block_sum(float v, float* scratch /* >= 16 floa
   return r;
 }
 
-enum Epi { EPI_STORE = 0, EPI_GELU = 1, EPI_RESID = 2, EPI_SWIGLU = 3 };
+// EPI_MOE: weighted scatter-add of routed rows into an fp32 residual (GEMMs
+// driven by a routed-row list only).
+enum Epi { EPI_STORE = 0, EPI_GELU = 1, EPI_RESID = 2, EPI_SWIGLU = 3, EPI_MOE = 4 };
 
 }  // namespace dev
 }  // namespace auvm

@@ -15,12 +15,20 @@ struct GemmArgs {
   uint8_t* c;         // [M,N]: f32 or bf16 output, f32 residual for EPI_RESID
   int epi;            // dev::Epi
   bool in_bf16, out_bf16;
+  // Routed rows (bf16 only): list[0] = count, list[1 + i] = entry j of GEMM
+  // row i, token j / topk.  Rows i >= min(count, M) are skipped.  With
+  // EPI_SWIGLU row i reads A row token(i) and writes C row i; with EPI_MOE it
+  // reads A row i and adds rw[j] * result into row token(i) of the fp32 C.
+  const int32_t* list = nullptr;
+  const float* rw = nullptr;
+  int topk = 1;
 };
 
 // Dispatch: bf16 with M <= 16 -> matrix-core GEMV (gemv.hip); bf16 with
 // M >= 512 and K % 64 == 0 -> 256 x 256 matrix-core GEMM fed by direct LDS
 // loads (gemm_big.hip); other bf16 -> 128 x 128 matrix-core GEMM
-// (gemm_mfma.hip); fp32 -> LDS-tiled FMA GEMM.
+// (gemm_mfma.hip); fp32 -> LDS-tiled FMA GEMM.  With a routed-row list:
+// M <= 16 -> the GEMV, else the 256 x 256 GEMM (K % 64 == 0).
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s);
 hipError_t launch_gemv_bf16(const GemmArgs& g, hipStream_t s);
 hipError_t launch_gemm_mfma_bf16(const GemmArgs& g, hipStream_t s);

@@ -130,6 +130,10 @@ hipError_t by_epi(const GemmArgs& g, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s) {
+  if (g.list) {
+    if (!g.in_bf16 || g.topk < 1) return hipErrorInvalidValue;
+    return g.M <= 16 ? launch_gemv_bf16(g, s) : launch_gemm_big_bf16(g, s);
+  }
   if (g.in_bf16) {
     if (g.M <= 16) return launch_gemv_bf16(g, s);
     if (g.M >= 512 && g.K % 64 == 0) return launch_gemm_big_bf16(g, s);

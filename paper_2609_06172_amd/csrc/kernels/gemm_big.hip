@@ -14,7 +14,8 @@
 // 16-byte chunks are stored at slot chunk ^ ((row >> 1) & 7), which keeps a
 // fragment read (32 rows, one chunk) free of LDS bank conflicts.  Rows past M or N are
 // clamped to the last row (every load stays in bounds) and their results are
-// dropped by the epilogue; K must be a multiple of 64.
+// dropped by the epilogue; K must be a multiple of 64.  The same kernel runs
+// the routed rows of an MoE expert from a routed-row list.
 #include <hip/hip_runtime.h>
 
 #include "common.h"
@@ -52,16 +53,20 @@ struct Shape {
 
 // One K step of operand rows into LDS stage buf.  Wave wv fills the 8-row
 // blocks wv, wv + 8, ...; lane l fills row 8 * block + l / 8 at slot l % 8
-// with the row's chunk (l % 8) ^ swz(row).  A device function, not a lambda:
+// with the row's chunk (l % 8) ^ swz(row).  The lane's A rows (blocks t <
+// kARowsPerLane) come precomputed in arow.  A device function, not a lambda:
 // the LDS-load builtin exists only in the device pass.
+constexpr int kARowsPerLane = 256 / (8 * kWaves);
+
 template <int EPI>
-__device__ __forceinline__ void load_stage(bf16_t* smem, const bf16_t* __restrict__ A, const bf16_t* __restrict__ W,
-                                           const bf16_t* __restrict__ W2, int64_t M, int64_t N, int64_t K,
-                                           int64_t m0, int64_t n0, int wv, int lane, int buf, int64_t k0) {
+__device__ __forceinline__ void load_stage(bf16_t* smem, const bf16_t* const* arow, const bf16_t* __restrict__ W,
+                                           const bf16_t* __restrict__ W2, int64_t N, int64_t K, int64_t n0,
+                                           int wv, int lane, int buf, int64_t k0) {
   using S = Shape<EPI>;
   constexpr bool DUAL = S::kDual;
   constexpr int BM = S::kBM, BN = S::kBN;
   static_assert(S::kRows % (8 * kWaves) == 0, "stage rows split evenly over the waves");
+  static_assert(BM == 8 * kWaves * kARowsPerLane, "A rows are the first blocks of a stage");
   bf16_t* base = smem + buf * S::kStage;
   const int rin = lane >> 3, slot = lane & 7;
 #pragma unroll
@@ -69,9 +74,8 @@ __device__ __forceinline__ void load_stage(bf16_t* smem, const bf16_t* __restric
     const int b = wv + kWaves * t;
     const int row = 8 * b + rin;
     const bf16_t* src;
-    if (row < BM) {
-      const int64_t r = m0 + row;
-      src = A + (r < M ? r : M - 1) * K;
+    if (t < kARowsPerLane) {
+      src = arow[t];
     } else {
       const int wrow = row - BM;
       const bool second = DUAL && wrow >= BN;
@@ -83,10 +87,15 @@ __device__ __forceinline__ void load_stage(bf16_t* smem, const bf16_t* __restric
   }
 }
 
-template <int EPI, class TC>
+// LIST: rows come from a routed-row list (GemmArgs::list): tiles past the
+// list's count exit at once, A rows are gathered by token (EPI_SWIGLU) or the
+// results scattered into token rows with the routing weight (EPI_MOE).
+template <int EPI, class TC, bool LIST>
 __global__ void __launch_bounds__(64 * kWaves) gemm_big(const bf16_t* __restrict__ A, const bf16_t* __restrict__ W,
                                                 const bf16_t* __restrict__ W2, TC* __restrict__ C,
-                                                int64_t M, int64_t N, int64_t K, int tilesN) {
+                                                int64_t M, int64_t N, int64_t K, int tilesN,
+                                                const int32_t* __restrict__ list, const float* __restrict__ rw,
+                                                int topk) {
   using S = Shape<EPI>;
   constexpr bool DUAL = S::kDual;
   constexpr int TM = S::kTM, TN = S::kTN, BM = S::kBM, BN = S::kBN;
@@ -103,6 +112,22 @@ __global__ void __launch_bounds__(64 * kWaves) gemm_big(const bf16_t* __restrict
   const int gm = (tilesM - first) < kGroupM ? (tilesM - first) : kGroupM;
   const int in = id - grp * gsize;
   const int64_t m0 = int64_t(first + in % gm) * BM, n0 = int64_t(in / gm) * BN;
+  int64_t rows = M;
+  if constexpr (LIST) {
+    rows = list[0] < M ? list[0] : M;
+    if (m0 >= rows) return;   // uniform over the workgroup
+  }
+  const bf16_t* arow[kARowsPerLane];
+#pragma unroll
+  for (int t = 0; t < kARowsPerLane; ++t) {
+    const int64_t r = m0 + 8 * (wv + kWaves * t) + (lane >> 3);
+    int64_t src = r < rows ? r : rows - 1;   // rows past the end are clamped, their results dropped
+    if constexpr (LIST && EPI != EPI_MOE) {
+      const int64_t tok = list[1 + src] / topk;
+      src = tok < 0 ? 0 : (tok < M ? tok : M - 1);
+    }
+    arow[t] = A + src * K;
+  }
 
   f32x16 acc[TM][TN], acc2[DUAL ? TM : 1][DUAL ? TN : 1];
 #pragma unroll
@@ -118,12 +143,12 @@ __global__ void __launch_bounds__(64 * kWaves) gemm_big(const bf16_t* __restrict
 
   const int lr = lane & 31, lc = lane >> 5;     // fragment row, chunk half
   const int64_t nk = K / kBK;
-  load_stage<EPI>(smem, A, W, W2, M, N, K, m0, n0, wv, lane, 0, 0);
+  load_stage<EPI>(smem, arow, W, W2, N, K, n0, wv, lane, 0, 0);
   for (int64_t kt = 0; kt < nk; ++kt) {
     __builtin_amdgcn_s_waitcnt(0);   // this wave's loads of stage kt have landed
     __syncthreads();                 // ... and every other wave's; stage kt-1 is free
     asm volatile("" ::: "memory");   // LDS now holds data written outside the compiler's view
-    if (kt + 1 < nk) load_stage<EPI>(smem, A, W, W2, M, N, K, m0, n0, wv, lane, int((kt + 1) & 1), (kt + 1) * kBK);
+    if (kt + 1 < nk) load_stage<EPI>(smem, arow, W, W2, N, K, n0, wv, lane, int((kt + 1) & 1), (kt + 1) * kBK);
     const bf16_t* stg = smem + int(kt & 1) * S::kStage;
     // fragments of sub-step ks into register set q
     bf16x8 a[2][TM], b[2][TN], b2[2][DUAL ? TN : 1];
@@ -181,11 +206,16 @@ __global__ void __launch_bounds__(64 * kWaves) gemm_big(const bf16_t* __restrict
 #pragma clang loop unroll(full)
       for (int e = 0; e < 16; ++e) {
         const int64_t row = m0 + wm * 32 * TM + 32 * i + 8 * (e >> 2) + 4 * lc + (e & 3);
-        if (row >= M) continue;
+        if (row >= rows) continue;
         float v = acc[i][j][e];
         if constexpr (EPI == EPI_GELU) v = gelu_erf(v);
         if constexpr (EPI == EPI_SWIGLU) v = silu(v) * acc2[i][j][e];
-        if constexpr (EPI == EPI_RESID) {
+        if constexpr (EPI == EPI_MOE) {
+          const int64_t jr = list[1 + row], lim = M * topk;
+          const int64_t jc = jr < 0 ? 0 : (jr < lim ? jr : lim - 1);
+          float* x = reinterpret_cast<float*>(C);
+          x[(jc / topk) * N + col] += rw[jc] * v;
+        } else if constexpr (EPI == EPI_RESID) {
           float* x = reinterpret_cast<float*>(C);
           x[row * N + col] += v;
         } else {
@@ -195,20 +225,25 @@ __global__ void __launch_bounds__(64 * kWaves) gemm_big(const bf16_t* __restrict
     }
 }
 
-template <int EPI, class TC>
+template <int EPI, class TC, bool LIST = false>
 hipError_t go(const GemmArgs& g, hipStream_t s) {
   using S = Shape<EPI>;
   const int tilesM = int((g.M + S::kBM - 1) / S::kBM), tilesN = int((g.N + S::kBN - 1) / S::kBN);
   const size_t lds = size_t(2) * S::kStage * sizeof(bf16_t);
-  hipLaunchKernelGGL((gemm_big<EPI, TC>), dim3(unsigned(tilesM * tilesN)), dim3(64 * kWaves), lds, s,
+  hipLaunchKernelGGL((gemm_big<EPI, TC, LIST>), dim3(unsigned(tilesM * tilesN)), dim3(64 * kWaves), lds, s,
                      reinterpret_cast<const bf16_t*>(g.a), reinterpret_cast<const bf16_t*>(g.w),
                      reinterpret_cast<const bf16_t*>(g.w2), reinterpret_cast<TC*>(g.c), g.M, g.N, g.K,
-                     tilesN);
+                     tilesN, g.list, g.rw, g.topk);
   return hipGetLastError();
 }
 
 template <class TC>
 hipError_t by_epi(const GemmArgs& g, hipStream_t s) {
+  if (g.list) {
+    if (g.epi == EPI_SWIGLU) return go<EPI_SWIGLU, TC, true>(g, s);
+    if (g.epi == EPI_MOE) return go<EPI_MOE, float, true>(g, s);
+    return hipErrorInvalidValue;
+  }
   switch (g.epi) {
     case EPI_STORE: return go<EPI_STORE, TC>(g, s);
     case EPI_GELU: return go<EPI_GELU, TC>(g, s);

@@ -5,6 +5,9 @@
 // 16 weight rows its N side, so every weight byte is read once from HBM and
 // fed straight from registers to the matrix core; no LDS staging.
 //
+// Routed rows (MoE experts): the same kernel over the rows of a routed-row
+// list, gathered by token on input or scattered by token on output.
+//
 // Work split: one 512-thread workgroup per 16 output features; its eight
 // waves take interleaved 32-wide K chunks (adjacent waves read adjacent 64 B
 // of every weight row), eight chunks in flight per wave, keep fp32 partial tiles in registers and reduce them
@@ -28,18 +31,31 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 constexpr int kUnroll = 8;  // K chunks in flight per wave
 constexpr int kWaves = 8;   // waves per workgroup, splitting K
 
-template <int EPI, class TC>
+// LIST: rows come from a routed-row list (GemmArgs::list): the row count is
+// read from the list, and A rows are gathered by token (EPI_SWIGLU) or the
+// results scattered into token rows with the routing weight (EPI_MOE).
+template <int EPI, class TC, bool LIST>
 __global__ void __launch_bounds__(64 * kWaves) gemv_mfma(const bf16_t* __restrict__ A, const bf16_t* __restrict__ W,
                                                  const bf16_t* __restrict__ W2, TC* __restrict__ C,
-                                                 int M, int64_t N, int64_t K) {
+                                                 int M, int64_t N, int64_t K, const int32_t* __restrict__ list,
+                                                 const float* __restrict__ rw, int topk) {
   constexpr bool DUAL = EPI == EPI_SWIGLU;
   __shared__ f32x4 part[kWaves][DUAL ? 2 : 1][64];
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int r = lane & 15, g = lane >> 4;
   const int64_t n0 = int64_t(blockIdx.x) * 16;
   const int64_t n = n0 + r;
-  const bool a_ok = r < M, w_ok = n < N;
-  const bf16_t* arow = A + int64_t(a_ok ? r : 0) * K + 8 * g;
+  int rows = M;
+  if constexpr (LIST) rows = list[0] < M ? list[0] : M;
+  const bool a_ok = r < rows, w_ok = n < N;
+  int64_t ar = a_ok ? r : 0;
+  if constexpr (LIST && EPI != EPI_MOE) {
+    if (a_ok) {
+      const int64_t t = list[1 + r] / topk;
+      ar = t < 0 ? 0 : (t < M ? t : M - 1);
+    }
+  }
+  const bf16_t* arow = A + ar * K + 8 * g;
   const bf16_t* wrow = W + (w_ok ? n : 0) * K + 8 * g;
   const bf16_t* w2row = DUAL ? W2 + (w_ok ? n : 0) * K + 8 * g : nullptr;
   const int64_t nch = K / 32;
@@ -78,11 +94,16 @@ __global__ void __launch_bounds__(64 * kWaves) gemv_mfma(const bf16_t* __restric
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int row = 4 * (lane >> 4) + i;
-    if (row >= M) continue;
+    if (row >= rows) continue;
     float v = s[i];
     if constexpr (EPI == EPI_GELU) v = gelu_erf(v);
     if constexpr (EPI == EPI_SWIGLU) v = silu(v) * s2[i];
-    if constexpr (EPI == EPI_RESID) {
+    if constexpr (EPI == EPI_MOE) {
+      const int64_t j = list[1 + row], lim = int64_t(M) * topk;
+      const int64_t jc = j < 0 ? 0 : (j < lim ? j : lim - 1);
+      float* x = reinterpret_cast<float*>(C);
+      x[(jc / topk) * N + col] += rw[jc] * v;
+    } else if constexpr (EPI == EPI_RESID) {
       float* x = reinterpret_cast<float*>(C);
       x[int64_t(row) * N + col] += v;
     } else {
@@ -91,17 +112,22 @@ __global__ void __launch_bounds__(64 * kWaves) gemv_mfma(const bf16_t* __restric
   }
 }
 
-template <int EPI, class TC>
+template <int EPI, class TC, bool LIST = false>
 hipError_t go(const GemmArgs& g, hipStream_t s) {
   dim3 grid(unsigned((g.N + 15) / 16));
-  hipLaunchKernelGGL((gemv_mfma<EPI, TC>), grid, dim3(64 * kWaves), 0, s, reinterpret_cast<const bf16_t*>(g.a),
+  hipLaunchKernelGGL((gemv_mfma<EPI, TC, LIST>), grid, dim3(64 * kWaves), 0, s, reinterpret_cast<const bf16_t*>(g.a),
                      reinterpret_cast<const bf16_t*>(g.w), reinterpret_cast<const bf16_t*>(g.w2),
-                     reinterpret_cast<TC*>(g.c), int(g.M), g.N, g.K);
+                     reinterpret_cast<TC*>(g.c), int(g.M), g.N, g.K, g.list, g.rw, g.topk);
   return hipGetLastError();
 }
 
 template <class TC>
 hipError_t by_epi(const GemmArgs& g, hipStream_t s) {
+  if (g.list) {
+    if (g.epi == EPI_SWIGLU) return go<EPI_SWIGLU, TC, true>(g, s);
+    if (g.epi == EPI_MOE) return go<EPI_MOE, float, true>(g, s);
+    return hipErrorInvalidValue;
+  }
   switch (g.epi) {
     case EPI_STORE: return go<EPI_STORE, TC>(g, s);
     case EPI_GELU: return go<EPI_GELU, TC>(g, s);

@@ -5,6 +5,7 @@
 #include "../kernels.h"
 #include "common.h"
 #include "gemm.h"
+#include "moe.h"
 #include "attention.h"
 
 namespace auvm {
@@ -306,6 +307,39 @@ hipError_t launch_op(const Kernel& k, const std::vector<Tensor>& T, uint8_t* con
               : k.op == AUVM_OP_LINEAR_RESID ? EPI_RESID : EPI_SWIGLU;
       g.in_bf16 = dt(0) == AUVM_BF16;
       g.out_bf16 = dt(sw ? 3 : 2) == AUVM_BF16;
+      return launch_gemm(g, s);
+    }
+    case AUVM_OP_MOE_ROUTE:
+      return launch_moe_route(p[0], p[1], reinterpret_cast<int32_t*>(p[2]), reinterpret_cast<float*>(p[3]), sh[0],
+                              sh[1], int(sh[2]), int(sh[3]), dt(0) == AUVM_BF16, s);
+    case AUVM_OP_MOE_DISPATCH:
+      return launch_moe_dispatch(reinterpret_cast<const int32_t*>(p[0]), reinterpret_cast<int32_t*>(p[1]),
+                                 reinterpret_cast<int32_t*>(p[2]), sh[0], int(sh[2]), int(sh[1]), sh[3], s);
+    case AUVM_OP_MOE_UP:
+    case AUVM_OP_MOE_DOWN: {
+      // the expert's row list is row e of the [E, M+1] list tensor
+      const bool up = k.op == AUVM_OP_MOE_UP;
+      GemmArgs g{};
+      g.M = sh[0];
+      g.N = sh[1];
+      g.K = sh[2];
+      g.list = reinterpret_cast<const int32_t*>(p[1]) + sh[3] * (sh[0] + 1);
+      g.topk = int(sh[5]);
+      g.in_bf16 = true;
+      g.a = p[0];
+      if (up) {
+        g.w = p[2];
+        g.w2 = p[3];
+        g.c = p[4];
+        g.epi = EPI_SWIGLU;
+        g.out_bf16 = true;
+      } else {
+        g.rw = reinterpret_cast<const float*>(p[2]);
+        g.w = p[3];
+        g.c = p[4];
+        g.epi = EPI_MOE;
+        g.out_bf16 = false;
+      }
       return launch_gemm(g, s);
     }
     case AUVM_OP_ATTN_QKV:

@@ -68,6 +68,24 @@ class Session:
         self.ctx.plan()
         return t
 
+    def retrace(self, w):
+        """Replace the trace by the kernels of ``w``, a workload over the same
+        tensors (for routed experts: the trace a profiling run recorded), and
+        plan again.  Execution restarts from an empty pool."""
+        same = [(t.nbytes, t.dtype, t.kind, t.off) for t in w.tensors]
+        if same != [(t.nbytes, t.dtype, t.kind, t.off) for t in self.w.tensors]:
+            raise ValueError("retrace needs a workload over the same tensors")
+        self.ctx.clear_kernels()
+        for k in w.kernels:
+            self.ctx.add_kernel(k.op, k.shape, k.operands, layer=k.layer)
+        self.w = w
+        self.ctx.plan()
+
+    def routing_counts(self):
+        """Per-expert row counts logged by the MoE dispatch kernels, [seg][layer][expert]."""
+        c = self.w.cfg
+        return self.read("moe_counts").reshape(1 + c.decode_steps, c.n_layers, c.n_experts)
+
     # -- host arena access ----------------------------------------------------
     def host_view(self, t):
         """uint8 numpy view of tensor t's host arena window."""

@@ -78,3 +78,34 @@ def random_trace(seed, n_tensors=None, n_kernels=None, max_ops=4, equal=False,
             kd["time_ns"] = r.choice([1, 2, 3, 5, 8, 13, 40, 10**6])
         kernels.append(kd)
     return tensors, kernels
+
+
+def oracle_routing_counts(cfg):
+    """Per-expert row counts [seg][layer][expert] of the fp64 oracle's own
+    greedy run of an MoE config (what the dispatch kernels would log)."""
+    import numpy as np
+
+    from oracle import forward as of
+    from workloads import init, trace
+    w = trace.build(cfg)
+    Wt = init.weights_f64(w)
+    ids = init.token_ids(cfg.seed, cfg.batch, cfg.prompt_len, cfg.vocab)
+    gen = of.llama_generate(cfg, Wt, ids)
+    counts = np.zeros((1 + cfg.decode_steps, cfg.n_layers, cfg.n_experts), np.int64)
+    for seg, layers in enumerate(gen["routes"]):
+        for l, (idx, _, _) in enumerate(layers):
+            counts[seg, l] = np.bincount(idx.reshape(-1), minlength=cfg.n_experts)
+    return counts
+
+
+def random_routing_counts(cfg, seed):
+    """Counts of a seeded random top-k choice per token (planning inputs only)."""
+    import numpy as np
+    rng = np.random.default_rng(seed)
+    counts = np.zeros((1 + cfg.decode_steps, cfg.n_layers, cfg.n_experts), np.int64)
+    for seg in range(1 + cfg.decode_steps):
+        M = cfg.tokens if seg == 0 else cfg.batch
+        for l in range(cfg.n_layers):
+            pick = np.argsort(rng.random((M, cfg.n_experts)), axis=1)[:, :cfg.top_k]
+            counts[seg, l] = np.bincount(pick.reshape(-1), minlength=cfg.n_experts)
+    return counts

@@ -4,6 +4,7 @@ import os
 import random
 import re
 
+import numpy as np
 import pytest
 
 import paper_2609_06172_amd as pkg
@@ -77,7 +78,7 @@ def test_shape_validation_rejects_out_of_bounds_operands():
 
 def test_every_config_trace_is_accepted():
     for cfg in configs.CONFIGS.values():
-        if cfg.name == "llama-7b":
+        if cfg.name in ("llama-7b", "moe-8x14336"):
             continue          # covered (truncated) below
         w = trace.build(cfg)
         from paper_2609_06172_amd.session import Session
@@ -244,3 +245,96 @@ def test_config_traces_with_measured_times_bit_exact(name):
     assert any(a != b for a, b in zip(r.static_cls, base.static_cls))
     assert r.schedule != base.schedule
     s.close()
+
+
+# ------------------------------------------------------- routed experts (MoE)
+@pytest.mark.parametrize("variant", VARIANTS)
+def test_moe_traces_bit_exact(variant):
+    from planner_cases import oracle_routing_counts
+    from paper_2609_06172_amd.session import Session
+    cfg = configs.MOE_SMALL
+    counts = oracle_routing_counts(cfg)
+    for routing in (None, counts):
+        w = trace.build(cfg, routing)
+        s = Session(w, device=-1, variant=variant)
+        assert_same_plan(s.ctx, op.plan_workload(w, s.M, variant=variant))
+        s.close()
+
+
+def test_full_shape_moe_trace_bit_exact_and_retrace():
+    # the 8 x 14336 trace, prefill + 2 decode steps, under a seeded random routing
+    import dataclasses
+    from planner_cases import random_routing_counts
+    from paper_2609_06172_amd.session import Session
+    cfg = dataclasses.replace(configs.MOE_8X, decode_steps=2)
+    full = trace.build(cfg)
+    routed = trace.build(cfg, random_routing_counts(cfg, 5))
+    assert len(routed.kernels) < len(full.kernels)
+    s = Session(full, device=-1)
+    s.retrace(routed)                    # the profiling trace swapped for the routed one
+    assert_same_plan(s.ctx, op.plan_workload(routed, s.M))
+    s.close()
+
+
+def test_routed_trace_moves_only_routed_experts():
+    # the profiling trace (every expert) against the recorded one: the same
+    # kernels run, but unrouted experts' weights are never fetched
+    from planner_cases import oracle_routing_counts
+    cfg = configs.MOE_SMALL
+    counts = oracle_routing_counts(cfg)
+    assert (counts == 0).any()            # some expert idles in some decode layer
+    full, routed = trace.build(cfg), trace.build(cfg, counts)
+    M = full.budget()
+    a, b = op.plan_workload(full, M), op.plan_workload(routed, M)
+    fa = a.counters["h2d_prefetch_B"] + a.counters["h2d_demand_B"]
+    fb = b.counters["h2d_prefetch_B"] + b.counters["h2d_demand_B"]
+    assert fb < fa
+    # every weight fetched under the routed trace belongs to a routed expert
+    names = {t.tid: t.name for t in routed.tensors}
+    routed_experts = set()
+    for seg in range(counts.shape[0]):
+        for l in range(cfg.n_layers):
+            routed_experts |= {f"L{l}.x{e}." for e in np.nonzero(counts[seg, l])[0]}
+    for e in b.schedule:
+        if e[0] in (0, 1) and ".x" in names[e[1]]:
+            assert names[e[1]].rsplit(".", 1)[0] + "." in routed_experts
+
+
+def test_moe_op_validation():
+    from workloads.format import OP_MOE_DISPATCH, OP_MOE_DOWN, OP_MOE_ROUTE, OP_MOE_UP
+    ctx = Context(-1)
+    ctx.arena_init(1 << 24)
+    off = [0]
+
+    def t(nbytes, dt, kind=KIND_ACT):
+        i = ctx.register_tensor(off[0], nbytes, dt, kind, 1 if kind != KIND_PARAM else 0)
+        off[0] += (nbytes + 255) // 256 * 256
+        return i
+    M, H, F, E, K = 32, 128, 192, 4, 2
+    h = t(M * H * 2, DT_BF16)
+    wr = t(E * H * 2, DT_BF16, KIND_PARAM)
+    rte, rtw = t(M * K * 4, DT_I32), t(M * K * 4, DT_F32)
+    lists, log = t(E * (M + 1) * 4, DT_I32), t(3 * E * 4, DT_I32)
+    wg, wu, wd = t(F * H * 2, DT_BF16, KIND_PARAM), t(F * H * 2, DT_BF16, KIND_PARAM), t(H * F * 2, DT_BF16, KIND_PARAM)
+    fe, x = t(M * F * 2, DT_BF16), t(M * H * 4, DT_F32)
+    R, W = MODE_R, MODE_W
+    ctx.add_kernel(OP_MOE_ROUTE, (M, H, E, K), [(h, R), (wr, R), (rte, W), (rtw, W)])
+    ctx.add_kernel(OP_MOE_DISPATCH, (M, E, K, 2), [(rte, R), (lists, W), (log, MODE_RW)])
+    ctx.add_kernel(OP_MOE_UP, (M, F, H, 3, M, K), [(h, R), (lists, R), (wg, R), (wu, R), (fe, W)])
+    ctx.add_kernel(OP_MOE_DOWN, (M, H, F, 3, 5, K), [(fe, R), (lists, R), (rtw, R), (wd, R), (x, MODE_RW)])
+    bad = [
+        (OP_MOE_ROUTE, (M, H, E, 5), [(h, R), (wr, R), (rte, W), (rtw, W)]),            # K > E
+        (OP_MOE_ROUTE, (M, H, 17, 2), [(h, R), (wr, R), (rte, W), (rtw, W)]),           # E > 16
+        (OP_MOE_ROUTE, (M, 124, E, K), [(h, R), (wr, R), (rte, W), (rtw, W)]),          # H % 8
+        (OP_MOE_DISPATCH, (M, E, K, 3), [(rte, R), (lists, W), (log, MODE_RW)]),         # log row beyond
+        (OP_MOE_DISPATCH, (M, E, K, 1), [(rte, R), (lists, W), (log, W)]),               # log must be RW
+        (OP_MOE_UP, (M, F, H, 4, M, K), [(h, R), (lists, R), (wg, R), (wu, R), (fe, W)]),   # expert beyond lists
+        (OP_MOE_UP, (M, F, H, 0, M + 1, K), [(h, R), (lists, R), (wg, R), (wu, R), (fe, W)]),  # n > M
+        (OP_MOE_UP, (M, F, 96, 0, M, K), [(h, R), (lists, R), (wg, R), (wu, R), (fe, W)]),  # K % 64
+        (OP_MOE_DOWN, (M, H, F, 0, M, K), [(fe, R), (lists, R), (rtw, R), (wd, R), (x, W)]),  # x must be RW
+    ]
+    for o, sh, ops in bad:
+        with pytest.raises(AuvmError) as e:
+            ctx.add_kernel(o, sh, ops)
+        assert e.value.code == op.E_INVAL, (o, sh)
+    ctx.destroy()

@@ -118,3 +118,78 @@ def test_replanning_from_measured_kernel_times():
     assert np.array_equal(s.read("logits"), logits)
     assert s.ctx.get_executed() == s.ctx.get_schedule()
     s.close()
+
+
+def _moe_walk(s, w):
+    """Run a MoE workload on the GPU in pieces, reading each layer's expert
+    choice right after its route kernel and the logits after each segment."""
+    from workloads.format import OP_MOE_ROUTE
+    c = w.cfg
+    segs = w.segments["prefill"] + w.segments["decode"]
+    routes, logits = [], []
+    for seg, (k0, n) in enumerate(segs):
+        layer_routes, start = [], k0
+        for k in range(k0, k0 + n):
+            if w.kernels[k].op == OP_MOE_ROUTE:
+                s.run(start, k + 1 - start)
+                start = k + 1
+                layer_routes.append(s.read("rte_p" if seg == 0 else "rte_d").copy())
+        s.run(start, k0 + n - start)
+        routes.append(layer_routes)
+        logits.append(s.read("logits").copy())
+    assert len(routes) == 1 + c.decode_steps and all(len(r) == c.n_layers for r in routes)
+    return routes, logits
+
+
+def test_moe_small_teacher_forced_tokens_and_routes():
+    from workloads import configs as C
+    cfg = C.MOE_SMALL
+    print("moe-small bf16 prefill + decode at 2x, every expert in the trace", flush=True)
+    s, w = _session(cfg, validate=1)
+    routes, logits = _moe_walk(s, w)
+    gen = s.read("gen")
+    assert s.ctx.get_executed() == s.ctx.get_schedule()
+    s.close()
+    Wt = init.weights_f64(w)
+    ids = init.token_ids(cfg.seed, cfg.batch, cfg.prompt_len, cfg.vocab)
+    ref = of.llama_generate(cfg, Wt, ids, forced=gen[:cfg.decode_steps], forced_routes=routes)
+    for st, (a, b) in enumerate(zip(logits, ref["logits"])):
+        assert rel_l2(a, b) < 2e-2, st
+    # where the oracle's k-th and (k+1)-th logits are clearly apart, the GPU
+    # chose the oracle's experts; near ties either choice is correct
+    n_clear = n_all = 0
+    for seg, layers in enumerate(ref["routes"]):
+        for l, (idx, wts, lg) in enumerate(layers):
+            own, _ = of.route_topk(lg, cfg.top_k)
+            srt = -np.sort(-lg, axis=1)
+            clear = (srt[:, cfg.top_k - 1] - srt[:, cfg.top_k]) > 2e-2 * np.abs(srt[:, :1]).max()
+            assert np.array_equal(routes[seg][l][clear], own[clear]), (seg, l)
+            n_clear += clear.sum()
+            n_all += len(clear)
+    assert n_clear > 0.8 * n_all
+
+
+def test_moe_small_recorded_trace_replays_bit_for_bit():
+    # profiling run with every expert, then the trace it recorded (routed
+    # experts only): same tokens, logits and routing, fewer bytes moved
+    from workloads import configs as C
+    cfg = C.MOE_SMALL
+    print("moe-small: profiling trace, then the recorded routed trace", flush=True)
+    s, w = _session(cfg)
+    s.run_all()
+    gen, logits = s.read("gen").copy(), s.read("logits").copy()
+    counts = s.routing_counts().copy()
+    c_full = s.ctx.get_counters()
+    routed = trace.build(cfg, counts)
+    assert len(routed.kernels) < len(w.kernels)
+    s.retrace(routed)
+    s.restore_inputs()
+    s.run_all()
+    assert np.array_equal(s.read("gen"), gen)
+    assert np.array_equal(s.read("logits"), logits)
+    assert np.array_equal(s.routing_counts(), counts)
+    assert s.ctx.get_executed() == s.ctx.get_schedule()
+    c_routed = s.ctx.get_counters()
+    moved = lambda c: c["h2d_prefetch_B"] + c["h2d_demand_B"]
+    assert moved(c_routed) < moved(c_full)
+    s.close()

@@ -175,3 +175,133 @@ def test_argmax_lowest_index(B, V):
     assert np.array_equal(res["tok"], ref)
     assert np.array_equal(res["gen"][row], ref)
     assert np.array_equal(res["gen"][:row], np.zeros((row, B), np.int32))
+
+
+# ------------------------------------------------------- routed experts (MoE)
+from workloads.format import OP_MOE_DISPATCH, OP_MOE_DOWN, OP_MOE_ROUTE, OP_MOE_UP  # noqa: E402
+
+
+def _topk_rows(logits, k):
+    idx, wts = of.route_topk(logits, k)
+    srt = -np.sort(-logits, axis=1)
+    gap = srt[:, k - 1] - srt[:, k] if k < logits.shape[1] else np.full(len(logits), np.inf)
+    return idx, wts, gap
+
+
+@pytest.mark.parametrize("dt", [DT_F32, DT_BF16])
+@pytest.mark.parametrize("M,H,E,K", [(1, 64, 4, 2), (37, 256, 4, 2), (300, 4096, 8, 2), (5, 128, 16, 4),
+                                     (9, 520, 3, 3), (64, 64, 8, 1), (2049, 1024, 8, 2)])
+def test_moe_route_topk(M, H, E, K, dt):
+    h, wr = rnd(M, H), rnd(E, H, scale=H ** -0.5)
+    ops = [("h", (M, H), dt, MODE_R, h), ("wr", (E, H), dt, MODE_R, wr),
+           ("rte", (M, K), DT_I32, MODE_W, None), ("rtw", (M, K), DT_F32, MODE_W, None)]
+    vals, res = _run(OP_MOE_ROUTE, (M, H, E, K), ops, ["rte", "rtw"])
+    logits = of.linear(vals["h"], vals["wr"])
+    idx, wts, gap = _topk_rows(logits, K)
+    # fp32 accumulation moves a logit by ~1e-6 of its scale: rows whose k-th and
+    # (k+1)-th logits are further apart must pick exactly the oracle's experts
+    clear = gap > 1e-4
+    assert clear.mean() > 0.9
+    assert np.array_equal(res["rte"][clear], idx[clear])
+    assert np.allclose(res["rtw"][clear], wts[clear], rtol=0, atol=2e-5)
+    # every row: distinct experts, descending logits, weights summing to 1
+    for m in range(M):
+        assert len(set(res["rte"][m])) == K and all(0 <= e < E for e in res["rte"][m])
+        assert np.all(np.diff(logits[m, res["rte"][m]]) <= 1e-4)
+    assert np.allclose(res["rtw"].sum(axis=1), 1, atol=1e-6)
+
+
+def test_moe_route_ties_go_to_the_lower_index():
+    M, H, E, K = 40, 256, 6, 3
+    h, wr = rnd(M, H), rnd(E, H, scale=H ** -0.5)
+    wr[4] = wr[1]                     # experts 1 and 4 tie exactly, so do 2 and 5
+    wr[5] = wr[2]
+    ops = [("h", (M, H), DT_BF16, MODE_R, h), ("wr", (E, H), DT_BF16, MODE_R, wr),
+           ("rte", (M, K), DT_I32, MODE_W, None), ("rtw", (M, K), DT_F32, MODE_W, None)]
+    vals, res = _run(OP_MOE_ROUTE, (M, H, E, K), ops, ["rte", "rtw"])
+    for m in range(M):
+        sel = list(res["rte"][m])
+        for lo, hi in ((1, 4), (2, 5)):
+            if hi in sel:
+                assert lo in sel and sel.index(lo) < sel.index(hi)
+
+
+def _routes(M, E, K, seed, skip=()):
+    """Random top-K choices (distinct per row) avoiding the experts in skip."""
+    g = np.random.default_rng(seed)
+    pool = [e for e in range(E) if e not in skip]
+    return np.stack([g.permutation(pool)[:K] for _ in range(M)]).astype(np.int32)
+
+
+@pytest.mark.parametrize("M,E,K,row,skip", [(1, 4, 2, 0, ()), (7, 4, 2, 1, (3,)), (600, 8, 2, 2, ()),
+                                            (3000, 8, 2, 0, (5,)), (32768, 8, 2, 3, ()), (100, 16, 4, 1, (0, 9))])
+def test_moe_dispatch_lists_are_exact(M, E, K, row, skip):
+    rte = _routes(M, E, K, M + E, skip)
+    log0 = np.arange((row + 2) * E, dtype=np.int32).reshape(row + 2, E) + 7
+    ops = [("rte", (M, K), DT_I32, MODE_R, rte), ("lists", (E, M + 1), DT_I32, MODE_W, None),
+           ("log", (row + 2, E), DT_I32, MODE_RW, log0)]
+    vals, res = _run(OP_MOE_DISPATCH, (M, E, K, row), ops, ["lists", "log"])
+    flat = rte.reshape(-1)
+    for e in range(E):
+        want = np.nonzero(flat == e)[0]
+        assert res["lists"][e, 0] == len(want)
+        assert np.array_equal(res["lists"][e, 1:1 + len(want)], want)
+    exp_log = log0.copy()
+    exp_log[row] = [np.count_nonzero(flat == e) for e in range(E)]
+    assert np.array_equal(res["log"], exp_log)     # other rows of the log untouched
+
+
+def _lists(M, E, K, rte):
+    L = np.zeros((E, M + 1), np.int32)
+    flat = rte.reshape(-1)
+    for e in range(E):
+        j = np.nonzero(flat == e)[0]
+        L[e, 0] = len(j)
+        L[e, 1:1 + len(j)] = j
+    return L
+
+
+# M <= 16: the routed-row GEMV; larger M: the 256 x 256 GEMM (tiles past the
+# count exit).  Expert 1 of 3; some shapes leave it with no rows.
+MOE_GEMM = [(1, 64, 64, ()), (8, 384, 256, ()), (16, 128, 64, (1,)), (80, 384, 256, ()),
+            (600, 192, 128, ()), (2048, 256, 512, ()), (300, 128, 64, (1,))]
+
+
+@pytest.mark.parametrize("M,F,H,skip", MOE_GEMM)
+def test_moe_expert_up(M, F, H, skip):
+    E, K, e = 3, 2, 1
+    rte = _routes(M, E, K, 3 * M + F, skip)
+    lists = _lists(M, E, K, rte)
+    n = int(lists[e, 0])
+    h, wg, wu = rnd(M, H), rnd(F, H, scale=H ** -0.5), rnd(F, H, scale=H ** -0.5)
+    ops = [("h", (M, H), DT_BF16, MODE_R, h), ("lists", (E, M + 1), DT_I32, MODE_R, lists),
+           ("wg", (F, H), DT_BF16, MODE_R, wg), ("wu", (F, H), DT_BF16, MODE_R, wu),
+           ("fe", (M, F), DT_BF16, MODE_W, None)]
+    vals, res = _run(OP_MOE_UP, (M, F, H, e, max(n, 1), K), ops, ["fe"])
+    tok = lists[e, 1:1 + n] // K
+    hr = vals["h"][tok]
+    want = of.silu(of.linear(hr, vals["wg"])) * of.linear(hr, vals["wu"])
+    if n:
+        assert rel_l2(res["fe"][:n], want) < TOL[DT_BF16]
+
+
+@pytest.mark.parametrize("M,F,H,skip", MOE_GEMM)
+def test_moe_expert_down(M, F, H, skip):
+    E, K, e = 3, 2, 1
+    rte = _routes(M, E, K, 5 * M + H, skip)
+    lists = _lists(M, E, K, rte)
+    n = int(lists[e, 0])
+    fe, wd = rnd(M, F), rnd(H, F, scale=F ** -0.5)
+    rtw, x0 = RNG.random((M, K)).astype(np.float32), rnd(M, H)
+    ops = [("fe", (M, F), DT_BF16, MODE_R, fe), ("lists", (E, M + 1), DT_I32, MODE_R, lists),
+           ("rtw", (M, K), DT_F32, MODE_R, rtw), ("wd", (H, F), DT_BF16, MODE_R, wd),
+           ("x", (M, H), DT_F32, MODE_RW, x0)]
+    vals, res = _run(OP_MOE_DOWN, (M, H, F, e, max(n, 1), K), ops, ["x"])
+    j = lists[e, 1:1 + n]
+    want = vals["x"].copy()
+    want[j // K] += vals["rtw"].reshape(-1)[j][:, None] * of.linear(vals["fe"][:n], vals["wd"])
+    routed = np.zeros(M, bool)
+    routed[j // K] = True
+    assert np.array_equal(res["x"][~routed], vals["x"][~routed])     # other rows untouched
+    if n:
+        assert rel_l2(res["x"][routed], want[routed]) < TOL[DT_F32]

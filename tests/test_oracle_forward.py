@@ -230,3 +230,160 @@ def test_llama_decode_equals_recompute_and_is_causal():
     for s in range(3):
         assert np.array_equal(g2["logits"][s], gen["logits"][s])
     assert not np.allclose(g2["logits"][3], gen["logits"][3])
+
+
+# -------------------------------------------------------------- MoE pins
+def test_route_topk_against_brute_force():
+    import itertools
+    rng = np.random.default_rng(11)
+    for E, k in ((4, 2), (8, 2), (5, 3), (3, 3), (6, 1)):
+        lg = rng.integers(-3, 4, size=(200, E)).astype(np.float64)   # many ties
+        idx, wts = of.route_topk(lg, k)
+        for m in range(lg.shape[0]):
+            # the chosen set is the best k-subset under (value, then lower index)
+            def key(sub):
+                return sorted(((-lg[m, e], e) for e in sub))
+            best = min(itertools.combinations(range(E), k), key=key)
+            assert sorted(idx[m]) == sorted(best)
+            # listed by decreasing logit, ties by increasing index
+            assert [tuple(x) for x in key(idx[m])] == [(-lg[m, e], e) for e in idx[m]]
+            ex = np.exp(lg[m, idx[m]] - lg[m, idx[m]].max())
+            assert np.allclose(wts[m], ex / ex.sum(), rtol=0, atol=1e-15)
+            assert abs(wts[m].sum() - 1) < 1e-15 and np.all(np.diff(wts[m]) <= 0)
+
+
+def _moe_weights(cfg, seed=3):
+    Wt = _weights(cfg)
+    rng = np.random.default_rng(seed)
+    for k in list(Wt):                 # randomise the gains so a dropped gain shows
+        if k.endswith("norm") or k == "norm_f":
+            Wt[k] = 1 + 0.1 * rng.standard_normal(Wt[k].shape)
+    return Wt
+
+
+def test_moe_matches_transformers_mixtral():
+    torch = pytest.importorskip("torch")
+    tf = pytest.importorskip("transformers")
+    cfg = configs.MOE_SMALL
+    Wt = _moe_weights(cfg)
+    ids = init.token_ids(0, cfg.batch, cfg.prompt_len, cfg.vocab)
+    gen = of.llama_generate(cfg, Wt, ids)
+    toks = np.stack(gen["tokens"])
+    full = np.concatenate([ids, toks[:-1].T], axis=1)
+    hc = tf.MixtralConfig(vocab_size=cfg.vocab, hidden_size=cfg.hidden, intermediate_size=cfg.ffn,
+                          num_hidden_layers=cfg.n_layers, num_attention_heads=cfg.n_heads,
+                          num_key_value_heads=cfg.n_heads, num_local_experts=cfg.n_experts,
+                          num_experts_per_tok=cfg.top_k, max_position_embeddings=cfg.kv_len,
+                          rms_norm_eps=1e-6, rope_theta=10000.0, tie_word_embeddings=False,
+                          sliding_window=None, router_jitter_noise=0.0)
+    hc._attn_implementation = "eager"
+    hc._experts_implementation = "eager"     # per-expert loop (the grouped GEMM has no fp64)
+    m = tf.MixtralForCausalLM(hc).to(torch.float64).eval()
+    sd = {"model.embed_tokens.weight": Wt["E"], "model.norm.weight": Wt["norm_f"],
+          "lm_head.weight": Wt["head"]}
+    names = dict(attn_norm="input_layernorm.weight", wq="self_attn.q_proj.weight",
+                 wk="self_attn.k_proj.weight", wv="self_attn.v_proj.weight",
+                 wo="self_attn.o_proj.weight", ffn_norm="post_attention_layernorm.weight",
+                 router="mlp.gate.weight")
+    E = cfg.n_experts
+    for l in range(cfg.n_layers):
+        for ours, theirs in names.items():
+            sd[f"model.layers.{l}.{theirs}"] = Wt[f"L{l}.{ours}"]
+        sd[f"model.layers.{l}.mlp.experts.gate_up_proj"] = np.stack(
+            [np.concatenate([Wt[f"L{l}.x{e}.wg"], Wt[f"L{l}.x{e}.wu"]], axis=0) for e in range(E)])
+        sd[f"model.layers.{l}.mlp.experts.down_proj"] = np.stack([Wt[f"L{l}.x{e}.wd"] for e in range(E)])
+    missing, unexpected = m.load_state_dict(
+        {k: torch.from_numpy(np.ascontiguousarray(v)) for k, v in sd.items()}, strict=False)
+    assert not unexpected and all("rotary" in k for k in missing), (missing, unexpected)
+    with torch.no_grad():
+        ref = m(torch.from_numpy(full.astype(np.int64))).logits.numpy()
+    S = cfg.prompt_len
+    for s in range(cfg.decode_steps + 1):
+        assert rel_l2(gen["logits"][s], ref[:, S - 1 + s]) < 1e-6, s
+
+
+def _dense_twin(cfg, Wt, expert=0):
+    """LLaMA config and weights whose MLP is expert `expert` of each layer."""
+    import dataclasses
+    dc = dataclasses.replace(cfg, style="llama", n_experts=0, top_k=0)
+    Wd = {k: v for k, v in Wt.items() if ".x" not in k and "router" not in k}
+    for l in range(cfg.n_layers):
+        for n in ("wg", "wu", "wd"):
+            Wd[f"L{l}.{n}"] = Wt[f"L{l}.x{expert}.{n}"]
+    return dc, Wd
+
+
+def test_moe_with_one_expert_is_the_dense_mlp():
+    import dataclasses
+    cfg = dataclasses.replace(configs.MOE_SMALL, n_experts=1, top_k=1)
+    Wt = _moe_weights(cfg)
+    ids = init.token_ids(0, cfg.batch, cfg.prompt_len, cfg.vocab)
+    a = of.llama_generate(cfg, Wt, ids)
+    dc, Wd = _dense_twin(cfg, Wt)
+    b = of.llama_generate(dc, Wd, ids)
+    for x, y in zip(a["logits"], b["logits"]):
+        assert rel_l2(x, y) < 1e-13
+
+
+def test_moe_with_identical_experts_ignores_the_router():
+    cfg = configs.MOE_SMALL
+    Wt = _moe_weights(cfg)
+    for l in range(cfg.n_layers):
+        for e in range(1, cfg.n_experts):
+            for n in ("wg", "wu", "wd"):
+                Wt[f"L{l}.x{e}.{n}"] = Wt[f"L{l}.x0.{n}"]
+    ids = init.token_ids(0, cfg.batch, cfg.prompt_len, cfg.vocab)
+    a = of.llama_generate(cfg, Wt, ids)
+    dc, Wd = _dense_twin(cfg, Wt)
+    b = of.llama_generate(dc, Wd, ids)
+    for x, y in zip(a["logits"], b["logits"]):
+        assert rel_l2(x, y) < 1e-13
+    # every token still picks top_k distinct experts
+    for seg in a["routes"]:
+        for idx, wts, _ in seg:
+            assert all(len(set(r)) == cfg.top_k for r in idx)
+
+
+def test_moe_all_experts_with_a_flat_router_average_them():
+    import dataclasses
+    cfg = dataclasses.replace(configs.MOE_SMALL, top_k=configs.MOE_SMALL.n_experts)
+    Wt = _moe_weights(cfg)
+    h = np.random.default_rng(2).standard_normal((7, cfg.hidden))
+    Lw = of.layer_weights(Wt, 0)
+    Lw["router"] = np.zeros_like(Lw["router"])
+    y, idx, wts, _ = of.moe_mlp(cfg, Lw, h)
+    assert np.array_equal(idx, np.tile(np.arange(cfg.n_experts, dtype=np.int32), (7, 1)))
+    mean = sum(of.expert_mlp(h, {n: Lw[f"x{e}.{n}"] for n in ("wg", "wu", "wd")})
+               for e in range(cfg.n_experts)) / cfg.n_experts
+    assert rel_l2(y, mean) < 1e-14
+
+
+def test_moe_is_invariant_to_expert_order():
+    cfg = configs.MOE_SMALL
+    Wt = _moe_weights(cfg)
+    h = np.random.default_rng(4).standard_normal((9, cfg.hidden))
+    Lw = of.layer_weights(Wt, 1)
+    y, idx, wts, _ = of.moe_mlp(cfg, Lw, h)
+    perm = np.array([2, 0, 3, 1])
+    Lp = dict(Lw)
+    Lp["router"] = Lw["router"][perm]
+    for new, old in enumerate(perm):
+        for n in ("wg", "wu", "wd"):
+            Lp[f"x{new}.{n}"] = Lw[f"x{old}.{n}"]
+    yp, idxp, wtsp, _ = of.moe_mlp(cfg, Lp, h)
+    assert rel_l2(yp, y) < 1e-14
+    assert np.array_equal(perm[idxp], idx) and np.allclose(wtsp, wts, atol=1e-15)
+
+
+def test_forced_routes_reproduce_or_change_the_run():
+    cfg = configs.MOE_SMALL
+    Wt = _moe_weights(cfg)
+    ids = init.token_ids(0, cfg.batch, cfg.prompt_len, cfg.vocab)
+    a = of.llama_generate(cfg, Wt, ids)
+    own = [[idx for idx, _, _ in seg] for seg in a["routes"]]
+    b = of.llama_generate(cfg, Wt, ids, forced_routes=own)
+    for x, y in zip(a["logits"], b["logits"]):
+        assert np.array_equal(x, y)
+    other = [[(idx + 1) % cfg.n_experts for idx in seg] for seg in own]
+    c = of.llama_generate(cfg, Wt, ids, forced_routes=other)
+    assert not np.allclose(c["logits"][0], a["logits"][0])

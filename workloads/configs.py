@@ -17,6 +17,7 @@ class DecoderConfig:
     name: str
     style: str              # "gpt": LayerNorm + GELU FFN + fused qkv, tied head
                             # "llama": RMSNorm + SwiGLU + RoPE + KV cache, untied head
+                            # "moe": llama attention, then top-k of n_experts SwiGLU experts
     n_layers: int
     hidden: int
     n_heads: int
@@ -30,6 +31,8 @@ class DecoderConfig:
     logits_all: bool = False           # gpt style: logits at every position (else last only)
     seed: int = 0
     iterations: int = 1                # gpt style: forward passes over the same ids
+    n_experts: int = 0                 # moe style: experts per layer (ffn is each expert's width)
+    top_k: int = 0                     # moe style: experts routed per token
 
     @property
     def head_dim(self) -> int:
@@ -67,4 +70,14 @@ LLAMA_SMALL = DecoderConfig("llama-small", "llama", 2, 256, 2, 512, 1000, DT_BF1
 GPT_SMALL = DecoderConfig("gpt-small", "gpt", 2, 256, 2, 640, 1000, DT_BF16,
                           2, 160, factor=(5, 4))
 
-CONFIGS = {c.name: c for c in (TINY, GPT_1P3B, LLAMA_7B, LLAMA_SMALL, GPT_SMALL)}
+# MoE decoder: 32 layers, hidden 4096, 32 heads, 8 SwiGLU experts of width
+# 14336 per layer with top-2 routing from a seeded random router, bf16; prefill
+# 8 x 4096 tokens then 128 greedy steps; budget = footprint / 2.
+MOE_8X = DecoderConfig("moe-8x14336", "moe", 32, 4096, 32, 14336, 32000, DT_BF16,
+                       8, 4096, decode_steps=128, factor=(2, 1), n_experts=8, top_k=2)
+
+# Small MoE for parity tests (4 experts, top-2).
+MOE_SMALL = DecoderConfig("moe-small", "moe", 2, 256, 2, 384, 1000, DT_BF16,
+                          2, 40, decode_steps=6, factor=(2, 1), n_experts=4, top_k=2)
+
+CONFIGS = {c.name: c for c in (TINY, GPT_1P3B, LLAMA_7B, LLAMA_SMALL, GPT_SMALL, MOE_8X, MOE_SMALL)}

@@ -35,13 +35,18 @@ OP_ATTN_QKV = 8       # (B, S, nH, d)        qkv R, o W   causal, fused qkv rows
 OP_ROPE_KV = 9        # (B, S, nH, d, Lmax, pos0)  q RW, k R, v R, Kc W|RW, Vc W|RW
 OP_ATTN_CACHE = 10    # (B, S, nH, d, Lmax, pos0)  q R, Kc R, Vc R, o W
 OP_ARGMAX = 11        # (B, V, gen_row)      logits R, tok W [, gen RW]
+OP_MOE_ROUTE = 12     # (M, H, E, K)         h R, Wr R, rte W, rtw W    top-K of E router logits
+OP_MOE_DISPATCH = 13  # (M, E, K, log_row)   rte R, lists W, log RW     per-expert ordered row lists
+OP_MOE_UP = 14        # (M, F, H, e, n, K)   h R, lists R, Wg R, Wu R, fe W   routed rows of expert e
+OP_MOE_DOWN = 15      # (M, H, F, e, n, K)   fe R, lists R, rtw R, Wd R, x RW  weighted scatter-add
 
 OP_NAMES = {
     OP_TOUCH: "touch", OP_EMBED: "embed", OP_LAYERNORM: "layernorm",
     OP_RMSNORM: "rmsnorm", OP_LINEAR: "linear", OP_LINEAR_GELU: "linear_gelu",
     OP_LINEAR_RESID: "linear_resid", OP_LINEAR_SWIGLU: "linear_swiglu",
     OP_ATTN_QKV: "attn_qkv", OP_ROPE_KV: "rope_kv", OP_ATTN_CACHE: "attn_cache",
-    OP_ARGMAX: "argmax",
+    OP_ARGMAX: "argmax", OP_MOE_ROUTE: "moe_route", OP_MOE_DISPATCH: "moe_dispatch",
+    OP_MOE_UP: "moe_up", OP_MOE_DOWN: "moe_down",
 }
 
 # planner policy variants (paper's ablation ladder plus the two demand baselines)

@@ -17,7 +17,8 @@ from .format import (ALIGN, DT_F32, DT_I32, DT_SIZE, FLAG_HOST_INIT, KIND_ACT,
                      KIND_KV, KIND_PARAM, MODE_R, MODE_RW, MODE_W, OP_ARGMAX,
                      OP_ATTN_CACHE, OP_ATTN_QKV, OP_EMBED, OP_LAYERNORM,
                      OP_LINEAR, OP_LINEAR_GELU, OP_LINEAR_RESID,
-                     OP_LINEAR_SWIGLU, OP_RMSNORM, OP_ROPE_KV)
+                     OP_LINEAR_SWIGLU, OP_MOE_DISPATCH, OP_MOE_DOWN,
+                     OP_MOE_ROUTE, OP_MOE_UP, OP_RMSNORM, OP_ROPE_KV)
 
 
 def align_up(n: int, a: int = ALIGN) -> int:
@@ -98,11 +99,20 @@ class Workload:
         return (self.footprint * den // num) // ALIGN * ALIGN
 
 
-def build(cfg: DecoderConfig) -> Workload:
+def build(cfg: DecoderConfig, routing=None) -> Workload:
+    """The workload of a config.
+
+    For MoE configs ``routing`` is the per-expert row count of every MoE layer
+    in every run segment (prefill, then each decode step), as the dispatch
+    kernels log it (``routing[seg][layer][expert]``).  The trace then holds the
+    expert kernels of routed experts only.  Without it every expert of every
+    layer gets its kernels (the profiling trace), each expected to see all
+    rows.
+    """
     if cfg.style == "gpt":
         return _build_gpt(cfg)
-    if cfg.style == "llama":
-        return _build_llama(cfg)
+    if cfg.style in ("llama", "moe"):
+        return _build_llama(cfg, routing)
     raise ValueError(cfg.style)
 
 
@@ -177,26 +187,37 @@ def _gpt_forward(w, c, layers, E, gf, bf, ids, x, h, qkv, attn, ffn, logits, hl)
     return segs
 
 
-def _build_llama(c: DecoderConfig) -> Workload:
+def _build_llama(c: DecoderConfig, routing=None) -> Workload:
     w = Workload(c)
     H, F, V, B, S = c.hidden, c.ffn, c.vocab, c.batch, c.prompt_len
     nH, d, Lmax, T = c.n_heads, c.head_dim, c.kv_len, c.tokens
     dt = c.dtype
+    moe = c.style == "moe"
+    nE, topk = c.n_experts, c.top_k
     E = w.tensor("E", (V, H), dt, KIND_PARAM, init="normal")
     layers = []
     for l in range(c.n_layers):
         p = f"L{l}."
-        layers.append(dict(
+        L = dict(
             g1=w.tensor(p + "attn_norm", (H,), dt, KIND_PARAM, init="ones"),
             wq=w.tensor(p + "wq", (H, H), dt, KIND_PARAM, init="normal"),
             wk=w.tensor(p + "wk", (H, H), dt, KIND_PARAM, init="normal"),
             wv=w.tensor(p + "wv", (H, H), dt, KIND_PARAM, init="normal"),
             wo=w.tensor(p + "wo", (H, H), dt, KIND_PARAM, init="normal"),
             g2=w.tensor(p + "ffn_norm", (H,), dt, KIND_PARAM, init="ones"),
-            wg=w.tensor(p + "wg", (F, H), dt, KIND_PARAM, init="normal"),
-            wu=w.tensor(p + "wu", (F, H), dt, KIND_PARAM, init="normal"),
-            wd=w.tensor(p + "wd", (H, F), dt, KIND_PARAM, init="normal"),
-        ))
+        )
+        if moe:
+            L["wr"] = w.tensor(p + "router", (nE, H), dt, KIND_PARAM, init="normal")
+            L["experts"] = [dict(
+                wg=w.tensor(p + f"x{e}.wg", (F, H), dt, KIND_PARAM, init="normal"),
+                wu=w.tensor(p + f"x{e}.wu", (F, H), dt, KIND_PARAM, init="normal"),
+                wd=w.tensor(p + f"x{e}.wd", (H, F), dt, KIND_PARAM, init="normal"),
+            ) for e in range(nE)]
+        else:
+            L["wg"] = w.tensor(p + "wg", (F, H), dt, KIND_PARAM, init="normal")
+            L["wu"] = w.tensor(p + "wu", (F, H), dt, KIND_PARAM, init="normal")
+            L["wd"] = w.tensor(p + "wd", (H, F), dt, KIND_PARAM, init="normal")
+        layers.append(L)
     gf = w.tensor("norm_f", (H,), dt, KIND_PARAM, init="ones")
     head = w.tensor("head", (V, H), dt, KIND_PARAM, init="normal")
     for l in range(c.n_layers):
@@ -224,10 +245,33 @@ def _build_llama(c: DecoderConfig) -> Workload:
     vd = w.tensor("v_d", (B, H), dt, KIND_ACT)
     ad = w.tensor("a_d", (B, H), dt, KIND_ACT)
     fd = w.tensor("f_d", (B, F), dt, KIND_ACT)
+    if moe:
+        # routing results and per-expert row lists of each phase, and the log
+        # of per-expert row counts (one row of n_experts per segment and layer)
+        rt = {ph: (w.tensor(f"rte_{ph}", (M, topk), DT_I32, KIND_ACT),
+                   w.tensor(f"rtw_{ph}", (M, topk), DT_F32, KIND_ACT),
+                   w.tensor(f"lists_{ph}", (nE, M + 1), DT_I32, KIND_ACT))
+              for ph, M in (("p", T), ("d", B))}
+        log = w.tensor("moe_counts", ((1 + c.decode_steps) * c.n_layers, nE), DT_I32, KIND_ACT,
+                       host_init=True, init="zeros")
 
     R, W_, RW = MODE_R, MODE_W, MODE_RW
 
-    def block(l, L, x, h, q, k, v, a, f, M, s_len, pos0, kv_mode):
+    def moe_ffn(l, L, x, h, f, M, seg):
+        rte, rtw, lists = rt["p" if seg == 0 else "d"]
+        w.kernel(OP_MOE_ROUTE, (M, H, nE, topk), [(h, R), (L["wr"], R), (rte, W_), (rtw, W_)], l, "route")
+        w.kernel(OP_MOE_DISPATCH, (M, nE, topk, seg * c.n_layers + l),
+                 [(rte, R), (lists, W_), (log, RW)], l, "dispatch")
+        for e, X in enumerate(L["experts"]):
+            n = M if routing is None else int(routing[seg][l][e])
+            if n == 0:
+                continue
+            w.kernel(OP_MOE_UP, (M, F, H, e, n, topk), [(h, R), (lists, R), (X["wg"], R), (X["wu"], R), (f, W_)],
+                     l, "expert_up")
+            w.kernel(OP_MOE_DOWN, (M, H, F, e, n, topk),
+                     [(f, R), (lists, R), (rtw, R), (X["wd"], R), (x, RW)], l, "expert_down")
+
+    def block(l, L, x, h, q, k, v, a, f, M, s_len, pos0, kv_mode, seg=0):
         w.kernel(OP_RMSNORM, (M, H, 1, 0), [(x, R), (L["g1"], R), (h, W_)], l, "attn_norm")
         w.kernel(OP_LINEAR, (M, H, H), [(h, R), (L["wq"], R), (q, W_)], l, "wq")
         w.kernel(OP_LINEAR, (M, H, H), [(h, R), (L["wk"], R), (k, W_)], l, "wk")
@@ -238,6 +282,9 @@ def _build_llama(c: DecoderConfig) -> Workload:
                  [(q, R), (L["K"], R), (L["V"], R), (a, W_)], l, "attn")
         w.kernel(OP_LINEAR_RESID, (M, H, H), [(a, R), (L["wo"], R), (x, RW)], l, "wo")
         w.kernel(OP_RMSNORM, (M, H, 1, 0), [(x, R), (L["g2"], R), (h, W_)], l, "ffn_norm")
+        if moe:
+            moe_ffn(l, L, x, h, f, M, seg)
+            return
         w.kernel(OP_LINEAR_SWIGLU, (M, F, H), [(h, R), (L["wg"], R), (L["wu"], R), (f, W_)], l, "gate_up")
         w.kernel(OP_LINEAR_RESID, (M, H, F), [(f, R), (L["wd"], R), (x, RW)], l, "wd")
 
@@ -257,7 +304,7 @@ def _build_llama(c: DecoderConfig) -> Workload:
         pos = S + s
         w.kernel(OP_EMBED, (B, H, V), [(tok, R), (E, R), (xd, W_)], 0, "embed")
         for l, L in enumerate(layers):
-            block(l, L, xd, hd, qd, kd, vd, ad, fd, B, 1, pos, RW)
+            block(l, L, xd, hd, qd, kd, vd, ad, fd, B, 1, pos, RW, seg=s + 1)
         w.kernel(OP_RMSNORM, (B, H, 1, 0), [(xd, R), (gf, R), (hl, W_)], c.n_layers, "norm_f")
         w.kernel(OP_LINEAR, (B, V, H), [(hl, R), (head, R), (logits, W_)], c.n_layers, "head")
         w.kernel(OP_ARGMAX, (B, V, s + 1), [(logits, R), (tok, W_), (gen, RW)], c.n_layers, "argmax")
