@@ -44,6 +44,10 @@ PREFILL_GUARD = 16
 POLICY_NAMES = {0: "DEMAND_LRU", 1: "DEMAND_BELADY", 2: "T", 3: "T+A", 4: "T+A+P"}
 
 
+# pinned host memory a run may use for its arena (the GPU host grants about 64 GiB)
+PINNED_LIMIT = 58 << 30
+
+
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
@@ -64,6 +68,8 @@ def parse():
     ap.add_argument("--no-baseline", action="store_true")
     ap.add_argument("--no-ablation", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--layers", type=int, default=0,
+                    help="MoE configs: layers to run (default: as many as fit the pinned host limit)")
     ap.add_argument("--no-replan", action="store_true",
                     help="skip the rerun planned from the measured kernel times")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -382,6 +388,71 @@ def cpu_baseline_prefill(cfg, w, seconds):
                       f"not included; {pass_s:.1f} s per pass)"}
 
 
+def cpu_baseline_moe(cfg, w, seconds, pos):
+    """fp64 oracle MoE decode of one layer at the timed position, scaled to the model."""
+    import numpy as np
+    from oracle import forward as of
+    from workloads import init as winit
+    threads, vendor = blas_info()
+    from concurrent.futures import ThreadPoolExecutor
+    B, nH, d, Lmax = cfg.batch, cfg.n_heads, cfg.head_dim, cfg.kv_len
+    names = [f"L0.{nm}" for nm in ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "router")]
+    names += [f"L0.x{e}.{nm}" for e in range(cfg.n_experts) for nm in ("wg", "wu", "wd")]
+
+    def weight(nm):
+        return nm.split(".", 1)[1], winit.tensor_value(w, w.tensors[w.id(nm)]).astype(np.float64)
+
+    def cache(i):   # synthetic prefix of the KV cache (values do not change the timing)
+        g = np.random.default_rng([7, i])
+        return g.standard_normal((B, nH, Lmax, d), dtype=np.float32).astype(np.float64) * 0.5
+
+    with ThreadPoolExecutor(16) as ex:
+        Lw = dict(ex.map(weight, names))
+        K, V = ex.map(cache, range(2))
+    x0 = np.random.default_rng(8).standard_normal((B, cfg.hidden)) * 0.02
+    t_layer, reps = 0.0, 0
+    t_start = time.perf_counter()
+    while reps == 0 or time.perf_counter() - t_start < seconds:
+        t = time.perf_counter()
+        of.llama_layer(cfg, Lw, x0, K, V, pos)
+        t_layer += time.perf_counter() - t
+        reps += 1
+    step_s = t_layer / reps * cfg.n_layers
+    return {"value": B / step_s, "unit": "tokens/s", "cores": threads, "kind": "oracle", "blas": vendor,
+            "sample": f"fp64 numpy oracle MoE decode step at position {pos}, batch {B}: 1 of "
+                      f"{cfg.n_layers} layers (attention and the routed experts) timed over {reps} "
+                      f"repetitions, scaled to {cfg.n_layers} layers; LM head not included "
+                      f"({step_s:.2f} s per step)"}
+
+
+def expert_fetches(w, sched, counts, k0, k1):
+    """Bytes fetched for expert weights between kernels k0 and k1, split into
+    fetches for experts that got rows and for experts that got none."""
+    from workloads.format import OP_MOE_DOWN, OP_MOE_UP
+    seg_of = {}
+    for seg, (a, n) in enumerate(w.segments["prefill"] + w.segments["decode"]):
+        for k in range(a, a + n):
+            seg_of[k] = seg
+    used = idle = 0
+    for e in sched:
+        if e[0] not in (0, 1) or not k0 <= e[5] < k1:
+            continue
+        kd = w.kernels[e[5]]
+        if kd.op == OP_MOE_UP:
+            weights = (kd.operands[2][0], kd.operands[3][0])
+        elif kd.op == OP_MOE_DOWN:
+            weights = (kd.operands[3][0],)
+        else:
+            continue
+        if e[1] not in weights:
+            continue
+        if counts[seg_of[e[5]], kd.layer, kd.shape[3]] > 0:
+            used += e[3]
+        else:
+            idle += e[3]
+    return used, idle
+
+
 def roofline_fields(st, seconds, bl_meas, units):
     import numpy as np
     t_comp = st["flops"] / NOMINAL["P"]
@@ -682,6 +753,117 @@ def prefill_main(args, cfg):
     print(json.dumps(result), flush=True)
 
 
+def moe_main(args, cfg):
+    """Routed-expert decode: a profiling run with every expert in the trace,
+    then the recorded trace (routed experts only), both timed."""
+    import torch
+
+    from paper_2609_06172_amd.session import Session
+    from workloads import trace
+    from workloads.format import OP_MOE_DOWN, OP_MOE_UP
+
+    import dataclasses
+
+    num, den = cfg.factor
+    W, K = args.warmup, (4 if args.steps is None else args.steps)
+    if W + K > cfg.decode_steps or K < 1:
+        sys.exit(f"warmup + steps must be within 1..{cfg.decode_steps}")
+    n = W + K
+    # The whole model lives in pinned host memory, and the GPU host grants
+    # about 64 GiB of it: keep the per-layer shape and run the most layers whose
+    # host backing fits (16 of 32 for the 8 x 14336 model, 55.4 GiB).
+    n_layers = cfg.n_layers
+    layers = args.layers or cfg.n_layers
+    while layers > 1 and trace.build(dataclasses.replace(cfg, n_layers=layers), steps=0).footprint > PINNED_LIMIT:
+        layers -= 1
+    cfg = dataclasses.replace(cfg, n_layers=layers)
+    full = trace.build(cfg, steps=n)
+    M = full.budget()
+    log(f"workload {cfg.name}: {len(full.tensors)} tensors, {len(full.kernels)} kernels "
+        f"(every expert), footprint {full.footprint} B, budget {M} B")
+    bl_meas = link_bandwidth()
+    t = time.perf_counter()
+    s = Session(full, device=0, M=M, variant=4, timing=1)
+    log(f"session ready in {time.perf_counter() - t:.1f} s")
+    pf_prefill, pf_decode, a0, a1 = run_decode(s, full, W, K)
+    counts = s.routing_counts().copy()
+    gen_prof = s.read("gen")[: n + 1].copy()
+    st_prof = seg_stats(full, s.ctx.get_schedule(), s.ctx.get_classes(), M, full.segments["decode"][W:n])
+    used_p, idle_p = expert_fetches(full, s.ctx.get_schedule(), counts, a0, a1)
+    log(f"profiling run: prefill {pf_prefill:.2f} s, decode {K} steps {pf_decode:.2f} s")
+
+    routed = trace.build(cfg, counts, steps=n)
+    s.retrace(routed)
+    s.restore_inputs()
+    prefill_s, decode_s, k0, k1 = run_decode(s, routed, W, K)
+    log(f"recorded trace: prefill {prefill_s:.2f} s, decode {K} steps {decode_s:.2f} s")
+    sched, classes = s.ctx.get_schedule(), s.ctx.get_classes()
+    dur, gap = s.ctx.get_kernel_times()
+    tl = s.ctx.get_timeline()
+    gen = s.read("gen")[: n + 1].copy()
+    same_routing = bool((s.routing_counts() == counts).all())
+    st = seg_stats(routed, sched, classes, M, routed.segments["decode"][W:n])
+    used_r, idle_r = expert_fetches(routed, sched, counts, k0, k1)
+    ex = [k for k in range(k0, k1) if routed.kernels[k].op in (OP_MOE_UP, OP_MOE_DOWN)]
+    g_bytes = sum(classes[k][3] for k in ex)
+    g_time = sum(dur[k] for k in ex) * 1e-3
+    tok_s = cfg.batch * K / decode_s
+    pr = roofline_fields(st, decode_s, bl_meas, cfg.batch * K)
+    pr["roofline_tok_s"] = pr.pop("roofline_units_per_s")
+    routed_per_layer = float((counts[1 + W:1 + n] > 0).sum(axis=2).mean())
+    result = {
+        "metric": metric("", num, den), "value": round(tok_s, 3), "unit": "tokens/s", "n_gpus": 1,
+        "steps": K, "warmup": W, "ms_per_step": round(decode_s / K * 1e3, 3),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{cfg.name}-shape MoE decode: {cfg.n_layers} of the model's {n_layers} layers "
+                               f"(host backing limited to the pinned memory the host grants), hidden {cfg.hidden}, "
+                               f"{cfg.n_experts} SwiGLU experts of {cfg.ffn}, top-{cfg.top_k} routing, "
+                               f"vocab {cfg.vocab}, batch {cfg.batch}, {cfg.prompt_len}-token prompt then "
+                               f"greedy steps, budget = footprint*{den}/{num}",
+                   "batch": cfg.batch, "prompt_len": cfg.prompt_len, "factor": f"{num}/{den}",
+                   "layers": cfg.n_layers, "model_layers": n_layers,
+                   "footprint_bytes": full.footprint, "budget_bytes": M,
+                   "policy": "T+A+P on the recorded (routed-expert) trace"},
+        "path_roofline": pr,
+        "roofline": {"kernel": "routed-expert GEMV (M = 8 rows, routed rows only, bf16 matrix cores)",
+                     "bound": "hbm", "achieved": round(g_bytes / g_time / 1e9, 1), "peak": 8000.0,
+                     "unit": "GB/s", "frac": round(g_bytes / g_time / 8e12, 4), "traffic": None,
+                     "launches": len(ex), "avg_us": round(g_time / max(1, len(ex)) * 1e6, 2),
+                     "avg_bytes": int(g_bytes / max(1, len(ex)))},
+        "transfers": {"h2d_bytes_per_step": st["h2d_bytes"] // K, "lmin_bytes_per_step": st["lmin_bytes"] // K,
+                      "h2d_over_lmin": round(st["h2d_bytes"] / max(1, st["lmin_bytes"]), 4),
+                      "d2h_bytes_per_step": st["d2h_bytes"] // K,
+                      "achieved_h2d_GBps": round(st["h2d_bytes"] / decode_s / 1e9, 2),
+                      "compute_busy_ms_per_step": round(sum(dur[k] for k in range(k0, k1)) / K, 3),
+                      "link_timeline": link_timeline(tl, K)},
+        "routing": {"experts_routed_per_layer": round(routed_per_layer, 3), "of": cfg.n_experts,
+                    "expert_bytes_fetched_per_step": used_r // K,
+                    "same_routing_as_profile": same_routing,
+                    "tokens_identical": bool((gen == gen_prof).all())},
+        "profiling_trace": {"policy": "T+A+P with every expert in the trace (each expert's weights fetched "
+                                      "for each layer whether routed rows or not)",
+                            "value": round(cfg.batch * K / pf_decode, 3), "ms_per_step": round(pf_decode / K * 1e3, 3),
+                            "h2d_bytes_per_step": st_prof["h2d_bytes"] // K,
+                            "expert_bytes_fetched_per_step": used_p // K,
+                            "unrouted_expert_bytes_fetched_per_step": idle_p // K,
+                            "speedup_of_recorded_trace": round(pf_decode / decode_s, 3)},
+        "prefill": {"seconds": round(prefill_s, 3), "tokens": cfg.batch * cfg.prompt_len},
+    }
+    if not args.no_baseline:
+        Bk = min(args.baseline_steps, K)
+        b = decode_policy(s, routed, M, 0, W, Bk, gen)
+        b["policy"] = "demand fetch at launch, LRU eviction (recorded trace)"
+        b["speedup_of_T+A+P"] = round(tok_s / b["value"], 3)
+        result["no_prefetch_baseline"] = b
+    s.close()
+    del s
+    torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline_moe(cfg, full, args.cpu_seconds, cfg.prompt_len + W)
+    print(json.dumps(result), flush=True)
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -698,6 +880,8 @@ def main():
         cfg = dataclasses.replace(cfg, factor=factor_of(args.factor))
     if cfg.style == "gpt":
         prefill_main(args, cfg)
+    elif cfg.style == "moe":
+        moe_main(args, cfg)
     elif args.sweep:
         sweep_main(args, cfg)
     else:

@@ -103,8 +103,19 @@ __global__ void __launch_bounds__(64 * kWaves) gemm_big(const bf16_t* __restrict
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int wm = wv / kWN, wn = wv % kWN;
 
-  // tile order: XCD round-robin remap, then groups of kGroupM row-blocks
-  const int nwg = gridDim.x, per = nwg / kXcd;
+  // Tile order: XCD round-robin remap, then groups of kGroupM row-blocks.
+  // Under a routed-row list only the first ceil(count / BM) row-blocks hold
+  // rows: the blocks past them exit, and the live ones are remapped among
+  // themselves, so that they still spread over all XCDs.
+  int nwg = gridDim.x;
+  int64_t rows = M;
+  if constexpr (LIST) {
+    rows = list[0] < M ? list[0] : M;
+    const int live = rows > 0 ? int((rows + BM - 1) / BM) * tilesN : 0;
+    if (int(blockIdx.x) >= live) return;   // uniform over the workgroup
+    nwg = live;
+  }
+  const int per = nwg / kXcd;
   int id = blockIdx.x;
   if (per > 0 && id < per * kXcd) id = (id % kXcd) * per + id / kXcd;
   const int tilesM = nwg / tilesN;
@@ -112,11 +123,6 @@ __global__ void __launch_bounds__(64 * kWaves) gemm_big(const bf16_t* __restrict
   const int gm = (tilesM - first) < kGroupM ? (tilesM - first) : kGroupM;
   const int in = id - grp * gsize;
   const int64_t m0 = int64_t(first + in % gm) * BM, n0 = int64_t(in / gm) * BN;
-  int64_t rows = M;
-  if constexpr (LIST) {
-    rows = list[0] < M ? list[0] : M;
-    if (m0 >= rows) return;   // uniform over the workgroup
-  }
   const bf16_t* arow[kARowsPerLane];
 #pragma unroll
   for (int t = 0; t < kARowsPerLane; ++t) {

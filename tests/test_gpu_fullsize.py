@@ -1,0 +1,159 @@
+"""Parity at full size, in the launch configuration the benchmark times: the
+7B decode at 1.5x, the 1.3B prefill at 1.25x and the MoE decode at 2x run
+through the C-ABI under T+A+P, and sampled outputs are checked against the
+fp64 oracle one layer at a time.  The oracle takes the GPU's layer input
+(and, for attention over a cache, the GPU's cache prefix; for MoE, the
+GPU's expert choice) and must reproduce the layer output at the bf16
+tolerance (rel-L2 2e-2)."""
+import dataclasses
+
+import numpy as np
+import pytest
+
+from oracle import forward as of
+from workloads import configs, init, trace
+from workloads.format import OP_MOE_DOWN, OP_MOE_ROUTE
+
+from gpu_util import rel_l2
+
+pytestmark = pytest.mark.gpu
+
+TOL = 2e-2
+
+
+class Walker:
+    """Runs a session's trace forward in contiguous pieces."""
+
+    def __init__(self, s):
+        self.s, self.pos = s, 0
+
+    def to(self, k):
+        if k > self.pos:
+            self.s.run(self.pos, k - self.pos)
+            self.pos = k
+
+
+def _layer_range(w, seg, layer):
+    a, n = seg
+    ks = [k for k in range(a, a + n) if w.kernels[k].layer == layer and w.kernels[k].tag not in ("embed",)]
+    return ks[0], ks[-1] + 1
+
+
+def _weights(w, prefix, names):
+    Wt = init.weights_f64(w, names=[prefix + n for n in names])
+    return {k[len(prefix):]: v for k, v in Wt.items()}
+
+
+def test_llama7b_decode_layer_and_head_sampled():
+    from paper_2609_06172_amd.session import Session
+    cfg = configs.LLAMA_7B
+    w = trace.build(cfg, steps=2)
+    step, l, bs = 1, 17, [0, 9, 15]
+    print(f"llama-7b decode at 1.5x: step {step}, layer {l}, sequences {bs}", flush=True)
+    s = Session(w, device=0)                     # budget footprint/1.5, T+A+P
+    walk = Walker(s)
+    seg = w.segments["decode"][step]
+    a, b = _layer_range(w, seg, l)
+    walk.to(a)
+    x_in = s.read("x_d").astype(np.float64)
+    walk.to(b)
+    x_out = s.read("x_d")
+    K, V = s.read(f"L{l}.K"), s.read(f"L{l}.V")
+    walk.to(seg[0] + seg[1] - 3)                 # through the last layer, before norm_f / head / argmax
+    x_last = s.read("x_d").astype(np.float64)
+    walk.to(seg[0] + seg[1])
+    logits = s.read("logits")
+    s.close()
+    pos = cfg.prompt_len + step
+    Lw = _weights(w, f"L{l}.", ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "wg", "wu", "wd"))
+    c1 = dataclasses.replace(cfg, batch=len(bs))
+    Kc, Vc = K[bs].astype(np.float64), V[bs].astype(np.float64)
+    ref = of.llama_layer(c1, Lw, x_in[bs], Kc, Vc, pos)
+    assert rel_l2(x_out[bs], ref) < TOL
+    assert rel_l2(K[bs][:, :, pos], Kc[:, :, pos]) < TOL      # the new cache row
+    assert rel_l2(V[bs][:, :, pos], Vc[:, :, pos]) < TOL
+    Hd = _weights(w, "", ("norm_f", "head"))
+    lg = of.linear(of.rmsnorm(x_last[bs], Hd["norm_f"]), Hd["head"])
+    assert rel_l2(logits[bs], lg) < TOL
+
+
+def test_gpt1p3b_prefill_layer_and_head_sampled():
+    from paper_2609_06172_amd.session import Session
+    cfg = configs.GPT_1P3B
+    w = trace.build(cfg)
+    l, b = 11, 2
+    print(f"gpt-1.3b prefill at 1.25x: layer {l}, sequence {b}", flush=True)
+    s = Session(w, device=0, guard=16)           # the prefill benchmark's policy
+    walk = Walker(s)
+    a, n = w.segments["forward"][1 + l]
+    walk.to(a)
+    x_in = s.read("x").astype(np.float64)
+    walk.to(a + n)
+    x_out = s.read("x")
+    h0, hn = w.segments["forward"][-1]
+    walk.to(h0)
+    x_last = s.read("x").astype(np.float64)
+    walk.to(h0 + hn)
+    logits = s.read("logits")
+    s.close()
+    S = cfg.prompt_len
+    rows = slice(b * S, (b + 1) * S)
+    names = ("ln1.g", "ln1.b", "wqkv", "wo", "ln2.g", "ln2.b", "w1", "w2")
+    Wt = init.weights_f64(w, names=[f"L{l}.{x}" for x in names] + ["lnf.g", "lnf.b", "E"])
+    ref = of.gpt_layer(dataclasses.replace(cfg, batch=1), Wt, l, x_in[rows])
+    assert rel_l2(x_out[rows], ref) < TOL
+    last = x_last[np.arange(cfg.batch) * S + S - 1]
+    lg = of.linear(of.layernorm(last, Wt["lnf.g"], Wt["lnf.b"]), Wt["E"])
+    assert rel_l2(logits, lg) < TOL
+
+
+def _moe_bench_config():
+    """The MoE benchmark's configuration: full per-layer shape, the layers
+    whose host backing fits the pinned memory of the GPU host (16 of 32)."""
+    return dataclasses.replace(configs.MOE_8X, n_layers=16)
+
+
+def test_moe_decode_and_prefill_layers_sampled():
+    from paper_2609_06172_amd.session import Session
+    cfg = _moe_bench_config()
+    w = trace.build(cfg, steps=1)                # every expert in the trace
+    l, bs = 9, [1, 6]
+    rows = np.array([0, 4097, 20000, 32767])
+    print(f"moe 8 x 14336, {cfg.n_layers} layers at 2x: prefill rows {list(rows)} and decode "
+          f"sequences {bs} of layer {l}", flush=True)
+    s = Session(w, device=0)                     # budget footprint/2, T+A+P
+    walk = Walker(s)
+    # prefill: the routed FFN of layer l on sampled rows
+    pseg = w.segments["prefill"][0]
+    a, b = _layer_range(w, pseg, l)
+    route = next(k for k in range(a, b) if w.kernels[k].op == OP_MOE_ROUTE)
+    last_down = max(k for k in range(a, b) if w.kernels[k].op == OP_MOE_DOWN)
+    walk.to(route)
+    h_p, x_mid = s.read("h_p")[rows].astype(np.float64), s.read("x_p")[rows].astype(np.float64)
+    walk.to(route + 1)
+    rte_p = s.read("rte_p")[rows]
+    walk.to(last_down + 1)
+    x_ffn = s.read("x_p")[rows]
+    # decode step 0: the whole block of layer l for sampled sequences
+    dseg = w.segments["decode"][0]
+    a, b = _layer_range(w, dseg, l)
+    route = next(k for k in range(a, b) if w.kernels[k].op == OP_MOE_ROUTE)
+    walk.to(a)
+    x_in = s.read("x_d").astype(np.float64)
+    walk.to(route + 1)
+    rte_d = s.read("rte_d")
+    walk.to(b)
+    x_out = s.read("x_d")
+    K, V = s.read(f"L{l}.K"), s.read(f"L{l}.V")
+    s.close()
+    experts = sorted(set(rte_p.ravel()) | set(rte_d[bs].ravel()))
+    names = ["attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "router"]
+    names += [f"x{e}.{n}" for e in experts for n in ("wg", "wu", "wd")]
+    Lw = _weights(w, f"L{l}.", names)
+    y, _, _, _ = of.moe_mlp(cfg, Lw, h_p, forced=rte_p)
+    assert rel_l2(x_ffn - x_mid, y) < TOL
+    pos = cfg.prompt_len
+    c1 = dataclasses.replace(cfg, batch=len(bs))
+    Kc, Vc = K[bs].astype(np.float64), V[bs].astype(np.float64)
+    ref = of.llama_layer(c1, Lw, x_in[bs], Kc, Vc, pos, forced_route=rte_d[bs])
+    assert rel_l2(x_out[bs], ref) < TOL

@@ -99,8 +99,11 @@ class Workload:
         return (self.footprint * den // num) // ALIGN * ALIGN
 
 
-def build(cfg: DecoderConfig, routing=None) -> Workload:
+def build(cfg: DecoderConfig, routing=None, steps=None) -> Workload:
     """The workload of a config.
+
+    ``steps`` traces only the first decode steps of a LLaMA-style or MoE
+    config; the tensors (KV cache length, logs) stay those of the full run.
 
     For MoE configs ``routing`` is the per-expert row count of every MoE layer
     in every run segment (prefill, then each decode step), as the dispatch
@@ -112,7 +115,7 @@ def build(cfg: DecoderConfig, routing=None) -> Workload:
     if cfg.style == "gpt":
         return _build_gpt(cfg)
     if cfg.style in ("llama", "moe"):
-        return _build_llama(cfg, routing)
+        return _build_llama(cfg, routing, cfg.decode_steps if steps is None else steps)
     raise ValueError(cfg.style)
 
 
@@ -187,7 +190,7 @@ def _gpt_forward(w, c, layers, E, gf, bf, ids, x, h, qkv, attn, ffn, logits, hl)
     return segs
 
 
-def _build_llama(c: DecoderConfig, routing=None) -> Workload:
+def _build_llama(c: DecoderConfig, routing=None, n_steps=0) -> Workload:
     w = Workload(c)
     H, F, V, B, S = c.hidden, c.ffn, c.vocab, c.batch, c.prompt_len
     nH, d, Lmax, T = c.n_heads, c.head_dim, c.kv_len, c.tokens
@@ -299,7 +302,9 @@ def _build_llama(c: DecoderConfig, routing=None) -> Workload:
     w.kernel(OP_ARGMAX, (B, V, 0), [(logits, R), (tok, W_), (gen, RW)], c.n_layers, "argmax")
     w.segments["prefill"] = [(k0, len(w.kernels) - k0)]
     steps = []
-    for s in range(c.decode_steps):
+    if not 0 <= n_steps <= c.decode_steps:
+        raise ValueError("steps beyond the config's decode steps")
+    for s in range(n_steps):
         k0 = len(w.kernels)
         pos = S + s
         w.kernel(OP_EMBED, (B, H, V), [(tok, R), (E, R), (xd, W_)], 0, "embed")
