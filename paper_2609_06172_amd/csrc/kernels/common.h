@@ -25,7 +25,21 @@ __device__ __forceinline__ float ld(const bf16_t* p, int64_t i) { return bf2f(p[
 __device__ __forceinline__ void st(float* p, int64_t i, float v) { p[i] = v; }
 __device__ __forceinline__ void st(bf16_t* p, int64_t i, float v) { p[i] = f2bf(v); }
 
-__device__ __forceinline__ float gelu_erf(float x) { return 0.5f * x * (1.0f + erff(x * 0.70710678118654752f)); }
+// Exact-erf GELU, 0.5 x (1 + erf(x / sqrt 2)), with erf from Abramowitz and
+// Stegun's rational approximation 7.1.26 (|error| <= 1.5e-7).  It is written
+// through erfc(z), z = |x| / sqrt 2, so one branch-free expression serves
+// both signs: 1 + erf(x / sqrt 2) is 2 - erfc(z) for x >= 0 and erfc(z)
+// otherwise, with erfc(z) ~= t (a1 + t (a2 + t (a3 + t (a4 + t a5)))) e^(-z^2),
+// t = 1 / (1 + p z).  About a third of the instructions of the library erff,
+// which matters in GEMM epilogues (128 results per lane).
+__device__ __forceinline__ float gelu_erf(float x) {
+  const float z = fabsf(x) * 0.70710678118654752f;
+  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, z, 1.0f));
+  const float poly =
+      t * fmaf(t, fmaf(t, fmaf(t, fmaf(t, 1.061405429f, -1.453152027f), 1.421413741f), -0.284496736f), 0.254829592f);
+  const float q = poly * __builtin_amdgcn_exp2f(-(z * z) * 1.4426950408889634f);
+  return 0.5f * x * (x >= 0.f ? 2.0f - q : q);
+}
 __device__ __forceinline__ float silu(float x) { return x / (1.0f + __expf(-x)); }
 
 // wave64 reductions
