@@ -56,7 +56,10 @@ enum { AUVM_F32 = 0, AUVM_BF16 = 1, AUVM_I32 = 2, AUVM_U8 = 3 };
 /* tensor kinds: parameters start valid on the host */
 enum { AUVM_PARAM = 0, AUVM_ACT = 1, AUVM_KV = 2 };
 /* registration flags: HOST_INIT marks a non-parameter with valid host contents */
-enum { AUVM_HOST_INIT = 1 };
+/* LIVE_OUT: the tensor's final value is read after the trace (model and
+ * optimizer state that the next training step uses): a dirty copy evicted
+ * after its last use is written back, not dropped. */
+enum { AUVM_HOST_INIT = 1, AUVM_LIVE_OUT = 2 };
 /* operand access modes */
 enum { AUVM_R = 1, AUVM_W = 2, AUVM_RW = 3 };
 
@@ -79,8 +82,10 @@ enum { AUVM_R = 1, AUVM_W = 2, AUVM_RW = 3 };
  *  ROPE_KV       (B,S,nH,d,Lmax,pos0) q RW, k R, v R [B*S, nH*d], Kc, Vc [B,nH,Lmax,d]:
  *                                    rotate-half RoPE (base 1e4) on q and k at
  *                                    positions pos0.., k and v stored at pos0..
- *  ATTN_CACHE    (B,S,nH,d,Lmax,pos0) q R, Kc R, Vc R, o W: query i attends to
- *                                    cache positions 0..pos0+i
+ *  ATTN_CACHE    (B,S,nH,d,Lmax,pos0) q R, Kc R, Vc R, o W [, lse W f32[B,nH,S]]:
+ *                                    query i attends to cache positions 0..pos0+i;
+ *                                    lse: the natural log-sum-exp of each query's
+ *                                    scaled scores (kept for the backward pass)
  *  ARGMAX        (B,V,row)           logits R f32[B,V], tok W i32[B], [gen RW i32[.,B]]:
  *                                    lowest index of the row maximum; also gen[row]
  * Routed-expert (MoE) FFN, top-K of E experts (K <= E <= 16), bf16 weights:
@@ -98,6 +103,34 @@ enum { AUVM_R = 1, AUVM_W = 2, AUVM_RW = 3 };
  *  MOE_DOWN      (M,H,F,e,n,K)       fe R, lists R, rtw R, Wd R [H,F], x RW f32[M,H]:
  *                                    for i < count(e): x[tok] += rtw[j] * (fe[i] Wd^T),
  *                                    j = lists[e][1+i], tok = j / K
+ * Training step (backward and optimizer), bf16 activations and weights with
+ * fp32 residual stream, gradients, master weights and moments:
+ *  COPY          (bytes)             a R, b W: device copy of the first bytes
+ *  TRANSPOSE     (R,C)               a R [R,C], b W [C,R] (same dtype)
+ *  SWIGLU_ACT    (T,F)               G R, U R, F W [T,F]: F = silu(G) * U
+ *  SWIGLU_BWD    (T,F)               G R, U R, dF R, dG W, dU W: the gradients of F
+ *  RMSNORM_BWD   (T,H,acc)           x R f32[T,H], g R [H], dy R f32[T,H], dx W|RW f32[T,H],
+ *                                    dxb W bf16[T,H], dg W f32[H], rstd W f32[T]: the
+ *                                    RMSNorm (eps 1e-6) gradients; dx is overwritten
+ *                                    (acc 0) or accumulated into (acc 1), dxb is dx in
+ *                                    bf16, rstd a workspace
+ *  ATTN_BWD      (B,S,nH,d)          q R, K R, V R, o R, lse R, do R, dq W, dK W, dV W, D W:
+ *                                    causal attention gradients from the forward's
+ *                                    operands (q, o, do, dq [B*S, nH*d]; K, V, dK, dV
+ *                                    [B,nH,S,d]; lse, D f32[B,nH,S], D a workspace); d = 128
+ *  ROPE_BWD      (B,S,nH,d)          dq RW, dK R, dV R, dk W, dv W: rotates dq and dK back
+ *                                    (rotate-half, base 1e4, positions 0..S-1), dk, dv
+ *                                    token-major [B*S, nH*d]
+ *  XENT          (T,V)               logits R f32[T,V], labels R i32[T], losses W f32[T],
+ *                                    dlogits W [T,V]: per-row cross-entropy and the
+ *                                    gradient of the mean loss, (softmax - onehot) / T
+ *  EMBED_BWD     (T,H,V)             ids R i32[T], dx R f32[T,H], dE W f32[V,H]: rows of dx
+ *                                    summed into their token's row, in token order
+ *  ADAM          (n,t,lr,b1,b2,eps,wd) g R f32[n], p32 RW f32, m RW f32, v RW f32, p W [n]:
+ *                                    AdamW at step t with decoupled weight decay and
+ *                                    bias correction; hyperparameters in fixed point
+ *                                    (lr*1e9, b1*1e6, b2*1e6, eps*1e12, wd*1e6); p is the
+ *                                    updated p32 in p's dtype
  * Activations between kernels use the tensors' own dtypes (f32 or bf16);
  * arithmetic accumulates in fp32. */
 enum {
@@ -105,7 +138,10 @@ enum {
   AUVM_OP_LINEAR = 4, AUVM_OP_LINEAR_GELU = 5, AUVM_OP_LINEAR_RESID = 6,
   AUVM_OP_LINEAR_SWIGLU = 7, AUVM_OP_ATTN_QKV = 8, AUVM_OP_ROPE_KV = 9,
   AUVM_OP_ATTN_CACHE = 10, AUVM_OP_ARGMAX = 11, AUVM_OP_MOE_ROUTE = 12,
-  AUVM_OP_MOE_DISPATCH = 13, AUVM_OP_MOE_UP = 14, AUVM_OP_MOE_DOWN = 15, AUVM_OP_COUNT = 16
+  AUVM_OP_MOE_DISPATCH = 13, AUVM_OP_MOE_UP = 14, AUVM_OP_MOE_DOWN = 15, AUVM_OP_COPY = 16,
+  AUVM_OP_TRANSPOSE = 17, AUVM_OP_SWIGLU_ACT = 18, AUVM_OP_SWIGLU_BWD = 19, AUVM_OP_RMSNORM_BWD = 20,
+  AUVM_OP_ATTN_BWD = 21, AUVM_OP_ROPE_BWD = 22, AUVM_OP_XENT = 23, AUVM_OP_EMBED_BWD = 24,
+  AUVM_OP_ADAM = 25, AUVM_OP_COUNT = 26
 };
 
 /* policy variants: the paper's ablation ladder (T, T+A, T+A+P; Sec. V-E)

@@ -11,7 +11,9 @@ from workloads.format import (DT_SIZE, MODE_RW, OP_ARGMAX, OP_ATTN_CACHE,
                               OP_LINEAR_GELU, OP_LINEAR_RESID,
                               OP_LINEAR_SWIGLU, OP_MOE_DISPATCH, OP_MOE_DOWN,
                               OP_MOE_ROUTE, OP_MOE_UP, OP_RMSNORM, OP_ROPE_KV,
-                              OP_TOUCH)
+                              OP_TOUCH, OP_COPY, OP_TRANSPOSE, OP_SWIGLU_ACT,
+                              OP_SWIGLU_BWD, OP_RMSNORM_BWD, OP_ATTN_BWD,
+                              OP_ROPE_BWD, OP_XENT, OP_EMBED_BWD, OP_ADAM)
 
 
 def kernel_cost(op, shape, operands, dtypes, nbytes):
@@ -56,6 +58,8 @@ def kernel_cost(op, shape, operands, dtypes, nbytes):
         pairs = S * pos0 + S * (S + 1) // 2
         F = Bt * nH * pairs * (4 * d + 4)
         B = Bt * S * nH * d * (es[0] + es[3]) + Bt * nH * (pos0 + S) * d * (es[1] + es[2])
+        if len(operands) > 4:            # row log-sum-exp for the backward pass
+            B += 4 * Bt * nH * S
         return F, B
     if op == OP_ARGMAX:
         Bt, V = sh[0], sh[1]
@@ -73,4 +77,36 @@ def kernel_cost(op, shape, operands, dtypes, nbytes):
     if op == OP_MOE_DOWN:
         M, H, F, n = sh[0], sh[1], sh[2], sh[4]
         return 2 * n * H * F + 2 * n * H, n * F * es[0] + 4 * (n + 1) + 4 * n + H * F * es[3] + 8 * n * H
+    # training step: every operand element read or written once
+    if op == OP_COPY:
+        return 0, 2 * sh[0]
+    if op == OP_TRANSPOSE:
+        return 0, 2 * sh[0] * sh[1] * es[0]
+    if op == OP_SWIGLU_ACT:
+        T, Fw = sh[0], sh[1]
+        return 5 * T * Fw, T * Fw * (es[0] + es[1] + es[2])
+    if op == OP_SWIGLU_BWD:
+        T, Fw = sh[0], sh[1]
+        return 10 * T * Fw, T * Fw * (es[0] + es[1] + es[2] + es[3] + es[4])
+    if op == OP_RMSNORM_BWD:
+        T, H, acc = sh[0], sh[1], sh[2]
+        return (10 * T * H, T * H * (es[0] + es[2] + es[4]) + T * H * es[3] * (2 if acc else 1)
+                + H * (es[1] + es[5]) + 4 * T)
+    if op == OP_ATTN_BWD:
+        Bt, S, nH, d = sh[0], sh[1], sh[2], sh[3]
+        pairs = S * (S + 1) // 2
+        return (Bt * nH * pairs * (10 * d + 8),
+                Bt * S * nH * d * sum(es[i] for i in (0, 1, 2, 3, 5, 6, 7, 8)) + 12 * Bt * nH * S)
+    if op == OP_ROPE_BWD:
+        n = sh[0] * sh[1] * sh[2] * sh[3]
+        return 6 * n, n * (2 * es[0] + es[1] + es[2] + es[3] + es[4])
+    if op == OP_XENT:
+        T, V = sh[0], sh[1]
+        return 4 * T * V, T * V * (es[0] + es[3]) + 8 * T
+    if op == OP_EMBED_BWD:
+        T, H, V = sh[0], sh[1], sh[2]
+        return T * H, 4 * T + T * H * es[1] + V * H * es[2]
+    if op == OP_ADAM:
+        n = sh[0]
+        return 12 * n, n * (es[0] + 2 * es[1] + 2 * es[2] + 2 * es[3] + es[4])
     raise ValueError(f"unknown op {op}")

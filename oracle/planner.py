@@ -117,7 +117,8 @@ def plan(tensors, kernels, M, roofs=DEFAULT_ROOFS, variant=VAR_T_A_P, lookahead=
          affinity_w=1, placement=PLACE_POOL, guard=None, bucket=None):
     """Replay the policy.
 
-    tensors: list of dicts with keys nbytes, dtype, kind, host_init.
+    tensors: list of dicts with keys nbytes, dtype, kind, host_init and
+             optionally live_out (the final value is read after the trace).
     kernels: list of dicts with keys op, shape, operands [(tid, mode)],
              optional flops / hbm_bytes (0 or missing: analytic cost) and
              time_ns (a measured kernel time; 0 or missing: the analytic
@@ -189,8 +190,12 @@ def _replay(tensors, kernels, M, roofs, variant, lookahead, affinity_w, placemen
         return uses[t][i] if i < len(uses[t]) else INF
 
     def live(t, k):
+        """The value held before kernel k is read later: by the next use if it
+        reads, or after the trace when the tensor is live-out."""
         i = bisect_left(uses[t], k)
-        return i < len(uses[t]) and bool(use_mode[t][i] & MODE_R)
+        if i == len(uses[t]):
+            return bool(tensors[t].get("live_out", False))
+        return bool(use_mode[t][i] & MODE_R)
 
     for k in range(K):
         F, B = FB[k]
@@ -404,8 +409,12 @@ def _retime(tensors, kernels, M, roofs, lookahead, base):
     A, uses, use_mode = _access(tensors, kernels)
 
     def live(t, k):
+        """The value held before kernel k is read later: by the next use if it
+        reads, or after the trace when the tensor is live-out."""
         i = bisect_left(uses[t], k)
-        return i < len(uses[t]) and bool(use_mode[t][i] & MODE_R)
+        if i == len(uses[t]):
+            return bool(tensors[t].get("live_out", False))
+        return bool(use_mode[t][i] & MODE_R)
 
     # demand timeline: placement units per boundary and residency intervals
     units = [[] for _ in range(K)]
@@ -524,8 +533,8 @@ def _retime(tensors, kernels, M, roofs, lookahead, base):
 
 def plan_workload(w, M=None, **kw):
     """Convenience: replay on a workloads.trace.Workload."""
-    tensors = [dict(nbytes=t.nbytes, dtype=t.dtype, kind=t.kind, host_init=t.host_init)
-               for t in w.tensors]
+    tensors = [dict(nbytes=t.nbytes, dtype=t.dtype, kind=t.kind, host_init=t.host_init,
+                    live_out=t.live_out) for t in w.tensors]
     times = kw.pop("times", None)
     kernels = [dict(op=k.op, shape=k.shape, operands=k.operands) for k in w.kernels]
     if times is not None:

@@ -79,7 +79,7 @@ auvm_status auvm_register_tensor(auvm_ctx* x, uint64_t arena_off, uint64_t bytes
   Ctx& c = x->c;
   if (!c.arena_set) return fail(x, AUVM_E_STATE, "arena_init must come first");
   if (!c.kernels.empty()) return fail(x, AUVM_E_STATE, "tensors must be registered before kernels");
-  if (dtype > AUVM_U8 || kind > AUVM_KV || (flags & ~uint32_t(AUVM_HOST_INIT)))
+  if (dtype > AUVM_U8 || kind > AUVM_KV || (flags & ~uint32_t(AUVM_HOST_INIT | AUVM_LIVE_OUT)))
     return fail(x, AUVM_E_INVAL, "bad dtype, kind or flags");
   if (bytes == 0 || arena_off % kAlign) return fail(x, AUVM_E_INVAL, "zero size or unaligned offset");
   uint64_t sz = align_up(bytes);

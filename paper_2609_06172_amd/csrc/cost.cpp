@@ -79,6 +79,7 @@ void kernel_cost(const Kernel& k, const std::vector<Tensor>& T, uint64_t* Fo, ui
       F = Bt * nH * pairs * (4 * d + 4);
       B = Bt * S * nH * d * (es(T, k, 0) + es(T, k, 3)) +
           Bt * nH * (pos0 + S) * d * (es(T, k, 1) + es(T, k, 2));
+      if (k.ids.size() > 4) B += 4 * Bt * nH * S;   // row log-sum-exp
       break;
     }
     case AUVM_OP_ARGMAX: {
@@ -111,6 +112,61 @@ void kernel_cost(const Kernel& k, const std::vector<Tensor>& T, uint64_t* Fo, ui
       uint64_t H = s[1], Fw = s[2], n = s[4];
       F = 2 * n * H * Fw + 2 * n * H;
       B = n * Fw * es(T, k, 0) + 4 * (n + 1) + 4 * n + H * Fw * es(T, k, 3) + 8 * n * H;
+      break;
+    }
+    // training step: every operand element read or written once
+    case AUVM_OP_COPY: B = 2 * uint64_t(s[0]); break;
+    case AUVM_OP_TRANSPOSE: B = 2 * uint64_t(s[0]) * s[1] * es(T, k, 0); break;
+    case AUVM_OP_SWIGLU_ACT: {
+      uint64_t n = uint64_t(s[0]) * s[1];
+      F = 5 * n;
+      B = n * (es(T, k, 0) + es(T, k, 1) + es(T, k, 2));
+      break;
+    }
+    case AUVM_OP_SWIGLU_BWD: {
+      uint64_t n = uint64_t(s[0]) * s[1];
+      F = 10 * n;
+      B = n * (es(T, k, 0) + es(T, k, 1) + es(T, k, 2) + es(T, k, 3) + es(T, k, 4));
+      break;
+    }
+    case AUVM_OP_RMSNORM_BWD: {
+      uint64_t Tn = s[0], H = s[1], n = Tn * H;
+      F = 10 * n;
+      B = n * (es(T, k, 0) + es(T, k, 2) + es(T, k, 4)) + n * es(T, k, 3) * (s[2] ? 2 : 1) +
+          H * (es(T, k, 1) + es(T, k, 5)) + 4 * Tn;
+      break;
+    }
+    case AUVM_OP_ATTN_BWD: {
+      uint64_t Bt = s[0], S = s[1], nH = s[2], d = s[3];
+      uint64_t pairs = S * (S + 1) / 2;
+      F = Bt * nH * pairs * (10 * d + 8);
+      uint64_t e = 0;
+      for (int i : {0, 1, 2, 3, 5, 6, 7, 8}) e += es(T, k, i);
+      B = Bt * S * nH * d * e + 12 * Bt * nH * S;
+      break;
+    }
+    case AUVM_OP_ROPE_BWD: {
+      uint64_t n = uint64_t(s[0]) * s[1] * s[2] * s[3];
+      F = 6 * n;
+      B = n * (2 * es(T, k, 0) + es(T, k, 1) + es(T, k, 2) + es(T, k, 3) + es(T, k, 4));
+      break;
+    }
+    case AUVM_OP_XENT: {
+      uint64_t Tn = s[0], V = s[1];
+      F = 4 * Tn * V;
+      B = Tn * V * (es(T, k, 0) + es(T, k, 3)) + 8 * Tn;
+      break;
+    }
+    case AUVM_OP_EMBED_BWD: {
+      uint64_t Tn = s[0], H = s[1], V = s[2];
+      F = Tn * H;
+      B = 4 * Tn + Tn * H * es(T, k, 1) + V * H * es(T, k, 2);
+      break;
+    }
+    case AUVM_OP_ADAM: {
+      uint64_t n = s[0];
+      F = 12 * n;
+      B = n * (es(T, k, 0) + 2 * es(T, k, 1) + 2 * es(T, k, 2) + 2 * es(T, k, 3) + es(T, k, 4));
       break;
     }
   }
@@ -259,7 +315,7 @@ std::string validate_kernel(const Kernel& k, const std::vector<Tensor>& T) {
     case AUVM_OP_ROPE_KV:
     case AUVM_OP_ATTN_CACHE: {
       bool rope = k.op == AUVM_OP_ROPE_KV;
-      v.count(rope ? 5 : 4, rope ? 5 : 4);
+      v.count(rope ? 5 : 4, 5);
       v.pos(0, "B"); v.pos(1, "S"); v.pos(2, "nH"); v.pos(3, "d"); v.pos(4, "Lmax");
       if (!v.ok) break;
       if (s[5] < 0 || s[5] + s[1] > s[4]) v.fail("positions exceed the cache length");
@@ -276,10 +332,13 @@ std::string validate_kernel(const Kernel& k, const std::vector<Tensor>& T) {
         v.need(1, FP, cache, "Kc"); v.mode(1, MR, "Kc");
         v.need(2, FP, cache, "Vc"); v.mode(2, MR, "Vc");
         v.need(3, FP, rows * hd, "o"); v.mode(3, MW | MRW, "o");
+        if (k.ids.size() > 4) {
+          v.need(4, F32, uint64_t(s[0]) * s[2] * s[1], "lse"); v.mode(4, MW | MRW, "lse");
+        }
       }
       if (!v.ok) break;
       uint32_t dt = T[k.ids[0]].dtype;
-      for (size_t i = 1; i < k.ids.size(); ++i)
+      for (size_t i = 1; i < k.ids.size() && i < 4; ++i)
         if (T[k.ids[i]].dtype != dt) v.fail("attention operand dtypes differ");
       if (s[3] != 32 && s[3] != 64 && s[3] != 128) v.fail("head dim must be 32, 64 or 128");
       break;
@@ -346,6 +405,108 @@ std::string validate_kernel(const Kernel& k, const std::vector<Tensor>& T) {
         v.need(3, BF16, N * Kd, "Wd"); v.mode(3, MR, "Wd");
         v.need(4, F32, M * N, "x"); v.mode(4, MRW, "x");
       }
+      break;
+    }
+    case AUVM_OP_COPY:
+      v.count(2, 2); v.pos(0, "bytes");
+      if (!v.ok) break;
+      v.need(0, F32 | BF16 | I32 | U8, 0, "a"); v.mode(0, MR, "a");
+      v.mode(1, MW | MRW, "b");
+      if (v.ok && (T[k.ids[0]].bytes < uint64_t(s[0]) || T[k.ids[1]].bytes < uint64_t(s[0])))
+        v.fail("copy longer than an operand");
+      break;
+    case AUVM_OP_TRANSPOSE: {
+      v.count(2, 2); v.pos(0, "R"); v.pos(1, "C");
+      if (!v.ok) break;
+      if (s[0] > (int64_t(1) << 22)) v.fail("transpose rows above 2^22");
+      uint64_t n = uint64_t(s[0]) * s[1];
+      v.need(0, FP, n, "a"); v.mode(0, MR, "a");
+      v.need(1, FP, n, "b"); v.mode(1, MW | MRW, "b");
+      if (v.ok && T[k.ids[0]].dtype != T[k.ids[1]].dtype) v.fail("transpose dtypes differ");
+      break;
+    }
+    case AUVM_OP_SWIGLU_ACT:
+    case AUVM_OP_SWIGLU_BWD: {
+      const bool bwd = k.op == AUVM_OP_SWIGLU_BWD;
+      v.count(bwd ? 5 : 3, bwd ? 5 : 3); v.pos(0, "T"); v.pos(1, "F");
+      if (!v.ok) break;
+      uint64_t n = uint64_t(s[0]) * s[1];
+      for (size_t i = 0; i < k.ids.size(); ++i) {
+        const bool in = i < (bwd ? 3u : 2u);
+        v.need(int(i), FP, n, "operand"); v.mode(int(i), in ? MR : (MW | MRW), "operand");
+        if (v.ok && T[k.ids[i]].dtype != T[k.ids[0]].dtype) v.fail("SwiGLU operand dtypes differ");
+      }
+      break;
+    }
+    case AUVM_OP_RMSNORM_BWD: {
+      v.count(7, 7); v.pos(0, "T"); v.pos(1, "H");
+      if (!v.ok) break;
+      if (s[2] != 0 && s[2] != 1) v.fail("acc must be 0 or 1");
+      uint64_t Tn = s[0], H = s[1];
+      v.need(0, F32, Tn * H, "x"); v.mode(0, MR, "x");
+      v.need(1, FP, H, "g"); v.mode(1, MR, "g");
+      v.need(2, F32, Tn * H, "dy"); v.mode(2, MR, "dy");
+      v.need(3, F32, Tn * H, "dx"); v.mode(3, s[2] ? MRW : (MW | MRW), "dx");
+      v.need(4, BF16, Tn * H, "dxb"); v.mode(4, MW | MRW, "dxb");
+      v.need(5, F32, H, "dg"); v.mode(5, MW | MRW, "dg");
+      v.need(6, F32, Tn, "rstd"); v.mode(6, MW | MRW, "rstd");
+      break;
+    }
+    case AUVM_OP_ATTN_BWD: {
+      v.count(10, 10); v.pos(0, "B"); v.pos(1, "S"); v.pos(2, "nH"); v.pos(3, "d");
+      if (!v.ok) break;
+      if (s[3] != 128) v.fail("attention backward needs head dim 128");
+      uint64_t n = uint64_t(s[0]) * s[1] * s[2] * s[3], rows = uint64_t(s[0]) * s[2] * s[1];
+      const char* nm[10] = {"q", "K", "V", "o", "lse", "do", "dq", "dK", "dV", "D"};
+      for (int i = 0; i < 10; ++i) {
+        const bool f32 = i == 4 || i == 9;
+        v.need(i, f32 ? F32 : BF16, f32 ? rows : n, nm[i]);
+        v.mode(i, i < 6 ? MR : (MW | MRW), nm[i]);
+      }
+      break;
+    }
+    case AUVM_OP_ROPE_BWD: {
+      v.count(5, 5); v.pos(0, "B"); v.pos(1, "S"); v.pos(2, "nH"); v.pos(3, "d");
+      if (!v.ok) break;
+      if (s[3] % 2) v.fail("head dim must be even");
+      uint64_t n = uint64_t(s[0]) * s[1] * s[2] * s[3];
+      const char* nm[5] = {"dq", "dK", "dV", "dk", "dv"};
+      const unsigned md[5] = {MRW, MR, MR, MW | MRW, MW | MRW};
+      for (int i = 0; i < 5; ++i) {
+        v.need(i, FP, n, nm[i]); v.mode(i, md[i], nm[i]);
+        if (v.ok && T[k.ids[i]].dtype != T[k.ids[0]].dtype) v.fail("RoPE backward dtypes differ");
+      }
+      break;
+    }
+    case AUVM_OP_XENT: {
+      v.count(4, 4); v.pos(0, "T"); v.pos(1, "V");
+      if (!v.ok) break;
+      uint64_t Tn = s[0], V = s[1];
+      v.need(0, F32, Tn * V, "logits"); v.mode(0, MR, "logits");
+      v.need(1, I32, Tn, "labels"); v.mode(1, MR, "labels");
+      v.need(2, F32, Tn, "losses"); v.mode(2, MW | MRW, "losses");
+      v.need(3, FP, Tn * V, "dlogits"); v.mode(3, MW | MRW, "dlogits");
+      break;
+    }
+    case AUVM_OP_EMBED_BWD: {
+      v.count(3, 3); v.pos(0, "T"); v.pos(1, "H"); v.pos(2, "V");
+      if (!v.ok) break;
+      v.need(0, I32, s[0], "ids"); v.mode(0, MR, "ids");
+      v.need(1, F32, uint64_t(s[0]) * s[1], "dx"); v.mode(1, MR, "dx");
+      v.need(2, F32, uint64_t(s[2]) * s[1], "dE"); v.mode(2, MW | MRW, "dE");
+      break;
+    }
+    case AUVM_OP_ADAM: {
+      v.count(5, 5); v.pos(0, "n"); v.pos(1, "step");
+      if (!v.ok) break;
+      if (s[2] < 0 || s[3] < 0 || s[3] >= 1000000 || s[4] < 0 || s[4] >= 1000000 || s[5] < 0 || s[6] < 0)
+        v.fail("AdamW hyperparameters out of range");
+      uint64_t n = s[0];
+      v.need(0, F32, n, "g"); v.mode(0, MR, "g");
+      v.need(1, F32, n, "p32"); v.mode(1, MRW, "p32");
+      v.need(2, F32, n, "m"); v.mode(2, MRW, "m");
+      v.need(3, F32, n, "v"); v.mode(3, MRW, "v");
+      v.need(4, FP, n, "p"); v.mode(4, MW | MRW, "p");
       break;
     }
     default:

@@ -18,6 +18,8 @@ struct AttnArgs {
   int64_t B, S, nH, d, pos0;
   int64_t q_rs, o_rs, kv_rs, kv_bstride, kv_hstride;
   bool bf16;
+  // optional [B, nH, S] output: natural log-sum-exp of each query's scaled scores
+  float* lse = nullptr;
 };
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s);

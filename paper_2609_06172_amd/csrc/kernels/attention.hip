@@ -65,6 +65,7 @@ __global__ void __launch_bounds__(256) attn_rowwave(AttnArgs a) {
   const float inv = 1.f / l;
   if (d0 < d) st(o, d0, acc0 * inv);
   if (d1 < d) st(o, d1, acc1 * inv);
+  if (a.lse && lane == 0) a.lse[bh * a.S + i] = m + logf(l);   // scores here are already scaled
 }
 
 // Decode attention, head dim 128, bf16: one workgroup per query row.
@@ -379,6 +380,8 @@ __global__ void __launch_bounds__(64 * FW, 2) attn_prefill_d128(AttnArgs a, int6
 #pragma unroll
       for (int e = 0; e < 16; ++e)
         O[qr * a.o_rs + 32 * dt + 8 * (e >> 2) + 4 * lh + (e & 3)] = f2bf(ot[dt][e] * inv);
+    // m is the raw-score maximum and l sums exp((s - m) / sqrt(128))
+    if (a.lse && lh == 0) a.lse[bh * a.S + qr] = m * 0.08838834764831845f + logf(l);
   }
 }
 
@@ -386,7 +389,7 @@ __global__ void __launch_bounds__(64 * FW, 2) attn_prefill_d128(AttnArgs a, int6
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
   const int64_t rows = a.B * a.nH * a.S;
-  if (a.bf16 && a.d == 128 && a.S <= 16) {
+  if (a.bf16 && a.d == 128 && a.S <= 16 && !a.lse) {
     hipLaunchKernelGGL(attn_decode_d128, dim3(unsigned(rows)), dim3(256), 0, s, a);
     return hipGetLastError();
   }

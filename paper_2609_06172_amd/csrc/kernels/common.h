@@ -42,6 +42,15 @@ __device__ __forceinline__ float gelu_erf(float x) {
 }
 __device__ __forceinline__ float silu(float x) { return x / (1.0f + __expf(-x)); }
 
+// Rotate-half RoPE angle of pair i (of d/2) at position pos, base 10000, in
+// fp32: 10000^(-2i/d) = 2^(-(2i/d) log2 10000).  The angle error at position
+// 4096 is ~4e-4 rad, below the bf16 storage step.  Forward and backward
+// kernels share it so that they rotate by identical angles.
+__device__ __forceinline__ float rope_angle(int64_t pos, int64_t i, int64_t d) {
+  const float lg = 13.287712379549449f;  // log2(10000)
+  return float(pos) * exp2f(-2.f * float(i) / float(d) * lg);
+}
+
 // wave64 reductions
 __device__ __forceinline__ float wave_sum(float v) {
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);

@@ -2,10 +2,13 @@
 // RMSNorm, RoPE + KV-cache append, argmax, and the op dispatch.
 #include <hip/hip_runtime.h>
 
+#include <cmath>
+
 #include "../kernels.h"
 #include "common.h"
 #include "gemm.h"
 #include "moe.h"
+#include "train.h"
 #include "attention.h"
 
 namespace auvm {
@@ -182,11 +185,8 @@ __global__ void rope_kv_kernel(T* q, const T* k, const T* v, T* Kc, T* Vc, int64
   const int64_t half = d / 2;
   const int64_t base = row * nH * d + h * d;
   const int64_t cbase = ((b * nH + h) * Lmax + pos) * d;
-  // inverse frequency 10000^(-2i/d) = 2^(-(2i/d) log2 10000); fp32 angle error
-  // at position 1280 is ~1e-4 rad, far below the bf16 storage step
-  const float lg = 13.287712379549449f;  // log2(10000)
   for (int64_t i = threadIdx.x; i < half; i += blockDim.x) {
-    const float ang = float(pos) * exp2f(-2.f * float(i) / float(d) * lg);
+    const float ang = rope_angle(pos, i, d);
     float sn, c;
     sincosf(ang, &sn, &c);
     float q1 = ld(q, base + i), q2 = ld(q, base + i + half);
@@ -309,6 +309,36 @@ hipError_t launch_op(const Kernel& k, const std::vector<Tensor>& T, uint8_t* con
       g.out_bf16 = dt(sw ? 3 : 2) == AUVM_BF16;
       return launch_gemm(g, s);
     }
+    case AUVM_OP_COPY:
+      return hipMemcpyAsync(p[1], p[0], size_t(sh[0]), hipMemcpyDeviceToDevice, s);
+    case AUVM_OP_TRANSPOSE:
+      return launch_transpose(p[0], p[1], sh[0], sh[1], dt(0) == AUVM_BF16, s);
+    case AUVM_OP_SWIGLU_ACT:
+    case AUVM_OP_SWIGLU_BWD:
+      return launch_swiglu(k.op == AUVM_OP_SWIGLU_BWD, p, sh[0] * sh[1], dt(0) == AUVM_BF16, s);
+    case AUVM_OP_RMSNORM_BWD:
+      return launch_rmsnorm_bwd(p, sh[0], sh[1], int(sh[2]), dt(1) == AUVM_BF16, s);
+    case AUVM_OP_ATTN_BWD:
+      return launch_attn_bwd(p, sh[0], sh[1], sh[2], s);
+    case AUVM_OP_ROPE_BWD:
+      return launch_rope_bwd(p, sh[0], sh[1], sh[2], sh[3], dt(0) == AUVM_BF16, s);
+    case AUVM_OP_XENT:
+      return launch_xent(p, sh[0], sh[1], dt(3) == AUVM_BF16, s);
+    case AUVM_OP_EMBED_BWD:
+      return launch_embed_bwd(p, sh[0], sh[1], sh[2], s);
+    case AUVM_OP_ADAM: {
+      // hyperparameters in fixed point; bias corrections in double on the host
+      const double lr = sh[2] * 1e-9, b1 = sh[3] * 1e-6, b2 = sh[4] * 1e-6, eps = sh[5] * 1e-12, wd = sh[6] * 1e-6;
+      const double t = double(sh[1]);
+      AdamArgs a;
+      a.b1 = float(b1);
+      a.b2 = float(b2);
+      a.eps = float(eps);
+      a.decay = float(1.0 - lr * wd);
+      a.step_size = float(lr / (1.0 - std::pow(b1, t)));
+      a.inv_bc2 = float(1.0 / (1.0 - std::pow(b2, t)));
+      return launch_adam(p, sh[0], a, dt(4) == AUVM_BF16, s);
+    }
     case AUVM_OP_MOE_ROUTE:
       return launch_moe_route(p[0], p[1], reinterpret_cast<int32_t*>(p[2]), reinterpret_cast<float*>(p[3]), sh[0],
                               sh[1], int(sh[2]), int(sh[3]), dt(0) == AUVM_BF16, s);
@@ -376,6 +406,7 @@ hipError_t launch_op(const Kernel& k, const std::vector<Tensor>& T, uint8_t* con
       }
       a.o_rs = nH * d;
       a.bf16 = dt(0) == AUVM_BF16;
+      if (!qkv && k.ids.size() > 4) a.lse = reinterpret_cast<float*>(p[4]);
       return launch_attention(a, s);
     }
     case AUVM_OP_ROPE_KV:

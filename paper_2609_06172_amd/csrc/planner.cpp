@@ -49,22 +49,29 @@ struct Span {
 struct Uses {
   std::vector<std::vector<int32_t>> k;     // kernel indices using each tensor
   std::vector<std::vector<uint8_t>> mode;
+  std::vector<uint8_t> out;                // live-out: read after the trace ends
   int64_t nu(int32_t t, int64_t kk) const {
     auto& v = k[t];
     auto it = std::lower_bound(v.begin(), v.end(), kk);
     return it == v.end() ? kInf : *it;
   }
+  // the value held before kernel kk is read later: by the next use, if it
+  // reads, or after the trace for a live-out tensor without further uses
   bool live(int32_t t, int64_t kk) const {
     auto& v = k[t];
     auto it = std::lower_bound(v.begin(), v.end(), kk);
-    return it != v.end() && (mode[t][it - v.begin()] & AUVM_R);
+    if (it == v.end()) return out[t] != 0;
+    return (mode[t][it - v.begin()] & AUVM_R) != 0;
   }
 };
 
-Uses build_uses(size_t nT, const std::vector<Kernel>& K) {
+Uses build_uses(const std::vector<Tensor>& T, const std::vector<Kernel>& K) {
+  const size_t nT = T.size();
   Uses u;
   u.k.resize(nT);
   u.mode.resize(nT);
+  u.out.resize(nT);
+  for (size_t t = 0; t < nT; ++t) u.out[t] = (T[t].flags & AUVM_LIVE_OUT) ? 1 : 0;
   for (size_t k = 0; k < K.size(); ++k)
     for (auto& a : K[k].acc) {
       u.k[a.first].push_back(int32_t(k));
@@ -101,7 +108,7 @@ class Replay {
     nT_ = T.size();
     size_.resize(nT_);
     for (size_t t = 0; t < nT_; ++t) size_[t] = T[t].size;
-    uses_ = build_uses(nT_, K);
+    uses_ = build_uses(T, K);
     belady_ = p.variant == AUVM_T_A_P || p.variant == AUVM_DEMAND_BELADY;
     affinity_ = p.variant == AUVM_T_A || p.variant == AUVM_T_A_P;
     D_ = p.lookahead ? p.lookahead : 1;
@@ -425,7 +432,7 @@ PlanResult retime(const std::vector<Tensor>& T, const std::vector<Kernel>& K, co
   const int64_t nK = int64_t(K.size());
   std::vector<uint64_t> size(nT);
   for (size_t t = 0; t < nT; ++t) size[t] = T[t].size;
-  Uses uses = build_uses(nT, K);
+  Uses uses = build_uses(T, K);
 
   // demand timeline: placement units per boundary, residency intervals
   std::vector<std::vector<Unit>> units(nK);

@@ -1,6 +1,6 @@
 """Helpers to load traces into a plan-only C-ABI context and compare with the oracle."""
 from paper_2609_06172_amd.capi import Context
-from workloads.format import ALIGN, FLAG_HOST_INIT, KIND_PARAM
+from workloads.format import ALIGN, FLAG_HOST_INIT, FLAG_LIVE_OUT, KIND_PARAM
 
 
 def plan_ctx(tensors, kernels, M, variant=4, lookahead=0, affinity_w=1, placement=0, roofs=None,
@@ -19,6 +19,7 @@ def plan_ctx(tensors, kernels, M, variant=4, lookahead=0, affinity_w=1, placemen
     ctx.arena_init(max(off, ALIGN))
     for t, o in zip(tensors, offs):
         flags = FLAG_HOST_INIT if (t["host_init"] and t["kind"] != KIND_PARAM) else 0
+        flags |= FLAG_LIVE_OUT if t.get("live_out") else 0
         ctx.register_tensor(o, t["nbytes"], t["dtype"], t["kind"], flags)
     for k in kernels:
         ctx.add_kernel(k["op"], k["shape"], k["operands"], k.get("flops", 0), k.get("hbm_bytes", 0))

@@ -14,8 +14,9 @@ def load_golden():
 
 
 def golden_inputs(case):
-    tensors = [dict(nbytes=b, dtype=DT_U8, kind=KIND_PARAM if k == "param" else KIND_ACT,
-                    host_init=(k == "param")) for b, k in case["tensors"]]
+    tensors = [dict(nbytes=e[0], dtype=DT_U8, kind=KIND_PARAM if e[1] == "param" else KIND_ACT,
+                    host_init=(e[1] == "param"), live_out=(len(e) > 2 and e[2] == "out"))
+               for e in case["tensors"]]
     n = len(case["kernels"])
     flops = case.get("flops", [1] * n)
     times = case.get("times", [0] * n)
@@ -26,7 +27,7 @@ def golden_inputs(case):
 
 
 def random_trace(seed, n_tensors=None, n_kernels=None, max_ops=4, equal=False,
-                 read_only=False, unit=256, touch=False, timed=False):
+                 read_only=False, unit=256, touch=False, timed=False, live_out=False):
     """Random trace of touch kernels with explicit or analytic costs.
 
     touch=True makes every kernel a well-formed touch op: tensor 0 is a log
@@ -34,7 +35,7 @@ def random_trace(seed, n_tensors=None, n_kernels=None, max_ops=4, equal=False,
     operands are distinct and their sizes are multiples of 4 bytes.
     timed=True gives most kernels a measured time (time_ns) drawn around the
     link time of a few hundred bytes, so both sides of the measured-time rule
-    occur.
+    occur.  live_out=True marks about a third of the tensors live-out.
     """
     r = random.Random(seed)
     nT = n_tensors or r.randint(1, 40)
@@ -46,7 +47,8 @@ def random_trace(seed, n_tensors=None, n_kernels=None, max_ops=4, equal=False,
         kind = KIND_PARAM if (read_only or r.random() < 0.6) else KIND_ACT
         nbytes = unit if equal else r.choice(sizes)
         tensors.append(dict(nbytes=nbytes, dtype=DT_U8, kind=kind,
-                            host_init=(kind == KIND_PARAM or r.random() < 0.3)))
+                            host_init=(kind == KIND_PARAM or r.random() < 0.3),
+                            live_out=live_out and r.random() < 0.35))
     if touch:
         tensors.insert(0, dict(nbytes=64 * nK, dtype=DT_U8, kind=KIND_ACT, host_init=True))
     first = 1 if touch else 0

@@ -141,7 +141,7 @@ def test_random_traces_bit_exact(seed):
             assert_same_plan(plan_ctx(tensors, kernels, M, roofs=roofs, **kw), r)
 
 
-@pytest.mark.parametrize("name", ["tiny", "gpt-small", "llama-small", "gpt-1.3b"])
+@pytest.mark.parametrize("name", ["tiny", "gpt-small", "llama-small", "gpt-1.3b", "train-small"])
 @pytest.mark.parametrize("variant", VARIANTS)
 def test_config_traces_bit_exact(name, variant):
     from paper_2609_06172_amd.session import Session
@@ -338,3 +338,31 @@ def test_moe_op_validation():
             ctx.add_kernel(o, sh, ops)
         assert e.value.code == op.E_INVAL, (o, sh)
     ctx.destroy()
+
+
+def test_training_step_trace_bit_exact():
+    # the 13B-shape training step, two layers, under the full method
+    import dataclasses
+    from paper_2609_06172_amd.session import Session
+    cfg = dataclasses.replace(configs.LLAMA_13B_TRAIN, n_layers=2)
+    w = trace.build(cfg)
+    s = Session(w, device=-1)
+    assert_same_plan(s.ctx, op.plan_workload(w, s.M))
+    s.close()
+
+
+@pytest.mark.parametrize("seed", range(30))
+def test_random_live_out_traces_bit_exact(seed):
+    tensors, kernels = random_trace(100 + seed, touch=True, live_out=True)
+    fp = sum(op.aligned(t["nbytes"]) for t in tensors)
+    rnd = random.Random(seed)
+    for variant in VARIANTS:
+        M = max(1024, (fp * rnd.choice([1, 2, 3]) // rnd.choice([2, 3, 4])) // 256 * 256)
+        try:
+            r = op.plan(tensors, kernels, M, variant=variant)
+        except op.PlanError as e:
+            with pytest.raises(AuvmError) as ee:
+                plan_ctx(tensors, kernels, M, variant=variant)
+            assert ee.value.code == e.code
+            continue
+        assert_same_plan(plan_ctx(tensors, kernels, M, variant=variant), r)

@@ -193,3 +193,35 @@ def test_moe_small_recorded_trace_replays_bit_for_bit():
     moved = lambda c: c["h2d_prefetch_B"] + c["h2d_demand_B"]
     assert moved(c_routed) < moved(c_full)
     s.close()
+
+
+def test_training_step_matches_the_oracle():
+    # one full step of the small LLaMA-style model under 2x oversubscription:
+    # loss, every gradient, and the AdamW update of every parameter
+    from oracle import train as ot
+    from workloads import configs as C
+    cfg = C.TRAIN_SMALL
+    print("train-small: forward, backward and AdamW at 2x", flush=True)
+    from paper_2609_06172_amd.session import Session
+    w = trace.build(cfg, keep_grads=True)      # gradients kept readable after the step
+    s = Session(w, device=0, validate=1)
+    s.run_all()
+    assert s.ctx.get_executed() == s.ctx.get_schedule()
+    names = init.param_names(w)
+    got = {n: dict(grad=s.read(n + ".grad"), master=s.read(n + ".master"), m=s.read(n + ".m"),
+                   v=s.read(n + ".v"), w=s.read(n)) for n in names}
+    loss = float(s.read("losses").astype(np.float64).mean())
+    s.close()
+    P = init.weights_f64(w, names=names)          # the bf16 weights the step used
+    master = init.master_f64(w)
+    state = init.adam_state_f64(w)
+    ids = init.token_ids(cfg.seed, cfg.batch, cfg.prompt_len, cfg.vocab)
+    ref = ot.train_step(cfg, P, ids, init.next_token_labels(ids), state, init.TRAIN_HP, master=master)
+    assert abs(loss - ref["loss"]) < 2e-3 * ref["loss"]
+    for n in names:
+        g = got[n]
+        assert rel_l2(g["grad"], ref["grads"][n]) < 3e-2, n
+        m2, v2 = ref["state"][n]
+        assert rel_l2(g["m"], m2) < 3e-2, n
+        assert rel_l2(g["master"] - master[n], ref["params"][n] - master[n]) < 3e-2, n
+        assert rel_l2(g["w"], ref["params"][n]) < 4e-3, n

@@ -305,3 +305,161 @@ def test_moe_expert_down(M, F, H, skip):
     assert np.array_equal(res["x"][~routed], vals["x"][~routed])     # other rows untouched
     if n:
         assert rel_l2(res["x"][routed], want[routed]) < TOL[DT_F32]
+
+
+# ------------------------------------------------------- training step ops
+from oracle import train as ot  # noqa: E402
+from workloads.format import (OP_ADAM, OP_ATTN_BWD, OP_COPY, OP_EMBED_BWD,  # noqa: E402
+                              OP_RMSNORM_BWD, OP_ROPE_BWD, OP_SWIGLU_ACT, OP_SWIGLU_BWD,
+                              OP_TRANSPOSE, OP_XENT)
+from workloads.trace import adam_shape  # noqa: E402
+
+
+@pytest.mark.parametrize("dt", [DT_F32, DT_BF16])
+@pytest.mark.parametrize("R,C", [(1, 1), (64, 64), (100, 37), (130, 2049), (1024, 160)])
+def test_transpose_and_copy(R, C, dt):
+    a = rnd(R, C)
+    vals, res = _run(OP_TRANSPOSE, (R, C), [("a", (R, C), dt, MODE_R, a), ("b", (C, R), dt, MODE_W, None)], ["b"])
+    assert np.array_equal(res["b"], vals["a"].T)
+    nb = R * C * (4 if dt == DT_F32 else 2)
+    vals, res = _run(OP_COPY, (nb,), [("a", (R, C), dt, MODE_R, a), ("b", (R, C), dt, MODE_W, None)], ["b"])
+    assert np.array_equal(res["b"], vals["a"])
+
+
+@pytest.mark.parametrize("T,F", [(3, 5), (160, 384), (777, 1000)])
+def test_swiglu_act_and_backward(T, F):
+    G, U, dF = rnd(T, F, scale=3), rnd(T, F), rnd(T, F)
+    ops = [("G", (T, F), DT_BF16, MODE_R, G), ("U", (T, F), DT_BF16, MODE_R, U), ("F", (T, F), DT_BF16, MODE_W, None)]
+    vals, res = _run(OP_SWIGLU_ACT, (T, F), ops, ["F"])
+    assert rel_l2(res["F"], of.silu(vals["G"]) * vals["U"]) < TOL[DT_BF16]
+    ops = [("G", (T, F), DT_BF16, MODE_R, G), ("U", (T, F), DT_BF16, MODE_R, U), ("dF", (T, F), DT_BF16, MODE_R, dF),
+           ("dG", (T, F), DT_BF16, MODE_W, None), ("dU", (T, F), DT_BF16, MODE_W, None)]
+    vals, res = _run(OP_SWIGLU_BWD, (T, F), ops, ["dG", "dU"])
+    g = vals["G"]
+    assert rel_l2(res["dG"], vals["dF"] * vals["U"] * ot.silu_grad(g)) < TOL[DT_BF16]
+    assert rel_l2(res["dU"], vals["dF"] * of.silu(g)) < TOL[DT_BF16]
+
+
+@pytest.mark.parametrize("acc", [0, 1])
+@pytest.mark.parametrize("T,H", [(1, 64), (37, 256), (300, 5120), (5, 130)])
+def test_rmsnorm_backward(T, H, acc):
+    x, g, dy, dx0 = rnd(T, H), 1 + 0.1 * rnd(H), rnd(T, H), rnd(T, H)
+    ops = [("x", (T, H), DT_F32, MODE_R, x), ("g", (H,), DT_BF16, MODE_R, g), ("dy", (T, H), DT_F32, MODE_R, dy),
+           ("dx", (T, H), DT_F32, MODE_RW if acc else MODE_W, dx0 if acc else None),
+           ("dxb", (T, H), DT_BF16, MODE_W, None), ("dg", (H,), DT_F32, MODE_W, None),
+           ("rstd", (T,), DT_F32, MODE_W, None)]
+    vals, res = _run(OP_RMSNORM_BWD, (T, H, acc), ops, ["dx", "dxb", "dg"])
+    dx, dg = ot.rmsnorm_backward(vals["x"], vals["g"], vals["dy"])
+    if acc:
+        dx = dx + vals["dx"]
+    assert rel_l2(res["dx"], dx) < TOL[DT_F32]
+    assert rel_l2(res["dxb"], dx) < TOL[DT_BF16]
+    assert rel_l2(res["dg"], dg) < TOL[DT_F32]
+
+
+def _attn_fwd_bwd_ref(q, K, V, dO, B, S, nH):
+    """Oracle attention (per head, causal) on the GPU's cache layout."""
+    d = 128
+    qh = q.reshape(B, S, nH, d)
+    do = dO.reshape(B, S, nH, d)
+    o = np.empty_like(qh)
+    lse = np.empty((B, nH, S))
+    dq, dK, dV = np.empty_like(qh), np.empty_like(K), np.empty_like(V)
+    for b in range(B):
+        for h in range(nH):
+            s = (qh[b, :, h] @ K[b, h].T) / np.sqrt(d)
+            s = np.where(np.arange(S)[None, :] <= np.arange(S)[:, None], s, -np.inf)
+            m = s.max(axis=1, keepdims=True)
+            lse[b, h] = (m + np.log(np.exp(s - m).sum(axis=1, keepdims=True)))[:, 0]
+            o[b, :, h] = of.causal_attention(qh[b, :, h], K[b, h], V[b, h])
+            dq[b, :, h], dK[b, h], dV[b, h] = ot.attention_backward(qh[b, :, h], K[b, h], V[b, h], do[b, :, h])
+    return o.reshape(B * S, nH * d), lse, dq.reshape(B * S, nH * d), dK, dV
+
+
+@pytest.mark.parametrize("B,S,nH", [(1, 1, 1), (1, 70, 2), (2, 160, 2), (1, 300, 1)])
+def test_attention_lse_and_backward(B, S, nH):
+    d = 128
+    q, K, V, dO = rnd(B * S, nH * d), rnd(B, nH, S, d), rnd(B, nH, S, d), rnd(B * S, nH * d)
+    o_ref = None
+    # forward with the log-sum-exp output (flash kernel)
+    ops = [("q", (B * S, nH * d), DT_BF16, MODE_R, q), ("K", (B, nH, S, d), DT_BF16, MODE_R, K),
+           ("V", (B, nH, S, d), DT_BF16, MODE_R, V), ("o", (B * S, nH * d), DT_BF16, MODE_W, None),
+           ("lse", (B, nH, S), DT_F32, MODE_W, None)]
+    vals, res = _run(OP_ATTN_CACHE, (B, S, nH, d, S, 0), ops, ["o", "lse"])
+    o_ref, lse_ref, _, _, _ = _attn_fwd_bwd_ref(vals["q"], vals["K"], vals["V"], np.zeros_like(vals["q"]), B, S, nH)
+    assert rel_l2(res["o"], o_ref) < TOL[DT_BF16]
+    assert np.abs(res["lse"] - lse_ref).max() < 1e-3
+    # backward from the GPU's own o and lse (the forward's outputs)
+    o_b = res["o"]
+    ops = [("q", (B * S, nH * d), DT_BF16, MODE_R, q), ("K", (B, nH, S, d), DT_BF16, MODE_R, K),
+           ("V", (B, nH, S, d), DT_BF16, MODE_R, V), ("o", (B * S, nH * d), DT_BF16, MODE_R, o_b),
+           ("lse", (B, nH, S), DT_F32, MODE_R, res["lse"]), ("do", (B * S, nH * d), DT_BF16, MODE_R, dO),
+           ("dq", (B * S, nH * d), DT_BF16, MODE_W, None), ("dK", (B, nH, S, d), DT_BF16, MODE_W, None),
+           ("dV", (B, nH, S, d), DT_BF16, MODE_W, None), ("D", (B, nH, S), DT_F32, MODE_W, None)]
+    vals, res = _run(OP_ATTN_BWD, (B, S, nH, d), ops, ["dq", "dK", "dV"])
+    _, _, dq, dK, dV = _attn_fwd_bwd_ref(vals["q"], vals["K"], vals["V"], vals["do"], B, S, nH)
+    # relative, with an absolute floor of 1e-4 per element: a single key gives
+    # dq = dK = 0 exactly, and the GPU's rounding leaves ~1e-7 there
+    for got, want in ((res["dq"], dq), (res["dK"], dK), (res["dV"], dV)):
+        err = np.linalg.norm(np.asarray(got, np.float64) - want)
+        assert err < 1e-2 * np.linalg.norm(want) + 1e-4 * np.sqrt(want.size)
+
+
+@pytest.mark.parametrize("B,S,nH,d", [(1, 1, 1, 128), (2, 75, 3, 64), (1, 200, 2, 128)])
+def test_rope_backward_is_the_inverse_rotation(B, S, nH, d):
+    dq, dK, dV = rnd(B * S, nH * d), rnd(B, nH, S, d), rnd(B, nH, S, d)
+    ops = [("dq", (B * S, nH * d), DT_F32, MODE_RW, dq), ("dK", (B, nH, S, d), DT_F32, MODE_R, dK),
+           ("dV", (B, nH, S, d), DT_F32, MODE_R, dV), ("dk", (B * S, nH * d), DT_F32, MODE_W, None),
+           ("dv", (B * S, nH * d), DT_F32, MODE_W, None)]
+    vals, res = _run(OP_ROPE_BWD, (B, S, nH, d), ops, ["dq", "dk", "dv"])
+    pos = np.tile(np.arange(S), B)[:, None]
+    want_q = of.rope(vals["dq"].reshape(B * S, nH, d), -pos).reshape(B * S, nH * d)
+    kt = vals["dK"].transpose(0, 2, 1, 3).reshape(B * S, nH, d)
+    want_k = of.rope(kt, -pos).reshape(B * S, nH * d)
+    # fp32 angles pos * 10000^(-2i/d): ~1e-5 rad of error at position 200
+    assert rel_l2(res["dq"], want_q) < 5e-5 and rel_l2(res["dk"], want_k) < 5e-5
+    assert np.array_equal(res["dv"], vals["dV"].transpose(0, 2, 1, 3).reshape(B * S, nH * d))
+
+
+@pytest.mark.parametrize("T,V", [(1, 7), (33, 1024), (160, 32000)])
+def test_cross_entropy_rows_and_gradient(T, V):
+    lg = rnd(T, V, scale=2)
+    labels = RNG.integers(0, V, T).astype(np.int32)
+    ops = [("logits", (T, V), DT_F32, MODE_R, lg), ("labels", (T,), DT_I32, MODE_R, labels),
+           ("losses", (T,), DT_F32, MODE_W, None), ("dlogits", (T, V), DT_BF16, MODE_W, None)]
+    vals, res = _run(OP_XENT, (T, V), ops, ["losses", "dlogits"])
+    loss, dl = ot.cross_entropy(vals["logits"], labels)
+    assert abs(res["losses"].astype(np.float64).mean() - loss) < 1e-5 * max(1, abs(loss))
+    assert rel_l2(res["dlogits"], dl) < TOL[DT_BF16]
+
+
+@pytest.mark.parametrize("T,H,V", [(1, 64, 5), (160, 256, 1024), (2000, 130, 70)])
+def test_embedding_backward_sums_in_token_order(T, H, V):
+    ids = RNG.integers(0, V, T).astype(np.int32)
+    dx = rnd(T, H)
+    ops = [("ids", (T,), DT_I32, MODE_R, ids), ("dx", (T, H), DT_F32, MODE_R, dx), ("dE", (V, H), DT_F32, MODE_W, None)]
+    vals, res = _run(OP_EMBED_BWD, (T, H, V), ops, ["dE"])
+    want = np.zeros((V, H))
+    np.add.at(want, ids, vals["dx"])
+    assert rel_l2(res["dE"], want) < 1e-6
+    assert np.all(res["dE"][np.setdiff1d(np.arange(V), ids)] == 0)
+
+
+@pytest.mark.parametrize("dt", [DT_F32, DT_BF16])
+@pytest.mark.parametrize("n", [1, 1000, 70001])
+def test_adamw_update(n, dt):
+    from workloads.init import TRAIN_HP as hp
+    g, p = rnd(n, scale=1e-3), rnd(n, scale=0.02)
+    m, v = rnd(n, scale=1e-4), np.square(rnd(n, scale=1e-4))
+    ops = [("g", (n,), DT_F32, MODE_R, g), ("p32", (n,), DT_F32, MODE_RW, p), ("m", (n,), DT_F32, MODE_RW, m),
+           ("v", (n,), DT_F32, MODE_RW, v), ("p", (n,), dt, MODE_W, None)]
+    vals, res = _run(OP_ADAM, adam_shape(n, hp), ops, ["p32", "m", "v", "p"])
+    p2, m2, v2 = ot.adamw(vals["p32"], vals["g"], vals["m"], vals["v"], hp["step"], hp["lr"], hp["b1"], hp["b2"],
+                          hp["eps"], hp["wd"])
+    # weights at fp32 precision: the update (lr-sized, ~1% of a weight) shows at 1e-6
+    assert rel_l2(res["p32"], p2) < 2e-6
+    # and the update itself, elementwise, up to one fp32 rounding of the weight
+    dg, dr = res["p32"] - vals["p32"], p2 - vals["p32"]
+    assert np.all(np.abs(dg - dr) <= 1e-3 * np.abs(dr) + 2.4e-7 * np.abs(p2))
+    assert rel_l2(res["m"], m2) < 1e-6 and rel_l2(res["v"], v2) < 1e-6
+    assert rel_l2(res["p"], p2) < TOL[dt]

@@ -18,6 +18,7 @@ class DecoderConfig:
     style: str              # "gpt": LayerNorm + GELU FFN + fused qkv, tied head
                             # "llama": RMSNorm + SwiGLU + RoPE + KV cache, untied head
                             # "moe": llama attention, then top-k of n_experts SwiGLU experts
+                            # "train": llama, one training step (forward, backward, AdamW)
     n_layers: int
     hidden: int
     n_heads: int
@@ -80,4 +81,16 @@ MOE_8X = DecoderConfig("moe-8x14336", "moe", 32, 4096, 32, 14336, 32000, DT_BF16
 MOE_SMALL = DecoderConfig("moe-small", "moe", 2, 256, 2, 384, 1000, DT_BF16,
                           2, 40, decode_steps=6, factor=(2, 1), n_experts=4, top_k=2)
 
-CONFIGS = {c.name: c for c in (TINY, GPT_1P3B, LLAMA_7B, LLAMA_SMALL, GPT_SMALL, MOE_8X, MOE_SMALL)}
+# 13B-shape LLaMA-style training step: 40 layers, hidden 5120, 40 heads,
+# SwiGLU 13824, RMSNorm, vocab 32k; batch 8 x 2048 random tokens (next-token
+# targets); bf16 weights with fp32 master weights and Adam moments; forward
+# and backward with all activations kept; budget = footprint / 2.
+LLAMA_13B_TRAIN = DecoderConfig("llama-13b-train", "train", 40, 5120, 40, 13824, 32000, DT_BF16,
+                                8, 2048, factor=(2, 1))
+
+# Small training step for parity tests (head dim 128).
+TRAIN_SMALL = DecoderConfig("train-small", "train", 2, 256, 2, 384, 1024, DT_BF16,
+                            2, 80, factor=(2, 1))
+
+CONFIGS = {c.name: c for c in (TINY, GPT_1P3B, LLAMA_7B, LLAMA_SMALL, GPT_SMALL, MOE_8X, MOE_SMALL,
+                               LLAMA_13B_TRAIN, TRAIN_SMALL)}

@@ -18,6 +18,7 @@ KIND_PARAM, KIND_ACT, KIND_KV = 0, 1, 2
 
 # registration flags
 FLAG_HOST_INIT = 1
+FLAG_LIVE_OUT = 2      # final value read after the trace: written back, never dropped
 
 # operand access modes
 MODE_R, MODE_W, MODE_RW = 1, 2, 3
@@ -39,6 +40,17 @@ OP_MOE_ROUTE = 12     # (M, H, E, K)         h R, Wr R, rte W, rtw W    top-K of
 OP_MOE_DISPATCH = 13  # (M, E, K, log_row)   rte R, lists W, log RW     per-expert ordered row lists
 OP_MOE_UP = 14        # (M, F, H, e, n, K)   h R, lists R, Wg R, Wu R, fe W   routed rows of expert e
 OP_MOE_DOWN = 15      # (M, H, F, e, n, K)   fe R, lists R, rtw R, Wd R, x RW  weighted scatter-add
+# training step (backward and update)
+OP_COPY = 16          # (nbytes,)            a R, b W
+OP_TRANSPOSE = 17     # (R, C)               a R [R,C], b W [C,R]
+OP_SWIGLU_ACT = 18    # (T, F)               G R, U R, F W          F = silu(G) * U
+OP_SWIGLU_BWD = 19    # (T, F)               G R, U R, dF R, dG W, dU W
+OP_RMSNORM_BWD = 20   # (T, H, acc)          x R, g R, dy R, dx W|RW, dxb W, dg W, rstd W
+OP_ATTN_BWD = 21      # (B, S, nH, d)        q R, K R, V R, o R, lse R, do R, dq W, dK W, dV W, D W
+OP_ROPE_BWD = 22      # (B, S, nH, d)        dq RW, dK R, dV R, dk W, dv W
+OP_XENT = 23          # (T, V)               logits R, labels R, losses W, dlogits W
+OP_EMBED_BWD = 24     # (T, H, V)            ids R, dx R, dE W
+OP_ADAM = 25          # (n, step, lr*1e9, b1*1e6, b2*1e6, eps*1e12, wd*1e6)  g R, p32 RW, m RW, v RW, p W
 
 OP_NAMES = {
     OP_TOUCH: "touch", OP_EMBED: "embed", OP_LAYERNORM: "layernorm",
@@ -46,7 +58,10 @@ OP_NAMES = {
     OP_LINEAR_RESID: "linear_resid", OP_LINEAR_SWIGLU: "linear_swiglu",
     OP_ATTN_QKV: "attn_qkv", OP_ROPE_KV: "rope_kv", OP_ATTN_CACHE: "attn_cache",
     OP_ARGMAX: "argmax", OP_MOE_ROUTE: "moe_route", OP_MOE_DISPATCH: "moe_dispatch",
-    OP_MOE_UP: "moe_up", OP_MOE_DOWN: "moe_down",
+    OP_MOE_UP: "moe_up", OP_MOE_DOWN: "moe_down", OP_COPY: "copy", OP_TRANSPOSE: "transpose",
+    OP_SWIGLU_ACT: "swiglu_act", OP_SWIGLU_BWD: "swiglu_bwd", OP_RMSNORM_BWD: "rmsnorm_bwd",
+    OP_ATTN_BWD: "attn_bwd", OP_ROPE_BWD: "rope_bwd", OP_XENT: "xent", OP_EMBED_BWD: "embed_bwd",
+    OP_ADAM: "adam",
 }
 
 # planner policy variants (paper's ablation ladder plus the two demand baselines)

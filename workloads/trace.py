@@ -13,12 +13,15 @@ from dataclasses import dataclass, field
 from typing import Dict, List, Optional, Tuple
 
 from .configs import DecoderConfig
-from .format import (ALIGN, DT_F32, DT_I32, DT_SIZE, FLAG_HOST_INIT, KIND_ACT,
+from .format import (ALIGN, DT_F32, DT_I32, DT_SIZE, FLAG_HOST_INIT, FLAG_LIVE_OUT, KIND_ACT,
                      KIND_KV, KIND_PARAM, MODE_R, MODE_RW, MODE_W, OP_ARGMAX,
                      OP_ATTN_CACHE, OP_ATTN_QKV, OP_EMBED, OP_LAYERNORM,
                      OP_LINEAR, OP_LINEAR_GELU, OP_LINEAR_RESID,
                      OP_LINEAR_SWIGLU, OP_MOE_DISPATCH, OP_MOE_DOWN,
-                     OP_MOE_ROUTE, OP_MOE_UP, OP_RMSNORM, OP_ROPE_KV)
+                     OP_MOE_ROUTE, OP_MOE_UP, OP_RMSNORM, OP_ROPE_KV, OP_ADAM,
+                     OP_ATTN_BWD, OP_COPY, OP_EMBED_BWD, OP_RMSNORM_BWD,
+                     OP_ROPE_BWD, OP_SWIGLU_ACT, OP_SWIGLU_BWD, OP_TRANSPOSE,
+                     OP_XENT, DT_BF16)
 
 
 def align_up(n: int, a: int = ALIGN) -> int:
@@ -32,9 +35,10 @@ class TensorSpec:
     dtype: int
     kind: int
     host_init: bool
-    init: str = "none"       # "normal" (weights), "ones" (norm gains), "zeros", "ids"
+    init: str = "none"       # "normal" (weights), "ones" (norm gains), "zeros", "ids", ...
     off: int = 0             # arena offset
     tid: int = -1
+    live_out: bool = False   # final value read after the trace (carried state)
 
     @property
     def nbytes(self) -> int:
@@ -45,7 +49,8 @@ class TensorSpec:
 
     @property
     def flags(self) -> int:
-        return FLAG_HOST_INIT if (self.host_init and self.kind != KIND_PARAM) else 0
+        f = FLAG_HOST_INIT if (self.host_init and self.kind != KIND_PARAM) else 0
+        return f | (FLAG_LIVE_OUT if self.live_out else 0)
 
 
 @dataclass
@@ -67,9 +72,9 @@ class Workload:
     arena_bytes: int = 0
 
     # -- construction helpers -------------------------------------------------
-    def tensor(self, name, shape, dtype, kind, host_init=False, init="none") -> int:
+    def tensor(self, name, shape, dtype, kind, host_init=False, init="none", live_out=False) -> int:
         t = TensorSpec(name, tuple(int(s) for s in shape), dtype, kind,
-                       host_init or kind == KIND_PARAM, init)
+                       host_init or kind == KIND_PARAM, init, live_out=live_out)
         t.tid = len(self.tensors)
         t.off = self.arena_bytes
         self.arena_bytes += align_up(t.nbytes)
@@ -99,11 +104,13 @@ class Workload:
         return (self.footprint * den // num) // ALIGN * ALIGN
 
 
-def build(cfg: DecoderConfig, routing=None, steps=None) -> Workload:
+def build(cfg: DecoderConfig, routing=None, steps=None, keep_grads=False) -> Workload:
     """The workload of a config.
 
     ``steps`` traces only the first decode steps of a LLaMA-style or MoE
     config; the tensors (KV cache length, logs) stay those of the full run.
+    ``keep_grads`` marks a training step's gradients live-out, so that they
+    can be read after the step (they are otherwise dead once applied).
 
     For MoE configs ``routing`` is the per-expert row count of every MoE layer
     in every run segment (prefill, then each decode step), as the dispatch
@@ -116,6 +123,8 @@ def build(cfg: DecoderConfig, routing=None, steps=None) -> Workload:
         return _build_gpt(cfg)
     if cfg.style in ("llama", "moe"):
         return _build_llama(cfg, routing, cfg.decode_steps if steps is None else steps)
+    if cfg.style == "train":
+        return _build_train(cfg, keep_grads)
     raise ValueError(cfg.style)
 
 
@@ -315,4 +324,161 @@ def _build_llama(c: DecoderConfig, routing=None, n_steps=0) -> Workload:
         w.kernel(OP_ARGMAX, (B, V, s + 1), [(logits, R), (tok, W_), (gen, RW)], c.n_layers, "argmax")
         steps.append((k0, len(w.kernels) - k0))
     w.segments["decode"] = steps
+    return w
+
+
+def adam_shape(n, hp):
+    """Shape integers of an ADAM kernel: the hyperparameters in fixed point."""
+    return (n, hp["step"], round(hp["lr"] * 1e9), round(hp["b1"] * 1e6), round(hp["b2"] * 1e6),
+            round(hp["eps"] * 1e12), round(hp["wd"] * 1e6))
+
+
+def _build_train(c: DecoderConfig, keep_grads=False) -> Workload:
+    """One training step of the LLaMA-style decoder: forward keeping every
+    layer's activations, cross-entropy against next-token targets, backward,
+    and AdamW on fp32 master weights (bf16 copies feed the GEMMs).  Backward
+    GEMMs run as C = A W^T over explicit transposes of their operands."""
+    from .init import TRAIN_HP
+    w = Workload(c)
+    H, F, V, B, S = c.hidden, c.ffn, c.vocab, c.batch, c.prompt_len
+    nH, d, T = c.n_heads, c.head_dim, c.tokens
+    dt = c.dtype
+    R, W_, RW = MODE_R, MODE_W, MODE_RW
+    params = []
+
+    # weights, master weights and moments are carried to the next step: live-out
+    def param(name, shape, init):
+        t = w.tensor(name, shape, dt, KIND_PARAM, init=init, live_out=True)
+        params.append(name)
+        return t
+    E = param("E", (V, H), "normal")
+    layers = []
+    for l in range(c.n_layers):
+        p = f"L{l}."
+        layers.append(dict(
+            g1=param(p + "attn_norm", (H,), "ones"), wq=param(p + "wq", (H, H), "normal"),
+            wk=param(p + "wk", (H, H), "normal"), wv=param(p + "wv", (H, H), "normal"),
+            wo=param(p + "wo", (H, H), "normal"), g2=param(p + "ffn_norm", (H,), "ones"),
+            wg=param(p + "wg", (F, H), "normal"), wu=param(p + "wu", (F, H), "normal"),
+            wd=param(p + "wd", (H, F), "normal")))
+    gf = param("norm_f", (H,), "ones")
+    head = param("head", (V, H), "normal")
+    opt = {}
+    for n in params:
+        shp = w.tensors[w.id(n)].shape
+        opt[n] = dict(master=w.tensor(n + ".master", shp, DT_F32, KIND_PARAM, init="master", live_out=True),
+                      m=w.tensor(n + ".m", shp, DT_F32, KIND_PARAM, init="adam_m", live_out=True),
+                      v=w.tensor(n + ".v", shp, DT_F32, KIND_PARAM, init="adam_v", live_out=True),
+                      grad=w.tensor(n + ".grad", shp, DT_F32, KIND_ACT, live_out=keep_grads))
+    ids = w.tensor("ids", (T,), DT_I32, KIND_ACT, host_init=True, init="ids")
+    labels = w.tensor("labels", (T,), DT_I32, KIND_ACT, host_init=True, init="labels")
+    # activations kept for the backward pass
+    for l, L in enumerate(layers):
+        p = f"L{l}."
+        for nm, shp, ty in (("x", (T, H), DT_F32), ("h1", (T, H), dt), ("q", (T, H), dt),
+                            ("K", (B, nH, S, d), dt), ("V", (B, nH, S, d), dt), ("o", (T, H), dt),
+                            ("lse", (B, nH, S), DT_F32), ("xm", (T, H), DT_F32), ("h2", (T, H), dt),
+                            ("G", (T, F), dt), ("U", (T, F), dt), ("F", (T, F), dt)):
+            L[nm] = w.tensor(p + nm, shp, ty, KIND_ACT)
+    xL = w.tensor("xL", (T, H), DT_F32, KIND_ACT)
+    hf = w.tensor("hf", (T, H), dt, KIND_ACT)
+    logits = w.tensor("logits", (T, V), DT_F32, KIND_ACT)
+    losses = w.tensor("losses", (T,), DT_F32, KIND_ACT)
+    dlogits = w.tensor("dlogits", (T, V), dt, KIND_ACT)
+    # temporaries shared by the layers
+    k_t = w.tensor("k_tmp", (T, H), dt, KIND_ACT)
+    v_t = w.tensor("v_tmp", (T, H), dt, KIND_ACT)
+    dx = w.tensor("dx", (T, H), DT_F32, KIND_ACT)
+    dxb = w.tensor("dxb", (T, H), dt, KIND_ACT)
+    dh = w.tensor("dh", (T, H), DT_F32, KIND_ACT)
+    dF = w.tensor("dF", (T, F), dt, KIND_ACT)
+    dG = w.tensor("dG", (T, F), dt, KIND_ACT)
+    dU = w.tensor("dU", (T, F), dt, KIND_ACT)
+    do_ = w.tensor("do", (T, H), dt, KIND_ACT)
+    dq = w.tensor("dq", (T, H), dt, KIND_ACT)
+    dK = w.tensor("dK", (B, nH, S, d), dt, KIND_ACT)
+    dV = w.tensor("dV", (B, nH, S, d), dt, KIND_ACT)
+    dk = w.tensor("dk", (T, H), dt, KIND_ACT)
+    dv = w.tensor("dv", (T, H), dt, KIND_ACT)
+    WT = w.tensor("WT", (max(F, V), H), dt, KIND_ACT)
+    AT1 = w.tensor("AT1", (max(F, V, H), T), dt, KIND_ACT)
+    AT2 = w.tensor("AT2", (max(F, H), T), dt, KIND_ACT)
+    rstd = w.tensor("rstd", (T,), DT_F32, KIND_ACT)
+    Dws = w.tensor("attn_D", (B, nH, S), DT_F32, KIND_ACT)
+
+    def lin(a, Wt, out, M, N, K, l, tag, op=OP_LINEAR):
+        w.kernel(op, (M, N, K), [(a, R), (Wt, R), (out, RW if op == OP_LINEAR_RESID else W_)], l, tag)
+
+    def tr(a, b, rows, cols, l, tag):
+        w.kernel(OP_TRANSPOSE, (rows, cols), [(a, R), (b, W_)], l, tag)
+
+    def dlin(dy, Wt, dX, X, gW, M, N, K, l, tag, acc=False):
+        """y[M,N] = X[M,K] W[N,K]^T: dX (+)= dy W (dy [M,N] bf16), gW = dy^T X."""
+        tr(Wt, WT, N, K, l, tag + ".wT")
+        lin(dy, WT, dX, M, K, N, l, tag + ".dX", OP_LINEAR_RESID if acc else OP_LINEAR)
+        tr(dy, AT1, M, N, l, tag + ".dyT")
+        if X is not None:
+            tr(X, AT2, M, K, l, tag + ".xT")
+        lin(AT1, AT2, gW, N, K, M, l, tag + ".dW")
+
+    kf = len(w.kernels)
+    # ---- forward
+    w.kernel(OP_EMBED, (T, H, V), [(ids, R), (E, R), (layers[0]["x"], W_)], 0, "embed")
+    for l, L in enumerate(layers):
+        x_next = layers[l + 1]["x"] if l + 1 < len(layers) else xL
+        w.kernel(OP_RMSNORM, (T, H, 1, 0), [(L["x"], R), (L["g1"], R), (L["h1"], W_)], l, "attn_norm")
+        lin(L["h1"], L["wq"], L["q"], T, H, H, l, "wq")
+        lin(L["h1"], L["wk"], k_t, T, H, H, l, "wk")
+        lin(L["h1"], L["wv"], v_t, T, H, H, l, "wv")
+        w.kernel(OP_ROPE_KV, (B, S, nH, d, S, 0), [(L["q"], RW), (k_t, R), (v_t, R), (L["K"], W_), (L["V"], W_)],
+                 l, "rope")
+        w.kernel(OP_ATTN_CACHE, (B, S, nH, d, S, 0), [(L["q"], R), (L["K"], R), (L["V"], R), (L["o"], W_),
+                                                      (L["lse"], W_)], l, "attn")
+        w.kernel(OP_COPY, (T * H * 4,), [(L["x"], R), (L["xm"], W_)], l, "copy")
+        lin(L["o"], L["wo"], L["xm"], T, H, H, l, "wo", OP_LINEAR_RESID)
+        w.kernel(OP_RMSNORM, (T, H, 1, 0), [(L["xm"], R), (L["g2"], R), (L["h2"], W_)], l, "ffn_norm")
+        lin(L["h2"], L["wg"], L["G"], T, F, H, l, "wg")
+        lin(L["h2"], L["wu"], L["U"], T, F, H, l, "wu")
+        w.kernel(OP_SWIGLU_ACT, (T, F), [(L["G"], R), (L["U"], R), (L["F"], W_)], l, "swiglu")
+        w.kernel(OP_COPY, (T * H * 4,), [(L["xm"], R), (x_next, W_)], l, "copy")
+        lin(L["F"], L["wd"], x_next, T, H, F, l, "wd", OP_LINEAR_RESID)
+    nl = c.n_layers
+    w.kernel(OP_RMSNORM, (T, H, 1, 0), [(xL, R), (gf, R), (hf, W_)], nl, "norm_f")
+    lin(hf, head, logits, T, V, H, nl, "head")
+    w.kernel(OP_XENT, (T, V), [(logits, R), (labels, R), (losses, W_), (dlogits, W_)], nl, "xent")
+    kb = len(w.kernels)
+    # ---- backward
+    dlin(dlogits, head, dh, hf, opt["head"]["grad"], T, V, H, nl, "head")
+    w.kernel(OP_RMSNORM_BWD, (T, H, 0), [(xL, R), (gf, R), (dh, R), (dx, W_), (dxb, W_),
+                                          (opt["norm_f"]["grad"], W_), (rstd, W_)], nl, "norm_f.bwd")
+    for l in reversed(range(c.n_layers)):
+        L = layers[l]
+        p = f"L{l}."
+        dlin(dxb, L["wd"], dF, L["F"], opt[p + "wd"]["grad"], T, H, F, l, "wd")
+        w.kernel(OP_SWIGLU_BWD, (T, F), [(L["G"], R), (L["U"], R), (dF, R), (dG, W_), (dU, W_)], l, "swiglu.bwd")
+        dlin(dG, L["wg"], dh, L["h2"], opt[p + "wg"]["grad"], T, F, H, l, "wg")
+        dlin(dU, L["wu"], dh, None, opt[p + "wu"]["grad"], T, F, H, l, "wu", acc=True)
+        w.kernel(OP_RMSNORM_BWD, (T, H, 1), [(L["xm"], R), (L["g2"], R), (dh, R), (dx, RW), (dxb, W_),
+                                              (opt[p + "ffn_norm"]["grad"], W_), (rstd, W_)], l, "ffn_norm.bwd")
+        dlin(dxb, L["wo"], do_, L["o"], opt[p + "wo"]["grad"], T, H, H, l, "wo")
+        w.kernel(OP_ATTN_BWD, (B, S, nH, d), [(L["q"], R), (L["K"], R), (L["V"], R), (L["o"], R), (L["lse"], R),
+                                              (do_, R), (dq, W_), (dK, W_), (dV, W_), (Dws, W_)], l, "attn.bwd")
+        w.kernel(OP_ROPE_BWD, (B, S, nH, d), [(dq, RW), (dK, R), (dV, R), (dk, W_), (dv, W_)], l, "rope.bwd")
+        dlin(dq, L["wq"], dh, L["h1"], opt[p + "wq"]["grad"], T, H, H, l, "wq")
+        dlin(dk, L["wk"], dh, None, opt[p + "wk"]["grad"], T, H, H, l, "wk", acc=True)
+        dlin(dv, L["wv"], dh, None, opt[p + "wv"]["grad"], T, H, H, l, "wv", acc=True)
+        w.kernel(OP_RMSNORM_BWD, (T, H, 1), [(L["x"], R), (L["g1"], R), (dh, R), (dx, RW), (dxb, W_),
+                                              (opt[p + "attn_norm"]["grad"], W_), (rstd, W_)], l, "attn_norm.bwd")
+    w.kernel(OP_EMBED_BWD, (T, H, V), [(ids, R), (dx, R), (opt["E"]["grad"], W_)], 0, "embed.bwd")
+    ka = len(w.kernels)
+    # ---- update
+    for n in params:
+        o = opt[n]
+        nel = w.tensors[w.id(n)].nbytes // DT_SIZE[dt]
+        w.kernel(OP_ADAM, adam_shape(nel, TRAIN_HP), [(o["grad"], R), (o["master"], RW), (o["m"], RW),
+                                                      (o["v"], RW), (w.id(n), W_)], 0, "adam")
+    w.segments["forward"] = [(kf, kb - kf)]
+    w.segments["backward"] = [(kb, ka - kb)]
+    w.segments["update"] = [(ka, len(w.kernels) - ka)]
+    w.segments["step"] = [(kf, len(w.kernels) - kf)]
     return w
