@@ -753,6 +753,156 @@ def prefill_main(args, cfg):
     print(json.dumps(result), flush=True)
 
 
+def cpu_baseline_train(cfg, seconds):
+    """fp64 oracle training step (forward, backward, AdamW) of a one-layer
+    model of the same width over one 2048-token sequence, split into the
+    layer's share and the embedding/head share, scaled to the run's layers
+    and batch."""
+    import dataclasses
+
+    import numpy as np
+    from oracle import train as ot
+    from workloads import init as winit
+    from workloads import trace
+    threads, vendor = blas_info()
+    c1 = dataclasses.replace(cfg, n_layers=1, batch=1, iterations=1)
+    w1 = trace.build(c1)
+    names = winit.param_names(w1)
+    P = winit.weights_f64(w1, names=names)
+    ids = winit.token_ids(c1.seed, 1, c1.prompt_len, c1.vocab)
+    labels = winit.next_token_labels(ids)
+    reps, t_all, t_head = 0, 0.0, 0.0
+    t_start = time.perf_counter()
+    while reps == 0 or time.perf_counter() - t_start < seconds:
+        t = time.perf_counter()
+        lg, cache = ot.forward(c1, P, ids)
+        loss, dl = ot.cross_entropy(lg, labels)
+        ot.backward(c1, P, ids, cache, dl)
+        t_all += time.perf_counter() - t
+        t = time.perf_counter()           # the head's share: logits, loss, both head gradients
+        hf = cache["hf"]
+        lg2 = ot.linear(hf, P["head"])
+        ot.cross_entropy(lg2, labels)
+        _ = dl.T @ hf, dl @ P["head"]
+        t_head += time.perf_counter() - t
+        reps += 1
+    t_all, t_head = t_all / reps, t_head / reps
+    # AdamW over one layer's parameters
+    lw = [n for n in names if n.startswith("L0.")]
+    t = time.perf_counter()
+    for n in lw:
+        ot.adamw(P[n], P[n], P[n], np.abs(P[n]), 10, 1e-4, 0.9, 0.95, 1e-8, 0.1)
+    t_adam_layer = time.perf_counter() - t
+    seq_s = t_head + (t_all - t_head + t_adam_layer) * cfg.n_layers
+    step_s = seq_s * cfg.batch
+    return {"value": cfg.tokens / step_s, "unit": "tokens/s", "cores": threads, "kind": "oracle", "blas": vendor,
+            "sample": f"fp64 numpy oracle training step (forward, backward, AdamW) of a 1-layer model of the "
+                      f"same width over one {cfg.prompt_len}-token sequence, timed over {reps} repetitions; "
+                      f"the layer's share ({t_all - t_head + t_adam_layer:.2f} s) scaled to {cfg.n_layers} layers "
+                      f"plus the head's ({t_head:.2f} s), times {cfg.batch} sequences ({step_s:.1f} s per step)"}
+
+
+def train_main(args, cfg):
+    """Training steps of the LLaMA-style model: warmup steps, then K timed."""
+    import dataclasses
+
+    import torch
+
+    from paper_2609_06172_amd.session import Session
+    from workloads import trace
+    from workloads.format import OP_ATTN_BWD, OP_LINEAR, OP_LINEAR_RESID
+
+    num, den = cfg.factor
+    W = max(1, args.warmup)
+    K = 2 if args.steps is None else args.steps
+    n_layers = cfg.n_layers
+    layers = args.layers or cfg.n_layers
+    while layers > 1 and trace.build(dataclasses.replace(cfg, n_layers=layers)).footprint > PINNED_LIMIT:
+        layers -= 1
+    cfg = dataclasses.replace(cfg, n_layers=layers, iterations=W + K)
+    w = trace.build(cfg)
+    M = w.budget()
+    steps = w.segments["step"]
+    log(f"workload {cfg.name}: {layers} of {n_layers} layers, {len(w.tensors)} tensors, "
+        f"{len(w.kernels)} kernels ({W + K} steps), footprint {w.footprint} B, budget {M} B")
+    bl_meas = link_bandwidth()
+    t = time.perf_counter()
+    s = Session(w, device=0, M=M, variant=4, timing=1)
+    log(f"session ready in {time.perf_counter() - t:.1f} s")
+
+    def run(sess):
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        sess.run(steps[0][0], steps[W][0] - steps[0][0])
+        torch.cuda.synchronize()
+        cold = time.perf_counter() - t
+        k0, k1 = steps[W][0], steps[-1][0] + steps[-1][1]
+        t = time.perf_counter()
+        sess.run(k0, k1 - k0)
+        torch.cuda.synchronize()
+        return cold, time.perf_counter() - t, k0, k1
+
+    cold_s, hot_s, k0, k1 = run(s)
+    log(f"{W} warmup step(s) {cold_s:.2f} s, {K} timed steps {hot_s:.2f} s")
+    sched, classes = s.ctx.get_schedule(), s.ctx.get_classes()
+    dur, gap = s.ctx.get_kernel_times()
+    tl = s.ctx.get_timeline()
+    loss = float(s.read("losses").astype("float64").mean())
+    st = seg_stats(w, sched, classes, M, steps[W:])
+    tokens = cfg.tokens * K
+    lin = [k for k in range(k0, k1) if w.kernels[k].op in (OP_LINEAR, OP_LINEAR_RESID)
+           and w.kernels[k].shape[2] % 64 == 0 and w.kernels[k].shape[0] >= 512]
+    g_flops = sum(classes[k][2] for k in lin)
+    g_time = sum(dur[k] for k in lin) * 1e-3
+    ab = [k for k in range(k0, k1) if w.kernels[k].op == OP_ATTN_BWD]
+    per_tag = {}
+    for k in range(k0, k1):
+        tag = w.kernels[k].tag.split(".")[-1] if "." in w.kernels[k].tag else w.kernels[k].tag
+        per_tag[tag] = per_tag.get(tag, 0.0) + dur[k]
+    pr = roofline_fields(st, hot_s, bl_meas, tokens)
+    pr["roofline_tok_s"] = pr.pop("roofline_units_per_s")
+    result = {
+        "metric": metric("training ", num, den), "value": round(tokens / hot_s, 1), "unit": "tokens/s",
+        "n_gpus": 1, "steps": K, "warmup": W, "ms_per_step": round(hot_s / K * 1e3, 3),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": f"{cfg.name}-shape training step: {layers} of the model's {n_layers} layers (host "
+                               f"backing limited to the pinned memory the host grants), hidden {cfg.hidden}, "
+                               f"SwiGLU {cfg.ffn}, vocab {cfg.vocab}, {cfg.batch} x {cfg.prompt_len} tokens, bf16 "
+                               f"weights with fp32 master weights and AdamW moments, budget = footprint*{den}/{num}",
+                   "tokens_per_step": cfg.tokens, "layers": layers, "model_layers": n_layers,
+                   "factor": f"{num}/{den}", "footprint_bytes": w.footprint, "budget_bytes": M, "policy": "T+A+P"},
+        "path_roofline": pr,
+        "roofline": {"kernel": "GEMMs of the step (forward, data and weight gradients; bf16 matrix cores)",
+                     "bound": "mfma", "achieved": round(g_flops / g_time / 1e12, 1), "peak": 2500.0,
+                     "unit": "TFLOP/s", "frac": round(g_flops / g_time / 2.5e15, 4), "traffic": None,
+                     "launches": len(lin), "avg_us": round(g_time / max(1, len(lin)) * 1e6, 2)},
+        "attention_backward": {"launches": len(ab), "ms_per_step": round(sum(dur[k] for k in ab) / K, 2),
+                               "TFLOPs": round(sum(classes[k][2] for k in ab) / max(1e-9, sum(dur[k] for k in ab) * 1e-3)
+                                               / 1e12, 1)},
+        "kernel_ms_per_step_by_tag": {t_: round(v / K, 2) for t_, v in sorted(per_tag.items(), key=lambda x: -x[1])[:12]},
+        "transfers": {"h2d_bytes_per_step": st["h2d_bytes"] // K, "d2h_bytes_per_step": st["d2h_bytes"] // K,
+                      "lmin_bytes_per_step": st["lmin_bytes"] // K,
+                      "compute_busy_ms_per_step": round(sum(dur[k] for k in range(k0, k1)) / K, 2),
+                      "link_timeline": link_timeline(tl, K)},
+        "loss_last_step": round(loss, 5),
+        "warmup": {"steps": W, "seconds": round(cold_s, 3)},
+    }
+    if not args.no_baseline:
+        s.set_policy(variant=0, timing=0)
+        s.ctx.reset()
+        s.restore_inputs()
+        _, hot_b, _, _ = run(s)
+        result["no_prefetch_baseline"] = {"policy": "demand fetch at launch, LRU eviction",
+                                          "value": round(tokens / hot_b, 1), "ms_per_step": round(hot_b / K * 1e3, 3),
+                                          "speedup_of_T+A+P": round(hot_b / hot_s, 3)}
+    s.close()
+    del s
+    torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline_train(cfg, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+
+
 def moe_main(args, cfg):
     """Routed-expert decode: a profiling run with every expert in the trace,
     then the recorded trace (routed experts only), both timed."""
@@ -882,6 +1032,8 @@ def main():
         prefill_main(args, cfg)
     elif cfg.style == "moe":
         moe_main(args, cfg)
+    elif cfg.style == "train":
+        train_main(args, cfg)
     elif args.sweep:
         sweep_main(args, cfg)
     else:

@@ -28,6 +28,7 @@ class Walker:
         self.s, self.pos = s, 0
 
     def to(self, k):
+        assert k >= self.pos, f"kernel {k} already ran (at {self.pos})"
         if k > self.pos:
             self.s.run(self.pos, k - self.pos)
             self.pos = k
@@ -157,3 +158,85 @@ def test_moe_decode_and_prefill_layers_sampled():
     Kc, Vc = K[bs].astype(np.float64), V[bs].astype(np.float64)
     ref = of.llama_layer(c1, Lw, x_in[bs], Kc, Vc, pos, forced_route=rte_d[bs])
     assert rel_l2(x_out[bs], ref) < TOL
+
+
+def test_training_step_13b_shape_sampled():
+    # two layers of the 13B shape at full width, 8 x 2048 tokens, 2x: each
+    # stage is checked on the GPU's own inputs, read at the point it runs
+    from oracle import train as ot
+    from paper_2609_06172_amd.session import Session
+    from workloads.format import OP_ADAM, OP_ATTN_BWD, OP_XENT
+    cfg = dataclasses.replace(configs.LLAMA_13B_TRAIN, n_layers=2)
+    w = trace.build(cfg)
+    T, H, F, V, S, nH = cfg.tokens, cfg.hidden, cfg.ffn, cfg.vocab, cfg.prompt_len, cfg.n_heads
+    print(f"13b-shape training step, 2 layers, {T} tokens at 2x", flush=True)
+    kb = w.segments["backward"][0][0]
+    ks = lambda pred: [k for k, kd in enumerate(w.kernels) if pred(k, kd)]
+    fwd1 = ks(lambda k, kd: k < kb and kd.layer == 1)
+    xent = ks(lambda k, kd: kd.op == OP_XENT)[0]
+    ab1 = ks(lambda k, kd: kd.op == OP_ATTN_BWD and kd.layer == 1)[0]
+    wd_tags = {kd.tag: k for k, kd in enumerate(w.kernels) if k > kb and kd.layer == 1 and kd.tag.startswith("wd.")}
+    adam = ks(lambda k, kd: kd.op == OP_ADAM and kd.operands[4][0] == w.id("L1.wd"))[0]
+    s = Session(w, device=0)
+    walk = Walker(s)
+    f64 = lambda n: s.read(n).astype(np.float64)
+    # forward of layer 1 on sequence 5
+    walk.to(fwd1[0])
+    x_in = f64("L1.x")
+    walk.to(fwd1[-1] + 1)
+    x_out = s.read("xL")
+    # loss and its gradient on sampled rows
+    walk.to(xent)
+    rows = np.array([0, 2047, 9000, 16383])
+    logits = s.read("logits")[rows].astype(np.float64)
+    walk.to(xent + 1)
+    losses, dlog = s.read("losses")[rows], s.read("dlogits")[rows]
+    # layer 1's down projection (the first of its backward): data gradient
+    # rows and weight gradient rows
+    walk.to(wd_tags["wd.wT"])
+    dxb, Fl = f64("dxb"), f64("L1.F")
+    walk.to(wd_tags["wd.dW"] + 1)
+    dF, gwd = s.read("dF"), s.read("L1.wd.grad")
+    # attention backward of layer 1 (the last of its backward), (b, h) = (3, 17)
+    walk.to(ab1)
+    b, h = 3, 17
+    tok = slice(b * S, (b + 1) * S)
+    q = f64("L1.q")[tok].reshape(S, nH, 128)[:, h]
+    K, Vv = f64("L1.K")[b, h], f64("L1.V")[b, h]
+    do = f64("do")[tok].reshape(S, nH, 128)[:, h]
+    walk.to(ab1 + 1)
+    dq = s.read("dq")[tok].reshape(S, nH, 128)[:, h]
+    dK, dV = s.read("dK")[b, h], s.read("dV")[b, h]
+    # AdamW of L1.wd
+    walk.to(adam)
+    before = {n: f64("L1.wd" + n) for n in (".grad", ".master", ".m", ".v")}
+    walk.to(adam + 1)
+    after = {n: s.read("L1.wd" + n) for n in (".master", ".m", ".v", "")}
+    s.close()
+
+    names = ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "wg", "wu", "wd")
+    Lw = _weights(w, "L1.", names)
+    c1 = dataclasses.replace(cfg, n_layers=1, batch=1)
+    seq = slice(5 * S, 6 * S)
+    # the layer on the GPU's input for one whole sequence (its own K/V, positions 0..S-1)
+    ref = of.llama_layer(dataclasses.replace(c1, style="llama"), Lw, x_in[seq],
+                         np.zeros((1, nH, S, 128)), np.zeros((1, nH, S, 128)), 0)
+    assert rel_l2(x_out[seq], ref) < TOL
+    labels = init.next_token_labels(init.token_ids(cfg.seed, cfg.batch, S, V)).reshape(-1)[rows]
+    lse = np.log(np.exp(logits - logits.max(1, keepdims=True)).sum(1)) + logits.max(1)
+    assert np.abs(losses - (lse - logits[np.arange(len(rows)), labels])).max() < 1e-4
+    _, dl = ot.cross_entropy(logits, labels)
+    assert rel_l2(dlog, dl * len(rows) / T) < TOL
+    rdq, rdk, rdv = ot.attention_backward(q, K, Vv, do)
+    for got, want in ((dq, rdq), (dK, rdk), (dV, rdv)):
+        assert rel_l2(got, want) < TOL
+    for n in (0, 777, H - 1):
+        assert rel_l2(gwd[n], dxb[:, n] @ Fl) < TOL
+    for t in (1, 8191, T - 1):
+        assert rel_l2(dF[t], dxb[t] @ Lw["wd"]) < TOL
+    hp = dict(init.TRAIN_HP)
+    p2, m2, v2 = ot.adamw(before[".master"], before[".grad"], before[".m"], before[".v"], hp["step"], hp["lr"],
+                          hp["b1"], hp["b2"], hp["eps"], hp["wd"])
+    assert rel_l2(after[".master"], p2) < 2e-6
+    assert rel_l2(after[".m"], m2) < 1e-6 and rel_l2(after[".v"], v2) < 1e-6
+    assert rel_l2(after[""], p2) < 4e-3

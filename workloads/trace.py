@@ -338,7 +338,6 @@ def _build_train(c: DecoderConfig, keep_grads=False) -> Workload:
     layer's activations, cross-entropy against next-token targets, backward,
     and AdamW on fp32 master weights (bf16 copies feed the GEMMs).  Backward
     GEMMs run as C = A W^T over explicit transposes of their operands."""
-    from .init import TRAIN_HP
     w = Workload(c)
     H, F, V, B, S = c.hidden, c.ffn, c.vocab, c.batch, c.prompt_len
     nH, d, T = c.n_heads, c.head_dim, c.tokens
@@ -406,6 +405,28 @@ def _build_train(c: DecoderConfig, keep_grads=False) -> Workload:
     rstd = w.tensor("rstd", (T,), DT_F32, KIND_ACT)
     Dws = w.tensor("attn_D", (B, nH, S), DT_F32, KIND_ACT)
 
+    g = dict(E=E, gf=gf, head=head, ids=ids, labels=labels, xL=xL, hf=hf, logits=logits, losses=losses,
+             dlogits=dlogits, k_t=k_t, v_t=v_t, dx=dx, dxb=dxb, dh=dh, dF=dF, dG=dG, dU=dU, do_=do_, dq=dq,
+             dK=dK, dV=dV, dk=dk, dv=dv, WT=WT, AT1=AT1, AT2=AT2, rstd=rstd, Dws=Dws)
+    for it in range(c.iterations):
+        _train_step(w, c, it, layers, params, opt, g)
+    return w
+
+
+def _train_step(w, c, it, layers, params, opt, g):
+    """Kernels of training step it (the AdamW step number advances with it);
+    g holds the tensors the layers share."""
+    from .init import TRAIN_HP
+    H, F, V, B, S = c.hidden, c.ffn, c.vocab, c.batch, c.prompt_len
+    nH, d, T = c.n_heads, c.head_dim, c.tokens
+    dt = c.dtype
+    R, W_, RW = MODE_R, MODE_W, MODE_RW
+    E, gf, head, ids, labels = g["E"], g["gf"], g["head"], g["ids"], g["labels"]
+    xL, hf, logits, losses, dlogits = g["xL"], g["hf"], g["logits"], g["losses"], g["dlogits"]
+    k_t, v_t, dx, dxb, dh = g["k_t"], g["v_t"], g["dx"], g["dxb"], g["dh"]
+    dF, dG, dU, do_, dq, dK, dV, dk, dv = (g[n] for n in ("dF", "dG", "dU", "do_", "dq", "dK", "dV", "dk", "dv"))
+    WT, AT1, AT2, rstd, Dws = g["WT"], g["AT1"], g["AT2"], g["rstd"], g["Dws"]
+
     def lin(a, Wt, out, M, N, K, l, tag, op=OP_LINEAR):
         w.kernel(op, (M, N, K), [(a, R), (Wt, R), (out, RW if op == OP_LINEAR_RESID else W_)], l, tag)
 
@@ -472,13 +493,12 @@ def _build_train(c: DecoderConfig, keep_grads=False) -> Workload:
     w.kernel(OP_EMBED_BWD, (T, H, V), [(ids, R), (dx, R), (opt["E"]["grad"], W_)], 0, "embed.bwd")
     ka = len(w.kernels)
     # ---- update
+    hp = dict(TRAIN_HP, step=TRAIN_HP["step"] + it)
     for n in params:
         o = opt[n]
         nel = w.tensors[w.id(n)].nbytes // DT_SIZE[dt]
-        w.kernel(OP_ADAM, adam_shape(nel, TRAIN_HP), [(o["grad"], R), (o["master"], RW), (o["m"], RW),
-                                                      (o["v"], RW), (w.id(n), W_)], 0, "adam")
-    w.segments["forward"] = [(kf, kb - kf)]
-    w.segments["backward"] = [(kb, ka - kb)]
-    w.segments["update"] = [(ka, len(w.kernels) - ka)]
-    w.segments["step"] = [(kf, len(w.kernels) - kf)]
-    return w
+        w.kernel(OP_ADAM, adam_shape(nel, hp), [(o["grad"], R), (o["master"], RW), (o["m"], RW),
+                                                (o["v"], RW), (w.id(n), W_)], 0, "adam")
+    for name, seg in (("forward", (kf, kb - kf)), ("backward", (kb, ka - kb)),
+                      ("update", (ka, len(w.kernels) - ka)), ("step", (kf, len(w.kernels) - kf))):
+        w.segments.setdefault(name, []).append(seg)
