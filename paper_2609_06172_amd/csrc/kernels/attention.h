@@ -24,4 +24,15 @@ struct AttnArgs {
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s);
 
+// Causal attention backward, head dim 128, bf16, positions 0..S-1: q, dO, dq
+// token-major [B*S, nH*128] (row stride q_rs = nH*128); K, V, dK, dV
+// [B, nH, S, 128]; lse (natural) and D = rowsum(dO o) fp32 [B, nH, S].
+struct AttnBwdArgs {
+  const uint8_t *q, *k, *v, *dO;
+  const float *lse, *D;
+  uint8_t *dq, *dk, *dv;
+  int64_t B, S, nH, q_rs;
+};
+hipError_t launch_attention_bwd_d128(const AttnBwdArgs& a, hipStream_t s);
+
 }  // namespace auvm

@@ -385,7 +385,241 @@ __global__ void __launch_bounds__(64 * FW, 2) attn_prefill_d128(AttnArgs a, int6
   }
 }
 
+// ---------------------------------------------------------------- backward (head dim 128)
+// Causal attention backward on matrix cores, from the forward's q, K, V, its
+// per-query log-sum-exp and D = rowsum(dO o).  Two passes, no atomics:
+//   dQ: one workgroup per (b, h, 128 queries), like the forward: S^T = K Q^T
+//     and dP^T = V dO^T (K, V tiles in LDS; Q^T, dO^T fragments of the
+//     wave's queries in registers), P^T = exp(S^T/sqrt(d) - lse),
+//     dS^T = P^T (dP^T - D), then dQ^T += K^T dS^T with K^T fragments by
+//     LDS transpose reads and dS^T traded into the B-operand layout;
+//   dK, dV: one workgroup per (b, h, 128 keys), the mirror image: S = Q K^T
+//     and dP = dO V^T (Q, dO tiles in LDS, the wave's K, V rows in
+//     registers), then dV^T += dO^T P and dK^T += Q^T dS.
+// A lane owns one query (dQ pass) or one key (dK, dV pass), so the 32 x 32
+// accumulator tiles map to one row of the output each.
+
+// the B-operand fragment (16 rows of k, this lane's column) of k-step s from
+// a pair of 32 x 32 C tiles t[0..1] (rows 0..31, 32..63): rows 16s.. of the
+// pair; the lane and its partner (lane ^ 32) trade one 4-row group each
+__device__ __forceinline__ bf16x8 c_to_b(const f32x16* t, int s, int lh) {
+  const int kt = s >> 1, g0 = 2 * (s & 1);
+  const uint32_t a0 = pack_bf16(t[kt][4 * g0 + 0], t[kt][4 * g0 + 1]);
+  const uint32_t a1 = pack_bf16(t[kt][4 * g0 + 2], t[kt][4 * g0 + 3]);
+  const uint32_t b0 = pack_bf16(t[kt][4 * g0 + 4], t[kt][4 * g0 + 5]);
+  const uint32_t b1 = pack_bf16(t[kt][4 * g0 + 6], t[kt][4 * g0 + 7]);
+  const uint32_t s0 = lh ? a0 : b0, s1 = lh ? a1 : b1;
+  const uint32_t r0 = uint32_t(__shfl_xor(int(s0), 32, 64)), r1 = uint32_t(__shfl_xor(int(s1), 32, 64));
+  const u32x4v pf = lh ? u32x4v{r0, r1, b0, b1} : u32x4v{a0, a1, r0, r1};
+  return __builtin_bit_cast(bf16x8, pf);
+}
+
+// the A-operand fragment of the transposed tile (dims 32 dt.., rows 16 s..)
+// from a row-major swizzled 64 x 128 tile, by two LDS transpose reads
+__device__ __forceinline__ bf16x8 tile_t_frag(const bf16_t* tile, int s, int dt, int lane) {
+  const int tg = lane >> 4, tj = lane & 15;
+  const int row = 16 * s + 8 * (tg >> 1) + (tj >> 2);
+  const int dim = 32 * dt + 16 * (tg & 1) + 4 * (tj & 3);
+  typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+  const i16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(tile + tile_at(row, dim)));
+  const i16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(tile + tile_at(row + 4, dim)));
+  typedef short i16x8 __attribute__((ext_vector_type(8)));
+  const i16x8 vv = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
+  return __builtin_bit_cast(bf16x8, vv);
+}
+
+constexpr float kBwdScale = 0.08838834764831845f;   // 1 / sqrt(128)
+constexpr float kLog2eF = 1.4426950408889634f;
+
+__global__ void __launch_bounds__(64 * FW, 1) attn_bwd_dq_d128(AttnBwdArgs a, int64_t nqb) {
+  extern __shared__ __align__(16) bf16_t fsm[];
+  bf16_t* Ks = fsm;                 // [2][FK][FD]
+  bf16_t* Vs = fsm + 2 * TS;        // [2][FK][FD]
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int lq = lane & 31, lh = lane >> 5;
+  const int64_t qb = nqb - 1 - int64_t(blockIdx.x) % nqb, bh = int64_t(blockIdx.x) / nqb;
+  const int64_t h = bh % a.nH, b = bh / a.nH, S = a.S;
+  const int64_t q0 = qb * FQ, qw = q0 + 32 * wv, qr = qw + lq;
+  const bf16_t* Q = reinterpret_cast<const bf16_t*>(a.q) + (b * S) * a.q_rs + h * FD;
+  const bf16_t* dO = reinterpret_cast<const bf16_t*>(a.dO) + (b * S) * a.q_rs + h * FD;
+  const bf16_t* Kg = reinterpret_cast<const bf16_t*>(a.k) + bh * S * FD;
+  const bf16_t* Vg = reinterpret_cast<const bf16_t*>(a.v) + bh * S * FD;
+  bf16x8 qf[8], df[8];
+#pragma unroll
+  for (int c = 0; c < 8; ++c) {
+    qf[c] = qr < S ? *reinterpret_cast<const bf16x8*>(Q + qr * a.q_rs + 16 * c + 8 * lh) : bf16x8{};
+    df[c] = qr < S ? *reinterpret_cast<const bf16x8*>(dO + qr * a.q_rs + 16 * c + 8 * lh) : bf16x8{};
+  }
+  const float lse2 = qr < S ? a.lse[bh * S + qr] * kLog2eF : 0.f;
+  const float Dq = qr < S ? a.D[bh * S + qr] : 0.f;
+  const float c2 = kBwdScale * kLog2eF;
+  f32x16 dqt[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) dqt[t] = f32x16{};
+  const int64_t klast = (q0 + FQ - 1 < S ? q0 + FQ - 1 : S - 1);
+  const int64_t wlast = qw + 31;
+  load_kv(Ks, Kg, FD, 0, klast, wv, lane);
+  load_kv(Vs, Vg, FD, 0, klast, wv, lane);
+  int buf = 0;
+  for (int64_t k0 = 0; k0 <= klast; k0 += FK, buf ^= 1) {
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    asm volatile("" ::: "memory");
+    if (k0 + FK <= klast) {
+      load_kv(Ks + (buf ^ 1) * TS, Kg, FD, k0 + FK, klast, wv, lane);
+      load_kv(Vs + (buf ^ 1) * TS, Vg, FD, k0 + FK, klast, wv, lane);
+    }
+    if (k0 > wlast) continue;
+    const bf16_t* ks = Ks + buf * TS;
+    const bf16_t* vs = Vs + buf * TS;
+    // S^T and dP^T tiles kt: element e is key k0 + 32 kt + 8 (e/4) + 4 lh + e%4 of query qr
+    f32x16 st[2], dpt[2];
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt) {
+      st[kt] = f32x16{};
+      dpt[kt] = f32x16{};
+#pragma unroll
+      for (int c = 0; c < 8; ++c) {
+        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(ks + tile_at(32 * kt + lq, 16 * c + 8 * lh));
+        st[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[c], st[kt], 0, 0, 0);
+        const bf16x8 vf = *reinterpret_cast<const bf16x8*>(vs + tile_at(32 * kt + lq, 16 * c + 8 * lh));
+        dpt[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, df[c], dpt[kt], 0, 0, 0);
+      }
+    }
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int64_t key = k0 + 32 * kt + 8 * (e >> 2) + 4 * lh + (e & 3);
+        const float p = (key <= qr && qr < S) ? __builtin_amdgcn_exp2f(fmaf(st[kt][e], c2, -lse2)) : 0.f;
+        st[kt][e] = p * (dpt[kt][e] - Dq);       // dS^T
+      }
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const bf16x8 dsb = c_to_b(st, s, lh);
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt)
+        dqt[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tile_t_frag(ks, s, dt, lane), dsb, dqt[dt], 0, 0, 0);
+    }
+  }
+  if (qr < S) {
+    bf16_t* dq = reinterpret_cast<bf16_t*>(a.dq) + (b * S) * a.q_rs + h * FD;
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+      for (int e = 0; e < 16; ++e)
+        dq[qr * a.q_rs + 32 * dt + 8 * (e >> 2) + 4 * lh + (e & 3)] = f2bf(dqt[dt][e] * kBwdScale);
+  }
+}
+
+__global__ void __launch_bounds__(64 * FW, 1) attn_bwd_dkv_d128(AttnBwdArgs a, int64_t nkb) {
+  extern __shared__ __align__(16) bf16_t fsm[];
+  bf16_t* Qs = fsm;                 // [2][FK][FD] query rows
+  bf16_t* Os = fsm + 2 * TS;        // [2][FK][FD] dO rows
+  __shared__ float lsS[2][FK], dsS[2][FK];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int lq = lane & 31, lh = lane >> 5;
+  const int64_t kb = int64_t(blockIdx.x) % nkb, bh = int64_t(blockIdx.x) / nkb;
+  const int64_t h = bh % a.nH, b = bh / a.nH, S = a.S;
+  const int64_t kbase = kb * FQ, kw = kbase + 32 * wv, kr = kw + lq;
+  const int64_t krc = kr < S ? kr : S - 1;
+  const bf16_t* Qg = reinterpret_cast<const bf16_t*>(a.q) + (b * S) * a.q_rs + h * FD;
+  const bf16_t* Og = reinterpret_cast<const bf16_t*>(a.dO) + (b * S) * a.q_rs + h * FD;
+  const bf16_t* K = reinterpret_cast<const bf16_t*>(a.k) + bh * S * FD;
+  const bf16_t* V = reinterpret_cast<const bf16_t*>(a.v) + bh * S * FD;
+  bf16x8 kf[8], vf[8];
+#pragma unroll
+  for (int c = 0; c < 8; ++c) {
+    kf[c] = *reinterpret_cast<const bf16x8*>(K + krc * FD + 16 * c + 8 * lh);
+    vf[c] = *reinterpret_cast<const bf16x8*>(V + krc * FD + 16 * c + 8 * lh);
+  }
+  const float c2 = kBwdScale * kLog2eF;
+  f32x16 dkt[4], dvt[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) dkt[t] = dvt[t] = f32x16{};
+  const int64_t qlast = S - 1;
+  auto stats = [&](int bb, int64_t q0) {   // per-query lse (base 2) and D of the block
+    if (tid < FK) {
+      const int64_t q = q0 + tid;
+      lsS[bb][tid] = q < S ? a.lse[bh * S + q] * kLog2eF : 0.f;
+      dsS[bb][tid] = q < S ? a.D[bh * S + q] : 0.f;
+    }
+  };
+  load_kv(Qs, Qg, a.q_rs, kbase, qlast, wv, lane);
+  load_kv(Os, Og, a.q_rs, kbase, qlast, wv, lane);
+  stats(0, kbase);
+  int buf = 0;
+  for (int64_t q0 = kbase; q0 <= qlast; q0 += FK, buf ^= 1) {
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    asm volatile("" ::: "memory");
+    if (q0 + FK <= qlast) {
+      load_kv(Qs + (buf ^ 1) * TS, Qg, a.q_rs, q0 + FK, qlast, wv, lane);
+      load_kv(Os + (buf ^ 1) * TS, Og, a.q_rs, q0 + FK, qlast, wv, lane);
+      stats(buf ^ 1, q0 + FK);
+    }
+    if (q0 + FK - 1 < kw) continue;      // every query of the block precedes this wave's keys
+    const bf16_t* qs = Qs + buf * TS;
+    const bf16_t* os = Os + buf * TS;
+    // S and dP tiles qt: element e is query q0 + 32 qt + 8 (e/4) + 4 lh + e%4 against key kr
+    f32x16 sc[2], dp[2];
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt) {
+      sc[qt] = f32x16{};
+      dp[qt] = f32x16{};
+#pragma unroll
+      for (int c = 0; c < 8; ++c) {
+        const bf16x8 qa = *reinterpret_cast<const bf16x8*>(qs + tile_at(32 * qt + lq, 16 * c + 8 * lh));
+        sc[qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa, kf[c], sc[qt], 0, 0, 0);
+        const bf16x8 oa = *reinterpret_cast<const bf16x8*>(os + tile_at(32 * qt + lq, 16 * c + 8 * lh));
+        dp[qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(oa, vf[c], dp[qt], 0, 0, 0);
+      }
+    }
+#pragma unroll
+    for (int qt = 0; qt < 2; ++qt)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int qrow = 32 * qt + 8 * (e >> 2) + 4 * lh + (e & 3);
+        const int64_t q = q0 + qrow;
+        const float p =
+            (q < S && kr <= q) ? __builtin_amdgcn_exp2f(fmaf(sc[qt][e], c2, -lsS[buf][qrow])) : 0.f;
+        sc[qt][e] = p;                                   // P
+        dp[qt][e] = p * (dp[qt][e] - dsS[buf][qrow]);    // dS
+      }
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      const bf16x8 pb = c_to_b(sc, s, lh), dsb = c_to_b(dp, s, lh);
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) {
+        dvt[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tile_t_frag(os, s, dt, lane), pb, dvt[dt], 0, 0, 0);
+        dkt[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tile_t_frag(qs, s, dt, lane), dsb, dkt[dt], 0, 0, 0);
+      }
+    }
+  }
+  if (kr < S) {
+    bf16_t* dK = reinterpret_cast<bf16_t*>(a.dk) + bh * S * FD;
+    bf16_t* dV = reinterpret_cast<bf16_t*>(a.dv) + bh * S * FD;
+#pragma unroll
+    for (int dt = 0; dt < 4; ++dt)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int dim = 32 * dt + 8 * (e >> 2) + 4 * lh + (e & 3);
+        dK[kr * FD + dim] = f2bf(dkt[dt][e] * kBwdScale);
+        dV[kr * FD + dim] = f2bf(dvt[dt][e]);
+      }
+  }
+}
+
 }  // namespace
+
+hipError_t launch_attention_bwd_d128(const AttnBwdArgs& a, hipStream_t s) {
+  const int64_t nb = (a.S + FQ - 1) / FQ;
+  hipLaunchKernelGGL(attn_bwd_dkv_d128, dim3(unsigned(a.B * a.nH * nb)), dim3(64 * FW), kFlashLds, s, a, nb);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(attn_bwd_dq_d128, dim3(unsigned(a.B * a.nH * nb)), dim3(64 * FW), kFlashLds, s, a, nb);
+  return hipGetLastError();
+}
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
   const int64_t rows = a.B * a.nH * a.S;

@@ -9,11 +9,8 @@
 //  rmsnorm_bwd    one workgroup per row for dx, then per-column sums of
 //                 dy x / r over all rows for the gain, four row groups
 //                 combined in fixed order
-//  attn_bwd       causal attention, head dim 128: D = rowsum(dO o); then
-//                 per block of 64 keys dK, dV over the queries that see them;
-//                 then per block of 64 queries dQ over the keys they see.
-//                 Four lanes share a row (32 dims each); scores are rebuilt
-//                 from q, K and the forward's log-sum-exp
+//  attn_bwd       causal attention, head dim 128: D = rowsum(dO o) here,
+//                 then the matrix-core dK/dV and dQ passes of attention.hip
 //  rope_bwd       rotation by the opposite angle, cache layout to token-major
 //  xent           per row: log-sum-exp, loss, (softmax - onehot) / T
 //  embed_bwd      one workgroup per 32 vocabulary rows, token order
@@ -21,6 +18,7 @@
 #include <hip/hip_runtime.h>
 
 #include "common.h"
+#include "attention.h"
 #include "train.h"
 
 namespace auvm {
@@ -127,34 +125,7 @@ __global__ void __launch_bounds__(256) rmsnorm_bwd_gain(const float* __restrict_
 }
 
 // ---------------------------------------------------------------- attention backward
-constexpr int kD = 128, kBlk = 64, kChunk = 16;
-constexpr float kScale = 0.08838834764831845f;   // 1 / sqrt(128)
-
-__device__ __forceinline__ void load32(const bf16_t* p, float* v) {
-#pragma unroll
-  for (int u = 0; u < 4; ++u) {
-    const uint4 w = *reinterpret_cast<const uint4*>(p + 8 * u);
-    const uint32_t a[4] = {w.x, w.y, w.z, w.w};
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      v[8 * u + 2 * i] = __uint_as_float(a[i] << 16);
-      v[8 * u + 2 * i + 1] = __uint_as_float(a[i] & 0xffff0000u);
-    }
-  }
-}
-
-__device__ __forceinline__ float dot32(const float* __restrict__ lds, const float* r) {
-  float s = 0.f;
-#pragma unroll
-  for (int x = 0; x < 32; x += 4) {
-    const float4 a = *reinterpret_cast<const float4*>(lds + x);
-    s = fmaf(a.x, r[x], s);
-    s = fmaf(a.y, r[x + 1], s);
-    s = fmaf(a.z, r[x + 2], s);
-    s = fmaf(a.w, r[x + 3], s);
-  }
-  return s;
-}
+constexpr int kD = 128;
 
 // D[b,h,i] = sum_d dO[i,d] o[i,d]: one wave per (token, head)
 __global__ void __launch_bounds__(256) attn_bwd_rowsum(const bf16_t* __restrict__ o, const bf16_t* __restrict__ dO,
@@ -167,114 +138,6 @@ __global__ void __launch_bounds__(256) attn_bwd_rowsum(const bf16_t* __restrict_
   const float s = wave_sum(bf2f(o[base + lane]) * bf2f(dO[base + lane]) +
                            bf2f(o[base + lane + 64]) * bf2f(dO[base + lane + 64]));
   if (lane == 0) D[(b * nH + h) * S + i] = s;
-}
-
-// dK, dV of 64 keys: lane group of 4 = one key, 32 dims per lane
-__global__ void __launch_bounds__(256) attn_bwd_dkv(const bf16_t* __restrict__ q, const bf16_t* __restrict__ K,
-                                                    const bf16_t* __restrict__ V, const float* __restrict__ lse,
-                                                    const float* __restrict__ D, const bf16_t* __restrict__ dO,
-                                                    bf16_t* __restrict__ dK, bf16_t* __restrict__ dV, int64_t S,
-                                                    int64_t nH, int64_t nkb) {
-  __shared__ __align__(16) float qs[kChunk][kD];
-  __shared__ __align__(16) float ds_[kChunk][kD];
-  __shared__ float ls[kChunk], Ds[kChunk];
-  const int64_t kb = blockIdx.x % nkb, bh = blockIdx.x / nkb, h = bh % nH, b = bh / nH;
-  const int t = threadIdx.x, qd = t & 3;
-  const int64_t j = kb * kBlk + (t >> 2);
-  const int64_t jc = j < S ? j : S - 1;
-  const int64_t crow = (bh * S + jc) * kD + 32 * qd;
-  float kj[32], vj[32], dk[32], dv[32];
-  load32(K + crow, kj);
-  load32(V + crow, vj);
-#pragma unroll
-  for (int x = 0; x < 32; ++x) dk[x] = dv[x] = 0.f;
-  for (int64_t i0 = kb * kBlk; i0 < S; i0 += kChunk) {
-    __syncthreads();
-    for (int e = t; e < kChunk * kD; e += 256) {
-      const int ii = e / kD, dd = e % kD;
-      const int64_t i = i0 + ii;
-      const int64_t at = ((b * S + i) * nH + h) * kD + dd;
-      qs[ii][dd] = i < S ? bf2f(q[at]) : 0.f;
-      ds_[ii][dd] = i < S ? bf2f(dO[at]) : 0.f;
-    }
-    if (t < kChunk) {
-      const int64_t i = i0 + t;
-      ls[t] = i < S ? lse[bh * S + i] : 0.f;
-      Ds[t] = i < S ? D[bh * S + i] : 0.f;
-    }
-    __syncthreads();
-    const int nq = int(S - i0 < kChunk ? S - i0 : kChunk);
-    for (int ii = 0; ii < nq; ++ii) {
-      float s = dot32(&qs[ii][32 * qd], kj), dp = dot32(&ds_[ii][32 * qd], vj);
-      s += __shfl_xor(s, 1, 64);
-      s += __shfl_xor(s, 2, 64);
-      dp += __shfl_xor(dp, 1, 64);
-      dp += __shfl_xor(dp, 2, 64);
-      const bool vis = j <= i0 + ii && j < S;
-      const float p = vis ? __builtin_amdgcn_exp2f((s * kScale - ls[ii]) * kLog2e) : 0.f;
-      const float gs = p * (dp - Ds[ii]) * kScale;
-#pragma unroll
-      for (int x = 0; x < 32; ++x) {
-        dv[x] = fmaf(p, ds_[ii][32 * qd + x], dv[x]);
-        dk[x] = fmaf(gs, qs[ii][32 * qd + x], dk[x]);
-      }
-    }
-  }
-  if (j < S) {
-#pragma unroll
-    for (int x = 0; x < 32; ++x) {
-      dK[crow + x] = f2bf(dk[x]);
-      dV[crow + x] = f2bf(dv[x]);
-    }
-  }
-}
-
-// dQ of 64 queries over the keys they see: lane group of 4 = one query
-__global__ void __launch_bounds__(256) attn_bwd_dq(const bf16_t* __restrict__ q, const bf16_t* __restrict__ K,
-                                                   const bf16_t* __restrict__ V, const float* __restrict__ lse,
-                                                   const float* __restrict__ D, const bf16_t* __restrict__ dO,
-                                                   bf16_t* __restrict__ dq, int64_t S, int64_t nH, int64_t nqb) {
-  __shared__ __align__(16) float ks[kChunk][kD];
-  __shared__ __align__(16) float vs[kChunk][kD];
-  const int64_t qb = blockIdx.x % nqb, bh = blockIdx.x / nqb, h = bh % nH, b = bh / nH;
-  const int t = threadIdx.x, qd = t & 3;
-  const int64_t i = qb * kBlk + (t >> 2);
-  const int64_t ic = i < S ? i : S - 1;
-  const int64_t at = ((b * S + ic) * nH + h) * kD + 32 * qd;
-  float qi[32], doi[32], g[32];
-  load32(q + at, qi);
-  load32(dO + at, doi);
-#pragma unroll
-  for (int x = 0; x < 32; ++x) g[x] = 0.f;
-  const float li = lse[bh * S + ic], Di = D[bh * S + ic];
-  const int64_t klast = (qb * kBlk + kBlk - 1 < S ? qb * kBlk + kBlk - 1 : S - 1);
-  for (int64_t j0 = 0; j0 <= klast; j0 += kChunk) {
-    __syncthreads();
-    for (int e = t; e < kChunk * kD; e += 256) {
-      const int jj = e / kD, dd = e % kD;
-      const int64_t j = j0 + jj;
-      ks[jj][dd] = j <= klast ? bf2f(K[(bh * S + j) * kD + dd]) : 0.f;
-      vs[jj][dd] = j <= klast ? bf2f(V[(bh * S + j) * kD + dd]) : 0.f;
-    }
-    __syncthreads();
-    const int nk = int(klast - j0 + 1 < kChunk ? klast - j0 + 1 : kChunk);
-    for (int jj = 0; jj < nk; ++jj) {
-      float s = dot32(&ks[jj][32 * qd], qi), dp = dot32(&vs[jj][32 * qd], doi);
-      s += __shfl_xor(s, 1, 64);
-      s += __shfl_xor(s, 2, 64);
-      dp += __shfl_xor(dp, 1, 64);
-      dp += __shfl_xor(dp, 2, 64);
-      const bool vis = j0 + jj <= i && i < S;
-      const float p = vis ? __builtin_amdgcn_exp2f((s * kScale - li) * kLog2e) : 0.f;
-      const float gs = p * (dp - Di) * kScale;
-#pragma unroll
-      for (int x = 0; x < 32; ++x) g[x] = fmaf(gs, ks[jj][32 * qd + x], g[x]);
-    }
-  }
-  if (i < S) {
-#pragma unroll
-    for (int x = 0; x < 32; ++x) dq[at + x] = f2bf(g[x]);
-  }
 }
 
 // RoPE is a rotation per pair; its transpose rotates by the opposite angle.
@@ -417,22 +280,26 @@ hipError_t launch_rmsnorm_bwd(uint8_t* const* p, int64_t T, int64_t H, int acc, 
 }
 
 hipError_t launch_attn_bwd(uint8_t* const* p, int64_t B, int64_t S, int64_t nH, hipStream_t s) {
-  const bf16_t *q = (const bf16_t*)p[0], *K = (const bf16_t*)p[1], *V = (const bf16_t*)p[2];
-  const bf16_t *o = (const bf16_t*)p[3], *dO = (const bf16_t*)p[5];
-  const float* lse = (const float*)p[4];
-  float* D = (float*)p[9];
   const int64_t rows = B * S * nH;
-  hipLaunchKernelGGL(attn_bwd_rowsum, dim3(unsigned((rows + 3) / 4)), dim3(256), 0, s, o, dO, D, B * S, S, nH);
+  hipLaunchKernelGGL(attn_bwd_rowsum, dim3(unsigned((rows + 3) / 4)), dim3(256), 0, s, (const bf16_t*)p[3],
+                     (const bf16_t*)p[5], (float*)p[9], B * S, S, nH);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  const int64_t nb = (S + kBlk - 1) / kBlk;
-  hipLaunchKernelGGL(attn_bwd_dkv, dim3(unsigned(B * nH * nb)), dim3(256), 0, s, q, K, V, lse, D, dO, (bf16_t*)p[7],
-                     (bf16_t*)p[8], S, nH, nb);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(attn_bwd_dq, dim3(unsigned(B * nH * nb)), dim3(256), 0, s, q, K, V, lse, D, dO, (bf16_t*)p[6], S,
-                     nH, nb);
-  return hipGetLastError();
+  AttnBwdArgs a;
+  a.q = p[0];
+  a.k = p[1];
+  a.v = p[2];
+  a.dO = p[5];
+  a.lse = (const float*)p[4];
+  a.D = (const float*)p[9];
+  a.dq = p[6];
+  a.dk = p[7];
+  a.dv = p[8];
+  a.B = B;
+  a.S = S;
+  a.nH = nH;
+  a.q_rs = nH * kD;
+  return launch_attention_bwd_d128(a, s);
 }
 
 hipError_t launch_rope_bwd(uint8_t* const* p, int64_t B, int64_t S, int64_t nH, int64_t d, bool bf16, hipStream_t s) {
