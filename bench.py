@@ -131,28 +131,62 @@ def calibrate_copy():
     del src, dst
 
 
+def link_lower_bound(w, a, n, M):
+    """(H2D, D2H) bytes kernels [a, a+n) must move over the host link at least.
+
+    At the boundary before kernel k, every tensor whose next access in the
+    unit is a read must be on the device when that kernel runs; at most M
+    bytes are there at the boundary, so at least (needed - M) bytes must
+    cross to the device after it.  Those off the device that the unit itself
+    writes were rewritten within the last repetition of the unit (decode
+    steps and training steps repeat the same trace), so each of them was
+    also written back; only needed tensors the unit never writes (weights
+    at inference, token ids) can be off the device with a current host copy.
+    Both bounds are taken at the boundary where their sum is largest (the
+    first boundary gives the bytes the unit reads before writing, minus M).
+    """
+    from workloads.format import MODE_R, MODE_W
+    written = set()
+    for kd in w.kernels[a:a + n]:
+        for t, m in kd.operands:
+            if m & MODE_W:
+                written.add(t)
+    needed, live, ro, best = set(), 0, 0, (0, 0)
+    for kd in reversed(w.kernels[a:a + n]):
+        merged = {}
+        for t, m in kd.operands:
+            merged[t] = merged.get(t, 0) | m
+        for t, m in merged.items():
+            size = (w.tensors[t].nbytes + 255) // 256 * 256
+            if m & MODE_R:
+                if t not in needed:
+                    needed.add(t)
+                    live += size
+                    ro += 0 if t in written else size
+            elif t in needed:
+                needed.remove(t)
+                live -= size
+                ro -= 0 if t in written else size
+        h2d = max(0, live - M)
+        d2h = max(0, live - M - ro)
+        if h2d + d2h > sum(best):
+            best = (h2d, d2h)
+    return best
+
+
 def seg_stats(w, sched, classes, M, segs):
     """Work and transfers of whole units (decode steps or forward passes) segs."""
-    from workloads.format import MODE_R
     k0 = segs[0][0]
     k1 = segs[-1][0] + segs[-1][1]
     F = sum(c[2] for c in classes[k0:k1])
     B = sum(c[3] for c in classes[k0:k1])
-    lmin = 0
-    for a, n in segs:
-        first = {}
-        for kd in w.kernels[a:a + n]:
-            merged = {}
-            for t, m in kd.operands:
-                merged[t] = merged.get(t, 0) | m
-            for t, m in merged.items():
-                first.setdefault(t, m)
-        read = sum((w.tensors[t].nbytes + 255) // 256 * 256 for t, m in first.items() if m & MODE_R)
-        lmin += max(0, read - M)
+    bounds = [link_lower_bound(w, a, n, M) for a, n in segs]
+    lmin = sum(b[0] for b in bounds)
+    lmin_d2h = sum(b[1] for b in bounds)
     h2d = sum(e[3] for e in sched if e[0] in (0, 1) and k0 <= e[4] < k1)
     d2h = sum(e[3] for e in sched if e[0] == 2 and k0 <= e[4] < k1)
     demand = sum(1 for e in sched if e[0] == 1 and k0 <= e[4] < k1)
-    return dict(flops=F, hbm_bytes=B, lmin_bytes=lmin, h2d_bytes=h2d, d2h_bytes=d2h,
+    return dict(flops=F, hbm_bytes=B, lmin_bytes=lmin, lmin_d2h_bytes=lmin_d2h, h2d_bytes=h2d, d2h_bytes=d2h,
                 demand_fetches=demand)
 
 
@@ -457,9 +491,12 @@ def roofline_fields(st, seconds, bl_meas, units):
     import numpy as np
     t_comp = st["flops"] / NOMINAL["P"]
     t_hbm = st["hbm_bytes"] / NOMINAL["Bh"]
-    t_link = st["lmin_bytes"] / NOMINAL["Bl"]
+    # both directions share the host link (concurrent H2D and D2H copies
+    # together reach the rate of one direction alone)
+    link = st["lmin_bytes"] + st["lmin_d2h_bytes"]
+    t_link = link / NOMINAL["Bl"]
     roof_s = max(t_comp, t_hbm, t_link)
-    roof_meas = max(t_comp, t_hbm, st["lmin_bytes"] / bl_meas)
+    roof_meas = max(t_comp, t_hbm, link / bl_meas)
     return {"bound": ["mfma", "hbm", "link"][int(np.argmax([t_comp, t_hbm, t_link]))],
             "roofline_units_per_s": round(units / roof_s, 3),
             "frac": round(roof_s / seconds, 4),
@@ -882,6 +919,9 @@ def train_main(args, cfg):
         "kernel_ms_per_step_by_tag": {t_: round(v / K, 2) for t_, v in sorted(per_tag.items(), key=lambda x: -x[1])[:12]},
         "transfers": {"h2d_bytes_per_step": st["h2d_bytes"] // K, "d2h_bytes_per_step": st["d2h_bytes"] // K,
                       "lmin_bytes_per_step": st["lmin_bytes"] // K,
+                      "lmin_d2h_bytes_per_step": st["lmin_d2h_bytes"] // K,
+                      "link_over_lmin": round((st["h2d_bytes"] + st["d2h_bytes"])
+                                              / max(1, st["lmin_bytes"] + st["lmin_d2h_bytes"]), 4),
                       "compute_busy_ms_per_step": round(sum(dur[k] for k in range(k0, k1)) / K, 2),
                       "link_timeline": link_timeline(tl, K)},
         "loss_last_step": round(loss, 5),

@@ -1,5 +1,6 @@
 """Pins of the oracle planner: hand-derived schedules, closed forms, exhaustive
 search, the schedule checker and the limits of the roofline gate."""
+import dataclasses
 import itertools
 import random
 
@@ -237,6 +238,32 @@ def test_ablation_ladder_directions_on_cyclic_decoder():
     moved = sum(e[3] for e in r_tap.schedule
                 if e[0] in (S_H2D_DEMAND, S_H2D_PREFETCH) and k0 <= e[4] < k0 + n)
     assert moved >= lmin
+
+
+@pytest.mark.parametrize("name", ["train-small", "llama-small"])
+def test_link_lower_bound_holds_for_every_variant(name):
+    """The benchmark's link bound per repeated unit (training step, decode
+    step) is met by every policy: H2D and D2H both at least the bound, and
+    for training the write-back part is not trivially zero."""
+    import bench
+    cfg = dataclasses.replace(configs.CONFIGS[name], iterations=4) if name == "train-small" \
+        else configs.CONFIGS[name]
+    w = trace.build(cfg)
+    M = w.budget()
+    seg = "step" if name == "train-small" else "decode"
+    units = w.segments[seg][1:-1]
+    bounds = [bench.link_lower_bound(w, a, n, M) for a, n in units]
+    assert all(b[0] > 0 for b in bounds)
+    if name == "train-small":
+        assert all(b[1] > 0 for b in bounds)
+    else:
+        assert all(b[1] == 0 for b in bounds)      # weights are never written at decode
+    for variant in (VAR_DEMAND_LRU, VAR_DEMAND_BELADY, VAR_T_A_P):
+        r = op.plan_workload(w, M, variant=variant)
+        for (a, n), (h_min, d_min) in zip(units, bounds):
+            h2d = sum(e[3] for e in r.schedule if e[0] in (S_H2D_DEMAND, S_H2D_PREFETCH) and a <= e[4] < a + n)
+            d2h = sum(e[3] for e in r.schedule if e[0] == S_D2H_WRITEBACK and a <= e[4] < a + n)
+            assert h2d >= h_min and d2h >= d_min, (variant, a, h2d, h_min, d2h, d_min)
 
 
 # ---- measured kernel times (the runtime monitor's re-classification, Sec. IV)
