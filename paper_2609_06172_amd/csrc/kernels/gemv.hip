@@ -2,18 +2,24 @@
 //
 // Y[m, n] = sum_k A[m, k] W[n, k] is HBM-bound on W (16 flop per weight
 // byte).  The 16 token rows fill the M side of v_mfma_f32_16x16x32_bf16 and
-// 16 weight rows its N side, so every weight byte is read once from HBM and
-// fed straight from registers to the matrix core; no LDS staging.
+// 16 weight rows its N side, so every weight byte is read once from HBM.
 //
 // Routed rows (MoE experts): the same kernel over the rows of a routed-row
 // list, gathered by token on input or scattered by token on output.
 //
 // Work split: one 512-thread workgroup per 16 output features; its eight
-// waves take interleaved 32-wide K chunks (adjacent waves read adjacent 64 B
-// of every weight row), eight chunks in flight per wave, keep fp32 partial tiles in registers and reduce them
-// through LDS in a fixed order (deterministic).  Lane (r, g) = (l % 16, l / 16)
-// holds A[r, 32c + 8g .. +8] and W[n0 + r, 32c + 8g .. +8] for chunk c, so
-// each weight row contributes one full 64-byte segment per load instruction.
+// waves take interleaved 64-wide K chunks (adjacent waves read adjacent 128 B
+// of every row), four chunks in flight per wave, keep fp32 partial tiles in
+// registers and reduce them through LDS in a fixed order (deterministic).
+//
+// Loads: the MFMA operand layout gives each row only four lanes (64 B) per
+// load instruction, which spends a cache-line request on half a line.  Each
+// load instead covers 8 rows x 128 B (lane L: row L / 8, 16-B piece L % 8),
+// and the chunk passes through a wave-private LDS tile (16 rows x 128 B) to
+// reach the operand layout: lane (r, g) = (l % 16, l / 16) then takes
+// A[r, 64c + 32h + 8g .. +8] and W[n0 + r, same k] for half h of chunk c.
+// Piece q of row r sits at slot q ^ (r >> 1) of the row, so the 16-lane
+// groups of both the stores and the fragment reads hit 16 distinct banks.
 #include <hip/hip_runtime.h>
 
 #include "common.h"
@@ -28,8 +34,11 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kUnroll = 8;  // K chunks in flight per wave
+constexpr int kUnroll = 4;  // 64-k chunks in flight per wave
 constexpr int kWaves = 8;   // waves per workgroup, splitting K
+
+// 16-B slot of piece q (0..7) of row r (0..15) in a chunk tile
+__device__ __forceinline__ int tslot(int r, int q) { return 8 * r + (q ^ (r >> 1)); }
 
 // LIST: rows come from a routed-row list (GemmArgs::list): the row count is
 // read from the list, and A rows are gathered by token (EPI_SWIGLU) or the
@@ -40,41 +49,74 @@ __global__ void __launch_bounds__(64 * kWaves) gemv_mfma(const bf16_t* __restric
                                                  int M, int64_t N, int64_t K, const int32_t* __restrict__ list,
                                                  const float* __restrict__ rw, int topk) {
   constexpr bool DUAL = EPI == EPI_SWIGLU;
+  constexpr int kParts = DUAL ? 3 : 2;   // A, W (, W2) tiles of a chunk
+  __shared__ bf16x8 tile[kWaves][kParts][128];
   __shared__ f32x4 part[kWaves][DUAL ? 2 : 1][64];
-  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
-  const int r = lane & 15, g = lane >> 4;
+  const int lane = threadIdx.x & 63;
+  const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // uniform: scalar chunk loop
+  const int r = lane & 15, g = lane >> 4;      // fragment row, k group
+  const int fr = lane >> 3, fp = lane & 7;     // load row (within 8), piece
   const int64_t n0 = int64_t(blockIdx.x) * 16;
-  const int64_t n = n0 + r;
   int rows = M;
   if constexpr (LIST) rows = list[0] < M ? list[0] : M;
-  const bool a_ok = r < rows, w_ok = n < N;
-  int64_t ar = a_ok ? r : 0;
-  if constexpr (LIST && EPI != EPI_MOE) {
-    if (a_ok) {
-      const int64_t t = list[1 + r] / topk;
-      ar = t < 0 ? 0 : (t < M ? t : M - 1);
+  // source rows of this lane's two loads: rows fr and 8 + fr of the tile;
+  // rows past the end are clamped, their results dropped
+  const bf16_t* ap[2];
+  const bf16_t* wp[2];
+  const bf16_t* w2p[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int rr = 8 * h + fr;
+    int64_t ar = rr < rows ? rr : 0;
+    if constexpr (LIST && EPI != EPI_MOE) {
+      if (rr < rows) {
+        const int64_t t = list[1 + rr] / topk;
+        ar = t < 0 ? 0 : (t < M ? t : M - 1);
+      }
     }
+    ap[h] = A + ar * K;
+    const int64_t wn = n0 + rr < N ? n0 + rr : N - 1;
+    wp[h] = W + wn * K;
+    w2p[h] = DUAL ? W2 + wn * K : nullptr;
   }
-  const bf16_t* arow = A + ar * K + 8 * g;
-  const bf16_t* wrow = W + (w_ok ? n : 0) * K + 8 * g;
-  const bf16_t* w2row = DUAL ? W2 + (w_ok ? n : 0) * K + 8 * g : nullptr;
-  const int64_t nch = K / 32;
-  const bf16x8 zero = {};
+  const int64_t nch = (K + 63) / 64;   // K % 32 == 0: the last chunk may hold one half
+  bf16x8* my = &tile[wv][0][0];
   f32x4 acc = {0.f, 0.f, 0.f, 0.f}, acc2 = {0.f, 0.f, 0.f, 0.f};
   for (int64_t c0 = wv; c0 < nch; c0 += kWaves * kUnroll) {
-    bf16x8 av[kUnroll], wvv[kUnroll], w2v[DUAL ? kUnroll : 1];
+    bf16x8 av[kUnroll][2], wt[kUnroll][2], w2t[DUAL ? kUnroll : 1][2];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) {
+      const int64_t c = c0 + kWaves * u < nch ? c0 + kWaves * u : nch - 1;   // loads stay in bounds
+      const int pc = 64 * c + 64 > K ? (fp & 3) : fp;                         // half chunk: first half only
+      const int64_t off = 64 * c + 8 * pc;
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        av[u][h] = *reinterpret_cast<const bf16x8*>(ap[h] + off);
+        wt[u][h] = *reinterpret_cast<const bf16x8*>(wp[h] + off);
+        if constexpr (DUAL) w2t[u][h] = *reinterpret_cast<const bf16x8*>(w2p[h] + off);
+      }
+    }
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) {
       const int64_t c = c0 + kWaves * u;
-      const bool in = c < nch;
-      av[u] = (in && a_ok) ? *reinterpret_cast<const bf16x8*>(arow + 32 * c) : zero;
-      wvv[u] = (in && w_ok) ? *reinterpret_cast<const bf16x8*>(wrow + 32 * c) : zero;
-      if constexpr (DUAL) w2v[u] = (in && w_ok) ? *reinterpret_cast<const bf16x8*>(w2row + 32 * c) : zero;
-    }
+      if (c >= nch) break;   // uniform over the wave
+      // the wave's own tile: stores, then reads, in order on the LDS queue
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) {
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[u], wvv[u], acc, 0, 0, 0);
-      if constexpr (DUAL) acc2 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[u], w2v[u], acc2, 0, 0, 0);
+      for (int h = 0; h < 2; ++h) {
+        const int sl = tslot(8 * h + fr, fp);
+        my[sl] = av[u][h];
+        my[128 + sl] = wt[u][h];
+        if constexpr (DUAL) my[256 + sl] = w2t[u][h];
+      }
+      const int halves = 64 * c + 64 > K ? 1 : 2;
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        if (hh >= halves) break;
+        const int sl = tslot(r, 4 * hh + g);
+        const bf16x8 a = my[sl];
+        acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, my[128 + sl], acc, 0, 0, 0);
+        if constexpr (DUAL) acc2 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, my[256 + sl], acc2, 0, 0, 0);
+      }
     }
   }
   part[wv][0][lane] = acc;
