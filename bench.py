@@ -925,7 +925,7 @@ def train_main(args, cfg):
                       "compute_busy_ms_per_step": round(sum(dur[k] for k in range(k0, k1)) / K, 2),
                       "link_timeline": link_timeline(tl, K)},
         "loss_last_step": round(loss, 5),
-        "warmup": {"steps": W, "seconds": round(cold_s, 3)},
+        "warmup_seconds": round(cold_s, 3),
     }
     if not args.no_baseline:
         s.set_policy(variant=0, timing=0)
