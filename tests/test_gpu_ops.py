@@ -39,10 +39,11 @@ def rnd(*shape, scale=1.0):
     return RNG.standard_normal(shape).astype(np.float32) * scale
 
 
-# bf16 kernels by shape: M <= 16 matrix-core GEMV; M >= 512 with K % 64 == 0 the
+# bf16 kernels by shape: M <= 16 matrix-core GEMV (K % 64 == 32 ends on a half
+# chunk); M >= 512 with K % 64 == 0 the
 # 256 x 256 direct-LDS GEMM (one exact tile, ragged edges, several tiles);
 # otherwise the 128 x 128 GEMM (including M >= 512 with K % 64 != 0)
-LIN_SHAPES = [(1, 64, 32), (5, 100, 64), (16, 4096 + 16, 256), (17, 96, 96), (100, 130, 160),
+LIN_SHAPES = [(1, 64, 32), (5, 100, 64), (7, 130, 160), (16, 33, 96), (16, 4096 + 16, 256), (17, 96, 96), (100, 130, 160),
               (257, 300, 512), (512, 256, 64), (600, 300, 128), (1030, 520, 192), (777, 1000, 256),
               (520, 130, 96)]
 
