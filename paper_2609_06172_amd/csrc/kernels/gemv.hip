@@ -7,7 +7,7 @@
 // Routed rows (MoE experts): the same kernel over the rows of a routed-row
 // list, gathered by token on input or scattered by token on output.
 //
-// Work split: one 512-thread workgroup per 16 output features; its eight
+// Work split: one 1024-thread workgroup per 16 output features; its sixteen
 // waves take interleaved 64-wide K chunks (adjacent waves read adjacent 128 B
 // of every row), four chunks in flight per wave, keep fp32 partial tiles in
 // registers and reduce them through LDS in a fixed order (deterministic).
@@ -35,7 +35,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kUnroll = 4;  // 64-k chunks in flight per wave
-constexpr int kWaves = 8;   // waves per workgroup, splitting K
+constexpr int kWaves = 16;  // waves per workgroup, splitting K
 
 // 16-B slot of piece q (0..7) of row r (0..15) in a chunk tile
 __device__ __forceinline__ int tslot(int r, int q) { return 8 * r + (q ^ (r >> 1)); }
@@ -92,8 +92,9 @@ __global__ void __launch_bounds__(64 * kWaves) gemv_mfma(const bf16_t* __restric
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         av[u][h] = *reinterpret_cast<const bf16x8*>(ap[h] + off);
-        wt[u][h] = *reinterpret_cast<const bf16x8*>(wp[h] + off);
-        if constexpr (DUAL) w2t[u][h] = *reinterpret_cast<const bf16x8*>(w2p[h] + off);
+        // weights are read once: non-temporal, so they do not displace the activations in L2
+        wt[u][h] = __builtin_nontemporal_load(reinterpret_cast<const bf16x8*>(wp[h] + off));
+        if constexpr (DUAL) w2t[u][h] = __builtin_nontemporal_load(reinterpret_cast<const bf16x8*>(w2p[h] + off));
       }
     }
 #pragma unroll
