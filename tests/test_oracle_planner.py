@@ -240,6 +240,44 @@ def test_ablation_ladder_directions_on_cyclic_decoder():
     assert moved >= lmin
 
 
+def test_link_lower_bound_hand_derived():
+    """The benchmark's link bound on two hand-built units of 256-byte tensors
+    (TOUCH kernels stand for any op; only the access modes matter).
+
+    Unit 1, M = 768: every kernel also reads and writes a 256-byte log; k0
+    writes a, k1 reads a and writes b, k2 reads a, b and the host-initialised
+    c.  Before k2 all four are needed (1024 B): 256 B must be fetched; the
+    unit writes the log, a and b but not c, so the shortfall can be met by c
+    alone and no write-back is forced.  Before k1 the log, a and c are
+    needed (b is written there): 768 B, no shortfall.  Bound (256, 0).
+
+    Unit 2, M = 256: k0 writes a, k1 writes b, k2 reads a and b.  Before k2,
+    512 B are needed, both written by the unit: 256 B must come back, and in
+    a repeated unit they were rewritten since, so 256 B were written back.
+    Bound (256, 256)."""
+    import bench
+    from workloads.format import MODE_R, MODE_RW, MODE_W
+    w = trace.Workload(None)
+    a = w.tensor("a", (256,), DT_U8, 1)
+    b = w.tensor("b", (256,), DT_U8, 1)
+    c = w.tensor("c", (256,), DT_U8, 1, host_init=True)
+    log = w.tensor("log", (64,), DT_U8, 1)
+    w.kernel(OP_TOUCH, (0,), [(log, MODE_RW), (a, MODE_W)])
+    w.kernel(OP_TOUCH, (0,), [(log, MODE_RW), (a, MODE_R), (b, MODE_W)])
+    w.kernel(OP_TOUCH, (0,), [(log, MODE_RW), (a, MODE_R), (b, MODE_R), (c, MODE_R)])
+    assert bench.link_lower_bound(w, 0, 3, 512 + 256) == (256, 0)
+    w2 = trace.Workload(None)
+    a = w2.tensor("a", (256,), DT_U8, 1)
+    b = w2.tensor("b", (256,), DT_U8, 1)
+    w2.kernel(OP_TOUCH, (0,), [(a, MODE_W)])
+    w2.kernel(OP_TOUCH, (0,), [(b, MODE_W)])
+    w2.kernel(OP_TOUCH, (0,), [(a, MODE_R), (b, MODE_R)])
+    assert bench.link_lower_bound(w2, 0, 3, 256) == (256, 256)
+    # a larger budget removes both; a smaller one grows both by the same bytes
+    assert bench.link_lower_bound(w2, 0, 3, 512) == (0, 0)
+    assert bench.link_lower_bound(w2, 0, 3, 0) == (512, 512)
+
+
 @pytest.mark.parametrize("name", ["train-small", "llama-small"])
 def test_link_lower_bound_holds_for_every_variant(name):
     """The benchmark's link bound per repeated unit (training step, decode
