@@ -9,7 +9,7 @@
 //
 // Work split: one 1024-thread workgroup per 16 output features; its sixteen
 // waves take interleaved 64-wide K chunks (adjacent waves read adjacent 128 B
-// of every row), four chunks in flight per wave, keep fp32 partial tiles in
+// of every row), two chunks in flight per wave, keep fp32 partial tiles in
 // registers and reduce them through LDS in a fixed order (deterministic).
 //
 // Loads: the MFMA operand layout gives each row only four lanes (64 B) per
@@ -34,7 +34,7 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kUnroll = 4;  // 64-k chunks in flight per wave
+constexpr int kUnroll = 2;  // 64-k chunks in flight per wave
 constexpr int kWaves = 16;  // waves per workgroup, splitting K
 
 // 16-B slot of piece q (0..7) of row r (0..15) in a chunk tile
