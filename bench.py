@@ -1058,8 +1058,8 @@ def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print("bench.py runs on one GPU: this build has no multi-GPU path "
-              "(the per-GPU hot path is what it measures)", file=sys.stderr)
+        print("bench.py runs on one GPU: the library has no multi-GPU path; it measures "
+              "one GPU's share of the hot path (--gpus 1)", file=sys.stderr)
         sys.exit(2)
     import dataclasses
 
