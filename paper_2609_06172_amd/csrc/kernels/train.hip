@@ -7,7 +7,7 @@
 //                 C = A W^T over transposed operands)
 //  swiglu         F = silu(G) U and its gradients, elementwise
 //  rmsnorm_bwd    one workgroup per row for dx, then per-column sums of
-//                 dy x / r over all rows for the gain, four row groups
+//                 dy x / r over all rows for the gain, sixteen row groups
 //                 combined in fixed order
 //  attn_bwd       causal attention, head dim 128: D = rowsum(dO o) here,
 //                 then the matrix-core dK/dV and dQ passes of attention.hip
@@ -109,19 +109,28 @@ __global__ void __launch_bounds__(256) rmsnorm_bwd_rows(const float* __restrict_
   if (threadIdx.x == 0) rstd[row] = inv;
 }
 
-// dg[j] = sum over rows of dy x / r: 64 columns per workgroup, four row groups
+// dg[j] = sum over rows of dy x / r: 16 columns per workgroup (H / 16
+// workgroups fill the chip at model widths), sixteen row groups of 16
+// threads, each reading 64-byte row segments; the groups are combined in a
+// fixed order
+constexpr int kGainCols = 16, kGainGroups = 16;
 __global__ void __launch_bounds__(256) rmsnorm_bwd_gain(const float* __restrict__ x, const float* __restrict__ dy,
                                                         const float* __restrict__ rstd, float* __restrict__ dg,
                                                         int64_t T, int64_t H) {
-  __shared__ float part[4][64];
-  const int c = threadIdx.x & 63, rg = threadIdx.x >> 6;
-  const int64_t col = int64_t(blockIdx.x) * 64 + c;
+  __shared__ float part[kGainGroups][kGainCols];
+  const int c = threadIdx.x % kGainCols, rg = threadIdx.x / kGainCols;
+  const int64_t col = int64_t(blockIdx.x) * kGainCols + c;
   float s = 0.f;
   if (col < H)
-    for (int64_t r = rg; r < T; r += 4) s = fmaf(dy[r * H + col] * x[r * H + col], rstd[r], s);
+    for (int64_t r = rg; r < T; r += kGainGroups) s = fmaf(dy[r * H + col] * x[r * H + col], rstd[r], s);
   part[rg][c] = s;
   __syncthreads();
-  if (rg == 0 && col < H) dg[col] = ((part[0][c] + part[1][c]) + part[2][c]) + part[3][c];
+  if (rg == 0 && col < H) {
+    float t = part[0][c];
+#pragma unroll
+    for (int g2 = 1; g2 < kGainGroups; ++g2) t += part[g2][c];
+    dg[col] = t;
+  }
 }
 
 // ---------------------------------------------------------------- attention backward
@@ -275,7 +284,8 @@ hipError_t launch_rmsnorm_bwd(uint8_t* const* p, int64_t T, int64_t H, int acc, 
                        (bf16_t*)p[4], rstd, H, acc);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(rmsnorm_bwd_gain, dim3(unsigned((H + 63) / 64)), dim3(256), 0, s, x, dy, rstd, (float*)p[5], T, H);
+  hipLaunchKernelGGL(rmsnorm_bwd_gain, dim3(unsigned((H + kGainCols - 1) / kGainCols)), dim3(256), 0, s, x, dy, rstd,
+                     (float*)p[5], T, H);
   return hipGetLastError();
 }
 
