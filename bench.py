@@ -192,18 +192,24 @@ def seg_stats(w, sched, classes, M, segs):
 
 def link_timeline(tl, K):
     """Host-to-device link over the timed run segment (the last one): busy and
-    idle time, and the part of each idle gap during which the host had not yet
-    issued the next copy (host and device clocks share the segment's start)."""
-    from paper_2609_06172_amd.capi import TL_H2D
+    idle time (copies run on two streams: busy is the union of their
+    intervals), and the part of each idle gap during which the host had not
+    yet issued the next copy (host and device clocks share the segment's
+    start)."""
+    from paper_2609_06172_amd.capi import TL_H2D, TL_H2D_B
     seg = max(e[1] for e in tl)
     cur = [e for e in tl if e[1] == seg]
-    h = sorted((e for e in cur if e[0] == TL_H2D), key=lambda e: e[5])
+    h = sorted((e for e in cur if e[0] in (TL_H2D, TL_H2D_B)), key=lambda e: e[5])
     span = max(e[6] for e in cur)
-    busy = sum(e[6] - e[5] for e in h)
-    late, prev = 0.0, 0.0
+    busy = late = 0.0
+    prev = 0.0                      # end of the busy union so far
     for e in h:
-        late += max(0.0, min(e[5], e[4]) - prev)
-        prev = e[6]
+        if e[5] > prev:             # a gap before this copy
+            late += max(0.0, min(e[5], e[4]) - prev)
+            busy += e[6] - e[5]
+        else:
+            busy += max(0.0, e[6] - prev)
+        prev = max(prev, e[6])
     nbytes = sum(e[3] for e in h)
     return {"h2d_busy_ms_per_step": round(busy / K, 3), "h2d_idle_ms_per_step": round((span - busy) / K, 3),
             "idle_before_host_issue_ms_per_step": round(late / K, 3),

@@ -320,8 +320,12 @@ auvm_status auvm_get_kernel_times(const auvm_ctx* ctx, float* dur_ms, float* gap
  * finished it (from an event recorded on the idle streams at the segment's
  * start).  This extends the runtime monitor's kernel timestamps (Sec. IV,
  * Online Executor, Runtime Monitor) to the copies, so that link busy time,
- * compute busy time and the stalls of each on the other can be measured. */
-enum { AUVM_TL_KERNEL = 0, AUVM_TL_H2D = 1, AUVM_TL_D2H = 2 };
+ * compute busy time and the stalls of each on the other can be measured.
+ * Host-to-device copies alternate between two streams by copy number (odd
+ * numbers, the first copy included, on the first): AUVM_TL_H2D entries come
+ * from one, AUVM_TL_H2D_B from the other; each stream's entries are in order,
+ * and the two may overlap. */
+enum { AUVM_TL_KERNEL = 0, AUVM_TL_H2D = 1, AUVM_TL_D2H = 2, AUVM_TL_H2D_B = 3 };
 typedef struct auvm_timeline_entry {
   int32_t kind;     /* AUVM_TL_* */
   int32_t segment;  /* run call ordinal since the last reset, from 0 */

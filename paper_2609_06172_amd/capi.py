@@ -54,7 +54,7 @@ class TimelineEntry(C.Structure):
                 ("host_ms", C.c_double), ("start_ms", C.c_double), ("end_ms", C.c_double)]
 
 
-TL_KERNEL, TL_H2D, TL_D2H = 0, 1, 2
+TL_KERNEL, TL_H2D, TL_D2H, TL_H2D_B = 0, 1, 2, 3
 
 
 class Counters(C.Structure):

@@ -1,8 +1,10 @@
 // Transfer engine and executor on the HIP runtime.
 //
-// Replays a plan on three streams: compute (kernels), h2d (pinned host arena
-// -> device pool copies) and d2h (write-backs).  Ordering is event based and
-// never blocks the host inside a run segment:
+// Replays a plan on four streams: compute (kernels), two h2d streams (pinned
+// host arena -> device pool copies, alternating by copy number, so that a copy
+// held back by its window's previous readers does not hold back the next one)
+// and d2h (write-backs).  Ordering is event based and never blocks the host
+// inside a run segment:
 //  * a copy into a pool window waits for the kernels that last used the
 //    tensors previously in that window and for write-backs out of it;
 //  * a demand fetch for kernel k additionally waits for kernel k-1, so it
@@ -12,7 +14,9 @@
 //  * a kernel waits for the copies that brought its operands and, for
 //    first-write allocations, for transfers still touching the window.
 // Streams are in-order, so each stream keeps the highest kernel/copy index it
-// already waits on and skips older waits.
+// already waits on and skips older waits; copies of the two h2d streams have
+// separate event rings and separate highest-waited indices, and a copy into a
+// window last written from the other h2d stream waits for that copy.
 //
 // Timing policy: kernels, host-to-device and device-to-host copies each get a
 // track of start/end events; times are chained from one base event per run
@@ -52,19 +56,20 @@ class Executor {
       return AUVM_E_HIP;
     std::vector<uint32_t> mask(size_t((ncu + 31) / 32), 0xffffffffu);
     if (ncu % 32) mask.back() = (1u << (ncu % 32)) - 1u;
-    hipStream_t* ss[3] = {&comp_, &h2d_, &d2h_};
-    for (int i = 0; i < 3; ++i) {
+    hipStream_t* ss[4] = {&comp_, &h2d_[0], &h2d_[1], &d2h_};
+    for (int i = 0; i < 4; ++i) {
       if (!ok(hipExtStreamCreateWithCUMask(ss[i], uint32_t(mask.size()), mask.data()), "hipExtStreamCreateWithCUMask"))
         return AUVM_E_HIP;
       own_[i] = true;
     }
-    for (auto* ring : {&kev_, &hev_, &dev_}) {
+    for (auto* ring : {&kev_, &hev_[0], &hev_[1], &dev_}) {
       ring->assign(kRing, nullptr);
       for (auto& e : *ring)
         if (!ok(hipEventCreateWithFlags(&e, hipEventDisableTiming), "hipEventCreate")) return AUVM_E_HIP;
     }
     kown_.assign(kRing, -1);
-    hown_.assign(kRing, -1);
+    hown_[0].assign(kRing, -1);
+    hown_[1].assign(kRing, -1);
     down_.assign(kRing, -1);
     return AUVM_OK;
   }
@@ -72,25 +77,26 @@ class Executor {
   void destroy() {
     if (c_.device < 0) return;
     (void)hipSetDevice(c_.device);
-    hipStream_t ss[3] = {comp_, h2d_, d2h_};
-    for (int i = 0; i < 3; ++i)
+    hipStream_t ss[4] = {comp_, h2d_[0], h2d_[1], d2h_};
+    for (int i = 0; i < 4; ++i)
       if (ss[i]) (void)hipStreamSynchronize(ss[i]);
-    for (auto* ring : {&kev_, &hev_, &dev_, &bases_})
+    for (auto* ring : {&kev_, &hev_[0], &hev_[1], &dev_, &bases_})
       for (auto& e : *ring)
         if (e) (void)hipEventDestroy(e);
-    for (Track* tr : {&ktr_, &htr_, &dtr_})
+    for (Track* tr : {&ktr_, &htr_[0], &htr_[1], &dtr_})
       for (auto* ring : {&tr->s, &tr->e})
         for (auto& e : *ring)
           if (e) (void)hipEventDestroy(e);
-    for (int i = 0; i < 3; ++i)
+    for (int i = 0; i < 4; ++i)
       if (own_[i] && ss[i]) (void)hipStreamDestroy(ss[i]);
-    comp_ = h2d_ = d2h_ = nullptr;
+    comp_ = h2d_[0] = h2d_[1] = d2h_ = nullptr;
   }
 
   auvm_status bind(void* comp, void* h2d, void* d2h) {
-    hipStream_t* ss[3] = {&comp_, &h2d_, &d2h_};
-    void* in[3] = {comp, h2d, d2h};
-    for (int i = 0; i < 3; ++i) {
+    // a caller's h2d stream carries both copy sequences (in order: still correct)
+    hipStream_t* ss[4] = {&comp_, &h2d_[0], &h2d_[1], &d2h_};
+    void* in[4] = {comp, h2d, h2d, d2h};
+    for (int i = 0; i < 4; ++i) {
       if (!in[i]) continue;
       if (*ss[i]) (void)hipStreamSynchronize(*ss[i]);
       if (own_[i] && *ss[i]) (void)hipStreamDestroy(*ss[i]);
@@ -111,18 +117,21 @@ class Executor {
     copy_seq_.assign(nT, 0);
     wb_seq_.assign(nT, 0);
     h2d_seq_ = d2h_seq_ = 0;
-    h2d_waited_k_ = d2h_waited_k_ = -1;
-    h2d_waited_d2h_ = comp_waited_h2d_ = comp_waited_d2h_ = 0;
-    pend_h2d_ = pend_d2h_ = 0;
+    d2h_waited_k_ = -1;
+    comp_waited_d2h_ = pend_d2h_ = 0;
+    for (int p = 0; p < 2; ++p) {
+      h2d_waited_k_[p] = -1;
+      h2d_waited_d2h_[p] = h2d_waited_h2d_[p] = comp_waited_h2d_[p] = pend_h2d_[p] = 0;
+      std::fill(hown_[p].begin(), hown_[p].end(), -1);
+    }
     std::fill(kown_.begin(), kown_.end(), -1);
-    std::fill(hown_.begin(), hown_.end(), -1);
     std::fill(down_.begin(), down_.end(), -1);
     hazards_.clear();
     log_.clear();
     kernels_run_ = 0;
     dur_.assign(K, 0.f);
     gap_.assign(K, 0.f);
-    for (Track* tr : {&ktr_, &htr_, &dtr_}) tr->restart();
+    for (Track* tr : {&ktr_, &htr_[0], &htr_[1], &dtr_}) tr->restart();
     tl_.clear();
     seg_ = -1;
     // kernels whose completion some transfer waits on
@@ -190,8 +199,9 @@ class Executor {
  private:
   struct Hazard {
     uint64_t end;
-    int64_t last_k, d2h, h2d;
+    int64_t last_k, d2h, h2d;   // h2d: the last copy (or poison fill) into the window
   };
+  static int par(int64_t seq) { return int(seq & 1); }   // h2d stream of copy number seq
 
   bool ok(hipError_t e, const char* what) {
     if (e == hipSuccess) return true;
@@ -200,7 +210,7 @@ class Executor {
   }
 
   bool sync_all() {
-    hipStream_t ss[3] = {comp_, h2d_, d2h_};
+    hipStream_t ss[4] = {comp_, h2d_[0], h2d_[1], d2h_};
     for (auto s : ss)
       if (s && !ok(hipStreamSynchronize(s), "hipStreamSynchronize")) return false;
     return true;
@@ -232,10 +242,12 @@ class Executor {
   void add_hazard(uint64_t off, uint64_t end, int64_t last_k, int64_t d2h, int64_t h2d) {
     hazards_[off] = Hazard{end, last_k, d2h, h2d};
   }
-  // Collect and remove the hazards overlapping [a, b), keeping uncovered parts.
-  void take_hazards(uint64_t a, uint64_t b, int64_t* last_k, int64_t* d2h, int64_t* h2d) {
+  // Collect and remove the hazards overlapping [a, b), keeping uncovered parts;
+  // h2d[p] is the latest copy into the range made on h2d stream p.
+  void take_hazards(uint64_t a, uint64_t b, int64_t* last_k, int64_t* d2h, int64_t h2d[2]) {
     *last_k = -1;
-    *d2h = *h2d = 0;
+    *d2h = 0;
+    h2d[0] = h2d[1] = 0;
     auto it = hazards_.lower_bound(a);
     if (it != hazards_.begin()) {
       auto p = std::prev(it);
@@ -246,7 +258,7 @@ class Executor {
       const Hazard& h = it->second;
       *last_k = std::max(*last_k, h.last_k);
       *d2h = std::max(*d2h, h.d2h);
-      *h2d = std::max(*h2d, h.h2d);
+      if (h.h2d) h2d[par(h.h2d)] = std::max(h2d[par(h.h2d)], h.h2d);
       if (it->first < a) keep.push_back({it->first, Hazard{a, h.last_k, h.d2h, h.h2d}});
       if (h.end > b) keep.push_back({b, Hazard{h.end, h.last_k, h.d2h, h.h2d}});
       it = hazards_.erase(it);
@@ -282,12 +294,17 @@ class Executor {
         }
         int64_t h2d = copy_seq_[t];
         if (c_.pol.validate) {
-          // poison the vacated window once its readers and write-back are done
-          if (last_use_[t] >= 0 && !wait(h2d_, kev_, kown_, last_use_[t], h2d_waited_k_)) return AUVM_E_HIP;
-          if (wb && !wait(h2d_, dev_, down_, wb, h2d_waited_d2h_)) return AUVM_E_HIP;
-          if (!ok(launch_poison(c_.pool + e.dev_off, e.bytes, h2d_), "poison")) return AUVM_E_HIP;
-          h2d = ++h2d_seq_;
-          if (!record(hev_, hown_, h2d, h2d_)) return AUVM_E_HIP;
+          // poison the vacated window once its readers, its fill and its write-back are done
+          const int64_t q = h2d_seq_ + 1;
+          const int sp = par(q);
+          hipStream_t st = h2d_[sp];
+          if (last_use_[t] >= 0 && !wait(st, kev_, kown_, last_use_[t], h2d_waited_k_[sp])) return AUVM_E_HIP;
+          if (wb && !wait(st, dev_, down_, wb, h2d_waited_d2h_[sp])) return AUVM_E_HIP;
+          if (h2d && par(h2d) != sp && !wait(st, hev_[1 - sp], hown_[1 - sp], h2d, h2d_waited_h2d_[sp]))
+            return AUVM_E_HIP;
+          if (!ok(launch_poison(c_.pool + e.dev_off, e.bytes, st), "poison")) return AUVM_E_HIP;
+          h2d = h2d_seq_ = q;
+          if (!record(hev_[sp], hown_[sp], h2d, st)) return AUVM_E_HIP;
         }
         add_hazard(e.dev_off, e.dev_off + e.bytes, last_use_[t], wb, h2d);
         where_[t] = -1;
@@ -296,34 +313,41 @@ class Executor {
       case AUVM_H2D_DEMAND:
       case AUVM_H2D_PREFETCH: {
         if (where_[t] >= 0) return internal("fetch of a resident tensor");
-        int64_t lk, d2h, h2d;
-        take_hazards(e.dev_off, e.dev_off + e.bytes, &lk, &d2h, &h2d);
-        if (lk >= 0 && !wait(h2d_, kev_, kown_, lk, h2d_waited_k_)) return AUVM_E_HIP;
+        int64_t lk, d2h, h2d[2];
+        take_hazards(e.dev_off, e.dev_off + e.bytes, &lk, &d2h, h2d);
+        const int64_t seq = h2d_seq_ + 1;
+        const int sp = par(seq);
+        hipStream_t st = h2d_[sp];
+        if (lk >= 0 && !wait(st, kev_, kown_, lk, h2d_waited_k_[sp])) return AUVM_E_HIP;
         if (e.op == AUVM_H2D_DEMAND && e.issue_k > 0 &&
-            !wait(h2d_, kev_, kown_, e.issue_k - 1, h2d_waited_k_))
+            !wait(st, kev_, kown_, e.issue_k - 1, h2d_waited_k_[sp]))
           return AUVM_E_HIP;
         int64_t dw = std::max(d2h, wb_seq_[t]);
-        if (dw && !wait(h2d_, dev_, down_, dw, h2d_waited_d2h_)) return AUVM_E_HIP;
+        if (dw && !wait(st, dev_, down_, dw, h2d_waited_d2h_[sp])) return AUVM_E_HIP;
+        // an earlier fill of the window from the other stream lands first
+        if (h2d[1 - sp] && !wait(st, hev_[1 - sp], hown_[1 - sp], h2d[1 - sp], h2d_waited_h2d_[sp]))
+          return AUVM_E_HIP;
         const Tensor& x = c_.tensors[t];
-        if (c_.pol.timing && !begin_item(htr_, h2d_, AUVM_TL_H2D, int64_t(cursor_), x.bytes))
-          return AUVM_E_HIP;
+        const int32_t kind = sp == 1 ? AUVM_TL_H2D : AUVM_TL_H2D_B;   // odd copy numbers: the first stream
+        if (c_.pol.timing && !begin_item(htr_[sp], st, kind, int64_t(cursor_), x.bytes)) return AUVM_E_HIP;
         if (!ok(hipMemcpyAsync(c_.pool + e.dev_off, c_.host + x.arena_off, x.bytes,
-                               hipMemcpyHostToDevice, h2d_), "hipMemcpyAsync H2D"))
+                               hipMemcpyHostToDevice, st), "hipMemcpyAsync H2D"))
           return AUVM_E_HIP;
-        if (c_.pol.timing && !end_item(htr_, h2d_)) return AUVM_E_HIP;
-        int64_t seq = ++h2d_seq_;
-        if (!record(hev_, hown_, seq, h2d_)) return AUVM_E_HIP;
+        if (c_.pol.timing && !end_item(htr_[sp], st)) return AUVM_E_HIP;
+        h2d_seq_ = seq;
+        if (!record(hev_[sp], hown_[sp], seq, st)) return AUVM_E_HIP;
         copy_seq_[t] = seq;
         where_[t] = int64_t(e.dev_off);
         return AUVM_OK;
       }
       case AUVM_ALLOC: {
         if (where_[t] >= 0) return internal("allocation of a resident tensor");
-        int64_t lk, d2h, h2d;
-        take_hazards(e.dev_off, e.dev_off + e.bytes, &lk, &d2h, &h2d);
+        int64_t lk, d2h, h2d[2];
+        take_hazards(e.dev_off, e.dev_off + e.bytes, &lk, &d2h, h2d);
         // previous readers ran earlier on the compute stream; transfers did not
         pend_d2h_ = std::max(pend_d2h_, d2h);
-        pend_h2d_ = std::max(pend_h2d_, h2d);
+        pend_h2d_[0] = std::max(pend_h2d_[0], h2d[0]);
+        pend_h2d_[1] = std::max(pend_h2d_[1], h2d[1]);
         copy_seq_[t] = 0;
         where_[t] = int64_t(e.dev_off);
         return AUVM_OK;
@@ -336,14 +360,16 @@ class Executor {
 
   auvm_status launch(int64_t k) {
     const Kernel& kd = c_.kernels[k];
-    int64_t need_h2d = pend_h2d_;
+    int64_t need_h2d[2] = {pend_h2d_[0], pend_h2d_[1]};
     for (auto& a : kd.acc) {
       if (where_[a.first] < 0) return internal("operand not resident at launch");
-      need_h2d = std::max(need_h2d, copy_seq_[a.first]);
+      const int64_t q = copy_seq_[a.first];
+      if (q) need_h2d[par(q)] = std::max(need_h2d[par(q)], q);
     }
-    if (need_h2d && !wait(comp_, hev_, hown_, need_h2d, comp_waited_h2d_)) return AUVM_E_HIP;
+    for (int p = 0; p < 2; ++p)
+      if (need_h2d[p] && !wait(comp_, hev_[p], hown_[p], need_h2d[p], comp_waited_h2d_[p])) return AUVM_E_HIP;
     if (pend_d2h_ && !wait(comp_, dev_, down_, pend_d2h_, comp_waited_d2h_)) return AUVM_E_HIP;
-    pend_h2d_ = pend_d2h_ = 0;
+    pend_h2d_[0] = pend_h2d_[1] = pend_d2h_ = 0;
     uint8_t* ptrs[16];
     for (size_t i = 0; i < kd.ids.size(); ++i) ptrs[i] = c_.pool + where_[kd.ids[i]];
     const bool timing = c_.pol.timing != 0;
@@ -379,7 +405,7 @@ class Executor {
   };
 
   bool begin_segment() {
-    for (Track* tr : {&ktr_, &htr_, &dtr_}) {
+    for (Track* tr : {&ktr_, &htr_[0], &htr_[1], &dtr_}) {
       if (!tr->s.empty()) continue;
       tr->s.assign(kTimeRing, nullptr);
       tr->e.assign(kTimeRing, nullptr);
@@ -453,29 +479,30 @@ class Executor {
     return true;
   }
   void harvest_all() {
-    for (Track* tr : {&ktr_, &htr_, &dtr_})
+    for (Track* tr : {&ktr_, &htr_[0], &htr_[1], &dtr_})
       while (tr->harvested < tr->n)
         if (!harvest(*tr, tr->harvested++)) return;
   }
 
   Ctx& c_;
-  hipStream_t comp_ = nullptr, h2d_ = nullptr, d2h_ = nullptr;
-  bool own_[3] = {false, false, false};
-  std::vector<hipEvent_t> kev_, hev_, dev_, bases_;
-  std::vector<int64_t> kown_, hown_, down_;
+  hipStream_t comp_ = nullptr, h2d_[2] = {nullptr, nullptr}, d2h_ = nullptr;
+  bool own_[4] = {false, false, false, false};   // comp_, h2d_[0], h2d_[1], d2h_
+  std::vector<hipEvent_t> kev_, hev_[2], dev_, bases_;   // hev_[p]: copies of h2d stream p
+  std::vector<int64_t> kown_, hown_[2], down_;
   size_t cursor_ = 0;
   int64_t next_k_ = 0;
   std::vector<int64_t> where_, last_use_, copy_seq_, wb_seq_;
   int64_t h2d_seq_ = 0, d2h_seq_ = 0;
-  int64_t h2d_waited_k_ = -1, d2h_waited_k_ = -1, h2d_waited_d2h_ = 0;
-  int64_t comp_waited_h2d_ = 0, comp_waited_d2h_ = 0;
-  int64_t pend_h2d_ = 0, pend_d2h_ = 0;
+  int64_t h2d_waited_k_[2] = {-1, -1}, d2h_waited_k_ = -1, h2d_waited_d2h_[2] = {0, 0};
+  int64_t h2d_waited_h2d_[2] = {0, 0};   // stream p: other stream's copies waited for
+  int64_t comp_waited_h2d_[2] = {0, 0}, comp_waited_d2h_ = 0;
+  int64_t pend_h2d_[2] = {0, 0}, pend_d2h_ = 0;
   std::map<uint64_t, Hazard> hazards_;
   std::vector<uint8_t> need_ev_;
   std::vector<auvm_sched_entry> log_;
   uint64_t kernels_run_ = 0;
   std::vector<float> dur_, gap_;
-  Track ktr_, htr_, dtr_;
+  Track ktr_, htr_[2], dtr_;
   std::vector<auvm_timeline_entry> tl_;
   int32_t seg_ = -1;
   std::chrono::steady_clock::time_point host0_;

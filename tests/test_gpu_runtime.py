@@ -91,10 +91,10 @@ def test_reset_and_rerun_gives_the_same_reads():
 @pytest.mark.parametrize("seed,variant", [(5, 0), (5, 4), (9, 1), (9, 4)])
 def test_timeline_is_complete_ordered_and_causal(seed, variant):
     """Timing policy: one timeline entry per kernel and per executed copy, each
-    stream's items in order without overlap, every kernel starting after the
-    copies that brought its operands, and demand fetches after the kernel
-    before their need."""
-    from paper_2609_06172_amd.capi import TL_D2H, TL_H2D, TL_KERNEL
+    stream's items in order without overlap (host-to-device copies run on two
+    streams), every kernel starting after the copies that brought its
+    operands, and demand fetches after the kernel before their need."""
+    from paper_2609_06172_amd.capi import TL_D2H, TL_H2D, TL_H2D_B, TL_KERNEL
     from workloads.format import S_ALLOC, S_D2H_WRITEBACK, S_H2D_DEMAND, S_H2D_PREFETCH, S_LAUNCH
     tensors, kernels = random_trace(seed, touch=True, n_kernels=90)
     M = feasible_budget(tensors, kernels, variant)
@@ -112,11 +112,14 @@ def test_timeline_is_complete_ordered_and_causal(seed, variant):
     kern = [e for e in tl if e[0] == TL_KERNEL]
     assert [e[2] for e in kern] == list(range(K))
     assert [e[1] for e in kern] == [0 if k < K // 2 else 1 for k in range(K)]
-    for kind, ops in ((TL_H2D, (S_H2D_PREFETCH, S_H2D_DEMAND)), (TL_D2H, (S_D2H_WRITEBACK,))):
-        got = [(e[2], e[3]) for e in tl if e[0] == kind]
+    for kinds, ops in (((TL_H2D, TL_H2D_B), (S_H2D_PREFETCH, S_H2D_DEMAND)), ((TL_D2H,), (S_D2H_WRITEBACK,))):
+        got = sorted((e[2], e[3]) for e in tl if e[0] in kinds)
         want = [(i, tensors[x[1]]["nbytes"]) for i, x in enumerate(sched) if x[0] in ops]
         assert got == want
-    for kind in (TL_KERNEL, TL_H2D, TL_D2H):
+    # copies alternate between the two host-to-device streams, the first on TL_H2D
+    h2d_kinds = [e[0] for e in sorted((e for e in tl if e[0] in (TL_H2D, TL_H2D_B)), key=lambda e: e[2])]
+    assert all(k == (TL_H2D, TL_H2D_B)[i % 2] for i, k in enumerate(h2d_kinds))
+    for kind in (TL_KERNEL, TL_H2D, TL_H2D_B, TL_D2H):
         items = [e for e in tl if e[0] == kind]
         for a, b in zip(items, items[1:]):
             assert b[5] <= b[6] + 1e-6 and a[5] >= -tol
@@ -126,7 +129,7 @@ def test_timeline_is_complete_ordered_and_causal(seed, variant):
     start = {e[2]: e[5] for e in kern}
     end = {e[2]: e[6] for e in kern}
     seg = {e[2]: e[1] for e in kern}
-    copy = {e[2]: e for e in tl if e[0] == TL_H2D}
+    copy = {e[2]: e for e in tl if e[0] in (TL_H2D, TL_H2D_B)}
     latest = {}
     for i, x in enumerate(sched):
         if x[0] in (S_H2D_PREFETCH, S_H2D_DEMAND):
@@ -147,7 +150,7 @@ def test_kernels_overlap_an_unrelated_prefetch():
     """Kernels that do not read a tensor being prefetched run while its copy is
     on the link: the compute and copy streams must not be serialized (as they
     are when two streams share a hardware queue)."""
-    from paper_2609_06172_amd.capi import TL_H2D, TL_KERNEL
+    from paper_2609_06172_amd.capi import TL_H2D, TL_H2D_B, TL_KERNEL
     from workloads.format import DT_U8, MODE_RW, OP_TOUCH
     tensors = [dict(nbytes=4096, dtype=DT_U8, kind=KIND_ACT, host_init=True),    # log: 64 slots
                dict(nbytes=128 << 20, dtype=DT_U8, kind=KIND_PARAM, host_init=False),
@@ -162,7 +165,7 @@ def test_kernels_overlap_an_unrelated_prefetch():
     tl = s.ctx.get_timeline()
     sched = s.ctx.get_schedule()
     s.close()
-    big = [e for e in tl if e[0] == TL_H2D and sched[e[2]][1] == 1]
+    big = [e for e in tl if e[0] in (TL_H2D, TL_H2D_B) and sched[e[2]][1] == 1]
     assert len(big) == 1
     kern = {e[2]: e for e in tl if e[0] == TL_KERNEL}
     assert big[0][5] < kern[1][5], "the prefetch is issued before the small kernels"
