@@ -324,7 +324,8 @@ auvm_status auvm_get_kernel_times(const auvm_ctx* ctx, float* dur_ms, float* gap
  * Host-to-device copies alternate between two streams by copy number (odd
  * numbers, the first copy included, on the first): AUVM_TL_H2D entries come
  * from one, AUVM_TL_H2D_B from the other; each stream's entries are in order,
- * and the two may overlap. */
+ * and the two may overlap.  A plan with write-backs keeps all its copies on
+ * the first stream. */
 enum { AUVM_TL_KERNEL = 0, AUVM_TL_H2D = 1, AUVM_TL_D2H = 2, AUVM_TL_H2D_B = 3 };
 typedef struct auvm_timeline_entry {
   int32_t kind;     /* AUVM_TL_* */

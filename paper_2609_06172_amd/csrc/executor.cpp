@@ -3,8 +3,10 @@
 // Replays a plan on four streams: compute (kernels), two h2d streams (pinned
 // host arena -> device pool copies, alternating by copy number, so that a copy
 // held back by its window's previous readers does not hold back the next one)
-// and d2h (write-backs).  Ordering is event based and never blocks the host
-// inside a run segment:
+// and d2h (write-backs).  A plan with write-backs keeps its copies on one h2d
+// stream: both directions share the host link, and a second copy in flight
+// halves the rate of the write-back that frees the first copy's window.
+// Ordering is event based and never blocks the host inside a run segment:
 //  * a copy into a pool window waits for the kernels that last used the
 //    tensors previously in that window and for write-backs out of it;
 //  * a demand fetch for kernel k additionally waits for kernel k-1, so it
@@ -134,6 +136,8 @@ class Executor {
     for (Track* tr : {&ktr_, &htr_[0], &htr_[1], &dtr_}) tr->restart();
     tl_.clear();
     seg_ = -1;
+    two_h2d_ = std::none_of(c_.plan.schedule.begin(), c_.plan.schedule.end(),
+                            [](const auvm_sched_entry& e) { return e.op == AUVM_D2H_WRITEBACK; });
     // kernels whose completion some transfer waits on
     need_ev_.assign(K, 0);
     std::vector<int64_t> last(nT, -1);
@@ -201,7 +205,10 @@ class Executor {
     uint64_t end;
     int64_t last_k, d2h, h2d;   // h2d: the last copy (or poison fill) into the window
   };
-  static int par(int64_t seq) { return int(seq & 1); }   // h2d stream of copy number seq
+  static int par(int64_t seq) { return int(seq & 1); }   // event ring of copy number seq
+  // h2d stream of copy number seq (the rings and waits stay per parity: with
+  // one stream for both they are only stronger than needed)
+  int lane(int64_t seq) const { return two_h2d_ ? par(seq) : 1; }
 
   bool ok(hipError_t e, const char* what) {
     if (e == hipSuccess) return true;
@@ -297,7 +304,7 @@ class Executor {
           // poison the vacated window once its readers, its fill and its write-back are done
           const int64_t q = h2d_seq_ + 1;
           const int sp = par(q);
-          hipStream_t st = h2d_[sp];
+          hipStream_t st = h2d_[lane(q)];
           if (last_use_[t] >= 0 && !wait(st, kev_, kown_, last_use_[t], h2d_waited_k_[sp])) return AUVM_E_HIP;
           if (wb && !wait(st, dev_, down_, wb, h2d_waited_d2h_[sp])) return AUVM_E_HIP;
           if (h2d && par(h2d) != sp && !wait(st, hev_[1 - sp], hown_[1 - sp], h2d, h2d_waited_h2d_[sp]))
@@ -316,8 +323,8 @@ class Executor {
         int64_t lk, d2h, h2d[2];
         take_hazards(e.dev_off, e.dev_off + e.bytes, &lk, &d2h, h2d);
         const int64_t seq = h2d_seq_ + 1;
-        const int sp = par(seq);
-        hipStream_t st = h2d_[sp];
+        const int sp = par(seq), ln = lane(seq);
+        hipStream_t st = h2d_[ln];
         if (lk >= 0 && !wait(st, kev_, kown_, lk, h2d_waited_k_[sp])) return AUVM_E_HIP;
         if (e.op == AUVM_H2D_DEMAND && e.issue_k > 0 &&
             !wait(st, kev_, kown_, e.issue_k - 1, h2d_waited_k_[sp]))
@@ -328,12 +335,12 @@ class Executor {
         if (h2d[1 - sp] && !wait(st, hev_[1 - sp], hown_[1 - sp], h2d[1 - sp], h2d_waited_h2d_[sp]))
           return AUVM_E_HIP;
         const Tensor& x = c_.tensors[t];
-        const int32_t kind = sp == 1 ? AUVM_TL_H2D : AUVM_TL_H2D_B;   // odd copy numbers: the first stream
-        if (c_.pol.timing && !begin_item(htr_[sp], st, kind, int64_t(cursor_), x.bytes)) return AUVM_E_HIP;
+        const int32_t kind = ln == 1 ? AUVM_TL_H2D : AUVM_TL_H2D_B;   // odd copy numbers: the first stream
+        if (c_.pol.timing && !begin_item(htr_[ln], st, kind, int64_t(cursor_), x.bytes)) return AUVM_E_HIP;
         if (!ok(hipMemcpyAsync(c_.pool + e.dev_off, c_.host + x.arena_off, x.bytes,
                                hipMemcpyHostToDevice, st), "hipMemcpyAsync H2D"))
           return AUVM_E_HIP;
-        if (c_.pol.timing && !end_item(htr_[sp], st)) return AUVM_E_HIP;
+        if (c_.pol.timing && !end_item(htr_[ln], st)) return AUVM_E_HIP;
         h2d_seq_ = seq;
         if (!record(hev_[sp], hown_[sp], seq, st)) return AUVM_E_HIP;
         copy_seq_[t] = seq;
@@ -497,6 +504,7 @@ class Executor {
   int64_t h2d_waited_h2d_[2] = {0, 0};   // stream p: other stream's copies waited for
   int64_t comp_waited_h2d_[2] = {0, 0}, comp_waited_d2h_ = 0;
   int64_t pend_h2d_[2] = {0, 0}, pend_d2h_ = 0;
+  bool two_h2d_ = true;   // the plan has no write-backs
   std::map<uint64_t, Hazard> hazards_;
   std::vector<uint8_t> need_ev_;
   std::vector<auvm_sched_entry> log_;

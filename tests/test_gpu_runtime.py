@@ -116,9 +116,13 @@ def test_timeline_is_complete_ordered_and_causal(seed, variant):
         got = sorted((e[2], e[3]) for e in tl if e[0] in kinds)
         want = [(i, tensors[x[1]]["nbytes"]) for i, x in enumerate(sched) if x[0] in ops]
         assert got == want
-    # copies alternate between the two host-to-device streams, the first on TL_H2D
+    # copies alternate between the two host-to-device streams, the first on
+    # TL_H2D, unless the plan writes back (then they share one stream)
     h2d_kinds = [e[0] for e in sorted((e for e in tl if e[0] in (TL_H2D, TL_H2D_B)), key=lambda e: e[2])]
-    assert all(k == (TL_H2D, TL_H2D_B)[i % 2] for i, k in enumerate(h2d_kinds))
+    if any(x[0] == S_D2H_WRITEBACK for x in sched):
+        assert set(h2d_kinds) <= {TL_H2D}
+    else:
+        assert all(k == (TL_H2D, TL_H2D_B)[i % 2] for i, k in enumerate(h2d_kinds))
     for kind in (TL_KERNEL, TL_H2D, TL_H2D_B, TL_D2H):
         items = [e for e in tl if e[0] == kind]
         for a, b in zip(items, items[1:]):
