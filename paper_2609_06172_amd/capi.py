@@ -112,6 +112,12 @@ def lib():
     if len(_hip_runtimes()) > 1:
         raise ImportError(f"two HIP runtimes are loaded ({sorted(_hip_runtimes())}); "
                           "import torch before any other HIP library")
+    _lib = bind_library(L)
+    return _lib
+
+
+def bind_library(L):
+    """Declare the C ABI's argument and result types on a loaded library."""
     P = C.c_void_p
     st = C.c_int32
     sig = {
@@ -146,15 +152,15 @@ def lib():
         f = getattr(L, name)
         f.restype = res
         f.argtypes = args
-    _lib = L
     return L
 
 
 class Context:
-    """One auvm_ctx.  hip_device < 0 gives a plan-only context."""
+    """One auvm_ctx.  hip_device < 0 gives a plan-only context.  library: a
+    library bound with bind_library (default: this package's)."""
 
-    def __init__(self, hip_device=-1):
-        self._L = lib()
+    def __init__(self, hip_device=-1, library=None):
+        self._L = lib() if library is None else library
         h = C.c_void_p()
         s = self._L.auvm_create(int(hip_device), C.byref(h))
         if s != OK:

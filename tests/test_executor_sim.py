@@ -1,0 +1,133 @@
+"""The executor on the CPU: the transfer engine's source, built against a
+queue simulator instead of the HIP runtime (tests/sim), runs random touch
+traces under every policy while operations execute in random orders allowed
+by the engine's event waits.  Every kernel must read exactly the version of
+each operand that the trace's order of writes implies, and the executed log
+must equal the plan.  Evicted windows are poisoned, so a read of a window
+that is not yet (or no longer) the tensor's shows up as a wrong version.
+
+A control run with the simulator's event waits dropped must fail: the
+traces are sensitive to missing ordering."""
+import ctypes as C
+import os
+import sys
+
+import numpy as np
+import pytest
+
+sys.path.insert(0, os.path.join(os.path.dirname(os.path.abspath(__file__)), "sim"))
+
+from oracle import planner as op
+from workloads.format import KIND_PARAM
+from workloads.trace import Workload
+
+from gpu_util import touch_expectations
+from planner_cases import random_trace
+
+_SIM = {}
+
+
+def sim_library():
+    if "L" not in _SIM:
+        import build_sim
+        from paper_2609_06172_amd.capi import bind_library
+        L = bind_library(C.CDLL(build_sim.build()))
+        L.auvm_sim_seed.restype = C.c_uint64
+        L.auvm_sim_seed.argtypes = [C.c_uint64]
+        L.auvm_sim_drop_waits.restype = None
+        L.auvm_sim_drop_waits.argtypes = [C.c_int]
+        _SIM["L"] = L
+    return _SIM["L"]
+
+
+def feasible_budget(tensors, kernels, variant, fracs=((1, 2), (2, 3), (3, 4), (5, 6), (1, 1))):
+    fp = sum(op.aligned(t["nbytes"]) for t in tensors)
+    for num, den in fracs:
+        M = max(1024, fp * num // den // 256 * 256)
+        try:
+            op.plan(tensors, kernels, M, variant=variant)
+            return M
+        except op.PlanError:
+            continue
+    raise AssertionError("no feasible budget")
+
+
+def run_touch_trace(seed, variant, order_seed, cuts=3, read_only=False):
+    """Runs a random touch trace on the simulated executor; returns (executed log
+    equals the plan, reads that saw the wrong version)."""
+    from paper_2609_06172_amd.capi import Context
+    L = sim_library()
+    n_kernels = (60 if read_only else 40) + (seed * 7) % 60
+    tensors, kernels = random_trace(seed, touch=True, n_kernels=n_kernels, read_only=read_only)
+    M = feasible_budget(tensors, kernels, variant)
+    w = Workload(None)
+    for i, t in enumerate(tensors):
+        w.tensor(f"t{i}", (t["nbytes"],), t["dtype"], t["kind"], host_init=t["host_init"])
+    ctx = Context(0, library=L)
+    ctx.arena_init(w.arena_bytes)
+    for t in w.tensors:
+        ctx.register_tensor(t.off, t.nbytes, t.dtype, t.kind, t.flags)
+    init = {}
+    for i, t in enumerate(tensors):
+        view = np.ctypeslib.as_array((C.c_uint8 * t["nbytes"]).from_address(ctx.tensor_host_ptr(i)))
+        if i == 0:
+            view[:] = 0                                  # the log
+        elif t["host_init"] or t["kind"] == KIND_PARAM:
+            init[i] = 1000 + i
+            view[:] = np.full(t["nbytes"] // 4, init[i], np.uint32).view(np.uint8)
+    for k in kernels:
+        ctx.add_kernel(k["op"], k["shape"], k["operands"])
+    ctx.set_budget(M)
+    ctx.set_policy(variant, validate=1)
+    ctx.plan()
+    L.auvm_sim_seed(order_seed)
+    K = len(kernels)
+    bounds = sorted(set([0, K] + [K * j // cuts for j in range(1, cuts)]))
+    for a, b in zip(bounds, bounds[1:]):
+        if b > a:
+            ctx.run(a, b - a)
+    executed_ok = ctx.get_executed() == ctx.get_schedule()
+    out = np.empty(tensors[0]["nbytes"], np.uint8)
+    ctx.read_tensor(0, out.ctypes.data, out.nbytes)
+    ctx.destroy()
+    log = out.view(np.uint32).reshape(-1, 16)
+    bad = [(slot, i, v, tuple(log[slot, 2 * i:2 * i + 2]))
+           for slot, i, v in touch_expectations(tensors, kernels, init)
+           if log[slot, 2 * i] != v or log[slot, 2 * i + 1] != v]
+    return executed_ok, bad
+
+
+@pytest.mark.parametrize("variant", [0, 1, 2, 3, 4])
+@pytest.mark.parametrize("seed", range(8))
+def test_touch_traces_read_latest_versions_in_any_order(seed, variant):
+    for order_seed in range(4):
+        executed_ok, bad = run_touch_trace(seed, variant, order_seed, cuts=1 + order_seed % 3)
+        assert executed_ok
+        assert not bad, (seed, variant, order_seed, bad[:4])
+
+
+@pytest.mark.parametrize("variant", [1, 2, 3, 4])
+@pytest.mark.parametrize("seed", range(12))
+def test_read_only_traces_on_two_copy_streams(seed, variant):
+    """Data operands only read: the plans have no write-backs, so copies
+    alternate between the two host-to-device streams; a kernel that ran
+    before its operand's copy, or a copy that overtook an earlier fill of the
+    same window, would read poison or another tensor's words."""
+    for order_seed in range(3):
+        executed_ok, bad = run_touch_trace(seed, variant, order_seed, cuts=1 + order_seed, read_only=True)
+        assert executed_ok
+        assert not bad, (seed, variant, order_seed, bad[:4])
+
+
+def test_dropping_the_event_waits_is_caught():
+    L = sim_library()
+    L.auvm_sim_drop_waits(1)
+    try:
+        failures = 0
+        for seed in range(6):
+            for order_seed in range(3):
+                _, bad = run_touch_trace(seed, 4, order_seed)
+                failures += bool(bad)
+        assert failures > 0
+    finally:
+        L.auvm_sim_drop_waits(0)
