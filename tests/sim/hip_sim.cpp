@@ -105,6 +105,12 @@ uint64_t auvm_sim_seed(uint64_t seed) {
 }
 // Control runs: drop every event wait (the engine's ordering disappears).
 void auvm_sim_drop_waits(int on) { g_drop_waits = on != 0; }
+// A stream for a caller to bind (auvm_bind_streams); never destroyed.
+void* auvm_sim_new_stream() {
+  hipStream_t s = nullptr;
+  hipExtStreamCreateWithCUMask(&s, 0, nullptr);
+  return s;
+}
 }
 
 const char* hipGetErrorString(hipError_t e) {

@@ -36,6 +36,8 @@ def sim_library():
         L.auvm_sim_seed.argtypes = [C.c_uint64]
         L.auvm_sim_drop_waits.restype = None
         L.auvm_sim_drop_waits.argtypes = [C.c_int]
+        L.auvm_sim_new_stream.restype = C.c_void_p
+        L.auvm_sim_new_stream.argtypes = []
         _SIM["L"] = L
     return _SIM["L"]
 
@@ -52,7 +54,7 @@ def feasible_budget(tensors, kernels, variant, fracs=((1, 2), (2, 3), (3, 4), (5
     raise AssertionError("no feasible budget")
 
 
-def run_touch_trace(seed, variant, order_seed, cuts=3, read_only=False):
+def run_touch_trace(seed, variant, order_seed, cuts=3, read_only=False, bind=None, timing=0, out=None):
     """Runs a random touch trace on the simulated executor; returns (executed log
     equals the plan, reads that saw the wrong version)."""
     from paper_2609_06172_amd.capi import Context
@@ -78,8 +80,10 @@ def run_touch_trace(seed, variant, order_seed, cuts=3, read_only=False):
     for k in kernels:
         ctx.add_kernel(k["op"], k["shape"], k["operands"])
     ctx.set_budget(M)
-    ctx.set_policy(variant, validate=1)
+    ctx.set_policy(variant, validate=1, timing=timing)
     ctx.plan()
+    if bind is not None:
+        ctx.bind_streams(*bind)
     L.auvm_sim_seed(order_seed)
     K = len(kernels)
     bounds = sorted(set([0, K] + [K * j // cuts for j in range(1, cuts)]))
@@ -87,10 +91,12 @@ def run_touch_trace(seed, variant, order_seed, cuts=3, read_only=False):
         if b > a:
             ctx.run(a, b - a)
     executed_ok = ctx.get_executed() == ctx.get_schedule()
-    out = np.empty(tensors[0]["nbytes"], np.uint8)
-    ctx.read_tensor(0, out.ctypes.data, out.nbytes)
+    if out is not None:
+        out.update(timeline=ctx.get_timeline(), schedule=ctx.get_schedule(), kernels=kernels, tensors=tensors)
+    logbuf = np.empty(tensors[0]["nbytes"], np.uint8)
+    ctx.read_tensor(0, logbuf.ctypes.data, logbuf.nbytes)
     ctx.destroy()
-    log = out.view(np.uint32).reshape(-1, 16)
+    log = logbuf.view(np.uint32).reshape(-1, 16)
     bad = [(slot, i, v, tuple(log[slot, 2 * i:2 * i + 2]))
            for slot, i, v in touch_expectations(tensors, kernels, init)
            if log[slot, 2 * i] != v or log[slot, 2 * i + 1] != v]
@@ -117,6 +123,60 @@ def test_read_only_traces_on_two_copy_streams(seed, variant):
         executed_ok, bad = run_touch_trace(seed, variant, order_seed, cuts=1 + order_seed, read_only=True)
         assert executed_ok
         assert not bad, (seed, variant, order_seed, bad[:4])
+
+
+@pytest.mark.parametrize("read_only", [False, True])
+@pytest.mark.parametrize("seed", range(6))
+def test_caller_bound_streams(seed, read_only):
+    """One caller stream for all copies (and callers' compute and write-back
+    streams): both copy sequences share it, and reads stay exact."""
+    L = sim_library()
+    streams = (L.auvm_sim_new_stream(), L.auvm_sim_new_stream(), L.auvm_sim_new_stream())
+    for variant in (0, 4):
+        if read_only and variant == 0:
+            continue
+        for order_seed in range(2):
+            executed_ok, bad = run_touch_trace(seed, variant, order_seed, read_only=read_only, bind=streams)
+            assert executed_ok and not bad, (seed, variant, order_seed, bad[:4])
+
+
+@pytest.mark.parametrize("read_only", [False, True])
+@pytest.mark.parametrize("seed", range(4))
+def test_timing_tracks(seed, read_only):
+    """Timing policy: one timeline entry per kernel and per copy, each
+    stream's items in order without overlap, kernels after the copies that
+    brought their operands (simulated clocks), and reads still exact."""
+    from paper_2609_06172_amd.capi import TL_D2H, TL_H2D, TL_H2D_B, TL_KERNEL
+    from workloads.format import S_ALLOC, S_D2H_WRITEBACK, S_H2D_DEMAND, S_H2D_PREFETCH, S_LAUNCH
+    rec = {}
+    executed_ok, bad = run_touch_trace(seed, 4, seed, cuts=2, read_only=read_only, timing=1, out=rec)
+    assert executed_ok and not bad
+    tl, sched, kernels, tensors = rec["timeline"], rec["schedule"], rec["kernels"], rec["tensors"]
+    kern = [e for e in tl if e[0] == TL_KERNEL]
+    assert sorted(e[2] for e in kern) == list(range(len(kernels)))
+    got = sorted((e[2], e[3]) for e in tl if e[0] in (TL_H2D, TL_H2D_B))
+    want = [(i, tensors[x[1]]["nbytes"]) for i, x in enumerate(sched) if x[0] in (S_H2D_PREFETCH, S_H2D_DEMAND)]
+    assert got == want
+    assert sum(1 for e in tl if e[0] == TL_D2H) == sum(1 for x in sched if x[0] == S_D2H_WRITEBACK)
+    for kind in (TL_KERNEL, TL_H2D, TL_H2D_B, TL_D2H):
+        items = [e for e in tl if e[0] == kind]
+        for a, b in zip(items, items[1:]):
+            if a[1] == b[1]:
+                assert b[5] >= a[6] and b[6] >= b[5]
+    start = {e[2]: e[5] for e in kern}
+    seg = {e[2]: e[1] for e in kern}
+    copy = {e[2]: e for e in tl if e[0] in (TL_H2D, TL_H2D_B)}
+    latest = {}
+    for i, x in enumerate(sched):
+        if x[0] in (S_H2D_PREFETCH, S_H2D_DEMAND):
+            latest[x[1]] = i
+        elif x[0] == S_LAUNCH:
+            for t, _ in kernels[x[4]]["operands"]:
+                j = latest.get(t)
+                if j is not None and copy[j][1] == seg[x[4]]:
+                    assert copy[j][6] <= start[x[4]], (x[4], t)
+        elif x[0] == S_ALLOC:
+            latest.pop(x[1], None)
 
 
 def test_dropping_the_event_waits_is_caught():
