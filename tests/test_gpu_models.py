@@ -99,6 +99,45 @@ def test_outputs_do_not_depend_on_the_policy():
             assert np.array_equal(a, b)
 
 
+def test_outputs_do_not_depend_on_the_budget():
+    # the same kernels on the same data, whatever is resident: logits and
+    # tokens bit-identical with everything resident, at 1.25x and at 2x
+    cfg = configs.LLAMA_SMALL
+    w = trace.build(cfg)
+    budgets = [w.footprint // 256 * 256 + 256, w.budget(5, 4), w.budget(2, 1)]
+    print(f"llama-small at budgets {budgets}", flush=True)
+    runs = [_llama_run(cfg, M=m) for m in budgets]
+    assert runs[0][3]["d2h_wb_n"] + runs[0][3]["drop_n"] == 0      # nothing evicted
+    assert runs[2][3]["drop_n"] > 0
+    for _, logits, gen, _, ex_ok in runs:
+        assert ex_ok
+        assert np.array_equal(gen, runs[0][2])
+        for a, b in zip(logits, runs[0][1]):
+            assert np.array_equal(a, b)
+
+
+def test_training_step_does_not_depend_on_the_budget():
+    # one training step with everything resident and at 2x: every gradient,
+    # moment, master weight and bf16 weight bit-identical (write-backs of the
+    # live-out state included)
+    from paper_2609_06172_amd.session import Session
+    from workloads import configs as C
+    w = trace.build(C.TRAIN_SMALL, keep_grads=True)
+    names = init.param_names(w)
+    out = []
+    for M in (w.footprint // 256 * 256 + 256, w.budget(2, 1)):
+        print(f"train-small at budget {M}", flush=True)
+        s = Session(w, device=0, M=M)
+        s.run_all()
+        out.append({n + sfx: s.read(n + sfx) for n in names for sfx in ("", ".grad", ".master", ".m", ".v")})
+        out[-1]["losses"] = s.read("losses")
+        c = s.ctx.get_counters()
+        s.close()
+    assert c["d2h_wb_n"] > 0
+    for k in out[0]:
+        assert np.array_equal(out[0][k], out[1][k]), k
+
+
 def test_replanning_from_measured_kernel_times():
     # runtime monitor: a timed run, classes again from the measured
     # durations, a new plan (the oracle's, bit for bit), the same outputs
