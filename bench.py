@@ -70,6 +70,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--layers", type=int, default=0,
                     help="MoE configs: layers to run (default: as many as fit the pinned host limit)")
+    ap.add_argument("--guard", type=int, default=None,
+                    help="victim guard of the T+A+P plan (default: 4; 16 for prefill configs)")
     ap.add_argument("--no-replan", action="store_true",
                     help="skip the rerun planned from the measured kernel times")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -539,7 +541,7 @@ def decode_main(args, cfg):
     log(f"measured pinned H2D: {bl_meas / 1e9:.1f} GB/s")
 
     t = time.perf_counter()
-    s = Session(w, device=0, M=M, variant=4, timing=1)
+    s = Session(w, device=0, M=M, variant=4, timing=1, guard=args.guard)
     log(f"session ready in {time.perf_counter() - t:.1f} s (plan {s.ctx.get_counters()['plan_ns'] / 1e9:.2f} s)")
     prefill_s, decode_s, k0, k1 = run_decode(s, w, W, K)
     log(f"prefill {prefill_s:.3f} s, decode {K} steps {decode_s:.3f} s")
@@ -615,7 +617,7 @@ def decode_main(args, cfg):
         def rerun():
             r = run_decode(s, w, W, Bk)
             return r[1], s.read("gen")[: W + Bk + 1].copy()
-        flips, moved, (da, ga), (dm, gm) = measured_replan(s, w, dur, None, rerun)
+        flips, moved, (da, ga), (dm, gm) = measured_replan(s, w, dur, args.guard, rerun)
         result["measured_replan"] = {
             "steps": Bk, "unit": "tokens/s", "kernels_timed": len(dur),
             "analytic_value": round(cfg.batch * Bk / da, 3), "value": round(cfg.batch * Bk / dm, 3),
@@ -630,7 +632,7 @@ def decode_main(args, cfg):
 
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline_decode(cfg, w, args.cpu_seconds, cfg.prompt_len + W, M)
-    print(json.dumps(result), flush=True)
+    emit(args, result)
 
 
 def sweep_main(args, cfg):
@@ -650,7 +652,7 @@ def sweep_main(args, cfg):
         c = dataclasses.replace(cfg, factor=(num, den))
         w = trace.build(c)
         M = w.budget()
-        s = Session(w, device=0, M=M, variant=4, timing=1)
+        s = Session(w, device=0, M=M, variant=4, timing=1, guard=args.guard)
         _, decode_s, k0, k1 = run_decode(s, w, W, K)
         segs = w.segments["decode"][W:W + K]
         st = seg_stats(w, s.ctx.get_schedule(), s.ctx.get_classes(), M, segs)
@@ -679,7 +681,7 @@ def sweep_main(args, cfg):
            "config": {"workload": f"{cfg.name}-shape decode, batch {cfg.batch}, {cfg.prompt_len}-token prompt",
                       "policy": "T+A+P"},
            "sweep": rows}
-    print(json.dumps(out), flush=True)
+    emit(args, out)
 
 
 def prefill_main(args, cfg):
@@ -706,7 +708,8 @@ def prefill_main(args, cfg):
     # victim guard buys overlap with bytes the link has time for; measured on
     # the 1.3B prefill: guard 4 / 8 / 16 / 24 / 32 -> 32.8 / 31.5 / 30.4 / 30.4 /
     # 31.0 ms per pass.  The link-bound decode is best at the default 4.
-    s = Session(w, device=0, M=M, variant=4, timing=1, guard=PREFILL_GUARD)
+    guard = PREFILL_GUARD if args.guard is None else args.guard
+    s = Session(w, device=0, M=M, variant=4, timing=1, guard=guard)
 
     def passes(sess):
         torch.cuda.synchronize()
@@ -745,7 +748,7 @@ def prefill_main(args, cfg):
                                f"GELU {cfg.ffn}, vocab {cfg.vocab}, {cfg.batch} x {cfg.prompt_len} tokens, "
                                f"budget = footprint*{den}/{num}",
                    "tokens_per_pass": cfg.tokens, "factor": f"{num}/{den}", "footprint_bytes": w.footprint,
-                   "budget_bytes": M, "policy": f"T+A+P (guard {PREFILL_GUARD})"},
+                   "budget_bytes": M, "policy": f"T+A+P (guard {guard})"},
         "path_roofline": pr,
         "roofline": {"kernel": "prefill projection GEMM (bf16 matrix cores)", "bound": "mfma",
                      "achieved": round(g_flops / g_time / 1e12, 1), "peak": 2500.0, "unit": "TFLOP/s",
@@ -779,7 +782,7 @@ def prefill_main(args, cfg):
         def rerun():
             r = passes(s)
             return r[1], s.read("logits").copy()
-        flips, moved, (ha, la), (hm, lm) = measured_replan(s, w, dur, PREFILL_GUARD, rerun)
+        flips, moved, (ha, la), (hm, lm) = measured_replan(s, w, dur, guard, rerun)
         result["measured_replan"] = {
             "unit": "tokens/s", "kernels_timed": len(dur),
             "analytic_value": round(cfg.tokens * I / ha, 1), "value": round(cfg.tokens * I / hm, 1),
@@ -793,7 +796,7 @@ def prefill_main(args, cfg):
     torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline_prefill(cfg, w, args.cpu_seconds)
-    print(json.dumps(result), flush=True)
+    emit(args, result)
 
 
 def cpu_baseline_train(cfg, seconds):
@@ -870,7 +873,7 @@ def train_main(args, cfg):
         f"{len(w.kernels)} kernels ({W + K} steps), footprint {w.footprint} B, budget {M} B")
     bl_meas = link_bandwidth()
     t = time.perf_counter()
-    s = Session(w, device=0, M=M, variant=4, timing=1)
+    s = Session(w, device=0, M=M, variant=4, timing=1, guard=args.guard)
     log(f"session ready in {time.perf_counter() - t:.1f} s")
 
     def run(sess):
@@ -946,7 +949,7 @@ def train_main(args, cfg):
     torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline_train(cfg, args.cpu_seconds)
-    print(json.dumps(result), flush=True)
+    emit(args, result)
 
 
 def moe_main(args, cfg):
@@ -979,7 +982,7 @@ def moe_main(args, cfg):
         f"(every expert), footprint {full.footprint} B, budget {M} B")
     bl_meas = link_bandwidth()
     t = time.perf_counter()
-    s = Session(full, device=0, M=M, variant=4, timing=1)
+    s = Session(full, device=0, M=M, variant=4, timing=1, guard=args.guard)
     log(f"session ready in {time.perf_counter() - t:.1f} s")
     pf_prefill, pf_decode, a0, a1 = run_decode(s, full, W, K)
     counts = s.routing_counts().copy()
@@ -1057,6 +1060,13 @@ def moe_main(args, cfg):
     torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline_moe(cfg, full, args.cpu_seconds, cfg.prompt_len + W)
+    emit(args, result)
+
+
+def emit(args, result):
+    """Print the bench line; a victim guard set on the command line is part of its config."""
+    if args.guard is not None:
+        result.setdefault("config", {})["guard"] = args.guard
     print(json.dumps(result), flush=True)
 
 
