@@ -41,6 +41,10 @@ sys.path.insert(0, ROOT)
 
 NOMINAL = dict(P=2.5e15, Bh=8.0e12, Bl=64.0e9)
 PREFILL_GUARD = 16
+# LLaMA-style decode with fused q, k, v projections (9 kernels per layer):
+# planned H2D per 7B step at 1.5x, guard 4 / 5 / 6 -> 7.579 / 7.528 / 7.528 GB
+# (the separate projections at guard 4: 7.527 GB)
+DECODE_GUARD = 5
 POLICY_NAMES = {0: "DEMAND_LRU", 1: "DEMAND_BELADY", 2: "T", 3: "T+A", 4: "T+A+P"}
 
 
@@ -71,7 +75,10 @@ def parse():
     ap.add_argument("--layers", type=int, default=0,
                     help="MoE configs: layers to run (default: as many as fit the pinned host limit)")
     ap.add_argument("--guard", type=int, default=None,
-                    help="victim guard of the T+A+P plan (default: 4; 16 for prefill configs)")
+                    help="victim guard of the T+A+P plan (default: 5 for LLaMA-style decode and the sweep, 16 for prefill configs, the library's 4 otherwise)")
+    ap.add_argument("--separate-qkv", action="store_true",
+                    help="LLaMA-style traces: q, k and v projections as three LINEAR kernels "
+                         "instead of one LINEAR_QKV")
     ap.add_argument("--no-replan", action="store_true",
                     help="skip the rerun planned from the measured kernel times")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -515,9 +522,11 @@ def roofline_fields(st, seconds, bl_meas, units):
 
 
 def linear_kernels(w, k0, k1):
-    from workloads.format import OP_LINEAR, OP_LINEAR_GELU, OP_LINEAR_RESID, OP_LINEAR_SWIGLU
+    from workloads.format import (OP_LINEAR, OP_LINEAR_GELU, OP_LINEAR_QKV, OP_LINEAR_RESID,
+                                  OP_LINEAR_SWIGLU)
     return [k for k in range(k0, k1)
-            if w.kernels[k].op in (OP_LINEAR, OP_LINEAR_GELU, OP_LINEAR_RESID, OP_LINEAR_SWIGLU)]
+            if w.kernels[k].op in (OP_LINEAR, OP_LINEAR_GELU, OP_LINEAR_RESID, OP_LINEAR_SWIGLU,
+                                   OP_LINEAR_QKV)]
 
 
 def decode_main(args, cfg):
@@ -541,7 +550,8 @@ def decode_main(args, cfg):
     log(f"measured pinned H2D: {bl_meas / 1e9:.1f} GB/s")
 
     t = time.perf_counter()
-    s = Session(w, device=0, M=M, variant=4, timing=1, guard=args.guard)
+    guard = DECODE_GUARD if args.guard is None else args.guard
+    s = Session(w, device=0, M=M, variant=4, timing=1, guard=guard)
     log(f"session ready in {time.perf_counter() - t:.1f} s (plan {s.ctx.get_counters()['plan_ns'] / 1e9:.2f} s)")
     prefill_s, decode_s, k0, k1 = run_decode(s, w, W, K)
     log(f"prefill {prefill_s:.3f} s, decode {K} steps {decode_s:.3f} s")
@@ -579,7 +589,8 @@ def decode_main(args, cfg):
                                f"{cfg.prompt_len}-token prompt then greedy steps, "
                                f"budget = footprint*{den}/{num}",
                    "batch": cfg.batch, "prompt_len": cfg.prompt_len, "factor": f"{num}/{den}",
-                   "footprint_bytes": w.footprint, "budget_bytes": M, "policy": "T+A+P"},
+                   "footprint_bytes": w.footprint, "budget_bytes": M, "policy": "T+A+P",
+                   "guard": guard, "qkv": "fused" if cfg.fuse_qkv else "separate"},
         "path_roofline": pr,
         "roofline": {"kernel": "decode projection GEMV (M=16, bf16 matrix cores)", "bound": "hbm",
                      "achieved": round(g_achieved, 1), "peak": 8000.0, "unit": "GB/s",
@@ -617,7 +628,7 @@ def decode_main(args, cfg):
         def rerun():
             r = run_decode(s, w, W, Bk)
             return r[1], s.read("gen")[: W + Bk + 1].copy()
-        flips, moved, (da, ga), (dm, gm) = measured_replan(s, w, dur, args.guard, rerun)
+        flips, moved, (da, ga), (dm, gm) = measured_replan(s, w, dur, guard, rerun)
         result["measured_replan"] = {
             "steps": Bk, "unit": "tokens/s", "kernels_timed": len(dur),
             "analytic_value": round(cfg.batch * Bk / da, 3), "value": round(cfg.batch * Bk / dm, 3),
@@ -652,7 +663,8 @@ def sweep_main(args, cfg):
         c = dataclasses.replace(cfg, factor=(num, den))
         w = trace.build(c)
         M = w.budget()
-        s = Session(w, device=0, M=M, variant=4, timing=1, guard=args.guard)
+        s = Session(w, device=0, M=M, variant=4, timing=1,
+                    guard=DECODE_GUARD if args.guard is None else args.guard)
         _, decode_s, k0, k1 = run_decode(s, w, W, K)
         segs = w.segments["decode"][W:W + K]
         st = seg_stats(w, s.ctx.get_schedule(), s.ctx.get_classes(), M, segs)
@@ -707,7 +719,7 @@ def prefill_main(args, cfg):
     # Prefill is compute-bound (the link idles most of a pass), so a longer
     # victim guard buys overlap with bytes the link has time for; measured on
     # the 1.3B prefill: guard 4 / 8 / 16 / 24 / 32 -> 32.8 / 31.5 / 30.4 / 30.4 /
-    # 31.0 ms per pass.  The link-bound decode is best at the default 4.
+    # 31.0 ms per pass.  The link-bound decode uses DECODE_GUARD.
     guard = PREFILL_GUARD if args.guard is None else args.guard
     s = Session(w, device=0, M=M, variant=4, timing=1, guard=guard)
 
@@ -1064,9 +1076,12 @@ def moe_main(args, cfg):
 
 
 def emit(args, result):
-    """Print the bench line; a victim guard set on the command line is part of its config."""
+    """Print the bench line; a victim guard or separate q, k, v projections set on
+    the command line are part of its config."""
     if args.guard is not None:
         result.setdefault("config", {})["guard"] = args.guard
+    if args.separate_qkv:
+        result.setdefault("config", {})["qkv"] = "separate"
     print(json.dumps(result), flush=True)
 
 
@@ -1084,6 +1099,8 @@ def main():
     cfg = configs.CONFIGS[args.config]
     if args.factor:
         cfg = dataclasses.replace(cfg, factor=factor_of(args.factor))
+    if args.separate_qkv:
+        cfg = dataclasses.replace(cfg, fuse_qkv=False)
     if cfg.style == "gpt":
         prefill_main(args, cfg)
     elif cfg.style == "moe":

@@ -77,6 +77,10 @@ enum { AUVM_R = 1, AUVM_W = 2, AUVM_RW = 3 };
  *  LINEAR_GELU   (M,N,K)             as LINEAR, c = gelu_erf(a W^T)
  *  LINEAR_RESID  (M,N,K)             a R, W R, x RW f32[M,N]: x += a W^T
  *  LINEAR_SWIGLU (M,N,K)             a R, Wg R, Wu R, c W: c = silu(a Wg^T) * (a Wu^T)
+ *  LINEAR_QKV    (M,N,K)             a R [M,K], Wq R, Wk R, Wv R [N,K], q W, k W, v W [M,N]:
+ *                                    three LINEARs of one input in one launch (the
+ *                                    attention's query, key and value projections);
+ *                                    each output equals its LINEAR bit for bit
  *  ATTN_QKV      (B,S,nH,d)          qkv R [B*S, 3*nH*d] (q|k|v column blocks),
  *                                    o W [B*S, nH*d]; causal within each sequence
  *  ROPE_KV       (B,S,nH,d,Lmax,pos0) q RW, k R, v R [B*S, nH*d], Kc, Vc [B,nH,Lmax,d]:
@@ -141,7 +145,7 @@ enum {
   AUVM_OP_MOE_DISPATCH = 13, AUVM_OP_MOE_UP = 14, AUVM_OP_MOE_DOWN = 15, AUVM_OP_COPY = 16,
   AUVM_OP_TRANSPOSE = 17, AUVM_OP_SWIGLU_ACT = 18, AUVM_OP_SWIGLU_BWD = 19, AUVM_OP_RMSNORM_BWD = 20,
   AUVM_OP_ATTN_BWD = 21, AUVM_OP_ROPE_BWD = 22, AUVM_OP_XENT = 23, AUVM_OP_EMBED_BWD = 24,
-  AUVM_OP_ADAM = 25, AUVM_OP_COUNT = 26
+  AUVM_OP_ADAM = 25, AUVM_OP_LINEAR_QKV = 26, AUVM_OP_COUNT = 27
 };
 
 /* policy variants: the paper's ablation ladder (T, T+A, T+A+P; Sec. V-E)

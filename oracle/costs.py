@@ -13,7 +13,8 @@ from workloads.format import (DT_SIZE, MODE_RW, OP_ARGMAX, OP_ATTN_CACHE,
                               OP_MOE_ROUTE, OP_MOE_UP, OP_RMSNORM, OP_ROPE_KV,
                               OP_TOUCH, OP_COPY, OP_TRANSPOSE, OP_SWIGLU_ACT,
                               OP_SWIGLU_BWD, OP_RMSNORM_BWD, OP_ATTN_BWD,
-                              OP_ROPE_BWD, OP_XENT, OP_EMBED_BWD, OP_ADAM)
+                              OP_ROPE_BWD, OP_XENT, OP_EMBED_BWD, OP_ADAM,
+                              OP_LINEAR_QKV)
 
 
 def kernel_cost(op, shape, operands, dtypes, nbytes):
@@ -42,6 +43,9 @@ def kernel_cost(op, shape, operands, dtypes, nbytes):
         F = 2 * M * N * K + {OP_LINEAR: 0, OP_LINEAR_GELU: 8 * M * N, OP_LINEAR_RESID: M * N}[op]
         out = M * N * es[2] * (2 if op == OP_LINEAR_RESID else 1)
         return F, M * K * es[0] + N * K * es[1] + out
+    if op == OP_LINEAR_QKV:
+        M, N, K = sh[0], sh[1], sh[2]
+        return 6 * M * N * K, M * K * es[0] + N * K * (es[1] + es[2] + es[3]) + M * N * (es[4] + es[5] + es[6])
     if op == OP_LINEAR_SWIGLU:
         M, N, K = sh[0], sh[1], sh[2]
         return 4 * M * N * K + 4 * M * N, M * K * es[0] + N * K * (es[1] + es[2]) + M * N * es[3]

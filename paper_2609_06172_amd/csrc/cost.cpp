@@ -54,6 +54,13 @@ void kernel_cost(const Kernel& k, const std::vector<Tensor>& T, uint64_t* Fo, ui
       B = M * K * es(T, k, 0) + N * K * es(T, k, 1) + out;
       break;
     }
+    case AUVM_OP_LINEAR_QKV: {
+      uint64_t M = s[0], N = s[1], K = s[2];
+      F = 6 * M * N * K;
+      B = M * K * es(T, k, 0) + N * K * (es(T, k, 1) + es(T, k, 2) + es(T, k, 3)) +
+          M * N * (es(T, k, 4) + es(T, k, 5) + es(T, k, 6));
+      break;
+    }
     case AUVM_OP_LINEAR_SWIGLU: {
       uint64_t M = s[0], N = s[1], K = s[2];
       F = 4 * M * N * K + 4 * M * N;
@@ -298,6 +305,31 @@ std::string validate_kernel(const Kernel& k, const std::vector<Tensor>& T) {
       if (da != dw || (sw && T[k.ids[2]].dtype != dw)) v.fail("activation and weight dtypes differ");
       if (da == AUVM_BF16 && K % 32) v.fail("bf16 GEMM needs K % 32 == 0");
       if (da == AUVM_F32 && T[k.ids[o]].dtype != AUVM_F32) v.fail("fp32 GEMM writes fp32");
+      break;
+    }
+    case AUVM_OP_LINEAR_QKV: {
+      v.count(7, 7);
+      v.pos(0, "M"); v.pos(1, "N"); v.pos(2, "K");
+      if (!v.ok) break;
+      uint64_t M = s[0], N = s[1], K = s[2];
+      static const char* const wn[3] = {"Wq", "Wk", "Wv"};
+      static const char* const on[3] = {"q", "k", "v"};
+      v.need(0, FP, M * K, "a"); v.mode(0, MR, "a");
+      for (int i = 0; i < 3; ++i) {
+        v.need(1 + i, FP, N * K, wn[i]); v.mode(1 + i, MR, wn[i]);
+        v.need(4 + i, FP, M * N, on[i]); v.mode(4 + i, MW | MRW, on[i]);
+      }
+      if (!v.ok) break;
+      uint32_t da = T[k.ids[0]].dtype;
+      for (int i = 1; i < 4; ++i)
+        if (T[k.ids[i]].dtype != da) v.fail("activation and weight dtypes differ");
+      for (int i = 5; i < 7; ++i)
+        if (T[k.ids[i]].dtype != T[k.ids[4]].dtype) v.fail("q, k and v dtypes differ");
+      for (int i = 4; i < 7; ++i)
+        for (int j = 0; j < i; ++j)
+          if (k.ids[i] == k.ids[j]) v.fail("q, k and v must be distinct tensors, none an input");
+      if (da == AUVM_BF16 && K % 32) v.fail("bf16 GEMM needs K % 32 == 0");
+      if (da == AUVM_F32 && T[k.ids[4]].dtype != AUVM_F32) v.fail("fp32 GEMM writes fp32");
       break;
     }
     case AUVM_OP_ATTN_QKV: {

@@ -22,13 +22,21 @@ struct GemmArgs {
   const int32_t* list = nullptr;
   const float* rw = nullptr;
   int topk = 1;
+  // Grouped products of one A (EPI_STORE, no list): groups > 1 computes
+  // C_i = A W_i^T for i < groups with W_i = gw[i], C_i = gc[i] (w and c
+  // unused).  The GEMV runs them as one grid; other routes launch once per
+  // product.  Each C_i equals the ungrouped product bit for bit.
+  int groups = 1;
+  const uint8_t* gw[3] = {};
+  uint8_t* gc[3] = {};
 };
 
 // Dispatch: bf16 with M <= 16 -> matrix-core GEMV (gemv.hip); bf16 with
 // M >= 512 and K % 64 == 0 -> 256 x 256 matrix-core GEMM fed by direct LDS
 // loads (gemm_big.hip); other bf16 -> 128 x 128 matrix-core GEMM
 // (gemm_mfma.hip); fp32 -> LDS-tiled FMA GEMM.  With a routed-row list:
-// M <= 16 -> the GEMV, else the 256 x 256 GEMM (K % 64 == 0).
+// M <= 16 -> the GEMV, else the 256 x 256 GEMM (K % 64 == 0).  Groups of up
+// to three products as described above.
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s);
 hipError_t launch_gemv_bf16(const GemmArgs& g, hipStream_t s);
 hipError_t launch_gemm_mfma_bf16(const GemmArgs& g, hipStream_t s);

@@ -130,6 +130,19 @@ hipError_t by_epi(const GemmArgs& g, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_gemm(const GemmArgs& g, hipStream_t s) {
+  if (g.groups != 1) {
+    if (g.groups < 1 || g.groups > 3 || g.list || g.epi != EPI_STORE) return hipErrorInvalidValue;
+    if (g.in_bf16 && g.M <= 16) return launch_gemv_bf16(g, s);
+    for (int i = 0; i < g.groups; ++i) {
+      GemmArgs one = g;
+      one.groups = 1;
+      one.w = g.gw[i];
+      one.c = g.gc[i];
+      const hipError_t e = launch_gemm(one, s);
+      if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+  }
   if (g.list) {
     if (!g.in_bf16 || g.topk < 1) return hipErrorInvalidValue;
     return g.M <= 16 ? launch_gemv_bf16(g, s) : launch_gemm_big_bf16(g, s);

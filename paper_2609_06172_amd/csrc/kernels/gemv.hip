@@ -7,6 +7,10 @@
 // Routed rows (MoE experts): the same kernel over the rows of a routed-row
 // list, gathered by token on input or scattered by token on output.
 //
+// Grouped products (the query, key and value projections): up to three
+// weights of the same shape against one A in one grid, group-major, so the
+// launch and its ramp are paid once for all three.
+//
 // Work split: one 1024-thread workgroup per 16 output features; its sixteen
 // waves take interleaved 64-wide K chunks (adjacent waves read adjacent 128 B
 // of every row), two chunks in flight per wave, keep fp32 partial tiles in
@@ -40,14 +44,24 @@ constexpr int kWaves = 16;  // waves per workgroup, splitting K
 // 16-B slot of piece q (0..7) of row r (0..15) in a chunk tile
 __device__ __forceinline__ int tslot(int r, int q) { return 8 * r + (q ^ (r >> 1)); }
 
+// weights and outputs of up to three grouped products (one when ungrouped)
+struct Group {
+  const bf16_t* w0;
+  const bf16_t* w1;
+  const bf16_t* w2;
+  void* c0;
+  void* c1;
+  void* c2;
+};
+
 // LIST: rows come from a routed-row list (GemmArgs::list): the row count is
 // read from the list, and A rows are gathered by token (EPI_SWIGLU) or the
 // results scattered into token rows with the routing weight (EPI_MOE).
 template <int EPI, class TC, bool LIST>
-__global__ void __launch_bounds__(64 * kWaves) gemv_mfma(const bf16_t* __restrict__ A, const bf16_t* __restrict__ W,
-                                                 const bf16_t* __restrict__ W2, TC* __restrict__ C,
-                                                 int M, int64_t N, int64_t K, const int32_t* __restrict__ list,
-                                                 const float* __restrict__ rw, int topk) {
+__global__ void __launch_bounds__(64 * kWaves) gemv_mfma(const bf16_t* __restrict__ A, Group grp,
+                                                 const bf16_t* __restrict__ W2, int M, int64_t N, int64_t K,
+                                                 const int32_t* __restrict__ list, const float* __restrict__ rw,
+                                                 int topk) {
   constexpr bool DUAL = EPI == EPI_SWIGLU;
   constexpr int kParts = DUAL ? 3 : 2;   // A, W (, W2) tiles of a chunk
   __shared__ bf16x8 tile[kWaves][kParts][128];
@@ -56,7 +70,12 @@ __global__ void __launch_bounds__(64 * kWaves) gemv_mfma(const bf16_t* __restric
   const int wv = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // uniform: scalar chunk loop
   const int r = lane & 15, g = lane >> 4;      // fragment row, k group
   const int fr = lane >> 3, fp = lane & 7;     // load row (within 8), piece
-  const int64_t n0 = int64_t(blockIdx.x) * 16;
+  // group of this workgroup (uniform; selects, so the choice stays scalar)
+  const int64_t nb = (N + 15) / 16, bx = blockIdx.x;
+  const int gi = bx >= 2 * nb ? 2 : bx >= nb ? 1 : 0;
+  const bf16_t* __restrict__ W = gi == 0 ? grp.w0 : gi == 1 ? grp.w1 : grp.w2;
+  TC* __restrict__ C = static_cast<TC*>(gi == 0 ? grp.c0 : gi == 1 ? grp.c1 : grp.c2);
+  const int64_t n0 = (bx - gi * nb) * 16;
   int rows = M;
   if constexpr (LIST) rows = list[0] < M ? list[0] : M;
   // source rows of this lane's two loads: rows fr and 8 + fr of the tile;
@@ -157,10 +176,25 @@ __global__ void __launch_bounds__(64 * kWaves) gemv_mfma(const bf16_t* __restric
 
 template <int EPI, class TC, bool LIST = false>
 hipError_t go(const GemmArgs& g, hipStream_t s) {
-  dim3 grid(unsigned((g.N + 15) / 16));
+  const bool grouped = g.groups > 1;
+  if (grouped && (EPI != EPI_STORE || LIST || g.groups > 3)) return hipErrorInvalidValue;
+  const int ng = grouped ? g.groups : 1;
+  Group grp;
+  const uint8_t* w[3] = {g.w, g.w, g.w};
+  uint8_t* c[3] = {g.c, g.c, g.c};
+  for (int i = 0; grouped && i < 3; ++i) {   // unused groups repeat the last one; no block reaches them
+    w[i] = g.gw[i < ng ? i : ng - 1];
+    c[i] = g.gc[i < ng ? i : ng - 1];
+  }
+  grp.w0 = reinterpret_cast<const bf16_t*>(w[0]);
+  grp.w1 = reinterpret_cast<const bf16_t*>(w[1]);
+  grp.w2 = reinterpret_cast<const bf16_t*>(w[2]);
+  grp.c0 = c[0];
+  grp.c1 = c[1];
+  grp.c2 = c[2];
+  dim3 grid(unsigned(ng * ((g.N + 15) / 16)));
   hipLaunchKernelGGL((gemv_mfma<EPI, TC, LIST>), grid, dim3(64 * kWaves), 0, s, reinterpret_cast<const bf16_t*>(g.a),
-                     reinterpret_cast<const bf16_t*>(g.w), reinterpret_cast<const bf16_t*>(g.w2),
-                     reinterpret_cast<TC*>(g.c), int(g.M), g.N, g.K, g.list, g.rw, g.topk);
+                     grp, reinterpret_cast<const bf16_t*>(g.w2), int(g.M), g.N, g.K, g.list, g.rw, g.topk);
   return hipGetLastError();
 }
 

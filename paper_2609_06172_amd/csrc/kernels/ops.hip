@@ -309,6 +309,22 @@ hipError_t launch_op(const Kernel& k, const std::vector<Tensor>& T, uint8_t* con
       g.out_bf16 = dt(sw ? 3 : 2) == AUVM_BF16;
       return launch_gemm(g, s);
     }
+    case AUVM_OP_LINEAR_QKV: {
+      GemmArgs g{};
+      g.M = sh[0];
+      g.N = sh[1];
+      g.K = sh[2];
+      g.a = p[0];
+      g.epi = EPI_STORE;
+      g.in_bf16 = dt(0) == AUVM_BF16;
+      g.out_bf16 = dt(4) == AUVM_BF16;
+      g.groups = 3;
+      for (int i = 0; i < 3; ++i) {
+        g.gw[i] = p[1 + i];
+        g.gc[i] = p[4 + i];
+      }
+      return launch_gemm(g, s);
+    }
     case AUVM_OP_COPY:
       return hipMemcpyAsync(p[1], p[0], size_t(sh[0]), hipMemcpyDeviceToDevice, s);
     case AUVM_OP_TRANSPOSE:

@@ -1,6 +1,7 @@
 """Builds the host-only executor test library: the library's C ABI, planner,
 cost model and executor sources compiled with g++ against the queue
 simulator in this directory instead of the HIP runtime (test infrastructure)."""
+import fcntl
 import glob
 import os
 import subprocess
@@ -17,13 +18,17 @@ def build():
     """Compile if any source or header is newer than the library; returns its path."""
     deps = SOURCES + glob.glob(os.path.join(CSRC, "*.h")) + glob.glob(os.path.join(ROOT, "include", "*.h")) + \
         glob.glob(os.path.join(HERE, "hip", "*.h"))
-    if os.path.exists(OUT) and os.path.getmtime(OUT) >= max(os.path.getmtime(d) for d in deps):
-        return OUT
     os.makedirs(os.path.dirname(OUT), exist_ok=True)
-    cmd = ["g++", "-O1", "-g", "-fPIC", "-shared", "-std=c++17", "-Wall", "-Wno-unused-function",
-           "-I" + HERE, "-I" + os.path.join(ROOT, "include"), "-I" + CSRC] + SOURCES + ["-o", OUT + ".tmp"]
-    subprocess.run(cmd, check=True)
-    os.replace(OUT + ".tmp", OUT)
+    # one build at a time (parallel test workers share the output)
+    with open(OUT + ".lock", "w") as lock:
+        fcntl.flock(lock, fcntl.LOCK_EX)
+        if os.path.exists(OUT) and os.path.getmtime(OUT) >= max(os.path.getmtime(d) for d in deps):
+            return OUT
+        tmp = f"{OUT}.{os.getpid()}.tmp"
+        cmd = ["g++", "-O1", "-g", "-fPIC", "-shared", "-std=c++17", "-Wall", "-Wno-unused-function",
+               "-I" + HERE, "-I" + os.path.join(ROOT, "include"), "-I" + CSRC] + SOURCES + ["-o", tmp]
+        subprocess.run(cmd, check=True)
+        os.replace(tmp, OUT)
     return OUT
 
 

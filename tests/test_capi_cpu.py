@@ -366,3 +366,56 @@ def test_random_live_out_traces_bit_exact(seed):
             assert ee.value.code == e.code
             continue
         assert_same_plan(plan_ctx(tensors, kernels, M, variant=variant), r)
+
+
+def test_linear_qkv_validation_and_cost():
+    """LINEAR_QKV: three LINEARs of one input.  Its cost is theirs with the
+    shared input read once; malformed operand lists are rejected."""
+    from oracle.costs import kernel_cost
+    from workloads.format import DT_SIZE, OP_LINEAR_QKV
+    M, N, K = 16, 64, 96
+    ctx = Context(-1)
+    ctx.arena_init(1 << 22)
+    off = [0]
+
+    def t(nbytes, dt, kind=KIND_ACT):
+        i = ctx.register_tensor(off[0], nbytes, dt, kind, 1 if kind != KIND_PARAM else 0)
+        off[0] += (nbytes + 255) // 256 * 256
+        return i
+    a = t(M * K * 2, DT_BF16)
+    wq, wk, wv = (t(N * K * 2, DT_BF16, KIND_PARAM) for _ in range(3))
+    q, k, v = (t(M * N * 2, DT_BF16) for _ in range(3))
+    w32 = t(N * K * 4, DT_F32, KIND_PARAM)
+    q32 = t(M * N * 4, DT_F32)
+    small = t(N * K, DT_BF16, KIND_PARAM)
+    R, W = MODE_R, MODE_W
+    good = [(a, R), (wq, R), (wk, R), (wv, R), (q, W), (k, W), (v, W)]
+    ctx.add_kernel(OP_LINEAR_QKV, (M, N, K), good)
+
+    def swap(i, e):
+        ops = list(good)
+        ops[i] = e
+        return ops
+    bad = [
+        good[:6],                                # six operands
+        swap(5, (q, W)),                         # k is q
+        swap(6, (a, W)),                         # v is the input
+        swap(2, (wk, W)),                        # a weight written
+        swap(3, (w32, R)),                       # weight dtype differs from a
+        swap(5, (q32, W)),                       # k's dtype differs from q's
+        swap(3, (small, R)),                     # Wv too small for N x K
+    ]
+    for ops in bad:
+        with pytest.raises(AuvmError) as e:
+            ctx.add_kernel(OP_LINEAR_QKV, (M, N, K), ops)
+        assert e.value.code == op.E_INVAL, ops
+    with pytest.raises(AuvmError):               # bf16 needs K % 32 == 0
+        ctx.add_kernel(OP_LINEAR_QKV, (M, N, 80), good)
+    ctx.destroy()
+    dtypes = {i: DT_BF16 for i in range(7)}
+    nbytes = {i: 0 for i in range(7)}
+    ops = [(i, m) for i, (_, m) in enumerate(good)]
+    F3, B3 = kernel_cost(OP_LINEAR_QKV, (M, N, K), ops, dtypes, nbytes)
+    F1, B1 = kernel_cost(OP_LINEAR, (M, N, K), [(0, R), (1, R), (4, W)], dtypes, nbytes)
+    assert F3 == 3 * F1 == 6 * M * N * K
+    assert B3 == 3 * B1 - 2 * M * K * DT_SIZE[DT_BF16]

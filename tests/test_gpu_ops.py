@@ -8,8 +8,8 @@ from oracle import forward as of
 from workloads.format import (DT_BF16, DT_F32, DT_I32, MODE_R, MODE_RW, MODE_W,
                               OP_ARGMAX, OP_ATTN_CACHE, OP_ATTN_QKV, OP_EMBED,
                               OP_LAYERNORM, OP_LINEAR, OP_LINEAR_GELU,
-                              OP_LINEAR_RESID, OP_LINEAR_SWIGLU, OP_RMSNORM,
-                              OP_ROPE_KV)
+                              OP_LINEAR_QKV, OP_LINEAR_RESID,
+                              OP_LINEAR_SWIGLU, OP_RMSNORM, OP_ROPE_KV)
 
 from gpu_util import rel_l2, single_kernel, write_inputs
 
@@ -71,6 +71,23 @@ def test_linear_family(op_, M, N, K, dt):
     elif op_ == OP_LINEAR_SWIGLU:
         y = of.silu(y) * of.linear(vals["a"], vals["W2"])
     assert rel_l2(res["c"], y) < TOL[out_dt]
+
+
+@pytest.mark.parametrize("dt", [DT_F32, DT_BF16])
+@pytest.mark.parametrize("M,N,K", LIN_SHAPES)
+def test_linear_qkv(M, N, K, dt):
+    """Grouped q, k, v projections: each output matches the oracle, and is bit
+    for bit the output of the same product run as its own LINEAR."""
+    a = rnd(M, K)
+    Ws = [rnd(N, K, scale=K ** -0.5) for _ in range(3)]
+    ops = [("a", (M, K), dt, MODE_R, a)] + [(f"W{i}", (N, K), dt, MODE_R, Ws[i]) for i in range(3)] + \
+          [(f"c{i}", (M, N), dt, MODE_W, None) for i in range(3)]
+    vals, res = _run(OP_LINEAR_QKV, (M, N, K), ops, ["c0", "c1", "c2"])
+    for i in range(3):
+        assert rel_l2(res[f"c{i}"], of.linear(vals["a"], vals[f"W{i}"])) < TOL[dt]
+        _, one = _run(OP_LINEAR, (M, N, K), [("a", (M, K), dt, MODE_R, a), ("W", (N, K), dt, MODE_R, Ws[i]),
+                                             ("c", (M, N), dt, MODE_W, None)], ["c"])
+        assert np.array_equal(res[f"c{i}"].view(np.uint8), one["c"].view(np.uint8)), i
 
 
 @pytest.mark.parametrize("dt", [DT_F32, DT_BF16])

@@ -34,6 +34,7 @@ class DecoderConfig:
     iterations: int = 1                # gpt style: forward passes over the same ids
     n_experts: int = 0                 # moe style: experts per layer (ffn is each expert's width)
     top_k: int = 0                     # moe style: experts routed per token
+    fuse_qkv: bool = True              # llama/moe style: q, k, v projections as one LINEAR_QKV kernel
 
     @property
     def head_dim(self) -> int:

@@ -51,6 +51,7 @@ OP_ROPE_BWD = 22      # (B, S, nH, d)        dq RW, dK R, dV R, dk W, dv W
 OP_XENT = 23          # (T, V)               logits R, labels R, losses W, dlogits W
 OP_EMBED_BWD = 24     # (T, H, V)            ids R, dx R, dE W
 OP_ADAM = 25          # (n, step, lr*1e9, b1*1e6, b2*1e6, eps*1e12, wd*1e6)  g R, p32 RW, m RW, v RW, p W
+OP_LINEAR_QKV = 26    # (M, N, K)            a R, Wq R, Wk R, Wv R, q W, k W, v W   q = a Wq^T (k, v alike)
 
 OP_NAMES = {
     OP_TOUCH: "touch", OP_EMBED: "embed", OP_LAYERNORM: "layernorm",
@@ -61,7 +62,7 @@ OP_NAMES = {
     OP_MOE_UP: "moe_up", OP_MOE_DOWN: "moe_down", OP_COPY: "copy", OP_TRANSPOSE: "transpose",
     OP_SWIGLU_ACT: "swiglu_act", OP_SWIGLU_BWD: "swiglu_bwd", OP_RMSNORM_BWD: "rmsnorm_bwd",
     OP_ATTN_BWD: "attn_bwd", OP_ROPE_BWD: "rope_bwd", OP_XENT: "xent", OP_EMBED_BWD: "embed_bwd",
-    OP_ADAM: "adam",
+    OP_ADAM: "adam", OP_LINEAR_QKV: "linear_qkv",
 }
 
 # planner policy variants (paper's ablation ladder plus the two demand baselines)

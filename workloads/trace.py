@@ -17,7 +17,7 @@ from .format import (ALIGN, DT_F32, DT_I32, DT_SIZE, FLAG_HOST_INIT, FLAG_LIVE_O
                      KIND_KV, KIND_PARAM, MODE_R, MODE_RW, MODE_W, OP_ARGMAX,
                      OP_ATTN_CACHE, OP_ATTN_QKV, OP_EMBED, OP_LAYERNORM,
                      OP_LINEAR, OP_LINEAR_GELU, OP_LINEAR_RESID,
-                     OP_LINEAR_SWIGLU, OP_MOE_DISPATCH, OP_MOE_DOWN,
+                     OP_LINEAR_SWIGLU, OP_LINEAR_QKV, OP_MOE_DISPATCH, OP_MOE_DOWN,
                      OP_MOE_ROUTE, OP_MOE_UP, OP_RMSNORM, OP_ROPE_KV, OP_ADAM,
                      OP_ATTN_BWD, OP_COPY, OP_EMBED_BWD, OP_RMSNORM_BWD,
                      OP_ROPE_BWD, OP_SWIGLU_ACT, OP_SWIGLU_BWD, OP_TRANSPOSE,
@@ -285,9 +285,13 @@ def _build_llama(c: DecoderConfig, routing=None, n_steps=0) -> Workload:
 
     def block(l, L, x, h, q, k, v, a, f, M, s_len, pos0, kv_mode, seg=0):
         w.kernel(OP_RMSNORM, (M, H, 1, 0), [(x, R), (L["g1"], R), (h, W_)], l, "attn_norm")
-        w.kernel(OP_LINEAR, (M, H, H), [(h, R), (L["wq"], R), (q, W_)], l, "wq")
-        w.kernel(OP_LINEAR, (M, H, H), [(h, R), (L["wk"], R), (k, W_)], l, "wk")
-        w.kernel(OP_LINEAR, (M, H, H), [(h, R), (L["wv"], R), (v, W_)], l, "wv")
+        if c.fuse_qkv:
+            w.kernel(OP_LINEAR_QKV, (M, H, H), [(h, R), (L["wq"], R), (L["wk"], R), (L["wv"], R),
+                                                (q, W_), (k, W_), (v, W_)], l, "wqkv")
+        else:
+            w.kernel(OP_LINEAR, (M, H, H), [(h, R), (L["wq"], R), (q, W_)], l, "wq")
+            w.kernel(OP_LINEAR, (M, H, H), [(h, R), (L["wk"], R), (k, W_)], l, "wk")
+            w.kernel(OP_LINEAR, (M, H, H), [(h, R), (L["wv"], R), (v, W_)], l, "wv")
         w.kernel(OP_ROPE_KV, (B, s_len, nH, d, Lmax, pos0),
                  [(q, RW), (k, R), (v, R), (L["K"], kv_mode), (L["V"], kv_mode)], l, "rope_kv")
         w.kernel(OP_ATTN_CACHE, (B, s_len, nH, d, Lmax, pos0),
