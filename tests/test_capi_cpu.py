@@ -419,3 +419,15 @@ def test_linear_qkv_validation_and_cost():
     F1, B1 = kernel_cost(OP_LINEAR, (M, N, K), [(0, R), (1, R), (4, W)], dtypes, nbytes)
     assert F3 == 3 * F1 == 6 * M * N * K
     assert B3 == 3 * B1 - 2 * M * K * DT_SIZE[DT_BF16]
+
+
+def test_separate_qkv_trace_bit_exact():
+    """The three-kernel q, k, v trace plans in the library exactly as in the oracle."""
+    import dataclasses
+    from paper_2609_06172_amd.session import Session
+    cfg = dataclasses.replace(configs.LLAMA_SMALL, fuse_qkv=False)
+    w = trace.build(cfg)
+    for variant in VARIANTS:
+        s = Session(w, device=-1, variant=variant)
+        assert_same_plan(s.ctx, op.plan_workload(w, s.M, variant=variant))
+        s.close()

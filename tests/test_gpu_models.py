@@ -116,6 +116,22 @@ def test_outputs_do_not_depend_on_the_budget():
             assert np.array_equal(a, b)
 
 
+def test_grouped_qkv_launch_matches_separate_projections():
+    # LINEAR_QKV computes each projection exactly as its own LINEAR does, so
+    # the two traces give bit-identical logits and tokens (at 1.5x)
+    runs = []
+    for fuse in (True, False):
+        cfg = dataclasses.replace(configs.LLAMA_SMALL, fuse_qkv=fuse)
+        print(f"llama-small fuse_qkv={fuse}", flush=True)
+        runs.append(_llama_run(cfg))
+    assert len(runs[0][0].kernels) < len(runs[1][0].kernels)
+    for _, logits, gen, _, ex_ok in runs:
+        assert ex_ok
+        assert np.array_equal(gen, runs[0][2])
+        for a, b in zip(logits, runs[0][1]):
+            assert np.array_equal(a, b)
+
+
 def test_training_step_does_not_depend_on_the_budget():
     # one training step with everything resident and at 2x: every gradient,
     # moment, master weight and bf16 weight bit-identical (write-backs of the
