@@ -71,11 +71,20 @@ __global__ void __launch_bounds__(256) attn_rowwave(AttnArgs a) {
 // Decode attention, head dim 128, bf16: one workgroup per query row.
 // A key (or value) row is 256 B = 16 lanes x 16 B, so a wave loads four
 // consecutive rows per instruction, fully coalesced.  Lane (grp, sub) =
-// (l / 16, l % 16) holds dims 8*sub..8*sub+7; a wave takes blocks of 32 keys
-// (key 32*blk + 4*u + grp for u = 0..7, eight loads of K and eight of V in
-// flight), the four waves interleave blocks, each keeps an online softmax and
-// the waves are merged through LDS.
-constexpr int kDecU = 8;
+// (l / 16, l % 16) holds dims 8*sub..8*sub+7; a wave takes blocks of 24 keys
+// (key 24*blk + 4*u + grp for u = 0..5, six loads of K and six of V in
+// flight), the eight waves interleave blocks, each keeps an online softmax and
+// the waves are merged through LDS.  Loaded rows stay packed bf16 in
+// registers until used (at most 128 VGPRs, no spills: two workgroups per
+// compute unit).
+constexpr int kDecU = 6;
+constexpr int kDecWaves = 8;
+
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// the two bf16 values packed in a word, as floats
+__device__ __forceinline__ float bf_lo(uint32_t v) { return __uint_as_float(v << 16); }
+__device__ __forceinline__ float bf_hi(uint32_t v) { return __uint_as_float(v & 0xffff0000u); }
 
 __device__ __forceinline__ void load8(const bf16_t* p, float* f) {
   typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -87,8 +96,8 @@ __device__ __forceinline__ void load8(const bf16_t* p, float* f) {
   }
 }
 
-__global__ void __launch_bounds__(256) attn_decode_d128(AttnArgs a) {
-  __shared__ float sm[4], sl[4], sacc[4][128];
+__global__ void __launch_bounds__(64 * kDecWaves, 4) attn_decode_d128(AttnArgs a) {
+  __shared__ float sm[kDecWaves], sl[kDecWaves], sacc[kDecWaves][128];
   const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
   const int grp = lane >> 4, sub = lane & 15;
   const int64_t row = blockIdx.x;
@@ -106,17 +115,17 @@ __global__ void __launch_bounds__(256) attn_decode_d128(AttnArgs a) {
   float m = -INFINITY, l = 0.f, acc[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) acc[e] = 0.f;
-  for (int64_t j0 = int64_t(wv) * 32; j0 <= last; j0 += 4 * 32) {
-    float kf[kDecU][8], vf[kDecU][8], sc[kDecU];
+  for (int64_t j0 = int64_t(wv) * 4 * kDecU; j0 <= last; j0 += kDecWaves * 4 * kDecU) {
+    u32x4 kr[kDecU], vr[kDecU];
+    float sc[kDecU];
 #pragma unroll
     for (int u = 0; u < kDecU; ++u) {
       const int64_t j = j0 + 4 * u + grp;
       if (j <= last) {
-        load8(kb + j * a.kv_rs, kf[u]);
-        load8(vb + j * a.kv_rs, vf[u]);
+        kr[u] = *reinterpret_cast<const u32x4*>(kb + j * a.kv_rs);
+        vr[u] = *reinterpret_cast<const u32x4*>(vb + j * a.kv_rs);
       } else {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) kf[u][e] = vf[u][e] = 0.f;
+        kr[u] = vr[u] = u32x4{0u, 0u, 0u, 0u};
       }
     }
     float mloc = -INFINITY;
@@ -124,7 +133,10 @@ __global__ void __launch_bounds__(256) attn_decode_d128(AttnArgs a) {
     for (int u = 0; u < kDecU; ++u) {
       float s = 0.f;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) s = fmaf(qf[e], kf[u][e], s);
+      for (int e = 0; e < 4; ++e) {
+        s = fmaf(qf[2 * e], bf_lo(kr[u][e]), s);
+        s = fmaf(qf[2 * e + 1], bf_hi(kr[u][e]), s);
+      }
       s += __shfl_xor(s, 8, 64);
       s += __shfl_xor(s, 4, 64);
       s += __shfl_xor(s, 2, 64);
@@ -144,7 +156,10 @@ __global__ void __launch_bounds__(256) attn_decode_d128(AttnArgs a) {
       const float p = __expf(sc[u] - mn);
       psum += p;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) acc[e] = fmaf(p, vf[u][e], acc[e]);
+      for (int e = 0; e < 4; ++e) {
+        acc[2 * e] = fmaf(p, bf_lo(vr[u][e]), acc[2 * e]);
+        acc[2 * e + 1] = fmaf(p, bf_hi(vr[u][e]), acc[2 * e + 1]);
+      }
     }
     psum += __shfl_xor(psum, 16, 64);
     psum += __shfl_xor(psum, 32, 64);
@@ -167,9 +182,9 @@ __global__ void __launch_bounds__(256) attn_decode_d128(AttnArgs a) {
   if (threadIdx.x < 128) {
     const int dd = threadIdx.x;
     float M = sm[0];
-    for (int w = 1; w < 4; ++w) M = fmaxf(M, sm[w]);
+    for (int w = 1; w < kDecWaves; ++w) M = fmaxf(M, sm[w]);
     float L = 0.f, r = 0.f;
-    for (int w = 0; w < 4; ++w) {
+    for (int w = 0; w < kDecWaves; ++w) {
       const float f = sm[w] == -INFINITY ? 0.f : __expf(sm[w] - M);
       L += sl[w] * f;
       r += sacc[w][dd] * f;
@@ -624,7 +639,7 @@ hipError_t launch_attention_bwd_d128(const AttnBwdArgs& a, hipStream_t s) {
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
   const int64_t rows = a.B * a.nH * a.S;
   if (a.bf16 && a.d == 128 && a.S <= 16 && !a.lse) {
-    hipLaunchKernelGGL(attn_decode_d128, dim3(unsigned(rows)), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(attn_decode_d128, dim3(unsigned(rows)), dim3(64 * kDecWaves), 0, s, a);
     return hipGetLastError();
   }
   if (a.bf16 && a.d == 128) {
