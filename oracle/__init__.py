@@ -6,7 +6,9 @@ Plain, slow, obviously-correct reimplementation of what the GPU path computes:
 * ``costs``    — analytic flops and algorithmic HBM bytes per kernel;
 * ``planner``  — the tensor-granular prefetch/evict policy replayed on a trace;
 * ``checker``  — semantic validation of any transfer schedule;
-* ``brute``    — exhaustive search on tiny instances.
+* ``brute``    — exhaustive search on tiny instances (least demand fetches,
+  least makespan in the unit-time prefetching model) and the timing of a
+  schedule in that model.
 
 Only the tests, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
 ``bench.py`` may import this package.  It shares no code with the HIP path and

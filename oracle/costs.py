@@ -4,7 +4,8 @@ The paper counts FLOP instructions and memory loads per kernel to place each
 kernel on its multi-level roofline (Sec. III-C, Sec. IV-G).  Here the counts
 are the algorithmic ones, written per op from its shape: every operand element
 is read or written once, a read-modify-write counts twice, and a GEMM costs
-2*M*N*K flops.  Integer arithmetic only.
+2*M*N*K flops; elements an op does not touch (rows it does not gather, cache
+positions past the valid prefix) do not count.  Integer arithmetic only.
 """
 from workloads.format import (DT_SIZE, MODE_RW, OP_ARGMAX, OP_ATTN_CACHE,
                               OP_ATTN_QKV, OP_EMBED, OP_LAYERNORM, OP_LINEAR,

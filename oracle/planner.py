@@ -35,11 +35,19 @@ notes) are:
   equally far so that, among them, the window evicting fewer bytes wins
   (bucket 1 is exact farthest-next-use), and (worst victim priority,
   -writeback bytes, -victim bytes, -offset) under LRU;
-* after each launch, the prefetch scan walks upcoming kernels in order and
-  fetches the missing read operands of each CGI kernel whose host value is
-  still live, stopping at the first operand that cannot be placed
-  (prefetch-ahead with farthest-next-use victims, the "aggressive"
-  integrated prefetching/caching strategy).
+* the ablation steps T and T+A prefetch, after each launch, the missing live
+  read operands of the next kernel only (look-ahead 1), with LRU victims, and
+  stop at the first operand that cannot be placed; T+A adds the affinity
+  pins;
+* the full method (T+A+P) is two passes.  The first is the demand timeline
+  with farthest-next-use victims, affinity pins and a victim guard (a victim
+  preferably unused by the ``guard`` kernels before the demand point).  The
+  second (``_retime``) keeps every replacement of the first and moves each
+  fetch of a CGI kernel to the earliest boundary at which every tensor that
+  held its window has had its last access, in demand order: the
+  "conservative" integrated prefetching/caching strategy of Cao, Felten,
+  Karlin and Li (optimal replacements, each fetch as early as possible).
+  Fetches of kernels that are not CGI stay at their kernel (on-demand).
 
 Integer arithmetic only; no state outside the function.  Slow and plain.
 """
