@@ -169,6 +169,9 @@ typedef struct {
   uint32_t layer;         /* reporting only */
 } auvm_kernel_desc;
 
+/* guard or bucket value that asks for the library's default for the variant */
+#define AUVM_POLICY_DEFAULT 0xFFFFFFFFu
+
 typedef struct {
   uint32_t variant;       /* AUVM_DEMAND_LRU .. AUVM_T_A_P (default T_A_P, guard 4, bucket 32) */
   uint32_t lookahead;     /* max kernels a fetch runs ahead; 0 = T/T+A: 1, T+A+P: unlimited */
@@ -178,11 +181,13 @@ typedef struct {
   uint32_t timing;        /* 1: record per-kernel start/end events during run */
   uint32_t guard;         /* T+A+P only: a demand at kernel j prefers victims not used by
                              kernels j-guard..j-1, so their replacement fetch can start
-                             that many kernels earlier (0 = plain farthest-next-use) */
+                             that many kernels earlier (0 = plain farthest-next-use;
+                             AUVM_POLICY_DEFAULT = 4 for T+A+P, 0 otherwise) */
   uint32_t bucket;        /* T+A+P and DEMAND_BELADY: victims' next uses are compared in
                              buckets of this many kernels, and within a bucket the pool
                              window that evicts fewer bytes wins (1 = exact
-                             farthest-next-use; 0 is read as 1; default 32 for T+A+P) */
+                             farthest-next-use; 0 is read as 1; AUVM_POLICY_DEFAULT = 32
+                             for T+A+P, 1 otherwise) */
 } auvm_policy;
 
 typedef struct {
@@ -218,6 +223,10 @@ typedef struct {
   uint64_t plan_ns;                       /* host time of the last auvm_plan */
   uint64_t run_ns;                        /* host wall time inside auvm_run calls */
   uint64_t kernels_run;                   /* launches executed since plan/reset */
+  uint64_t stall_ns;                      /* timing policy: compute-stream idle time between
+                                             consecutive kernels of each run segment since
+                                             plan/reset (kernels waiting for their operands'
+                                             copies, or for the host); 0 without timing */
 } auvm_counters;
 
 /* Create a context bound to HIP device `hip_device`; a negative device gives a

@@ -56,13 +56,15 @@ class TimelineEntry(C.Structure):
 
 TL_KERNEL, TL_H2D, TL_D2H, TL_H2D_B = 0, 1, 2, 3
 
+POLICY_DEFAULT = 0xFFFFFFFF      # guard / bucket: the library's default for the variant
+
 
 class Counters(C.Structure):
     _fields_ = [(n, C.c_uint64) for n in (
         "h2d_prefetch_n", "h2d_prefetch_B", "h2d_demand_n", "h2d_demand_B", "d2h_wb_n",
         "d2h_wb_B", "drop_n", "alloc_n", "useless_prefetch_n", "useless_prefetch_B")] + [
         ("class_n", C.c_uint64 * 3), ("plan_ns", C.c_uint64), ("run_ns", C.c_uint64),
-        ("kernels_run", C.c_uint64)]
+        ("kernels_run", C.c_uint64), ("stall_ns", C.c_uint64)]
 
     def as_dict(self):
         d = {n: getattr(self, n) for n, _ in self._fields_ if n != "class_n"}
@@ -219,11 +221,9 @@ class Context:
 
     def set_policy(self, variant=4, lookahead=0, affinity_w=1, placement=0, validate=0, timing=0,
                    guard=None, bucket=None):
-        if guard is None:
-            guard = 4 if variant == 4 else 0
-        if bucket is None:
-            bucket = 32 if variant == 4 else 1
-        p = Policy(variant, lookahead, affinity_w, placement, validate, timing, guard, bucket)
+        """guard / bucket None: the library applies its own default for the variant."""
+        p = Policy(variant, lookahead, affinity_w, placement, validate, timing,
+                   POLICY_DEFAULT if guard is None else guard, POLICY_DEFAULT if bucket is None else bucket)
         self._check(self._L.auvm_set_policy(self._h, C.byref(p)))
 
     def plan(self):

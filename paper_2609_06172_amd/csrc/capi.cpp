@@ -195,6 +195,9 @@ auvm_status auvm_set_policy(auvm_ctx* x, const auvm_policy* p) {
   if (p->variant > AUVM_T_A_P || p->placement > AUVM_PLACE_IDEAL)
     return fail(x, AUVM_E_INVAL, "bad policy");
   x->c.pol = *p;
+  const bool full = p->variant == AUVM_T_A_P;
+  if (p->guard == AUVM_POLICY_DEFAULT) x->c.pol.guard = full ? 4 : 0;
+  if (p->bucket == AUVM_POLICY_DEFAULT) x->c.pol.bucket = full ? 32 : 1;
   x->c.planned = false;
   return AUVM_OK;
 }
@@ -280,6 +283,7 @@ auvm_status auvm_get_counters(const auvm_ctx* x, auvm_counters* o) {
   o->plan_ns = c.plan_ns;
   o->run_ns = c.run_ns;
   o->kernels_run = c.exec ? exec_kernels_run(c) : 0;
+  o->stall_ns = c.exec ? exec_stall_ns(c) : 0;
   return AUVM_OK;
 }
 

@@ -49,6 +49,7 @@ auvm_status exec_reset(Ctx& c);
 auvm_status exec_read(Ctx& c, int32_t id, void* dst, uint64_t bytes);
 const std::vector<auvm_sched_entry>& exec_log(const Ctx& c);
 uint64_t exec_kernels_run(const Ctx& c);
+uint64_t exec_stall_ns(const Ctx& c);
 auvm_status exec_kernel_times(const Ctx& c, float* dur, float* gap, uint64_t cap, uint64_t* n);
 const std::vector<auvm_timeline_entry>& exec_timeline(const Ctx& c);
 auvm_status host_alloc_pinned(Ctx& c, uint64_t bytes);

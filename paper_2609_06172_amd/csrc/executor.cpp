@@ -28,6 +28,7 @@
 
 #include <algorithm>
 #include <chrono>
+#include <cmath>
 #include <vector>
 #include <cstring>
 #include <map>
@@ -131,6 +132,7 @@ class Executor {
     hazards_.clear();
     log_.clear();
     kernels_run_ = 0;
+    stall_ms_ = 0;
     dur_.assign(K, 0.f);
     gap_.assign(K, 0.f);
     for (Track* tr : {&ktr_, &htr_[0], &htr_[1], &dtr_}) tr->restart();
@@ -188,6 +190,7 @@ class Executor {
 
   const std::vector<auvm_sched_entry>& log() const { return log_; }
   uint64_t kernels_run() const { return kernels_run_; }
+  uint64_t stall_ns() const { return uint64_t(std::llround(stall_ms_ * 1e6)); }
 
   auvm_status times(float* dur, float* gap, uint64_t cap, uint64_t* n) const {
     const uint64_t m = uint64_t(ktr_.n);
@@ -481,7 +484,10 @@ class Executor {
     if (&tr == &ktr_) {
       dur_[j] = ms;
       // the gap before the first kernel of a run segment includes host time: not reported
-      if (chained) gap_[j + 1] = g;
+      if (chained) {
+        gap_[j + 1] = g;
+        stall_ms_ += g;
+      }
     }
     return true;
   }
@@ -509,6 +515,7 @@ class Executor {
   std::vector<uint8_t> need_ev_;
   std::vector<auvm_sched_entry> log_;
   uint64_t kernels_run_ = 0;
+  double stall_ms_ = 0;   // sum of the reported gaps
   std::vector<float> dur_, gap_;
   Track ktr_, htr_[2], dtr_;
   std::vector<auvm_timeline_entry> tl_;
@@ -535,6 +542,7 @@ auvm_status exec_reset(Ctx& c) { return c.exec->reset(); }
 auvm_status exec_read(Ctx& c, int32_t id, void* dst, uint64_t) { return c.exec->read(id, dst); }
 const std::vector<auvm_sched_entry>& exec_log(const Ctx& c) { return c.exec->log(); }
 uint64_t exec_kernels_run(const Ctx& c) { return c.exec->kernels_run(); }
+uint64_t exec_stall_ns(const Ctx& c) { return c.exec->stall_ns(); }
 auvm_status exec_kernel_times(const Ctx& c, float* d, float* g, uint64_t cap, uint64_t* n) {
   return c.exec->times(d, g, cap, n);
 }

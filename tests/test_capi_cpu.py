@@ -431,3 +431,33 @@ def test_separate_qkv_trace_bit_exact():
         s = Session(w, device=-1, variant=variant)
         assert_same_plan(s.ctx, op.plan_workload(w, s.M, variant=variant))
         s.close()
+
+
+@pytest.mark.parametrize("variant", VARIANTS)
+def test_the_library_applies_its_own_policy_defaults(variant):
+    """guard and bucket left unset travel as AUVM_POLICY_DEFAULT, and the
+    library's defaults for the variant plan exactly what the oracle's do."""
+    from paper_2609_06172_amd import capi
+    seen = {}
+    real = capi.Policy
+
+    class Spy(real):
+        def __init__(self, *a):
+            super().__init__(*a)
+            seen["guard"], seen["bucket"] = self.guard, self.bucket
+    capi.Policy = Spy
+    try:
+        tensors, kernels = random_trace(4242 + variant, touch=True)
+        fp = sum(op.aligned(t["nbytes"]) for t in tensors)
+        for num, den in ((1, 2), (2, 3), (3, 4), (5, 6), (1, 1)):
+            M = max(1024, fp * num // den // 256 * 256)
+            try:
+                ref = op.plan(tensors, kernels, M, variant=variant)
+                break
+            except op.PlanError:
+                continue
+        ctx = plan_ctx(tensors, kernels, M, variant=variant)
+    finally:
+        capi.Policy = real
+    assert seen == {"guard": capi.POLICY_DEFAULT, "bucket": capi.POLICY_DEFAULT}
+    assert_same_plan(ctx, ref)

@@ -92,7 +92,8 @@ def run_touch_trace(seed, variant, order_seed, cuts=3, read_only=False, bind=Non
             ctx.run(a, b - a)
     executed_ok = ctx.get_executed() == ctx.get_schedule()
     if out is not None:
-        out.update(timeline=ctx.get_timeline(), schedule=ctx.get_schedule(), kernels=kernels, tensors=tensors)
+        out.update(timeline=ctx.get_timeline(), schedule=ctx.get_schedule(), kernels=kernels, tensors=tensors,
+                   counters=ctx.get_counters(), kernel_times=ctx.get_kernel_times())
     logbuf = np.empty(tensors[0]["nbytes"], np.uint8)
     ctx.read_tensor(0, logbuf.ctypes.data, logbuf.nbytes)
     ctx.destroy()
@@ -177,6 +178,20 @@ def test_timing_tracks(seed, read_only):
                     assert copy[j][6] <= start[x[4]], (x[4], t)
         elif x[0] == S_ALLOC:
             latest.pop(x[1], None)
+    # the stall counter is the compute stream's idle time between consecutive
+    # kernels of a segment, as the timeline shows it
+    idle = sum(b[5] - a[6] for a, b in zip(kern, kern[1:]) if a[1] == b[1])
+    _, gaps = rec["kernel_times"]
+    assert abs(rec["counters"]["stall_ns"] - idle * 1e6) <= 1e-3 * max(1.0, idle * 1e6)
+    assert abs(sum(gaps) * 1e6 - rec["counters"]["stall_ns"]) <= 1e-3 * max(1.0, idle * 1e6)
+    assert idle > 0
+
+
+def test_no_stall_counted_without_timing():
+    rec = {}
+    executed_ok, bad = run_touch_trace(3, 4, 1, cuts=2, out=rec)
+    assert executed_ok and not bad
+    assert rec["counters"]["stall_ns"] == 0
 
 
 def test_dropping_the_event_waits_is_caught():

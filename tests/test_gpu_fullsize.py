@@ -3,8 +3,9 @@
 through the C-ABI under T+A+P, and sampled outputs are checked against the
 fp64 oracle one layer at a time.  The oracle takes the GPU's layer input
 (and, for attention over a cache, the GPU's cache prefix; for MoE, the
-GPU's expert choice) and must reproduce the layer output at the bf16
-tolerance (rel-L2 2e-2)."""
+GPU's expert choice) and must reproduce what the layer adds to the residual
+stream (its output minus its input) at the bf16 tolerance (rel-L2 2e-2),
+with every element within a per-element bound for a layer of bf16 stages."""
 import dataclasses
 
 import numpy as np
@@ -14,11 +15,14 @@ from oracle import forward as of
 from workloads import configs, init, trace
 from workloads.format import OP_MOE_DOWN, OP_MOE_ROUTE
 
-from gpu_util import rel_l2
+from gpu_util import (ELEM_BF16, ELEM_LAYER, assert_close, assert_within, attention_backward_bounds,
+                      rel_l2)
 
 pytestmark = pytest.mark.gpu
 
 TOL = 2e-2
+DECODE_GUARD = 5          # the decode benchmark's victim guard
+PREFILL_GUARD = 16        # the prefill benchmark's
 
 
 class Walker:
@@ -51,7 +55,7 @@ def test_llama7b_decode_layer_and_head_sampled():
     w = trace.build(cfg, steps=2)
     step, l, bs = 1, 17, [0, 9, 15]
     print(f"llama-7b decode at 1.5x: step {step}, layer {l}, sequences {bs}", flush=True)
-    s = Session(w, device=0)                     # budget footprint/1.5, T+A+P
+    s = Session(w, device=0, guard=DECODE_GUARD)  # budget footprint/1.5, T+A+P
     walk = Walker(s)
     seg = w.segments["decode"][step]
     a, b = _layer_range(w, seg, l)
@@ -70,12 +74,14 @@ def test_llama7b_decode_layer_and_head_sampled():
     c1 = dataclasses.replace(cfg, batch=len(bs))
     Kc, Vc = K[bs].astype(np.float64), V[bs].astype(np.float64)
     ref = of.llama_layer(c1, Lw, x_in[bs], Kc, Vc, pos)
-    assert rel_l2(x_out[bs], ref) < TOL
-    assert rel_l2(K[bs][:, :, pos], Kc[:, :, pos]) < TOL      # the new cache row
-    assert rel_l2(V[bs][:, :, pos], Vc[:, :, pos]) < TOL
+    e = assert_close(x_out[bs] - x_in[bs], ref - x_in[bs], TOL, ELEM_LAYER, "layer increment")
+    print(f"layer {l} increment: rel-L2 {e[0]:.2e}, max |error| / rms {e[1]:.2e}")
+    assert_close(K[bs][:, :, pos], Kc[:, :, pos], TOL, ELEM_LAYER, "new K row")
+    assert_close(V[bs][:, :, pos], Vc[:, :, pos], TOL, ELEM_LAYER, "new V row")
     Hd = _weights(w, "", ("norm_f", "head"))
     lg = of.linear(of.rmsnorm(x_last[bs], Hd["norm_f"]), Hd["head"])
-    assert rel_l2(logits[bs], lg) < TOL
+    e = assert_close(logits[bs], lg, TOL, ELEM_LAYER, "logits")
+    print(f"logits: rel-L2 {e[0]:.2e}, max |error| / rms {e[1]:.2e}")
 
 
 def test_gpt1p3b_prefill_layer_and_head_sampled():
@@ -84,7 +90,7 @@ def test_gpt1p3b_prefill_layer_and_head_sampled():
     w = trace.build(cfg)
     l, b = 11, 2
     print(f"gpt-1.3b prefill at 1.25x: layer {l}, sequence {b}", flush=True)
-    s = Session(w, device=0, guard=16)           # the prefill benchmark's policy
+    s = Session(w, device=0, guard=PREFILL_GUARD)   # the prefill benchmark's policy
     walk = Walker(s)
     a, n = w.segments["forward"][1 + l]
     walk.to(a)
@@ -102,10 +108,11 @@ def test_gpt1p3b_prefill_layer_and_head_sampled():
     names = ("ln1.g", "ln1.b", "wqkv", "wo", "ln2.g", "ln2.b", "w1", "w2")
     Wt = init.weights_f64(w, names=[f"L{l}.{x}" for x in names] + ["lnf.g", "lnf.b", "E"])
     ref = of.gpt_layer(dataclasses.replace(cfg, batch=1), Wt, l, x_in[rows])
-    assert rel_l2(x_out[rows], ref) < TOL
+    e = assert_close(x_out[rows] - x_in[rows], ref - x_in[rows], TOL, ELEM_LAYER, "layer increment")
+    print(f"layer {l} increment: rel-L2 {e[0]:.2e}, max |error| / rms {e[1]:.2e}")
     last = x_last[np.arange(cfg.batch) * S + S - 1]
     lg = of.linear(of.layernorm(last, Wt["lnf.g"], Wt["lnf.b"]), Wt["E"])
-    assert rel_l2(logits, lg) < TOL
+    assert_close(logits, lg, TOL, ELEM_LAYER, "logits")
 
 
 def _moe_bench_config():
@@ -152,12 +159,12 @@ def test_moe_decode_and_prefill_layers_sampled():
     names += [f"x{e}.{n}" for e in experts for n in ("wg", "wu", "wd")]
     Lw = _weights(w, f"L{l}.", names)
     y, _, _, _ = of.moe_mlp(cfg, Lw, h_p, forced=rte_p)
-    assert rel_l2(x_ffn - x_mid, y) < TOL
+    assert_close(x_ffn - x_mid, y, TOL, ELEM_LAYER, "routed FFN increment")
     pos = cfg.prompt_len
     c1 = dataclasses.replace(cfg, batch=len(bs))
     Kc, Vc = K[bs].astype(np.float64), V[bs].astype(np.float64)
     ref = of.llama_layer(c1, Lw, x_in[bs], Kc, Vc, pos, forced_route=rte_d[bs])
-    assert rel_l2(x_out[bs], ref) < TOL
+    assert_close(x_out[bs] - x_in[bs], ref - x_in[bs], TOL, ELEM_LAYER, "layer increment")
 
 
 def test_training_step_13b_shape_sampled():
@@ -221,19 +228,22 @@ def test_training_step_13b_shape_sampled():
     # the layer on the GPU's input for one whole sequence (its own K/V, positions 0..S-1)
     ref = of.llama_layer(dataclasses.replace(c1, style="llama"), Lw, x_in[seq],
                          np.zeros((1, nH, S, 128)), np.zeros((1, nH, S, 128)), 0)
-    assert rel_l2(x_out[seq], ref) < TOL
+    assert_close(x_out[seq] - x_in[seq], ref - x_in[seq], TOL, ELEM_LAYER, "layer increment")
     labels = init.next_token_labels(init.token_ids(cfg.seed, cfg.batch, S, V)).reshape(-1)[rows]
     lse = np.log(np.exp(logits - logits.max(1, keepdims=True)).sum(1)) + logits.max(1)
     assert np.abs(losses - (lse - logits[np.arange(len(rows)), labels])).max() < 1e-4
     _, dl = ot.cross_entropy(logits, labels)
-    assert rel_l2(dlog, dl * len(rows) / T) < TOL
+    assert_close(dlog, dl * len(rows) / T, TOL, ELEM_BF16, "dlogits")
     rdq, rdk, rdv = ot.attention_backward(q, K, Vv, do)
-    for got, want in ((dq, rdq), (dK, rdk), (dV, rdv)):
-        assert rel_l2(got, want) < TOL
+    refs, bounds = attention_backward_bounds(q, K, Vv, do)
+    for name, got, want, alt, bd in zip(("dq", "dK", "dV"), (dq, dK, dV), (rdq, rdk, rdv), refs, bounds):
+        assert rel_l2(alt, want) < 1e-12                  # the bound's own recompute is the oracle's
+        e = assert_within(got, want, bd, TOL, name)
+        print(f"attention backward {name}: rel-L2 {e[0]:.2e}, max |error| / bound {e[1]:.2f}")
     for n in (0, 777, H - 1):
-        assert rel_l2(gwd[n], dxb[:, n] @ Fl) < TOL
+        assert_close(gwd[n], dxb[:, n] @ Fl, TOL, ELEM_LAYER, f"weight gradient row {n}")
     for t in (1, 8191, T - 1):
-        assert rel_l2(dF[t], dxb[t] @ Lw["wd"]) < TOL
+        assert_close(dF[t], dxb[t] @ Lw["wd"], TOL, ELEM_LAYER, f"data gradient row {t}")
     hp = dict(init.TRAIN_HP)
     p2, m2, v2 = ot.adamw(before[".master"], before[".grad"], before[".m"], before[".v"], hp["step"], hp["lr"],
                           hp["b1"], hp["b2"], hp["eps"], hp["wd"])

@@ -273,10 +273,22 @@ def test_training_step_matches_the_oracle():
     ids = init.token_ids(cfg.seed, cfg.batch, cfg.prompt_len, cfg.vocab)
     ref = ot.train_step(cfg, P, ids, init.next_token_labels(ids), state, init.TRAIN_HP, master=master)
     assert abs(loss - ref["loss"]) < 2e-3 * ref["loss"]
+    worst = {}
     for n in names:
         g = got[n]
-        assert rel_l2(g["grad"], ref["grads"][n]) < 3e-2, n
         m2, v2 = ref["state"][n]
-        assert rel_l2(g["m"], m2) < 3e-2, n
-        assert rel_l2(g["master"] - master[n], ref["params"][n] - master[n]) < 3e-2, n
+        errs = dict(grad=rel_l2(g["grad"], ref["grads"][n]), m=rel_l2(g["m"], m2), v=rel_l2(g["v"], v2),
+                    update=rel_l2(g["master"] - master[n], ref["params"][n] - master[n]),
+                    w=rel_l2(g["w"], ref["params"][n]))
+        for k, e in errs.items():
+            if e > worst.get(k, (0, ""))[0]:
+                worst[k] = (e, n)
+    print("train-small worst rel-L2:", {k: f"{e:.2e} ({n})" for k, (e, n) in worst.items()})
+    for n in names:
+        g = got[n]
+        m2, v2 = ref["state"][n]
+        assert rel_l2(g["grad"], ref["grads"][n]) < 2e-2, n
+        assert rel_l2(g["m"], m2) < 2e-2, n
+        assert rel_l2(g["v"], v2) < 2e-2, n
+        assert rel_l2(g["master"] - master[n], ref["params"][n] - master[n]) < 2e-2, n
         assert rel_l2(g["w"], ref["params"][n]) < 4e-3, n
