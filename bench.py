@@ -72,6 +72,10 @@ def parse():
     ap.add_argument("--no-baseline", action="store_true")
     ap.add_argument("--no-ablation", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-sweep", action="store_true",
+                    help="default decode line: skip the factor sweep (5/4, 3/2, 7/4, 2/1, one session)")
+    ap.add_argument("--no-prefill-leg", action="store_true",
+                    help="default decode line: skip the 1.3B prefill leg (1 cold + 4 timed passes)")
     ap.add_argument("--layers", type=int, default=0,
                     help="MoE configs: layers to run (default: as many as fit the pinned host limit)")
     ap.add_argument("--guard", type=int, default=None,
@@ -126,6 +130,59 @@ def counted_traffic(profile, source):
         return meta["traffic_bytes_per_launch"]
     except (OSError, KeyError, ValueError):
         return None
+
+
+def microbench_peaks():
+    """Same-run peaks of the three roofs, measured with PyTorch's own kernels
+    (not this package's), each after two warm-up calls, as the best of 3
+    groups of back-to-back calls timed with events: a device-to-device copy of
+    2 GiB (bytes read + written per second), a streaming read (a sum over
+    4 GiB), and a bf16 GEMM 8192 x 8192 x 8192 through torch.matmul (the
+    vendor BLAS)."""
+    import torch
+
+    def best_rate(fn, work, reps):
+        for _ in range(2):
+            fn()
+        best = 0.0
+        for _ in range(3):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            a.record()
+            for _ in range(reps):
+                fn()
+            b.record()
+            torch.cuda.synchronize()
+            best = max(best, work * reps / (a.elapsed_time(b) * 1e-3))
+        return best
+
+    out = {}
+    n = 2 << 30
+    a = torch.empty(n, dtype=torch.uint8, device="cuda")
+    b = torch.empty(n, dtype=torch.uint8, device="cuda")
+    out["hbm_copy_GBps"] = round(best_rate(lambda: b.copy_(a), 2 * n, 5) / 1e9, 1)
+    del a, b
+    x = torch.ones((1 << 30,), dtype=torch.float32, device="cuda")
+    out["hbm_read_GBps"] = round(best_rate(lambda: x.sum(), 4 * x.numel(), 5) / 1e9, 1)
+    del x
+    m = 8192
+    A = torch.randn((m, m), dtype=torch.bfloat16, device="cuda")
+    Bm = torch.randn((m, m), dtype=torch.bfloat16, device="cuda")
+    out["mfma_bf16_TFLOPs"] = round(best_rate(lambda: torch.matmul(A, Bm), 2 * m ** 3, 10) / 1e12, 1)
+    del A, Bm
+    torch.cuda.empty_cache()
+    return out
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def calibrate_copy():
@@ -278,11 +335,14 @@ def run_decode(s, w, W, K):
     first = steps[W][0]
     last = steps[W + K - 1]
     nk = last[0] + last[1] - first
+    stall0 = s.ctx.get_counters()["stall_ns"]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     s.run(first, nk)
     torch.cuda.synchronize()
-    return prefill_s, time.perf_counter() - t0, first, first + nk
+    dt = time.perf_counter() - t0
+    s.timed_stall_ns = s.ctx.get_counters()["stall_ns"] - stall0   # timing policy only
+    return prefill_s, dt, first, first + nk
 
 
 def decode_policy(s, w, M, variant, W, K, ref_gen):
@@ -367,7 +427,7 @@ def blas_info():
 
 
 def cpu_baseline_decode(cfg, w, seconds, pos, M):
-    """fp64 oracle decode of a few layers at the timed position, scaled to the model."""
+    """fp32 oracle decode of a few layers at the timed position, scaled to the model."""
     import numpy as np
     from oracle import forward as of
     from workloads import init as winit
@@ -379,11 +439,11 @@ def cpu_baseline_decode(cfg, w, seconds, pos, M):
              ("attn_norm", "wq", "wk", "wv", "wo", "ffn_norm", "wg", "wu", "wd")] + ["head", "norm_f"]
 
     def weight(nm):
-        return nm, winit.tensor_value(w, w.tensors[w.id(nm)]).astype(np.float64)
+        return nm, winit.tensor_value(w, w.tensors[w.id(nm)]).astype(np.float32)
 
     def cache(i):   # synthetic prefix of the KV cache (values do not change the timing)
         g = np.random.default_rng([7, i])
-        return g.standard_normal((B, nH, Lmax, d), dtype=np.float32).astype(np.float64) * 0.5
+        return g.standard_normal((B, nH, Lmax, d), dtype=np.float32) * np.float32(0.5)
 
     with ThreadPoolExecutor(16) as ex:
         Wt = dict(ex.map(weight, names))
@@ -391,7 +451,7 @@ def cpu_baseline_decode(cfg, w, seconds, pos, M):
     Wl = [({nm.split(".", 1)[1]: v for nm, v in Wt.items() if nm.startswith(f"L{l}.")},
            kv[2 * l], kv[2 * l + 1]) for l in range(L)]
     head, gf = Wt["head"], Wt["norm_f"]
-    x0 = np.random.default_rng(8).standard_normal((B, cfg.hidden)) * 0.02
+    x0 = (np.random.default_rng(8).standard_normal((B, cfg.hidden)) * 0.02).astype(np.float32)
     t_layers, reps = 0.0, 0
     t_start = time.perf_counter()
     while reps == 0 or time.perf_counter() - t_start < seconds:
@@ -404,10 +464,11 @@ def cpu_baseline_decode(cfg, w, seconds, pos, M):
     t = time.perf_counter()
     of.linear(of.rmsnorm(x, gf), head)
     t_head = time.perf_counter() - t
+    assert x.dtype == np.float32
     step_s = t_layers / reps / L * cfg.n_layers + t_head
     return {"value": B / step_s, "unit": "tokens/s", "cores": threads, "kind": "oracle",
-            "blas": vendor,
-            "sample": f"fp64 numpy oracle decode step at position {pos}, batch {B}: {L} of "
+            "blas": vendor, "cpu": cpu_model(), "precision": "fp32",
+            "sample": f"fp32 numpy oracle decode step at position {pos}, batch {B}: {L} of "
                       f"{cfg.n_layers} layers timed over {reps} repetitions plus the LM head, "
                       f"scaled to {cfg.n_layers} layers ({step_s:.2f} s per step)",
             "planner": planner_replay(cfg, M, 16)}
@@ -420,8 +481,8 @@ def cpu_baseline_prefill(cfg, w, seconds):
     from workloads import init as winit
     threads, vendor = blas_info()
     names = [n for n in ("L0.ln1.g", "L0.ln1.b", "L0.wqkv", "L0.wo", "L0.ln2.g", "L0.ln2.b", "L0.w1", "L0.w2")]
-    Wt = {nm: winit.tensor_value(w, w.tensors[w.id(nm)]).astype(np.float64) for nm in names}
-    x0 = np.random.default_rng(8).standard_normal((cfg.tokens, cfg.hidden)) * 0.02
+    Wt = {nm: winit.tensor_value(w, w.tensors[w.id(nm)]).astype(np.float32) for nm in names}
+    x0 = (np.random.default_rng(8).standard_normal((cfg.tokens, cfg.hidden)) * 0.02).astype(np.float32)
     reps, t_layer = 0, 0.0
     t_start = time.perf_counter()
     while reps == 0 or time.perf_counter() - t_start < seconds:
@@ -431,8 +492,8 @@ def cpu_baseline_prefill(cfg, w, seconds):
         reps += 1
     pass_s = t_layer / reps * cfg.n_layers
     return {"value": cfg.tokens / pass_s, "unit": "tokens/s", "cores": threads, "kind": "oracle",
-            "blas": vendor,
-            "sample": f"fp64 numpy oracle: 1 of {cfg.n_layers} layers over {cfg.batch} x {cfg.prompt_len} "
+            "blas": vendor, "cpu": cpu_model(), "precision": "fp32",
+            "sample": f"fp32 numpy oracle: 1 of {cfg.n_layers} layers over {cfg.batch} x {cfg.prompt_len} "
                       f"tokens timed over {reps} repetitions, scaled to {cfg.n_layers} layers (LM head "
                       f"not included; {pass_s:.1f} s per pass)"}
 
@@ -468,6 +529,7 @@ def cpu_baseline_moe(cfg, w, seconds, pos):
         reps += 1
     step_s = t_layer / reps * cfg.n_layers
     return {"value": B / step_s, "unit": "tokens/s", "cores": threads, "kind": "oracle", "blas": vendor,
+            "cpu": cpu_model(), "precision": "fp64",
             "sample": f"fp64 numpy oracle MoE decode step at position {pos}, batch {B}: 1 of "
                       f"{cfg.n_layers} layers (attention and the routed experts) timed over {reps} "
                       f"repetitions, scaled to {cfg.n_layers} layers; LM head not included "
@@ -502,7 +564,10 @@ def expert_fetches(w, sched, counts, k0, k1):
     return used, idle
 
 
-def roofline_fields(st, seconds, bl_meas, units):
+def roofline_fields(st, seconds, bl_meas, units, peaks=None):
+    """The path's roofline: max of compute, HBM and host-link times at the
+    nominal roofs; the same with the measured link; and, with same-run
+    microbenchmark peaks, the same against all three measured roofs."""
     import numpy as np
     t_comp = st["flops"] / NOMINAL["P"]
     t_hbm = st["hbm_bytes"] / NOMINAL["Bh"]
@@ -512,10 +577,15 @@ def roofline_fields(st, seconds, bl_meas, units):
     t_link = link / NOMINAL["Bl"]
     roof_s = max(t_comp, t_hbm, t_link)
     roof_meas = max(t_comp, t_hbm, link / bl_meas)
+    extra = {}
+    if peaks:
+        hbm = max(peaks["hbm_copy_GBps"], peaks["hbm_read_GBps"]) * 1e9
+        roof_peaks = max(st["flops"] / (peaks["mfma_bf16_TFLOPs"] * 1e12), st["hbm_bytes"] / hbm, link / bl_meas)
+        extra = {"frac_measured_peaks": round(roof_peaks / seconds, 4)}
     return {"bound": ["mfma", "hbm", "link"][int(np.argmax([t_comp, t_hbm, t_link]))],
             "roofline_units_per_s": round(units / roof_s, 3),
             "frac": round(roof_s / seconds, 4),
-            "frac_measured_link": round(roof_meas / seconds, 4),
+            "frac_measured_link": round(roof_meas / seconds, 4), **extra,
             "link_GBps_nominal": NOMINAL["Bl"] / 1e9, "link_GBps_measured": round(bl_meas / 1e9, 2),
             "t_mfma_ms": round(t_comp * 1e3, 3), "t_hbm_ms": round(t_hbm * 1e3, 3),
             "t_link_ms": round(t_link * 1e3, 3), "t_measured_ms": round(seconds * 1e3, 3)}
@@ -548,6 +618,8 @@ def decode_main(args, cfg):
         calibrate_copy()
     bl_meas = link_bandwidth()
     log(f"measured pinned H2D: {bl_meas / 1e9:.1f} GB/s")
+    peaks = microbench_peaks()
+    log(f"same-run peaks: {peaks}")
 
     t = time.perf_counter()
     guard = DECODE_GUARD if args.guard is None else args.guard
@@ -573,11 +645,12 @@ def decode_main(args, cfg):
         e = per_op.setdefault(w.kernels[k].tag, [0, 0.0])
         e[0] += 1
         e[1] += dur[k]
-    stall_ms = sum(gap[k] for k in range(k0 + 1, k1))
+    stall_ms = s.timed_stall_ns / 1e6          # the library's counter over the timed segment
     busy_ms = sum(dur[k] for k in range(k0, k1))
+    hbm_peak = max(peaks["hbm_copy_GBps"], peaks["hbm_read_GBps"])
 
     tok_s = cfg.batch * K / decode_s
-    pr = roofline_fields(st, decode_s, bl_meas, cfg.batch * K)
+    pr = roofline_fields(st, decode_s, bl_meas, cfg.batch * K, peaks)
     pr["roofline_tok_s"] = pr.pop("roofline_units_per_s")
     result = {
         "metric": metric("", num, den), "value": round(tok_s, 3), "unit": "tokens/s", "n_gpus": 1,
@@ -595,6 +668,7 @@ def decode_main(args, cfg):
         "roofline": {"kernel": "decode projection GEMV (M=16, bf16 matrix cores)", "bound": "hbm",
                      "achieved": round(g_achieved, 1), "peak": 8000.0, "unit": "GB/s",
                      "frac": round(g_achieved / 8000.0, 4),
+                     "frac_measured_peak": round(g_achieved / hbm_peak, 4),
                      "traffic": counted_traffic("gemv_mfma_traffic_llama7b_decode.json", "gemv.hip"),
                      "launches": len(lin), "avg_us": round(g_time / max(1, len(lin)) * 1e6, 2),
                      "avg_bytes": int(g_bytes / max(1, len(lin)))},
@@ -607,6 +681,7 @@ def decode_main(args, cfg):
                       "compute_stall_ms_per_step": round(stall_ms / K, 3),
                       "link_timeline": link_timeline(tl, K)},
         "prefill": {"seconds": round(prefill_s, 3), "tokens": cfg.batch * cfg.prompt_len},
+        "microbench": {**peaks, "link_GBps": round(bl_meas / 1e9, 2)},
         "per_kernel_ms_per_step": {k: round(v[1] / K, 4) for k, v in sorted(per_op.items())},
         "per_layer": per_layer(w, tl, segs, cfg.n_layers),
         "step_ms_per_32_steps": step_series(tl, segs),
@@ -637,19 +712,68 @@ def decode_main(args, cfg):
             "schedule_entries_changed": moved,
             "tokens_identical": bool((gm == gen_tap[: W + Bk + 1]).all() and (ga == gm).all())}
         log(f"re-planned from measured times: {result['measured_replan']}")
+    if not args.no_sweep:
+        # the same session re-budgeted at each factor: 4 untimed, 16 timed steps
+        rows = sweep_in_session(s, w, cfg, DEFAULT_SWEEP.split(","), 4, 16,
+                                0 if args.no_baseline else 4, bl_meas, guard, peaks)
+        result["factor_sweep"] = {"steps": 16, "warmup": 4, "demand_lru_steps": 0 if args.no_baseline else 4,
+                                  "rows": rows}
     s.close()
     del s
     torch.cuda.empty_cache()
 
+    if not args.no_prefill_leg:
+        from workloads import configs
+        pf = prefill_measure(configs.GPT_1P3B, 4, PREFILL_GUARD, bl_meas, peaks, baseline=not args.no_baseline,
+                             replan=False)
+        result["prefill_1p3b"] = {k: pf[k] for k in ("value", "unit", "ms_per_step", "path_roofline", "roofline",
+                                                     "attention", "transfers", "cold_pass", "no_prefetch_baseline")
+                                  if k in pf}
+        result["prefill_1p3b"]["config"] = pf["config"]
+        log(f"1.3b prefill: {pf['value']} tok/s, path frac {pf['path_roofline']['frac']}")
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline_decode(cfg, w, args.cpu_seconds, cfg.prompt_len + W, M)
     emit(args, result)
 
 
-def sweep_main(args, cfg):
-    """The decode at several oversubscription factors, one session each."""
-    import dataclasses
+DEFAULT_SWEEP = "5/4,3/2,7/4,2/1"
 
+
+def sweep_in_session(s, w, cfg, factors, W, K, Bk, bl_meas, guard, peaks=None):
+    """The decode at several oversubscription factors: the same session (host
+    arena, tensors, trace) re-budgeted for each factor and planned again; W
+    untimed and K timed steps of T+A+P each, then Bk steps of DEMAND_LRU."""
+    rows = []
+    for f in factors:
+        num, den = factor_of(f)
+        M = w.budget(num, den)
+        s.set_budget(M, plan=False)
+        s.set_policy(variant=4, timing=1, guard=guard)
+        s.restore_inputs()
+        _, decode_s, k0, k1 = run_decode(s, w, W, K)
+        segs = w.segments["decode"][W:W + K]
+        st = seg_stats(w, s.ctx.get_schedule(), s.ctx.get_classes(), M, segs)
+        gen = s.read("gen")[: W + K + 1].copy()
+        pr = roofline_fields(st, decode_s, bl_meas, cfg.batch * K, peaks)
+        row = {"factor": f"{num}/{den}", "budget_bytes": M, "value": round(cfg.batch * K / decode_s, 3),
+               "ms_per_step": round(decode_s / K * 1e3, 3), "roofline_tok_s": pr["roofline_units_per_s"],
+               "bound": pr["bound"], "frac": pr["frac"], "frac_measured_link": pr["frac_measured_link"],
+               "h2d_bytes_per_step": st["h2d_bytes"] // K, "lmin_bytes_per_step": st["lmin_bytes"] // K,
+               "h2d_over_lmin": round(st["h2d_bytes"] / max(1, st["lmin_bytes"]), 4),
+               "compute_stall_ms_per_step": round(s.timed_stall_ns / 1e6 / K, 3),
+               "link_timeline": link_timeline(s.ctx.get_timeline(), K)}
+        if Bk:
+            b = decode_policy(s, w, M, 0, W, Bk, gen)
+            row["demand_lru_value"] = b["value"]
+            row["speedup_over_demand_lru"] = round(row["value"] / b["value"], 3)
+            row["tokens_identical"] = b["tokens_identical"]
+        log(f"factor {num}/{den}: {row['value']} tok/s, frac {row['frac']}")
+        rows.append(row)
+    return rows
+
+
+def sweep_main(args, cfg):
+    """The decode at several oversubscription factors in one session."""
     import torch
 
     from paper_2609_06172_amd.session import Session
@@ -657,36 +781,14 @@ def sweep_main(args, cfg):
 
     W, K = args.warmup, (32 if args.steps is None else args.steps)
     bl_meas = link_bandwidth()
-    rows = []
-    for f in args.sweep.split(","):
-        num, den = factor_of(f)
-        c = dataclasses.replace(cfg, factor=(num, den))
-        w = trace.build(c)
-        M = w.budget()
-        s = Session(w, device=0, M=M, variant=4, timing=1,
-                    guard=DECODE_GUARD if args.guard is None else args.guard)
-        _, decode_s, k0, k1 = run_decode(s, w, W, K)
-        segs = w.segments["decode"][W:W + K]
-        st = seg_stats(w, s.ctx.get_schedule(), s.ctx.get_classes(), M, segs)
-        gen = s.read("gen")[: W + K + 1].copy()
-        pr = roofline_fields(st, decode_s, bl_meas, c.batch * K)
-        row = {"factor": f"{num}/{den}", "budget_bytes": M, "value": round(c.batch * K / decode_s, 3),
-               "ms_per_step": round(decode_s / K * 1e3, 3), "roofline_tok_s": pr["roofline_units_per_s"],
-               "bound": pr["bound"], "frac": pr["frac"], "frac_measured_link": pr["frac_measured_link"],
-               "h2d_bytes_per_step": st["h2d_bytes"] // K, "lmin_bytes_per_step": st["lmin_bytes"] // K,
-               "h2d_over_lmin": round(st["h2d_bytes"] / max(1, st["lmin_bytes"]), 4),
-               "link_timeline": link_timeline(s.ctx.get_timeline(), K)}
-        if not args.no_baseline:
-            Bk = min(args.baseline_steps, K)
-            b = decode_policy(s, w, M, 0, W, Bk, gen)
-            row["demand_lru_value"] = b["value"]
-            row["speedup_over_demand_lru"] = round(row["value"] / b["value"], 3)
-            row["tokens_identical"] = b["tokens_identical"]
-        log(f"factor {num}/{den}: {row['value']} tok/s, frac {row['frac']}")
-        rows.append(row)
-        s.close()
-        del s
-        torch.cuda.empty_cache()
+    w = trace.build(cfg)
+    guard = DECODE_GUARD if args.guard is None else args.guard
+    s = Session(w, device=0, variant=4, timing=1, guard=guard)
+    rows = sweep_in_session(s, w, cfg, args.sweep.split(","), W, K,
+                            0 if args.no_baseline else min(args.baseline_steps, K), bl_meas, guard)
+    s.close()
+    del s
+    torch.cuda.empty_cache()
     out = {"metric": "tokens/sec per oversubscription factor; fraction of max(compute,HBM,link) roofline",
            "unit": "tokens/s", "n_gpus": 1, "steps": K, "warmup": W, "higher_is_better": True,
            "dtype": "bf16", "data": "synthetic", "link_GBps_measured": round(bl_meas / 1e9, 2),
@@ -698,6 +800,24 @@ def sweep_main(args, cfg):
 
 def prefill_main(args, cfg):
     """GPT-style prefill: one cold pass, then timed passes over the same ids."""
+    if args.calibrate_copy:
+        calibrate_copy()
+    bl_meas = link_bandwidth()
+    peaks = microbench_peaks()
+    guard = PREFILL_GUARD if args.guard is None else args.guard
+    result = prefill_measure(cfg, args.iterations, guard, bl_meas, peaks, baseline=not args.no_baseline,
+                             replan=not args.no_replan)
+    result["microbench"] = peaks
+    if not args.no_cpu_baseline:
+        from workloads import trace
+        result["cpu_baseline"] = cpu_baseline_prefill(cfg, trace.build(cfg), args.cpu_seconds)
+    emit(args, result)
+
+
+def prefill_measure(cfg, I, guard, bl_meas, peaks=None, baseline=True, replan=True):
+    """One cold pass, then I timed passes over the same ids under T+A+P, with
+    the GEMM and attention rooflines; DEMAND_LRU over the same passes and the
+    measured-time re-plan on request."""
     import dataclasses
 
     import torch
@@ -706,21 +826,16 @@ def prefill_main(args, cfg):
     from workloads import trace
 
     num, den = cfg.factor
-    I = args.iterations
     cfg = dataclasses.replace(cfg, iterations=1 + I)
     w = trace.build(cfg)
     M = w.budget()
     its = w.segments["iterations"]
     log(f"workload {cfg.name}: {len(w.tensors)} tensors, {len(w.kernels)} kernels, "
         f"footprint {w.footprint} B, budget {M} B")
-    if args.calibrate_copy:
-        calibrate_copy()
-    bl_meas = link_bandwidth()
     # Prefill is compute-bound (the link idles most of a pass), so a longer
     # victim guard buys overlap with bytes the link has time for; measured on
     # the 1.3B prefill: guard 4 / 8 / 16 / 24 / 32 -> 32.8 / 31.5 / 30.4 / 30.4 /
     # 31.0 ms per pass.  The link-bound decode uses DECODE_GUARD.
-    guard = PREFILL_GUARD if args.guard is None else args.guard
     s = Session(w, device=0, M=M, variant=4, timing=1, guard=guard)
 
     def passes(sess):
@@ -750,8 +865,9 @@ def prefill_main(args, cfg):
     a_flops = sum(classes[k][2] for k in attn)
     a_time = sum(dur[k] for k in attn) * 1e-3
     tok_s = cfg.tokens * I / hot_s
-    pr = roofline_fields(st, hot_s, bl_meas, cfg.tokens * I)
+    pr = roofline_fields(st, hot_s, bl_meas, cfg.tokens * I, peaks)
     pr["roofline_tok_s"] = pr.pop("roofline_units_per_s")
+    stall_ns = s.ctx.get_counters()["stall_ns"]
     result = {
         "metric": metric("prefill ", num, den), "value": round(tok_s, 1), "unit": "tokens/s", "n_gpus": 1,
         "steps": I, "warmup": 1, "ms_per_step": round(hot_s / I * 1e3, 3), "higher_is_better": True,
@@ -765,6 +881,8 @@ def prefill_main(args, cfg):
         "roofline": {"kernel": "prefill projection GEMM (bf16 matrix cores)", "bound": "mfma",
                      "achieved": round(g_flops / g_time / 1e12, 1), "peak": 2500.0, "unit": "TFLOP/s",
                      "frac": round(g_flops / g_time / 2.5e15, 4),
+                     **({"frac_measured_peak": round(g_flops / g_time / 1e12 / peaks["mfma_bf16_TFLOPs"], 4)}
+                        if peaks else {}),
                      "traffic": counted_traffic("gemm_big_traffic_gpt1p3b_prefill.json", "gemm_big.hip"),
                      "launches": len(lin),
                      "avg_us": round(g_time / max(1, len(lin)) * 1e6, 2),
@@ -776,11 +894,12 @@ def prefill_main(args, cfg):
                       "d2h_bytes_per_pass": st["d2h_bytes"] // I,
                       "compute_busy_ms_per_pass": round(sum(dur[k] for k in range(k0, k1)) / I, 3),
                       "compute_stall_ms_per_pass": round(sum(gap[k] for k in range(k0 + 1, k1)) / I, 3),
+                      "compute_stall_ms_all_passes_counter": round(stall_ns / 1e6, 3),
                       "link_timeline": link_timeline(tl, I)},
         "cold_pass": {"seconds": round(cold_s, 4), "h2d_bytes": st0["h2d_bytes"]},
         "per_layer": per_layer(w, tl, [w.segments["iterations"][1]], cfg.n_layers),
     }
-    if not args.no_baseline:
+    if baseline:
         s.set_policy(variant=0, timing=0)
         s.ctx.reset()
         s.restore_inputs()
@@ -790,7 +909,7 @@ def prefill_main(args, cfg):
             "unit": "tokens/s", "ms_per_pass": round(hot_b / I * 1e3, 3),
             "speedup_of_T+A+P": round(hot_b / hot_s, 3),
             "logits_identical": bool((s.read("logits") == logits).all())}
-    if not args.no_replan:
+    if replan:
         def rerun():
             r = passes(s)
             return r[1], s.read("logits").copy()
@@ -806,9 +925,7 @@ def prefill_main(args, cfg):
     s.close()
     del s
     torch.cuda.empty_cache()
-    if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline_prefill(cfg, w, args.cpu_seconds)
-    emit(args, result)
+    return result
 
 
 def cpu_baseline_train(cfg, seconds):
@@ -854,6 +971,7 @@ def cpu_baseline_train(cfg, seconds):
     seq_s = t_head + (t_all - t_head + t_adam_layer) * cfg.n_layers
     step_s = seq_s * cfg.batch
     return {"value": cfg.tokens / step_s, "unit": "tokens/s", "cores": threads, "kind": "oracle", "blas": vendor,
+            "cpu": cpu_model(), "precision": "fp64",
             "sample": f"fp64 numpy oracle training step (forward, backward, AdamW) of a 1-layer model of the "
                       f"same width over one {cfg.prompt_len}-token sequence, timed over {reps} repetitions; "
                       f"the layer's share ({t_all - t_head + t_adam_layer:.2f} s) scaled to {cfg.n_layers} layers "

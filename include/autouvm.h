@@ -188,6 +188,17 @@ typedef struct {
                              window that evicts fewer bytes wins (1 = exact
                              farthest-next-use; 0 is read as 1; AUVM_POLICY_DEFAULT = 32
                              for T+A+P, 1 otherwise) */
+  uint64_t object_bytes;  /* 0 (default): tensor granularity, the method.  > 0: the same variant
+                             at the granularity of a pooling allocator's blocks, the contrast
+                             of the paper's Sec. III-B (Fig. 3): consecutive tensors in
+                             registration order share a block until the next would take it
+                             past object_bytes (a larger tensor gets its own); blocks move and
+                             are evicted whole, a fetch moves every member with a host value,
+                             a write-back every dirty member, and a block's members count as
+                             live while any access to the block remains.  The schedule lists
+                             member tensors (contiguous in the block's window);
+                             useless_prefetch_n/B count member fetches whose value no kernel
+                             reads while resident. */
 } auvm_policy;
 
 typedef struct {
@@ -218,7 +229,9 @@ typedef struct {
   uint64_t h2d_demand_n, h2d_demand_B;    /* demand fetches ("faults") */
   uint64_t d2h_wb_n, d2h_wb_B;
   uint64_t drop_n, alloc_n;
-  uint64_t useless_prefetch_n, useless_prefetch_B;
+  uint64_t useless_prefetch_n, useless_prefetch_B;   /* prefetches dropped before their kernel;
+                                             at object granularity: member fetches never read
+                                             while resident */
   uint64_t class_n[3];                    /* kernels per dynamic class */
   uint64_t plan_ns;                       /* host time of the last auvm_plan */
   uint64_t run_ns;                        /* host wall time inside auvm_run calls */
@@ -261,7 +274,12 @@ auvm_status auvm_add_kernel(auvm_ctx* ctx, const auvm_kernel_desc* desc, int32_t
 
 /* Device budget M (rounded down to 256) and the pool it is carved from.
  * device_pool == NULL: the context allocates M bytes (never in plan-only
- * contexts).  Otherwise the caller lends a device buffer of >= M bytes. */
+ * contexts).  Otherwise the caller lends a device buffer of >= M bytes.
+ * Called again, it replaces budget and pool (the oversubscription factor of
+ * the same tensors and trace): it waits for outstanding work, frees a pool
+ * the context allocated, forgets device residency as auvm_reset does and
+ * drops the plan, so read outputs first and call auvm_plan before the next
+ * run.  A borrowed old pool may be released once this returns. */
 auvm_status auvm_set_budget(auvm_ctx* ctx, uint64_t device_bytes, void* device_pool);
 /* Roofs in flop/s and byte/s (integers).  Default: 2.5e15, 8e12, 64e9. */
 auvm_status auvm_set_roofs(auvm_ctx* ctx, uint64_t peak_flops, uint64_t hbm_Bps, uint64_t link_Bps);

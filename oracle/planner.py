@@ -122,7 +122,7 @@ class Result:
 
 
 def plan(tensors, kernels, M, roofs=DEFAULT_ROOFS, variant=VAR_T_A_P, lookahead=0,
-         affinity_w=1, placement=PLACE_POOL, guard=None, bucket=None):
+         affinity_w=1, placement=PLACE_POOL, guard=None, bucket=None, object_bytes=0):
     """Replay the policy.
 
     tensors: list of dicts with keys nbytes, dtype, kind, host_init and
@@ -140,7 +140,13 @@ def plan(tensors, kernels, M, roofs=DEFAULT_ROOFS, variant=VAR_T_A_P, lookahead=
     allows it, not have been used by the ``guard`` kernels before the demand
     point, so that the moved fetch overlaps those kernels (default 4; 0 gives
     plain farthest-next-use).  The other variants are one pass.
+
+    object_bytes > 0 plans at object granularity instead (``plan_objects``).
     """
+    if object_bytes:
+        return plan_objects(tensors, kernels, M, object_bytes, roofs=roofs, variant=variant,
+                            lookahead=lookahead, affinity_w=affinity_w, placement=placement,
+                            guard=guard, bucket=bucket)
     if variant == VAR_T_A_P and placement == PLACE_IDEAL:
         raise PlanError(E_INVAL, "the full method retimes fetches into physical pool windows")
     if guard is None:
@@ -185,7 +191,7 @@ def _replay(tensors, kernels, M, roofs, variant, lookahead, affinity_w, placemen
     FB = []
     for k, kd in enumerate(kernels):
         F, B = kd.get("flops", 0), kd.get("hbm_bytes", 0)
-        if F == 0 or B == 0:
+        if (F == 0 or B == 0) and not kd.get("resolved"):
             aF, aB = kernel_cost(kd["op"], kd["shape"], kd["operands"], dtypes, raw)
             F = F or aF
             B = B or aB
@@ -536,6 +542,145 @@ def _retime(tensors, kernels, M, roofs, lookahead, base):
                             key=lambda v: where[v]):
                 evict(t, k)
             put(u, k, S_H2D_PREFETCH, u["entry"][4])
+    return res
+
+
+def pool_objects(tensors, object_bytes):
+    """Tensors grouped into the blocks of a pooling allocator: consecutive
+    tensors in registration order share a block until the next one would take
+    it past object_bytes (a larger tensor gets a block of its own).  Returns
+    the member lists."""
+    objs, cur, cur_b = [], [], 0
+    for t, td in enumerate(tensors):
+        s = aligned(td["nbytes"])
+        if cur and cur_b + s > object_bytes:
+            objs.append(cur)
+            cur, cur_b = [], 0
+        cur.append(t)
+        cur_b += s
+    if cur:
+        objs.append(cur)
+    return objs
+
+
+def plan_objects(tensors, kernels, M, object_bytes, **policy):
+    """The same policy at object granularity, the contrast of the paper's
+    Sec. III-B (Fig. 3): a prefetcher that sees allocator blocks, not tensors,
+    moves and evicts whole blocks, and cannot tell which of a block's tensors
+    are live.
+
+    The trace is coarsened: each object is one planning unit of its members'
+    bytes, valid on the host if any member is; a kernel accesses the objects
+    of its operands.  An object's first access by a kernel that only writes
+    it needs no fetch (mode W); every later access reads it (liveness is
+    unknown per member, so the whole block is live while any access
+    remains).  The object plan is then expanded to member tensors in the
+    object's window (members contiguous, in registration order): a fetch
+    moves every member with a host value (dead or alive) and allocates the
+    rest, a write-back copies every member dirty on the device, a drop drops
+    them.  A member fetch whose value no kernel reads while it stays
+    resident (evicted, overwritten or never accessed first) counts as
+    useless (useless_prefetch_n/B); classes and residency are those of the
+    object plan."""
+    objs = pool_objects(tensors, object_bytes)
+    obj_of, rel = {}, {}
+    for o, mem in enumerate(objs):
+        r = 0
+        for t in mem:
+            obj_of[t], rel[t] = o, r
+            r += aligned(tensors[t]["nbytes"])
+    valid0 = [any(tensors[t]["kind"] == KIND_PARAM or tensors[t]["host_init"] for t in mem) for mem in objs]
+    otensors = [dict(nbytes=sum(aligned(tensors[t]["nbytes"]) for t in mem), dtype=tensors[mem[0]]["dtype"],
+                     kind=KIND_PARAM if valid0[o] else tensors[mem[0]]["kind"], host_init=valid0[o],
+                     live_out=any(tensors[t].get("live_out", False) for t in mem))
+                for o, mem in enumerate(objs)]
+    dtypes = [t["dtype"] for t in tensors]
+    raw = [t["nbytes"] for t in tensors]
+    touched = [False] * len(objs)
+    okernels = []
+    for kd in kernels:
+        F, B = kd.get("flops", 0), kd.get("hbm_bytes", 0)
+        if F == 0 or B == 0:
+            aF, aB = kernel_cost(kd["op"], kd["shape"], kd["operands"], dtypes, raw)
+            F, B = F or aF, B or aB
+        modes, order = {}, []
+        for t, m in merge_operands(kd["operands"]):
+            o = obj_of[t]
+            if o not in modes:
+                order.append(o)
+                modes[o] = 0
+            modes[o] |= m
+        ops = []
+        for o in order:
+            m = modes[o]
+            if touched[o] or valid0[o]:
+                m = MODE_R | (m & MODE_W)
+            ops.append((o, m))
+            touched[o] = True
+        okernels.append(dict(op=kd["op"], shape=kd["shape"], operands=ops, flops=F, hbm_bytes=B,
+                             time_ns=kd.get("time_ns", 0), resolved=True))
+    base = plan(otensors, okernels, M, **policy)
+
+    # expansion to member tensors
+    res = Result()
+    res.static_cls, res.dyn_cls, res.costs = base.static_cls, base.dyn_cls, base.costs
+    C = res.counters
+    C["class_n"] = list(base.counters["class_n"])
+    EMPTY = 4                                   # resident, no value yet
+    val = [HOST if (t["kind"] == KIND_PARAM or t["host_init"]) else NONE for t in tensors]
+    pending = {}                                # member fetch not yet read: tensor -> bytes
+    size = [aligned(t["nbytes"]) for t in tensors]
+    resident = set()
+
+    def useless(t):
+        if t in pending:
+            C["useless_prefetch_n"] += 1
+            C["useless_prefetch_B"] += pending.pop(t)
+
+    for op_, o, off, nb, ik, nk in base.schedule:
+        if op_ == S_LAUNCH:
+            res.residency.append((ik, len(resident), sum(size[t] for t in resident)))
+            res.schedule.append((S_LAUNCH, -1, 0, 0, ik, nk))
+            for t, m in merge_operands(kernels[ik]["operands"]):
+                if (m & MODE_R) and val[t] in (NONE, EMPTY):
+                    raise PlanError(E_INVAL, f"kernel {ik} reads tensor {t} before any write")
+                if t in pending:
+                    if m & MODE_R:
+                        del pending[t]
+                    else:
+                        useless(t)
+                if m & MODE_W:
+                    val[t] = DEV_DIRTY
+            continue
+        for t in objs[o]:
+            a = off + rel[t]
+            if op_ in (S_H2D_PREFETCH, S_H2D_DEMAND, S_ALLOC):
+                resident.add(t)
+                if op_ != S_ALLOC and val[t] == HOST:
+                    res.schedule.append((op_, t, a, size[t], ik, nk))
+                    key = "h2d_prefetch" if op_ == S_H2D_PREFETCH else "h2d_demand"
+                    C[key + "_n"] += 1
+                    C[key + "_B"] += size[t]
+                    pending[t] = size[t]
+                    val[t] = DEV_CLEAN
+                else:
+                    res.schedule.append((S_ALLOC, t, a, size[t], ik, nk))
+                    C["alloc_n"] += 1
+                    val[t] = EMPTY
+            else:
+                resident.discard(t)
+                useless(t)
+                if op_ == S_D2H_WRITEBACK and val[t] == DEV_DIRTY:
+                    res.schedule.append((S_D2H_WRITEBACK, t, a, size[t], ik, -1))
+                    C["d2h_wb_n"] += 1
+                    C["d2h_wb_B"] += size[t]
+                    val[t] = HOST
+                else:
+                    res.schedule.append((S_DROP, t, a, size[t], ik, -1))
+                    C["drop_n"] += 1
+                    val[t] = HOST if val[t] == DEV_CLEAN else NONE
+    for t in list(pending):
+        useless(t)
     return res
 
 

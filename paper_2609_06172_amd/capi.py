@@ -32,7 +32,7 @@ class KernelDesc(C.Structure):
 class Policy(C.Structure):
     _fields_ = [("variant", C.c_uint32), ("lookahead", C.c_uint32), ("affinity_w", C.c_uint32),
                 ("placement", C.c_uint32), ("validate", C.c_uint32), ("timing", C.c_uint32),
-                ("guard", C.c_uint32), ("bucket", C.c_uint32)]
+                ("guard", C.c_uint32), ("bucket", C.c_uint32), ("object_bytes", C.c_uint64)]
 
 
 class SchedEntry(C.Structure):
@@ -220,10 +220,11 @@ class Context:
         self._check(self._L.auvm_set_roofs(self._h, int(peak_flops), int(hbm_Bps), int(link_Bps)))
 
     def set_policy(self, variant=4, lookahead=0, affinity_w=1, placement=0, validate=0, timing=0,
-                   guard=None, bucket=None):
+                   guard=None, bucket=None, object_bytes=0):
         """guard / bucket None: the library applies its own default for the variant."""
         p = Policy(variant, lookahead, affinity_w, placement, validate, timing,
-                   POLICY_DEFAULT if guard is None else guard, POLICY_DEFAULT if bucket is None else bucket)
+                   POLICY_DEFAULT if guard is None else guard, POLICY_DEFAULT if bucket is None else bucket,
+                   int(object_bytes))
         self._check(self._L.auvm_set_policy(self._h, C.byref(p)))
 
     def plan(self):

@@ -146,9 +146,18 @@ auvm_status auvm_add_kernel(auvm_ctx* x, const auvm_kernel_desc* d, int32_t* out
 auvm_status auvm_set_budget(auvm_ctx* x, uint64_t device_bytes, void* device_pool) {
   if (!x) return AUVM_E_INVAL;
   Ctx& c = x->c;
-  if (c.budget_set) return fail(x, AUVM_E_STATE, "budget already set");
   uint64_t M = device_bytes / kAlign * kAlign;
   if (M == 0) return fail(x, AUVM_E_INVAL, "budget below 256 bytes");
+  if (c.budget_set) {
+    // a new budget: wait for the old pool's work, forget residency and the plan
+    if (c.exec) {
+      auvm_status s = exec_reset(c);
+      if (s != AUVM_OK) return s;
+    }
+    release_pool(c);
+    c.planned = false;
+    c.budget_set = false;
+  }
   c.M = M;
   if (device_pool) {
     c.pool = static_cast<uint8_t*>(device_pool);

@@ -31,7 +31,7 @@ struct Ctx {
   bool pool_owned = false;
   bool budget_set = false;
   Roofs roofs;
-  auvm_policy pol{AUVM_T_A_P, 0, 1, AUVM_PLACE_POOL, 0, 0, 4, 32};
+  auvm_policy pol{AUVM_T_A_P, 0, 1, AUVM_PLACE_POOL, 0, 0, 4, 32, 0};
   // plan and execution
   bool planned = false;
   PlanResult plan;
@@ -55,5 +55,6 @@ const std::vector<auvm_timeline_entry>& exec_timeline(const Ctx& c);
 auvm_status host_alloc_pinned(Ctx& c, uint64_t bytes);
 auvm_status device_alloc_pool(Ctx& c, uint64_t bytes);
 void free_owned(Ctx& c);
+void release_pool(Ctx& c);   // frees an owned pool, forgets a borrowed one
 
 }  // namespace auvm

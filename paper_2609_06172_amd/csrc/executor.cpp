@@ -570,6 +570,15 @@ auvm_status device_alloc_pool(Ctx& c, uint64_t bytes) {
   return AUVM_OK;
 }
 
+void release_pool(Ctx& c) {
+  if (c.pool_owned && c.pool) {
+    if (c.device >= 0) (void)hipSetDevice(c.device);
+    (void)hipFree(c.pool);
+  }
+  c.pool = nullptr;
+  c.pool_owned = false;
+}
+
 void free_owned(Ctx& c) {
   if (c.device >= 0) (void)hipSetDevice(c.device);
   if (c.pool_owned && c.pool) (void)hipFree(c.pool);

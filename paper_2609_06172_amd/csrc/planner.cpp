@@ -584,11 +584,15 @@ PlanResult retime(const std::vector<Tensor>& T, const std::vector<Kernel>& K, co
   return R;
 }
 
+PlanResult plan_objects(const std::vector<Tensor>& T, const std::vector<Kernel>& K, uint64_t M,
+                        const Roofs& roofs, auvm_policy pol);
+
 }  // namespace
 
 PlanResult plan(const std::vector<Tensor>& T, const std::vector<Kernel>& K, uint64_t M,
                 const Roofs& roofs, const auvm_policy& pol) {
   if (pol.variant > AUVM_T_A_P) throw PlanError{AUVM_E_INVAL, "unknown policy variant"};
+  if (pol.object_bytes) return plan_objects(T, K, M, roofs, pol);
   if (pol.variant == AUVM_T_A_P && pol.placement == AUVM_PLACE_IDEAL)
     throw PlanError{AUVM_E_INVAL, "the full method retimes fetches into physical pool windows"};
   bool scan = pol.variant == AUVM_T || pol.variant == AUVM_T_A;
@@ -604,5 +608,169 @@ PlanResult plan(const std::vector<Tensor>& T, const std::vector<Kernel>& K, uint
   if (pol.variant != AUVM_T_A_P) return base;
   return retime(T, K, roofs, pol.lookahead, base);
 }
+
+namespace {
+
+// Object granularity (the contrast of Sec. III-B, Fig. 3): the policy plans
+// the allocator's blocks, then each block move is expanded to its members.
+PlanResult plan_objects(const std::vector<Tensor>& T, const std::vector<Kernel>& K, uint64_t M,
+                        const Roofs& roofs, auvm_policy pol) {
+  const uint64_t ob = pol.object_bytes;
+  pol.object_bytes = 0;
+  const size_t nT = T.size();
+  // blocks: consecutive tensors until the next would pass object_bytes
+  std::vector<std::vector<int32_t>> objs;
+  {
+    std::vector<int32_t> cur;
+    uint64_t cb = 0;
+    for (size_t t = 0; t < nT; ++t) {
+      if (!cur.empty() && cb + T[t].size > ob) {
+        objs.push_back(cur);
+        cur.clear();
+        cb = 0;
+      }
+      cur.push_back(int32_t(t));
+      cb += T[t].size;
+    }
+    if (!cur.empty()) objs.push_back(cur);
+  }
+  const size_t nO = objs.size();
+  std::vector<int32_t> obj_of(nT);
+  std::vector<uint64_t> rel(nT);
+  std::vector<Tensor> OT(nO);
+  std::vector<uint8_t> valid0(nO, 0);
+  for (size_t o = 0; o < nO; ++o) {
+    uint64_t r = 0;
+    bool out = false;
+    for (int32_t t : objs[o]) {
+      obj_of[t] = int32_t(o);
+      rel[t] = r;
+      r += T[t].size;
+      if (T[t].host_valid0()) valid0[o] = 1;
+      if (T[t].flags & AUVM_LIVE_OUT) out = true;
+    }
+    Tensor& x = OT[o];
+    x.bytes = x.size = r;
+    x.dtype = T[objs[o][0]].dtype;
+    x.kind = valid0[o] ? uint32_t(AUVM_PARAM) : T[objs[o][0]].kind;
+    x.flags = out ? uint32_t(AUVM_LIVE_OUT) : 0u;
+  }
+  // the coarse trace: a block's first access by a writing kernel needs no
+  // fetch; every later access reads the block
+  std::vector<Kernel> OK(K.size());
+  std::vector<uint8_t> touched(nO, 0);
+  for (size_t k = 0; k < K.size(); ++k) {
+    Kernel& x = OK[k];
+    x.op = K[k].op;
+    std::copy(K[k].shape, K[k].shape + 8, x.shape);
+    x.flops = K[k].flops;
+    x.hbm = K[k].hbm;
+    x.time_ns = K[k].time_ns;
+    x.layer = K[k].layer;
+    for (auto& a : K[k].acc) {
+      const int32_t o = obj_of[a.first];
+      auto it = std::find_if(x.acc.begin(), x.acc.end(), [&](const std::pair<int32_t, uint8_t>& b) {
+        return b.first == o;
+      });
+      if (it == x.acc.end())
+        x.acc.emplace_back(o, a.second);
+      else
+        it->second |= a.second;
+    }
+    for (auto& a : x.acc) {
+      if (touched[a.first] || valid0[a.first]) a.second = uint8_t(AUVM_R | (a.second & AUVM_W));
+      touched[a.first] = 1;
+    }
+  }
+  PlanResult base = plan(OT, OK, M, roofs, pol);
+
+  // expansion to member tensors, in each block's window
+  PlanResult R;
+  R.static_cls = base.static_cls;
+  R.dyn_cls = base.dyn_cls;
+  PlanCounters& C = R.counters;
+  for (int i = 0; i < 3; ++i) C.class_n[i] = base.counters.class_n[i];
+  constexpr uint8_t EMPTY = 4;   // resident, no value yet
+  std::vector<uint8_t> val(nT), res(nT, 0);
+  for (size_t t = 0; t < nT; ++t) val[t] = T[t].host_valid0() ? HOST : NONE;
+  std::vector<uint64_t> pending(nT, 0);   // bytes of a member fetch not yet read
+  int32_t n_res = 0;
+  uint64_t used = 0;
+  auto useless = [&](int32_t t) {
+    if (pending[t]) {
+      ++C.useless_prefetch_n;
+      C.useless_prefetch_B += pending[t];
+      pending[t] = 0;
+    }
+  };
+  for (const auvm_sched_entry& e : base.schedule) {
+    if (e.op == AUVM_LAUNCH) {
+      auvm_residency rr;
+      rr.k = e.issue_k;
+      rr.n_resident = n_res;
+      rr.resident_bytes = used;
+      R.residency.push_back(rr);
+      R.schedule.push_back(e);
+      for (auto& a : K[e.issue_k].acc) {
+        const int32_t t = a.first;
+        if ((a.second & AUVM_R) && (val[t] == NONE || val[t] == EMPTY))
+          throw PlanError{AUVM_E_INVAL, "kernel " + std::to_string(e.issue_k) + " reads tensor " +
+                                            std::to_string(t) + " before any write"};
+        if (pending[t]) {
+          if (a.second & AUVM_R)
+            pending[t] = 0;
+          else
+            useless(t);
+        }
+        if (a.second & AUVM_W) val[t] = DEV_DIRTY;
+      }
+      continue;
+    }
+    for (int32_t t : objs[e.tensor]) {
+      const uint64_t a = e.dev_off + rel[t];
+      const uint64_t s = T[t].size;
+      if (e.op == AUVM_H2D_PREFETCH || e.op == AUVM_H2D_DEMAND || e.op == AUVM_ALLOC) {
+        res[t] = 1;
+        ++n_res;
+        used += s;
+        if (e.op != AUVM_ALLOC && val[t] == HOST) {
+          R.schedule.push_back(entry(e.op, t, a, s, e.issue_k, e.need_k));
+          if (e.op == AUVM_H2D_PREFETCH) {
+            ++C.h2d_prefetch_n;
+            C.h2d_prefetch_B += s;
+          } else {
+            ++C.h2d_demand_n;
+            C.h2d_demand_B += s;
+          }
+          pending[t] = s;
+          val[t] = DEV_CLEAN;
+        } else {
+          R.schedule.push_back(entry(AUVM_ALLOC, t, a, s, e.issue_k, e.need_k));
+          ++C.alloc_n;
+          val[t] = EMPTY;
+        }
+      } else {
+        res[t] = 0;
+        --n_res;
+        used -= s;
+        useless(t);
+        if (e.op == AUVM_D2H_WRITEBACK && val[t] == DEV_DIRTY) {
+          R.schedule.push_back(entry(AUVM_D2H_WRITEBACK, t, a, s, e.issue_k, -1));
+          ++C.d2h_wb_n;
+          C.d2h_wb_B += s;
+          val[t] = HOST;
+        } else {
+          R.schedule.push_back(entry(AUVM_DROP, t, a, s, e.issue_k, -1));
+          ++C.drop_n;
+          val[t] = val[t] == DEV_CLEAN ? HOST : NONE;
+        }
+      }
+    }
+  }
+  for (size_t t = 0; t < nT; ++t) useless(int32_t(t));
+  return R;
+}
+
+}  // namespace
 
 }  // namespace auvm

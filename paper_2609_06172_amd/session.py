@@ -46,9 +46,21 @@ class Session:
             ctx.set_roofs(*roofs)
         self.set_policy(variant, lookahead, affinity_w, placement, validate, timing, guard, bucket)
 
+    def set_budget(self, M, plan=True):
+        """The same trace under a new device budget (a new pool); plans again
+        unless plan is False (then set_policy plans)."""
+        import torch
+        pool = torch.empty(M, dtype=torch.uint8, device=f"cuda:{self.device}")
+        self.ctx.set_budget(M, pool.data_ptr())
+        self._torch_refs = [pool]          # the old pool is idle once set_budget returned
+        self.M = M
+        if plan:
+            self.ctx.plan()
+
     def set_policy(self, variant=4, lookahead=0, affinity_w=1, placement=0, validate=0, timing=0,
-                   guard=None, bucket=None):
-        self.ctx.set_policy(variant, lookahead, affinity_w, placement, validate, timing, guard, bucket)
+                   guard=None, bucket=None, object_bytes=0):
+        self.ctx.set_policy(variant, lookahead, affinity_w, placement, validate, timing, guard, bucket,
+                            object_bytes)
         self.ctx.plan()
 
     def measured_kernel_times_ns(self):

@@ -4,7 +4,7 @@ from workloads.format import ALIGN, FLAG_HOST_INIT, FLAG_LIVE_OUT, KIND_PARAM
 
 
 def plan_ctx(tensors, kernels, M, variant=4, lookahead=0, affinity_w=1, placement=0, roofs=None,
-             guard=None, bucket=None):
+             guard=None, bucket=None, object_bytes=0):
     """Register a trace (oracle-style dicts) in a plan-only context and plan it.
 
     Kernels that carry a measured time (time_ns) hand the whole list to
@@ -26,7 +26,8 @@ def plan_ctx(tensors, kernels, M, variant=4, lookahead=0, affinity_w=1, placemen
     ctx.set_budget(M)
     if roofs is not None:
         ctx.set_roofs(*roofs)
-    ctx.set_policy(variant, lookahead, affinity_w, placement, guard=guard, bucket=bucket)
+    ctx.set_policy(variant, lookahead, affinity_w, placement, guard=guard, bucket=bucket,
+                   object_bytes=object_bytes)
     times = [k.get("time_ns", 0) for k in kernels]
     if any(times):
         ctx.set_kernel_times(times)

@@ -97,11 +97,14 @@ def test_golden_schedules_through_the_library(case):
         ops = [(t + 1, m) for t, m in k["operands"]]
         ks.append(dict(op=OP_TOUCH, shape=(0,), operands=[(0, MODE_RW)] + ops, flops=k["flops"],
                        hbm_bytes=1, time_ns=k["time_ns"]))
-    M = case["M"] + 256
+    ob = case.get("object_bytes", 0)
+    M = case["M"] + (768 if ob else 256)       # the log shares a block with a data tensor
     ctx = plan_ctx(tensors, ks, M, variant=case["variant"], affinity_w=case["affinity_w"],
-                   placement=case["placement"], guard=case.get("guard"), bucket=case.get("bucket"))
+                   placement=case["placement"], guard=case.get("guard"), bucket=case.get("bucket"),
+                   object_bytes=ob)
     r = op.plan(tensors, ks, M, variant=case["variant"], affinity_w=case["affinity_w"],
-                placement=case["placement"], guard=case.get("guard"), bucket=case.get("bucket"))
+                placement=case["placement"], guard=case.get("guard"), bucket=case.get("bucket"),
+                object_bytes=ob)
     assert_same_plan(ctx, r)
 
 
@@ -461,3 +464,47 @@ def test_the_library_applies_its_own_policy_defaults(variant):
         capi.Policy = real
     assert seen == {"guard": capi.POLICY_DEFAULT, "bucket": capi.POLICY_DEFAULT}
     assert_same_plan(ctx, ref)
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_object_granularity_bit_exact(seed):
+    """Blocks of a pooling allocator (object_bytes > 0), every variant: the
+    library's expanded member schedule, residency, classes and counters
+    (useless member fetches included) equal the oracle's, and the schedule
+    passes the checker."""
+    from oracle import checker
+    tensors, kernels = random_trace(seed, touch=True)
+    fp = sum(op.aligned(t["nbytes"]) for t in tensors)
+    rnd = random.Random(9000 + seed)
+    for variant in VARIANTS:
+        ob = rnd.choice([512, 2048, 4096, 16384])
+        for num, den in ((1, 1), (5, 6), (3, 4), (2, 3)):
+            M = max(1024, fp * num // den // 256 * 256)
+            try:
+                r = op.plan(tensors, kernels, M, variant=variant, object_bytes=ob)
+            except op.PlanError as e:
+                with pytest.raises(AuvmError) as x:
+                    plan_ctx(tensors, kernels, M, variant=variant, object_bytes=ob)
+                assert x.value.code == e.code
+                continue
+            checker.check(tensors, kernels, M, r.schedule)
+            assert_same_plan(plan_ctx(tensors, kernels, M, variant=variant, object_bytes=ob), r)
+
+
+@pytest.mark.parametrize("name", ["llama-small", "gpt-small", "moe-small", "train-small"])
+def test_object_granularity_config_traces(name):
+    from oracle import checker
+    cfg = configs.CONFIGS[name]
+    w = trace.build(cfg)
+    tensors = [dict(nbytes=t.nbytes, dtype=t.dtype, kind=t.kind, host_init=t.host_init, live_out=t.live_out)
+               for t in w.tensors]
+    kernels = [dict(op=k.op, shape=k.shape, operands=k.operands) for k in w.kernels]
+    ob = 1 << 20
+    try:
+        r = op.plan(tensors, kernels, w.budget(), object_bytes=ob)
+    except op.PlanError:
+        r = None
+    if r is None:
+        pytest.skip("blocks do not fit the budget")
+    checker.check(tensors, kernels, w.budget(), r.schedule)
+    assert_same_plan(plan_ctx(tensors, kernels, w.budget(), object_bytes=ob), r)

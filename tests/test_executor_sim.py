@@ -206,3 +206,46 @@ def test_dropping_the_event_waits_is_caught():
         assert failures > 0
     finally:
         L.auvm_sim_drop_waits(0)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_a_new_budget_replans_the_same_trace(seed):
+    """set_budget again on a context that has run: the plan at the new budget
+    is the oracle's, and a rerun from the first kernel reads exact versions
+    (read-only data, so the host contents the rerun starts from are intact)."""
+    from paper_2609_06172_amd.capi import Context
+    L = sim_library()
+    tensors, kernels = random_trace(seed, touch=True, n_kernels=70, read_only=True)
+    fp = sum(op.aligned(t["nbytes"]) for t in tensors)
+    w = Workload(None)
+    for i, t in enumerate(tensors):
+        w.tensor(f"t{i}", (t["nbytes"],), t["dtype"], t["kind"], host_init=t["host_init"])
+    ctx = Context(0, library=L)
+    ctx.arena_init(w.arena_bytes)
+    for t in w.tensors:
+        ctx.register_tensor(t.off, t.nbytes, t.dtype, t.kind, t.flags)
+    init = {}
+    for i, t in enumerate(tensors):
+        view = np.ctypeslib.as_array((C.c_uint8 * t["nbytes"]).from_address(ctx.tensor_host_ptr(i)))
+        if i == 0:
+            view[:] = 0
+        else:
+            init[i] = 1000 + i
+            view[:] = np.full(t["nbytes"] // 4, init[i], np.uint32).view(np.uint8)
+    for k in kernels:
+        ctx.add_kernel(k["op"], k["shape"], k["operands"], flops=k["flops"], hbm_bytes=k["hbm_bytes"])
+    budgets = [fp // 256 * 256, feasible_budget(tensors, kernels, 4)]
+    for i, M in enumerate(budgets):
+        ctx.set_budget(M)
+        ctx.set_policy(4, validate=1)
+        ctx.plan()
+        assert ctx.get_schedule() == op.plan(tensors, kernels, M).schedule
+        L.auvm_sim_seed(seed + i)
+        ctx.run(0, len(kernels))
+        logbuf = np.empty(tensors[0]["nbytes"], np.uint8)
+        ctx.read_tensor(0, logbuf.ctypes.data, logbuf.nbytes)
+        log = logbuf.view(np.uint32).reshape(-1, 16)
+        bad = [(s, j, v) for s, j, v in touch_expectations(tensors, kernels, init)
+               if log[s, 2 * j] != v or log[s, 2 * j + 1] != v]
+        assert not bad, (M, bad[:4])
+    ctx.destroy()

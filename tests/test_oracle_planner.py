@@ -26,7 +26,7 @@ def test_golden_schedules(case):
     tensors, kernels = golden_inputs(case)
     r = op.plan(tensors, kernels, case["M"], variant=case["variant"],
                 affinity_w=case["affinity_w"], placement=case["placement"], guard=case.get("guard"),
-                bucket=case.get("bucket"))
+                bucket=case.get("bucket"), object_bytes=case.get("object_bytes", 0))
     assert [list(e) for e in r.schedule] == case["schedule"]
     if "residency" in case:
         assert [list(e) for e in r.residency] == case["residency"]
