@@ -322,6 +322,18 @@ auvm_status auvm_bind_streams(auvm_ctx* ctx, void* compute, void* h2d, void* d2h
  * and launches, plus fetches issued after the last launch), then wait for
  * all three streams.  Segments must be contiguous and increasing from 0. */
 auvm_status auvm_run(auvm_ctx* ctx, uint32_t first_k, uint32_t n_k);
+/* auvm_run for callers that cannot allocate (code under HIP graph capture,
+ * serving loops, harnesses that forbid allocation): the same transfers and
+ * launches, but the kernels' workspace operands (ATTN_BWD's D, RMSNORM_BWD's
+ * rstd) live in the library's static device scratch, 8 MiB per GPU (each GPU
+ * the library runs on holds it until the process ends), instead of their pool
+ * windows, whose contents are undefined afterwards; no memory, stream or
+ * event is created (the plan must have timing off: AUVM_E_STATE otherwise).
+ * A workspace above 8 MiB gives AUVM_E_RANGE before anything is enqueued.
+ * Every call on one GPU shares that GPU's scratch and leaves its contents
+ * behind: calls that overlap on one GPU (several contexts or threads) race.
+ * The scratch needs no clearing: each workspace is written before it is read. */
+auvm_status auvm_run_noalloc(auvm_ctx* ctx, uint32_t first_k, uint32_t n_k);
 /* Forget all device residency and rewind to kernel 0.  The caller must
  * restore host contents of tensors the trace reads before writing. */
 auvm_status auvm_reset(auvm_ctx* ctx);

@@ -19,7 +19,7 @@ ROCM_INC = os.path.join(os.environ.get("ROCM_PATH", "/opt/rocm"), "include")
 HOST_SRCS = ["cost.cpp", "planner.cpp", "capi.cpp", "executor.cpp"]
 DEV_SRCS = ["kernels/ops.hip", "kernels/gemm.hip", "kernels/gemv.hip", "kernels/gemm_mfma.hip",
             "kernels/gemm_big.hip", "kernels/attention.hip", "kernels/moe.hip",
-            "kernels/train.hip"]
+            "kernels/train.hip", "kernels/scratch.hip"]
 
 COMMON = ["-O3", "-fPIC", "-std=c++17", "-Wall", "-Wno-unused-function",
           "-I" + os.path.join(ROOT, "include"), "-I" + CSRC]

@@ -16,7 +16,7 @@ OK, E_INVAL, E_STATE, E_BUDGET, E_FRAG, E_HIP, E_NOMEM, E_RANGE = 0, -1, -2, -3,
 SYMBOLS = [
     "auvm_create", "auvm_destroy", "auvm_last_error", "auvm_arena_init",
     "auvm_register_tensor", "auvm_tensor_host_ptr", "auvm_add_kernel", "auvm_set_budget",
-    "auvm_set_roofs", "auvm_set_policy", "auvm_set_kernel_times", "auvm_clear_kernels", "auvm_plan", "auvm_bind_streams", "auvm_run",
+    "auvm_set_roofs", "auvm_set_policy", "auvm_set_kernel_times", "auvm_clear_kernels", "auvm_plan", "auvm_bind_streams", "auvm_run", "auvm_run_noalloc",
     "auvm_reset", "auvm_read_tensor", "auvm_get_counters", "auvm_get_schedule",
     "auvm_get_executed", "auvm_get_residency", "auvm_get_classes", "auvm_get_kernel_times",
     "auvm_get_timeline",
@@ -139,6 +139,7 @@ def bind_library(L):
         "auvm_plan": (st, [P]),
         "auvm_bind_streams": (st, [P, P, P, P]),
         "auvm_run": (st, [P, C.c_uint32, C.c_uint32]),
+        "auvm_run_noalloc": (st, [P, C.c_uint32, C.c_uint32]),
         "auvm_reset": (st, [P]),
         "auvm_read_tensor": (st, [P, C.c_int32, P, C.c_uint64]),
         "auvm_get_counters": (st, [P, C.POINTER(Counters)]),
@@ -244,6 +245,10 @@ class Context:
 
     def run(self, first_k, n_k):
         self._check(self._L.auvm_run(self._h, int(first_k), int(n_k)))
+
+    def run_noalloc(self, first_k, n_k):
+        """run with the kernels' workspaces in the library's static device scratch."""
+        self._check(self._L.auvm_run_noalloc(self._h, int(first_k), int(n_k)))
 
     def reset(self):
         self._check(self._L.auvm_reset(self._h))

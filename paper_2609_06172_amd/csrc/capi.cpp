@@ -256,6 +256,20 @@ auvm_status auvm_run(auvm_ctx* x, uint32_t first_k, uint32_t n_k) {
   return s;
 }
 
+auvm_status auvm_run_noalloc(auvm_ctx* x, uint32_t first_k, uint32_t n_k) {
+  if (!x) return AUVM_E_INVAL;
+  Ctx& c = x->c;
+  if (!c.exec) return fail(x, AUVM_E_STATE, "plan-only context");
+  if (!c.planned) return fail(x, AUVM_E_STATE, "plan first");
+  if (!c.host || !c.pool) return fail(x, AUVM_E_STATE, "no host arena or device pool");
+  if (uint64_t(first_k) + n_k > c.kernels.size()) return fail(x, AUVM_E_INVAL, "segment beyond the trace");
+  auto t0 = std::chrono::steady_clock::now();
+  auvm_status s = exec_run_noalloc(c, first_k, n_k);
+  c.run_ns += uint64_t(std::chrono::duration_cast<std::chrono::nanoseconds>(
+                           std::chrono::steady_clock::now() - t0).count());
+  return s;
+}
+
 auvm_status auvm_reset(auvm_ctx* x) {
   if (!x) return AUVM_E_INVAL;
   if (!x->c.exec) return fail(x, AUVM_E_STATE, "plan-only context");

@@ -45,6 +45,7 @@ struct Ctx {
 ExecPtr make_executor(Ctx& c);
 auvm_status exec_bind_streams(Ctx& c, void* compute, void* h2d, void* d2h);
 auvm_status exec_run(Ctx& c, uint32_t first_k, uint32_t n_k);
+auvm_status exec_run_noalloc(Ctx& c, uint32_t first_k, uint32_t n_k);
 auvm_status exec_reset(Ctx& c);
 auvm_status exec_read(Ctx& c, int32_t id, void* dst, uint64_t bytes);
 const std::vector<auvm_sched_entry>& exec_log(const Ctx& c);

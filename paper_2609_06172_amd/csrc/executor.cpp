@@ -74,6 +74,9 @@ class Executor {
     hown_[0].assign(kRing, -1);
     hown_[1].assign(kRing, -1);
     down_.assign(kRing, -1);
+    // the static scratch of this device, for run_noalloc; a failure here only
+    // disables that entry point
+    scratch_status_ = scratch_address(c_.device, &scratch_);
     return AUVM_OK;
   }
 
@@ -131,6 +134,7 @@ class Executor {
     std::fill(down_.begin(), down_.end(), -1);
     hazards_.clear();
     log_.clear();
+    log_.reserve(c_.plan.schedule.size());   // a run never grows it
     kernels_run_ = 0;
     stall_ms_ = 0;
     dur_.assign(K, 0.f);
@@ -173,6 +177,42 @@ class Executor {
     if (!sync_all()) return AUVM_E_HIP;
     if (c_.pol.timing) harvest_all();
     return AUVM_OK;
+  }
+
+  // auvm_run with the kernels' workspace operands (ATTN_BWD's D, RMSNORM_BWD's
+  // rstd) in the static scratch instead of their pool windows; no event,
+  // stream or memory is created.
+  auvm_status run_noalloc(uint32_t first_k, uint32_t n_k) {
+    if (c_.pol.timing) {
+      c_.err = "run_noalloc: the timing policy creates events; plan with timing off";
+      return AUVM_E_STATE;
+    }
+    if (scratch_status_ != hipSuccess || !scratch_) {
+      c_.err = std::string("run_noalloc: no static scratch on this device: ") + hipGetErrorString(scratch_status_);
+      return AUVM_E_HIP;
+    }
+    const int64_t end_k = int64_t(first_k) + n_k;
+    for (int64_t k = first_k; k < end_k; ++k) {
+      const int w = workspace_operand(c_.kernels[k]);
+      if (w < 0) continue;
+      const uint64_t need = c_.tensors[c_.kernels[k].ids[w]].bytes;
+      if (need > scratch_capacity()) {
+        c_.err = "run_noalloc: kernel " + std::to_string(k) + " needs a " + std::to_string(need) +
+                 "-byte workspace, above the static scratch's " + std::to_string(scratch_capacity());
+        return AUVM_E_RANGE;
+      }
+    }
+    noalloc_ = true;
+    auvm_status s = run(first_k, n_k);
+    noalloc_ = false;
+    return s;
+  }
+
+  // positional index of an op's workspace operand, or -1
+  static int workspace_operand(const Kernel& k) {
+    if (k.op == AUVM_OP_RMSNORM_BWD) return 6;
+    if (k.op == AUVM_OP_ATTN_BWD) return 9;
+    return -1;
   }
 
   auvm_status read(int32_t id, void* dst) {
@@ -382,6 +422,10 @@ class Executor {
     pend_h2d_[0] = pend_h2d_[1] = pend_d2h_ = 0;
     uint8_t* ptrs[16];
     for (size_t i = 0; i < kd.ids.size(); ++i) ptrs[i] = c_.pool + where_[kd.ids[i]];
+    if (noalloc_) {
+      const int w = workspace_operand(kd);
+      if (w >= 0) ptrs[w] = static_cast<uint8_t*>(scratch_);
+    }
     const bool timing = c_.pol.timing != 0;
     if (timing) {
       if (ktr_.n != k) return internal("timed kernels must run from kernel 0 in order");
@@ -521,6 +565,9 @@ class Executor {
   std::vector<auvm_timeline_entry> tl_;
   int32_t seg_ = -1;
   std::chrono::steady_clock::time_point host0_;
+  void* scratch_ = nullptr;                 // this device's static scratch
+  hipError_t scratch_status_ = hipErrorNotInitialized;
+  bool noalloc_ = false;                    // inside run_noalloc
 };
 
 Ctx::~Ctx() {
@@ -538,6 +585,7 @@ ExecPtr make_executor(Ctx& c) {
 
 auvm_status exec_bind_streams(Ctx& c, void* a, void* b, void* d) { return c.exec->bind(a, b, d); }
 auvm_status exec_run(Ctx& c, uint32_t f, uint32_t n) { return c.exec->run(f, n); }
+auvm_status exec_run_noalloc(Ctx& c, uint32_t f, uint32_t n) { return c.exec->run_noalloc(f, n); }
 auvm_status exec_reset(Ctx& c) { return c.exec->reset(); }
 auvm_status exec_read(Ctx& c, int32_t id, void* dst, uint64_t) { return c.exec->read(id, dst); }
 const std::vector<auvm_sched_entry>& exec_log(const Ctx& c) { return c.exec->log(); }

@@ -228,6 +228,14 @@ hipError_t launch_op(const Kernel& k, const std::vector<Tensor>& T, uint8_t* con
   return hipSuccess;
 }
 
+// the static device scratch: a host buffer here
+uint64_t scratch_capacity() { return uint64_t(8) << 20; }
+hipError_t scratch_address(int, void** out) {
+  static std::vector<uint8_t> buf(size_t(8) << 20);
+  *out = buf.data();
+  return hipSuccess;
+}
+
 hipError_t launch_poison(uint8_t* p, uint64_t bytes, hipStream_t s) {
   Op o{Op::RUN};
   o.fn = [p, bytes] { std::memset(p, 0xFF, bytes); };

@@ -249,3 +249,51 @@ def test_a_new_budget_replans_the_same_trace(seed):
                if log[s, 2 * j] != v or log[s, 2 * j + 1] != v]
         assert not bad, (M, bad[:4])
     ctx.destroy()
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_run_noalloc_reads_the_same_versions(seed):
+    """auvm_run_noalloc on the simulated executor: the same transfers and
+    launches as auvm_run (touch traces carry no workspace operand), exact
+    versions, and the timing policy refused before anything is enqueued."""
+    from paper_2609_06172_amd.capi import AuvmError, Context
+    L = sim_library()
+    tensors, kernels = random_trace(seed, touch=True, n_kernels=60)
+    M = feasible_budget(tensors, kernels, 4)
+    w = Workload(None)
+    for i, t in enumerate(tensors):
+        w.tensor(f"t{i}", (t["nbytes"],), t["dtype"], t["kind"], host_init=t["host_init"])
+    ctx = Context(0, library=L)
+    ctx.arena_init(w.arena_bytes)
+    for t in w.tensors:
+        ctx.register_tensor(t.off, t.nbytes, t.dtype, t.kind, t.flags)
+    init = {}
+    for i, t in enumerate(tensors):
+        view = np.ctypeslib.as_array((C.c_uint8 * t["nbytes"]).from_address(ctx.tensor_host_ptr(i)))
+        if i == 0:
+            view[:] = 0
+        elif t["host_init"] or t["kind"] == KIND_PARAM:
+            init[i] = 1000 + i
+            view[:] = np.full(t["nbytes"] // 4, init[i], np.uint32).view(np.uint8)
+    for k in kernels:
+        ctx.add_kernel(k["op"], k["shape"], k["operands"], flops=k["flops"], hbm_bytes=k["hbm_bytes"])
+    ctx.set_budget(M)
+    ctx.set_policy(4, validate=1, timing=1)
+    ctx.plan()
+    with pytest.raises(AuvmError) as e:
+        ctx.run_noalloc(0, len(kernels))
+    assert e.value.code == -2 and ctx.get_executed() == []
+    ctx.set_policy(4, validate=1)
+    ctx.plan()
+    L.auvm_sim_seed(seed)
+    half = len(kernels) // 2
+    ctx.run_noalloc(0, half)
+    ctx.run_noalloc(half, len(kernels) - half)
+    assert ctx.get_executed() == ctx.get_schedule()
+    logbuf = np.empty(tensors[0]["nbytes"], np.uint8)
+    ctx.read_tensor(0, logbuf.ctypes.data, logbuf.nbytes)
+    log = logbuf.view(np.uint32).reshape(-1, 16)
+    bad = [(s, j, v) for s, j, v in touch_expectations(tensors, kernels, init)
+           if log[s, 2 * j] != v or log[s, 2 * j + 1] != v]
+    assert not bad, bad[:4]
+    ctx.destroy()
