@@ -345,9 +345,9 @@ def run_decode(s, w, W, K):
     return prefill_s, dt, first, first + nk
 
 
-def decode_policy(s, w, M, variant, W, K, ref_gen):
+def decode_policy(s, w, M, variant, W, K, ref_gen, object_bytes=0, guard=None):
     """Rerun the decode under another policy (timing off) and summarise it."""
-    s.set_policy(variant=variant, timing=0)
+    s.set_policy(variant=variant, timing=0, object_bytes=object_bytes, guard=guard)
     s.ctx.reset()
     s.restore_inputs()
     pb, db, _, _ = run_decode(s, w, W, K)
@@ -359,6 +359,38 @@ def decode_policy(s, w, M, variant, W, K, ref_gen):
             "h2d_bytes_per_step": st["h2d_bytes"] // K, "d2h_bytes_per_step": st["d2h_bytes"] // K,
             "demand_fetches_per_step": round(st["demand_fetches"] / K, 2),
             "tokens_identical": bool((gen == ref_gen[: W + K + 1]).all())}
+
+
+def plan_only_sweeps(s, w, M, segs, guard):
+    """Plans of the same session, not run: host-to-device bytes per timed step
+    for T+A at several affinity windows, and for T+A+P on allocator blocks
+    of several sizes, with the useless and useful fetched bytes of the whole
+    plan (member fetches no kernel reads while resident, and the rest)."""
+    a, n = segs[0][0], segs[-1][0] + segs[-1][1] - segs[0][0]
+    K = len(segs)
+
+    def step_bytes():
+        sched = s.ctx.get_schedule()
+        return sum(e[3] for e in sched if e[0] in (0, 1) and a <= e[4] < a + n) // K
+
+    out = {"affinity_window": [], "allocator_blocks": []}
+    for Wa in (1, 4, 16, 64):
+        s.set_policy(variant=3, affinity_w=Wa)
+        out["affinity_window"].append({"policy": "T+A", "W": Wa, "h2d_bytes_per_step": step_bytes()})
+    for ob in (0, 64 << 20, 256 << 20, 1 << 30):
+        try:
+            s.set_policy(variant=4, guard=guard, object_bytes=ob)
+        except Exception as e:       # blocks that do not fit the budget
+            out["allocator_blocks"].append({"object_bytes": ob, "error": str(e)})
+            continue
+        c = s.ctx.get_counters()
+        fetched = c["h2d_prefetch_B"] + c["h2d_demand_B"]
+        out["allocator_blocks"].append({
+            "object_bytes": ob, "h2d_bytes_per_step": step_bytes(),
+            "useless_fetched_bytes": c["useless_prefetch_B"] if ob else 0,
+            "useful_fetched_bytes": fetched - (c["useless_prefetch_B"] if ob else 0)})
+    s.set_policy(variant=4, timing=0, guard=guard)
+    return out
 
 
 def measured_replan(s, w, dur, guard, rerun):
@@ -696,7 +728,18 @@ def decode_main(args, cfg):
         log(f"baseline {Bk} steps {Bk / b['value'] * cfg.batch:.3f} s")
         if not args.no_ablation:
             result["ablation"] = [decode_policy(s, w, M, v, W, Bk, gen_tap) for v in (1, 2, 3)]
+            # the object-level contrast: the full method on 1 GiB allocator blocks
+            ob = 1 << 30
+            row = decode_policy(s, w, M, 4, W, Bk, gen_tap, object_bytes=ob, guard=guard)
+            c = s.ctx.get_counters()
+            fetched = c["h2d_prefetch_B"] + c["h2d_demand_B"]
+            row.update(policy="T+A+P on 1 GiB allocator blocks", object_bytes=ob,
+                       useless_to_useful_fetched_bytes=round(c["useless_prefetch_B"] /
+                                                             max(1, fetched - c["useless_prefetch_B"]), 4),
+                       speedup_of_tensor_granularity=round(tok_s / row["value"], 3))
+            result["ablation"].append(row)
             log("ablation: " + ", ".join(f"{a['policy']} {a['value']}" for a in result["ablation"]))
+            result["plan_only"] = plan_only_sweeps(s, w, M, segs, guard)
     if not args.no_replan:
         Bk = min(args.baseline_steps, K)
 

@@ -20,7 +20,8 @@ NP_DTYPE = {DT_F32: np.float32, DT_I32: np.int32, DT_U8: np.uint8, DT_BF16: np.u
 
 class Session:
     def __init__(self, w, device=-1, M=None, variant=4, lookahead=0, affinity_w=1, placement=0,
-                 validate=0, timing=0, roofs=None, fill=True, threads=16, guard=None, bucket=None):
+                 validate=0, timing=0, roofs=None, fill=True, threads=16, guard=None, bucket=None,
+                 object_bytes=0):
         self.w = w
         self.device = device
         self.ctx = Context(device)
@@ -44,7 +45,8 @@ class Session:
             ctx.set_budget(self.M)
         if roofs is not None:
             ctx.set_roofs(*roofs)
-        self.set_policy(variant, lookahead, affinity_w, placement, validate, timing, guard, bucket)
+        self.set_policy(variant, lookahead, affinity_w, placement, validate, timing, guard, bucket,
+                        object_bytes)
 
     def set_budget(self, M, plan=True):
         """The same trace under a new device budget (a new pool); plans again

@@ -42,26 +42,27 @@ def sim_library():
     return _SIM["L"]
 
 
-def feasible_budget(tensors, kernels, variant, fracs=((1, 2), (2, 3), (3, 4), (5, 6), (1, 1))):
+def feasible_budget(tensors, kernels, variant, fracs=((1, 2), (2, 3), (3, 4), (5, 6), (1, 1)), object_bytes=0):
     fp = sum(op.aligned(t["nbytes"]) for t in tensors)
     for num, den in fracs:
         M = max(1024, fp * num // den // 256 * 256)
         try:
-            op.plan(tensors, kernels, M, variant=variant)
+            op.plan(tensors, kernels, M, variant=variant, object_bytes=object_bytes)
             return M
         except op.PlanError:
             continue
     raise AssertionError("no feasible budget")
 
 
-def run_touch_trace(seed, variant, order_seed, cuts=3, read_only=False, bind=None, timing=0, out=None):
+def run_touch_trace(seed, variant, order_seed, cuts=3, read_only=False, bind=None, timing=0, out=None,
+                    object_bytes=0):
     """Runs a random touch trace on the simulated executor; returns (executed log
     equals the plan, reads that saw the wrong version)."""
     from paper_2609_06172_amd.capi import Context
     L = sim_library()
     n_kernels = (60 if read_only else 40) + (seed * 7) % 60
     tensors, kernels = random_trace(seed, touch=True, n_kernels=n_kernels, read_only=read_only)
-    M = feasible_budget(tensors, kernels, variant)
+    M = feasible_budget(tensors, kernels, variant, object_bytes=object_bytes)
     w = Workload(None)
     for i, t in enumerate(tensors):
         w.tensor(f"t{i}", (t["nbytes"],), t["dtype"], t["kind"], host_init=t["host_init"])
@@ -80,7 +81,7 @@ def run_touch_trace(seed, variant, order_seed, cuts=3, read_only=False, bind=Non
     for k in kernels:
         ctx.add_kernel(k["op"], k["shape"], k["operands"])
     ctx.set_budget(M)
-    ctx.set_policy(variant, validate=1, timing=timing)
+    ctx.set_policy(variant, validate=1, timing=timing, object_bytes=object_bytes)
     ctx.plan()
     if bind is not None:
         ctx.bind_streams(*bind)
@@ -297,3 +298,16 @@ def test_run_noalloc_reads_the_same_versions(seed):
            if log[s, 2 * j] != v or log[s, 2 * j + 1] != v]
     assert not bad, bad[:4]
     ctx.destroy()
+
+
+@pytest.mark.parametrize("variant", [0, 1, 4])
+@pytest.mark.parametrize("seed", range(6))
+def test_object_plans_read_latest_versions(seed, variant):
+    """Plans at object granularity (whole allocator blocks moved, members
+    allocated or written back together) run on the executor unchanged and
+    read exact versions in any allowed order."""
+    for order_seed in range(3):
+        executed_ok, bad = run_touch_trace(seed, variant, order_seed, cuts=1 + order_seed,
+                                           object_bytes=(1024, 4096, 16384)[order_seed])
+        assert executed_ok
+        assert not bad, (seed, variant, order_seed, bad[:4])

@@ -116,6 +116,45 @@ def test_outputs_do_not_depend_on_the_budget():
             assert np.array_equal(a, b)
 
 
+def test_object_granularity_moves_more_and_computes_the_same():
+    # whole allocator blocks (1 MiB, registration order) instead of tensors:
+    # the same kernels on the same values, so logits and tokens are
+    # bit-identical, while the link carries more bytes, part of them members
+    # no kernel reads while they are resident
+    cfg = configs.LLAMA_SMALL
+    print("llama-small at 1.5x: tensors, then 1 MiB allocator blocks", flush=True)
+    _, lt, gt, ct, ok_t = _llama_run(cfg, validate=1)
+    _, lo, go, co, ok_o = _llama_run(cfg, validate=1, object_bytes=1 << 20)
+    assert ok_t and ok_o
+    assert np.array_equal(go, gt)
+    for a, b in zip(lo, lt):
+        assert np.array_equal(a, b)
+    moved = lambda c: c["h2d_prefetch_B"] + c["h2d_demand_B"]
+    assert moved(co) > moved(ct) and co["useless_prefetch_B"] > 0
+
+
+def test_training_step_at_object_granularity():
+    # a whole train-small step at 2x with 4 MiB blocks: dirty members of
+    # evicted blocks are written back, and every gradient, moment, master and
+    # weight equals the tensor-granular step's bit for bit
+    from paper_2609_06172_amd.session import Session
+    cfg = configs.TRAIN_SMALL
+    w = trace.build(cfg, keep_grads=True)
+    names = init.param_names(w)
+    outs, counters = [], []
+    for ob in (0, 4 << 20):
+        print(f"train-small at 2x, object_bytes {ob}", flush=True)
+        s = Session(w, device=0, validate=1, object_bytes=ob)
+        s.run_all()
+        assert s.ctx.get_executed() == s.ctx.get_schedule()
+        outs.append({n + x: s.read(n + x) for n in names for x in (".grad", ".master", ".m", ".v", "")})
+        counters.append(s.ctx.get_counters())
+        s.close()
+    for k in outs[0]:
+        assert outs[1][k].tobytes() == outs[0][k].tobytes(), k
+    assert counters[1]["d2h_wb_n"] > 0 and counters[1]["useless_prefetch_B"] > 0
+
+
 def test_grouped_qkv_launch_matches_separate_projections():
     # LINEAR_QKV computes each projection exactly as its own LINEAR does, so
     # the two traces give bit-identical logits and tokens (at 1.5x)
