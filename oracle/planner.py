@@ -54,7 +54,7 @@ Integer arithmetic only; no state outside the function.  Slow and plain.
 from bisect import bisect_left, bisect_right
 
 from workloads.format import (ALIGN, CLS_CGI, CLS_COMPUTE, CLS_MEMORY,
-                              KIND_PARAM, MODE_R, MODE_W, PLACE_IDEAL,
+                              KIND_KV, KIND_PARAM, MODE_R, MODE_W, PLACE_IDEAL,
                               PLACE_POOL, S_ALLOC, S_D2H_WRITEBACK, S_DROP,
                               S_H2D_DEMAND, S_H2D_PREFETCH, S_LAUNCH,
                               VAR_DEMAND_BELADY, VAR_DEMAND_LRU, VAR_T,
@@ -241,8 +241,12 @@ def _replay(tensors, kernels, M, roofs, variant, lookahead, affinity_w, placemen
     def writes_back(u, kp):
         return val[u] == DEV_DIRTY and (variant == VAR_DEMAND_LRU or live(u, kp))
 
-    def place(t, eligible, kp):
-        """Returns (offset, victims) or None."""
+    def place(t, eligible, kp, top=False):
+        """Returns (offset, victims) or None.  top: a first write of a
+        KV-cache tensor, which also tries the windows flush against the
+        pool's end and against the start of every resident tensor, and takes
+        a free window at the highest address (the long-lived cache packs at
+        the top of the pool, with no holes between its tensors)."""
         s = size[t]
         if placement == PLACE_IDEAL:
             if M - used_bytes[0] >= s:
@@ -265,7 +269,12 @@ def _replay(tensors, kernels, M, roofs, variant, lookahead, affinity_w, placemen
         spans = sorted((o, o + size[u], u) for u, o in off.items())
         starts_ = [sp[0] for sp in spans]
         ends_ = [sp[1] for sp in spans]
-        cand_starts = sorted(set([0] + ends_))
+        cands = set([0] + ends_)
+        if top:
+            cands |= set(o - s for o in starts_ if o >= s)
+            if M >= s:
+                cands.add(M - s)
+        cand_starts = sorted(cands)
         best, best_key = None, None
         for a in cand_starts:
             if a + s > M:
@@ -278,7 +287,9 @@ def _replay(tensors, kernels, M, roofs, variant, lookahead, affinity_w, placemen
             minpr = min((prio(u, kp) for u in over), default=INF)
             wb = sum(size[u] for u in over if writes_back(u, kp))
             vb = sum(size[u] for u in over)
-            if belady:
+            if top:
+                key = (-wb, vb == 0, near(minpr, kp), -vb, minpr, a)
+            elif belady:
                 key = (-wb, near(minpr, kp), -vb, minpr, -a)
             else:
                 key = (minpr, -wb, -vb, -a)
@@ -325,13 +336,14 @@ def _replay(tensors, kernels, M, roofs, variant, lookahead, affinity_w, placemen
 
             def elig_guarded(u, k=k):
                 return elig(u) and last[u] < k - guard
-            r = place(t, elig_guarded, k) if guard else None
+            top = belady and not (m & MODE_R) and tensors[t]["kind"] == KIND_KV
+            r = place(t, elig_guarded, k, top) if guard else None
             if r is None:
-                r = place(t, elig, k)
+                r = place(t, elig, k, top)
             if r is None:
                 for u in range(nT):
                     pin[u] = -1
-                r = place(t, elig, k)
+                r = place(t, elig, k, top)
                 if r is None:
                     need = sum(size[u] for u, _ in A[k])
                     if need > M:

@@ -108,6 +108,8 @@ class Replay {
     nT_ = T.size();
     size_.resize(nT_);
     for (size_t t = 0; t < nT_; ++t) size_[t] = T[t].size;
+    kinds_.resize(nT_);
+    for (size_t t = 0; t < nT_; ++t) kinds_[t] = T[t].kind;
     uses_ = build_uses(T, K);
     belady_ = p.variant == AUVM_T_A_P || p.variant == AUVM_DEMAND_BELADY;
     affinity_ = p.variant == AUVM_T_A || p.variant == AUVM_T_A_P;
@@ -147,10 +149,12 @@ class Replay {
         auto guarded = [&](int32_t u) { return elig(u) && last_[u] < k - guard_; };
         uint64_t a_off;
         std::vector<int32_t> victims;
-        bool placed = guard_ > 0 && place(t, guarded, k, &a_off, &victims);
-        if (!placed && !place(t, elig, k, &a_off, &victims)) {
+        // a first write of a KV-cache tensor under farthest-next-use victims
+        const bool top = belady_ && !(m & AUVM_R) && kinds_[t] == AUVM_KV;
+        bool placed = guard_ > 0 && place(t, guarded, k, &a_off, &victims, top);
+        if (!placed && !place(t, elig, k, &a_off, &victims, top)) {
           std::fill(pin_.begin(), pin_.end(), -1);
-          if (!place(t, elig, k, &a_off, &victims)) {
+          if (!place(t, elig, k, &a_off, &victims, top)) {
             uint64_t need = 0;
             for (auto& b : kd.acc) need += size_[b.first];
             if (need > M_)
@@ -212,7 +216,8 @@ class Replay {
   }
 
   template <class Elig>
-  bool place(int32_t t, Elig elig, int64_t kp, uint64_t* a_out, std::vector<int32_t>* victims) {
+  bool place(int32_t t, Elig elig, int64_t kp, uint64_t* a_out, std::vector<int32_t>* victims,
+             bool top = false) {
     const uint64_t s = size_[t];
     victims->clear();
     if (pol_.placement == AUVM_PLACE_IDEAL) {
@@ -258,33 +263,42 @@ class Replay {
       *a_out = 0;
       return true;
     }
-    // pool windows: candidate starts are 0 and the end of every resident span
+    // pool windows: candidate starts are 0 and the end of every resident
+    // span; a first write of a KV-cache tensor (top) also tries the windows
+    // flush against the pool's end and against the start of every resident
+    // span, and prefers a free window at the highest address, so the
+    // long-lived cache packs at the top of the pool and leaves no holes
+    // between its tensors for the streamed weights to fragment
     bool found = false;
     int64_t b_pr = 0;
     uint64_t b_wb = 0, b_vb = 0, b_a = 0;
     size_t b_lo = 0, b_hi = 0;
     const size_t n = spans_.size();
-    for (size_t i = 0; i <= n; ++i) {
-      uint64_t a = i == 0 ? 0 : spans_[i - 1].end;
-      if (a + s > M_) continue;
+    // a: window start; i: the first span ending after a
+    auto consider = [&](uint64_t a, size_t i) {
+      if (a + s > M_) return;
       int64_t pr = kInf;
       uint64_t wb = 0, vb = 0;
-      bool ok = true;
       size_t j = i;
       for (; j < n && spans_[j].off < a + s; ++j) {
         int32_t u = spans_[j].t;
-        if (!elig(u)) {
-          ok = false;
-          break;
-        }
+        if (!elig(u)) return;
         pr = std::min(pr, prio(u, kp));
         if (writes_back(u, kp)) wb += size_[u];
         vb += size_[u];
       }
-      if (!ok) continue;
       bool better;
       if (!found) {
         better = true;
+      } else if (top) {      // (-writeback bytes, free, bucket of worst next use, -victim bytes, worst next use, offset)
+        const int64_t nb = near(pr, kp), bnb = near(b_pr, kp);
+        const bool fr = vb == 0, bfr = b_vb == 0;
+        better = wb < b_wb ||
+                 (wb == b_wb &&
+                  (fr > bfr ||
+                   (fr == bfr &&
+                    (nb > bnb ||
+                     (nb == bnb && (vb < b_vb || (vb == b_vb && (pr > b_pr || (pr == b_pr && a > b_a)))))))));
       } else if (belady_) {  // (-writeback bytes, bucket of worst next use, -victim bytes, worst next use)
         const int64_t nb = near(pr, kp), bnb = near(b_pr, kp);
         better = wb < b_wb ||
@@ -301,6 +315,17 @@ class Replay {
         b_lo = i;
         b_hi = j;
       }
+    };
+    for (size_t i = 0; i <= n; ++i) consider(i == 0 ? 0 : spans_[i - 1].end, i);
+    if (top) {
+      auto first_after = [&](uint64_t a) {
+        return size_t(std::upper_bound(spans_.begin(), spans_.end(), a,
+                                       [](uint64_t v, const Span& x) { return v < x.end; }) -
+                      spans_.begin());
+      };
+      if (M_ >= s) consider(M_ - s, first_after(M_ - s));
+      for (size_t j = 0; j < n; ++j)
+        if (spans_[j].off >= s) consider(spans_[j].off - s, first_after(spans_[j].off - s));
     }
     if (!found) return false;
     for (size_t j = b_lo; j < b_hi; ++j) victims->push_back(spans_[j].t);
@@ -406,6 +431,7 @@ class Replay {
   std::vector<uint64_t> off_;
   std::vector<int64_t> lru_, pin_, pf_need_, mark_, prot_, last_;
   int64_t guard_ = 0, bucket_ = 1;
+  std::vector<uint32_t> kinds_;
   int64_t scan_id_ = 0;
   std::vector<Span> spans_;  // resident windows sorted by offset (insertion order for IDEAL)
   uint64_t used_ = 0;

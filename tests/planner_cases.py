@@ -3,7 +3,7 @@ import json
 import os
 import random
 
-from workloads.format import DT_U8, KIND_ACT, KIND_PARAM, OP_TOUCH
+from workloads.format import DT_U8, KIND_ACT, KIND_KV, KIND_PARAM, OP_TOUCH
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "planner_cases.json")
 
@@ -14,7 +14,8 @@ def load_golden():
 
 
 def golden_inputs(case):
-    tensors = [dict(nbytes=e[0], dtype=DT_U8, kind=KIND_PARAM if e[1] == "param" else KIND_ACT,
+    kinds = {"param": KIND_PARAM, "act": KIND_ACT, "kv": KIND_KV}
+    tensors = [dict(nbytes=e[0], dtype=DT_U8, kind=kinds[e[1]],
                     host_init=(e[1] == "param"), live_out=(len(e) > 2 and e[2] == "out"))
                for e in case["tensors"]]
     n = len(case["kernels"])
@@ -27,7 +28,7 @@ def golden_inputs(case):
 
 
 def random_trace(seed, n_tensors=None, n_kernels=None, max_ops=4, equal=False,
-                 read_only=False, unit=256, touch=False, timed=False, live_out=False):
+                 read_only=False, unit=256, touch=False, timed=False, live_out=False, kv=False):
     """Random trace of touch kernels with explicit or analytic costs.
 
     touch=True makes every kernel a well-formed touch op: tensor 0 is a log
@@ -36,6 +37,7 @@ def random_trace(seed, n_tensors=None, n_kernels=None, max_ops=4, equal=False,
     timed=True gives most kernels a measured time (time_ns) drawn around the
     link time of a few hundred bytes, so both sides of the measured-time rule
     occur.  live_out=True marks about a third of the tensors live-out.
+    kv=True makes about half of the non-parameter tensors KV-cache tensors.
     """
     r = random.Random(seed)
     nT = n_tensors or r.randint(1, 40)
@@ -45,6 +47,8 @@ def random_trace(seed, n_tensors=None, n_kernels=None, max_ops=4, equal=False,
         [1, 200, 256, 300, 512, 1000, 2048, 4096, 777]
     for t in range(nT):
         kind = KIND_PARAM if (read_only or r.random() < 0.6) else KIND_ACT
+        if kv and kind == KIND_ACT and r.random() < 0.5:
+            kind = KIND_KV
         nbytes = unit if equal else r.choice(sizes)
         tensors.append(dict(nbytes=nbytes, dtype=DT_U8, kind=kind,
                             host_init=(kind == KIND_PARAM or r.random() < 0.3),

@@ -508,3 +508,27 @@ def test_object_granularity_config_traces(name):
         pytest.skip("blocks do not fit the budget")
     checker.check(tensors, kernels, w.budget(), r.schedule)
     assert_same_plan(plan_ctx(tensors, kernels, w.budget(), object_bytes=ob), r)
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_kv_tensors_bit_exact(seed):
+    """Traces with KV-cache tensors, whose first writes pack at the top of
+    the pool under farthest-next-use victims: the library plans exactly what
+    the oracle plans, and the checker accepts it."""
+    from oracle import checker
+    tensors, kernels = random_trace(seed, touch=True, kv=True)
+    fp = sum(op.aligned(t["nbytes"]) for t in tensors)
+    rnd = random.Random(7000 + seed)
+    for variant in VARIANTS:
+        for num, den in ((1, 2), (2, 3), (5, 6)):
+            M = max(1024, fp * num // den // 256 * 256)
+            kw = dict(variant=variant, guard=rnd.choice([None, 0, 3]), bucket=rnd.choice([None, 1, 8]))
+            try:
+                r = op.plan(tensors, kernels, M, **kw)
+            except op.PlanError as e:
+                with pytest.raises(AuvmError) as x:
+                    plan_ctx(tensors, kernels, M, **kw)
+                assert x.value.code == e.code
+                continue
+            checker.check(tensors, kernels, M, r.schedule)
+            assert_same_plan(plan_ctx(tensors, kernels, M, **kw), r)
