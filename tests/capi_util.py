@@ -1,5 +1,24 @@
 """Helpers to load traces into a plan-only C-ABI context and compare with the oracle."""
+import os
+
 from paper_2609_06172_amd.capi import Context
+
+_LIB = {}
+
+
+def plan_library():
+    """None (the package's library) unless AUVM_SIM_SANITIZE=1: then the
+    host-only build of the same sources with the sanitizers."""
+    if os.environ.get("AUVM_SIM_SANITIZE") != "1":
+        return None
+    if "L" not in _LIB:
+        import ctypes
+        import sys
+        sys.path.insert(0, os.path.join(os.path.dirname(os.path.abspath(__file__)), "sim"))
+        import build_sim
+        from paper_2609_06172_amd.capi import bind_library
+        _LIB["L"] = bind_library(ctypes.CDLL(build_sim.build()))
+    return _LIB["L"]
 from workloads.format import ALIGN, FLAG_HOST_INIT, FLAG_LIVE_OUT, KIND_PARAM
 
 
@@ -10,7 +29,7 @@ def plan_ctx(tensors, kernels, M, variant=4, lookahead=0, affinity_w=1, placemen
     Kernels that carry a measured time (time_ns) hand the whole list to
     set_kernel_times before planning.
     """
-    ctx = Context(-1)
+    ctx = Context(-1, library=plan_library())
     off = 0
     offs = []
     for t in tensors:
