@@ -260,6 +260,16 @@ __device__ __forceinline__ void load_kv(bf16_t* tile, const bf16_t* __restrict__
   }
 }
 
+// The same rows for a block wholly before klast, from per-lane byte offsets
+// (row * rs + 8 * chunk elements, computed once) off a uniform base: no
+// clamp and no 64-bit address arithmetic per load.
+__device__ __forceinline__ void load_kv_rows(bf16_t* tile, const char* base, const uint32_t* boff, int wv) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    __builtin_amdgcn_global_load_lds(reinterpret_cast<const bf16_t*>(base + boff[i]), tile + (16 * i + 4 * wv) * FD,
+                                     16, 0, 0);
+}
+
 __global__ void __launch_bounds__(64 * FW, 2) attn_prefill_d128(AttnArgs a, int64_t nqb) {
   extern __shared__ __align__(16) bf16_t fsm[];
   bf16_t* Ks = fsm;                 // [2][FK][FD]
@@ -286,7 +296,7 @@ __global__ void __launch_bounds__(64 * FW, 2) attn_prefill_d128(AttnArgs a, int6
       qf[c] = bf16x8{};
   }
   // softmax in base 2 on raw scores: p = 2^(c*s - c*max) with c = log2(e)/sqrt(128)
-  const float c2 = 0.12751743074565512f;
+  constexpr float c2 = 0.12751743074565512f;
   // O^T tile dt: element e is dim 32*dt + 8*(e/4) + 4*lh + e%4 of this lane's query
   f32x16 ot[4];
 #pragma unroll
@@ -299,17 +309,30 @@ __global__ void __launch_bounds__(64 * FW, 2) attn_prefill_d128(AttnArgs a, int6
 
   // transpose-read address of this lane as a source: row +(j/4), dims +4*(j%4)
   const int tg = lane >> 4, tj = lane & 15;
-  load_kv(Ks, Kg, a.kv_rs, 0, klast, wv, lane);
-  load_kv(Vs, Vg, a.kv_rs, 0, klast, wv, lane);
+  // byte offsets of the rows this lane stages, within a block
+  uint32_t boff[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row = 16 * i + 4 * wv + (lane >> 4);
+    boff[i] = uint32_t((row * a.kv_rs + 8 * ((lane & 15) ^ kv_swz(row))) * int64_t(sizeof(bf16_t)));
+  }
+  const int64_t rsb = a.kv_rs * int64_t(sizeof(bf16_t));
+  auto stage = [&](int64_t k1, int b2) {
+    if (k1 + FK - 1 <= klast) {
+      load_kv_rows(Ks + b2 * TS, reinterpret_cast<const char*>(Kg) + k1 * rsb, boff, wv);
+      load_kv_rows(Vs + b2 * TS, reinterpret_cast<const char*>(Vg) + k1 * rsb, boff, wv);
+    } else {                         // the last block: rows past klast clamped
+      load_kv(Ks + b2 * TS, Kg, a.kv_rs, k1, klast, wv, lane);
+      load_kv(Vs + b2 * TS, Vg, a.kv_rs, k1, klast, wv, lane);
+    }
+  };
+  stage(0, 0);
   int buf = 0;
   for (int64_t k0 = 0; k0 <= klast; k0 += FK, buf ^= 1) {
     __builtin_amdgcn_s_waitcnt(0);   // this wave's loads of the block have landed
     __syncthreads();                 // ... and every other wave's; the other buffer is free
     asm volatile("" ::: "memory");   // LDS now holds data written outside the compiler's view
-    if (k0 + FK <= klast) {
-      load_kv(Ks + (buf ^ 1) * TS, Kg, a.kv_rs, k0 + FK, klast, wv, lane);
-      load_kv(Vs + (buf ^ 1) * TS, Vg, a.kv_rs, k0 + FK, klast, wv, lane);
-    }
+    if (k0 + FK <= klast) stage(k0 + FK, buf ^ 1);
     if (k0 > wlast) continue;
     const bf16_t* ks = Ks + buf * TS;
     const bf16_t* vs = Vs + buf * TS;
@@ -325,11 +348,12 @@ __global__ void __launch_bounds__(64 * FW, 2) attn_prefill_d128(AttnArgs a, int6
       }
     }
     if (k0 + FK - 1 > a.pos0 + qw) {   // the block crosses this wave's diagonal
+      const int kq = int(qpos - k0);   // keys of the block past this one are masked
 #pragma unroll
       for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
         for (int e = 0; e < 16; ++e)
-          if (k0 + 32 * kt + 8 * (e >> 2) + 4 * lh + (e & 3) > qpos) st[kt][e] = -INFINITY;
+          if (32 * kt + 8 * (e >> 2) + 4 * lh + (e & 3) > kq) st[kt][e] = -INFINITY;
     }
     float mx = -INFINITY;
 #pragma unroll
@@ -337,11 +361,21 @@ __global__ void __launch_bounds__(64 * FW, 2) attn_prefill_d128(AttnArgs a, int6
 #pragma unroll
       for (int e = 0; e < 16; ++e) mx = fmaxf(mx, st[kt][e]);
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float mn = fmaxf(m, mx);
+    // m is the score the exponentials are taken against.  It moves (and the
+    // running sum and output are rescaled) only when a block's maximum
+    // exceeds it by more than kGrow raw-score units, so p stays below 2^8;
+    // the common factor cancels in o and in the log-sum-exp.
+    constexpr float kGrow = 8.f / c2;
+    if (__any(mx > m + kGrow)) {   // rare after the first blocks
+      const bool grow = mx > m + kGrow;
+      const float corr = grow ? __builtin_amdgcn_exp2f((m - mx) * c2) : 1.f;   // 0 while m = -inf
+      m = grow ? mx : m;
+      l *= corr;
+#pragma unroll
+      for (int t = 0; t < 4; ++t) ot[t] *= corr;
+    }
     // a query with no visible key yet keeps m = -inf and contributes nothing
-    const bool none = mn == -INFINITY;
-    const float corr = none ? 1.f : __builtin_amdgcn_exp2f((m - mn) * c2);
-    const float off = none ? 0.f : mn * c2;
+    const float off = m == -INFINITY ? 0.f : m * c2;
     float sum = 0.f;
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
@@ -352,12 +386,7 @@ __global__ void __launch_bounds__(64 * FW, 2) attn_prefill_d128(AttnArgs a, int6
         sum += p;
       }
     sum += __shfl_xor(sum, 32, 64);
-    l = l * corr + sum;
-    m = mn;
-    if (__any(corr != 1.f)) {   // the running max moved for some query of this wave
-#pragma unroll
-      for (int t = 0; t < 4; ++t) ot[t] *= corr;
-    }
+    l += sum;
     // key step s covers keys 16s..16s+15 of the block: lane lh = 0 needs
     // 16s..+7, lh = 1 needs 16s+8..+15.  In tile kt = s/2 a lane holds
     // groups g of 4 keys (8g + 4*lh ..); group g0 = 2*(s%2) and g0+1 are
