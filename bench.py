@@ -257,12 +257,14 @@ def seg_stats(w, sched, classes, M, segs):
 
 
 def link_timeline(tl, K):
-    """Host-to-device link over the timed run segment (the last one): busy and
-    idle time (copies run on two streams: busy is the union of their
-    intervals), and the part of each idle gap during which the host had not
+    """Host link over the timed run segment (the last one): host-to-device
+    busy and idle time (those copies run on two streams: busy is the union of
+    their intervals), the part of each idle gap during which the host had not
     yet issued the next copy (host and device clocks share the segment's
-    start)."""
-    from paper_2609_06172_amd.capi import TL_H2D, TL_H2D_B
+    start), and, where the plan writes back, the device-to-host busy time and
+    how much of it ran while a host-to-device copy was also in flight (copies
+    in the two directions share one rate when they overlap)."""
+    from paper_2609_06172_amd.capi import TL_D2H, TL_H2D, TL_H2D_B
     seg = max(e[1] for e in tl)
     cur = [e for e in tl if e[1] == seg]
     h = sorted((e for e in cur if e[0] in (TL_H2D, TL_H2D_B)), key=lambda e: e[5])
@@ -277,10 +279,36 @@ def link_timeline(tl, K):
             busy += max(0.0, e[6] - prev)
         prev = max(prev, e[6])
     nbytes = sum(e[3] for e in h)
-    return {"h2d_busy_ms_per_step": round(busy / K, 3), "h2d_idle_ms_per_step": round((span - busy) / K, 3),
-            "idle_before_host_issue_ms_per_step": round(late / K, 3),
-            "h2d_GBps_while_busy": round(nbytes / (busy * 1e-3) / 1e9, 2) if busy > 0 else None,
-            "copies_per_step": round(len(h) / K, 2)}
+    out = {"h2d_busy_ms_per_step": round(busy / K, 3), "h2d_idle_ms_per_step": round((span - busy) / K, 3),
+           "idle_before_host_issue_ms_per_step": round(late / K, 3),
+           "h2d_GBps_while_busy": round(nbytes / (busy * 1e-3) / 1e9, 2) if busy > 0 else None,
+           "copies_per_step": round(len(h) / K, 2)}
+    d = sorted((e for e in cur if e[0] == TL_D2H), key=lambda e: e[5])
+    if d:
+        def union(es):
+            u = []
+            for e in es:
+                if u and e[5] <= u[-1][1]:
+                    u[-1][1] = max(u[-1][1], e[6])
+                else:
+                    u.append([e[5], e[6]])
+            return u
+        hu, du = union(h), union(d)
+        dbusy = sum(b - a for a, b in du)
+        both, i = 0.0, 0
+        for a, b in du:
+            while i < len(hu) and hu[i][1] <= a:
+                i += 1
+            j = i
+            while j < len(hu) and hu[j][0] < b:
+                both += max(0.0, min(b, hu[j][1]) - max(a, hu[j][0]))
+                j += 1
+        out.update({"d2h_busy_ms_per_step": round(dbusy / K, 3),
+                    "d2h_GBps_while_busy": round(sum(e[3] for e in d) / (dbusy * 1e-3) / 1e9, 2) if dbusy > 0 else None,
+                    "d2h_copies_per_step": round(len(d) / K, 2),
+                    "both_directions_busy_ms_per_step": round(both / K, 3),
+                    "link_busy_ms_per_step": round((busy + dbusy - both) / K, 3)})
+    return out
 
 
 def per_layer(w, tl, segs, n_layers):
