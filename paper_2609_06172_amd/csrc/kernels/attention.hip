@@ -214,7 +214,7 @@ __global__ void __launch_bounds__(64 * kDecWaves, 4) attn_decode_d128(AttnArgs a
 // barrier per block.  Rows past the last visible key are clamped to it: those
 // keys are masked, so they contribute exactly zero.  A wave skips blocks
 // wholly past its queries; only blocks crossing its diagonal are masked.
-// Heaviest query blocks are dispatched first.
+// Blocks are ordered per XCD, heaviest first (xcd_order).
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
@@ -270,14 +270,32 @@ __device__ __forceinline__ void load_kv_rows(bf16_t* tile, const char* base, con
                                      16, 0, 0);
 }
 
+// Workgroup order of the flash kernels (grid = nblk blocks of each of nbh
+// (batch, head) pairs).  Workgroup w runs on XCD w % 8 (round-robin
+// dispatch), and each XCD has its own L2: all blocks of one (b, h) go to the
+// same XCD, so its K and V (or Q and dO) are fetched into one L2 only, and
+// each XCD starts the heaviest blocks (rank 0) of all its heads first.
+// Without eight-way divisible heads the order is rank-major.
+__device__ __forceinline__ void xcd_order(int64_t w, int64_t nbh, int64_t* rank, int64_t* bh) {
+  if (nbh % 8 == 0) {
+    const int64_t x = w % 8, slot = w / 8, hx = nbh / 8;
+    *rank = slot / hx;
+    *bh = (slot % hx) * 8 + x;
+  } else {
+    *rank = w / nbh;
+    *bh = w % nbh;
+  }
+}
+
 __global__ void __launch_bounds__(64 * FW, 2) attn_prefill_d128(AttnArgs a, int64_t nqb) {
   extern __shared__ __align__(16) bf16_t fsm[];
   bf16_t* Ks = fsm;                 // [2][FK][FD]
   bf16_t* Vs = fsm + 2 * TS;        // [2][FK][FD]
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int lq = lane & 31, lh = lane >> 5;
-  const int64_t wg = blockIdx.x;
-  const int64_t qb = nqb - 1 - wg % nqb, bh = wg / nqb;
+  int64_t rank, bh;
+  xcd_order(blockIdx.x, int64_t(gridDim.x) / nqb, &rank, &bh);
+  const int64_t qb = nqb - 1 - rank;
   const int64_t h = bh % a.nH, b = bh / a.nH;
   const int64_t q0 = qb * FQ, qw = q0 + 32 * wv;
   const bf16_t* Q = reinterpret_cast<const bf16_t*>(a.q) + (b * a.S) * a.q_rs + h * FD;
@@ -481,7 +499,9 @@ __global__ void __launch_bounds__(64 * FW, 1) attn_bwd_dq_d128(AttnBwdArgs a, in
   bf16_t* Vs = fsm + 2 * TS;        // [2][FK][FD]
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int lq = lane & 31, lh = lane >> 5;
-  const int64_t qb = nqb - 1 - int64_t(blockIdx.x) % nqb, bh = int64_t(blockIdx.x) / nqb;
+  int64_t rank, bh;
+  xcd_order(blockIdx.x, int64_t(gridDim.x) / nqb, &rank, &bh);
+  const int64_t qb = nqb - 1 - rank;
   const int64_t h = bh % a.nH, b = bh / a.nH, S = a.S;
   const int64_t q0 = qb * FQ, qw = q0 + 32 * wv, qr = qw + lq;
   const bf16_t* Q = reinterpret_cast<const bf16_t*>(a.q) + (b * S) * a.q_rs + h * FD;
@@ -563,7 +583,8 @@ __global__ void __launch_bounds__(64 * FW, 1) attn_bwd_dkv_d128(AttnBwdArgs a, i
   __shared__ float lsS[2][FK], dsS[2][FK];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int lq = lane & 31, lh = lane >> 5;
-  const int64_t kb = int64_t(blockIdx.x) % nkb, bh = int64_t(blockIdx.x) / nkb;
+  int64_t kb, bh;   // key block 0 sees every query: the heaviest
+  xcd_order(blockIdx.x, int64_t(gridDim.x) / nkb, &kb, &bh);
   const int64_t h = bh % a.nH, b = bh / a.nH, S = a.S;
   const int64_t kbase = kb * FQ, kw = kbase + 32 * wv, kr = kw + lq;
   const int64_t krc = kr < S ? kr : S - 1;

@@ -154,7 +154,6 @@ __global__ void __launch_bounds__(64 * kWaves) gemm_big(const bf16_t* __restrict
     __builtin_amdgcn_s_waitcnt(0);   // this wave's loads of stage kt have landed
     __syncthreads();                 // ... and every other wave's; stage kt-1 is free
     asm volatile("" ::: "memory");   // LDS now holds data written outside the compiler's view
-    if (kt + 1 < nk) load_stage<EPI>(smem, arow, W, W2, N, K, n0, wv, lane, int((kt + 1) & 1), (kt + 1) * kBK);
     const bf16_t* stg = smem + int(kt & 1) * S::kStage;
     // fragments of sub-step ks into register set q
     bf16x8 a[2][TM], b[2][TN], b2[2][DUAL ? TN : 1];
@@ -175,7 +174,16 @@ __global__ void __launch_bounds__(64 * kWaves) gemm_big(const bf16_t* __restrict
         }
       }
     };
+    // Sub-step ks is one scheduling region (fenced by sched_barrier): its first
+    // MFMA, whose fragments were read during sub-step ks-1, then the reads of
+    // sub-step ks+1 alternating with its other MFMAs.  The compiler waits for
+    // every outstanding LDS read before a region's first MFMA, so reads
+    // issued at the top of a region, before that MFMA, would stall it; issued
+    // after it, they have the rest of the region to land.  Stage kt+1's
+    // global loads go out right after sub-step 0's reads.
     frag(0, 0);
+    if (kt + 1 < nk) load_stage<EPI>(smem, arow, W, W2, N, K, n0, wv, lane, int((kt + 1) & 1), (kt + 1) * kBK);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int ks = 0; ks < kBK / 16; ++ks) {
       const int q = ks & 1;
@@ -188,15 +196,16 @@ __global__ void __launch_bounds__(64 * kWaves) gemm_big(const bf16_t* __restrict
           if constexpr (DUAL) acc2[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[q][i], b2[q][j], acc2[i][j], 0, 0, 0);
         }
       if (ks + 1 < kBK / 16) {
-        // one fragment read after every MFMA pair (or single MFMA when there are fewer)
         constexpr int kReads = TM + TN * (DUAL ? 2 : 1), kMfma = TM * TN * (DUAL ? 2 : 1);
-        constexpr int kPer = kMfma / kReads > 0 ? kMfma / kReads : 1;
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
 #pragma unroll
         for (int t = 0; t < kReads; ++t) {
-          __builtin_amdgcn_sched_group_barrier(0x008, kPer, 0);   // MFMA
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);      // LDS read
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
         }
+        __builtin_amdgcn_sched_group_barrier(0x008, kMfma - 1 - kReads, 0);
       }
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
 
