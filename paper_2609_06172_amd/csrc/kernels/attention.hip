@@ -200,13 +200,15 @@ __global__ void __launch_bounds__(64 * kDecWaves, 4) attn_decode_d128(AttnArgs a
 //   S^T = K Q^T: A = a 32-key x 16-dim K fragment (LDS), B = Q^T (registers),
 //     2 key tiles x 8 dim steps of v_mfma_f32_32x32x16_bf16 per 64-key block;
 //   online softmax: a query's 64 scores sit in lanes l and l+32 (32 each), so
-//     its max and sum are one exchange between the two;
+//     its max and sum are one exchange between the two (v_permlane32_swap,
+//     which swaps the upper half of one register with the lower half of
+//     another, on the VALU rather than through LDS);
 //   O^T += V^T P^T: A = a 32-dim x 16-key fragment of V^T, read from the
 //     row-major V tile with the LDS transpose read (ds_read_b64_tr_b16: within
 //     each 16-lane group, lane 4a+b receives element b of the 8-byte rows that
 //     lanes a, a+4, a+8, a+12 address), B = P^T assembled in registers (each
-//     lane trades four values with its partner lane); 4 dim tiles x 4 key
-//     steps per block.
+//     lane trades four values with its partner lane, by the same swap); 4 dim
+//     tiles x 4 key steps per block.
 // K and V blocks of 64 keys go from global memory straight into one of two
 // LDS buffers (16-byte global_load_lds; a 256-byte row's chunks are permuted
 // by a row-dependent XOR that keeps fragment and transpose reads free of bank
@@ -270,6 +272,48 @@ __device__ __forceinline__ void load_kv_rows(bf16_t* tile, const char* base, con
                                      16, 0, 0);
 }
 
+// the B-operand fragment (16 rows of k, this lane's column) of k-step s from
+// a pair of 32 x 32 C tiles t[0..1] (rows 0..31, 32..63): rows 16s.. of the
+// pair; the lane and its partner (lane ^ 32) trade one 4-row group each
+__device__ __forceinline__ bf16x8 c_to_b(const f32x16* t, int s) {
+  const int kt = s >> 1, g0 = 2 * (s & 1);
+  const uint32_t a0 = pack_bf16(t[kt][4 * g0 + 0], t[kt][4 * g0 + 1]);
+  const uint32_t a1 = pack_bf16(t[kt][4 * g0 + 2], t[kt][4 * g0 + 3]);
+  const uint32_t b0 = pack_bf16(t[kt][4 * g0 + 4], t[kt][4 * g0 + 5]);
+  const uint32_t b1 = pack_bf16(t[kt][4 * g0 + 6], t[kt][4 * g0 + 7]);
+  // v_permlane32_swap(x, y) returns x' = (lanes < 32: x, lanes >= 32: y of
+  // lane - 32) and y' = (lanes < 32: x of lane + 32, lanes >= 32: y): lane
+  // l < 32 gets {its a, its partner's a}, lane l >= 32 {its partner's b, its b}
+  const auto x0 = __builtin_amdgcn_permlane32_swap(a0, b0, false, false);
+  const auto x1 = __builtin_amdgcn_permlane32_swap(a1, b1, false, false);
+  const u32x4v pf = {x0[0], x1[0], x0[1], x1[1]};
+  return __builtin_bit_cast(bf16x8, pf);
+}
+
+// the A-operand fragment of the transposed tile (dims 32 dt.., rows 16 s..)
+// from a row-major swizzled 64 x 128 tile, by two LDS transpose reads
+__device__ __forceinline__ bf16x8 tile_t_frag(const bf16_t* tile, int s, int dt, int lane) {
+  const int tg = lane >> 4, tj = lane & 15;
+  const int row = 16 * s + 8 * (tg >> 1) + (tj >> 2);
+  const int dim = 32 * dt + 16 * (tg & 1) + 4 * (tj & 3);
+  typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+  const i16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(tile + tile_at(row, dim)));
+  const i16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(tile + tile_at(row + 4, dim)));
+  typedef short i16x8 __attribute__((ext_vector_type(8)));
+  const i16x8 vv = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
+  return __builtin_bit_cast(bf16x8, vv);
+}
+
+// max and sum of a value and its partner lane's (lane ^ 32), the same on both lanes
+__device__ __forceinline__ float swap_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float swap_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // Workgroup order of the flash kernels (grid = nblk blocks of each of nbh
 // (batch, head) pairs).  Workgroup w runs on XCD w % 8 (round-robin
 // dispatch), and each XCD has its own L2: all blocks of one (b, h) go to the
@@ -325,8 +369,6 @@ __global__ void __launch_bounds__(64 * FW, 2) attn_prefill_d128(AttnArgs a, int6
   const int64_t klast = a.pos0 + qlast;
   const int64_t wlast = a.pos0 + qw + 31;
 
-  // transpose-read address of this lane as a source: row +(j/4), dims +4*(j%4)
-  const int tg = lane >> 4, tj = lane & 15;
   // byte offsets of the rows this lane stages, within a block
   uint32_t boff[4];
 #pragma unroll
@@ -354,17 +396,48 @@ __global__ void __launch_bounds__(64 * FW, 2) attn_prefill_d128(AttnArgs a, int6
     if (k0 > wlast) continue;
     const bf16_t* ks = Ks + buf * TS;
     const bf16_t* vs = Vs + buf * TS;
-    // S^T tile kt: element e is key k0 + 32*kt + 8*(e/4) + 4*lh + e%4 of this lane's query
-    f32x16 st[2];
+    // S^T tile kt: element e is key k0 + 32*kt + 8*(e/4) + 4*lh + e%4 of this
+    // lane's query.  Dim steps go in pairs; each pair is one scheduling region
+    // whose first MFMA takes fragments read during the previous region, and
+    // whose other MFMAs alternate with the reads of the next pair (the
+    // compiler waits for every outstanding LDS read before a region's first
+    // MFMA).
+    f32x16 st[2] = {f32x16{}, f32x16{}};
+    bf16x8 kf[2][4];   // [pair parity][2 * (dim step in pair) + kt]
+    auto kread = [&](int cp, int set) {
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt) {
-      st[kt] = f32x16{};
+      for (int u = 0; u < 2; ++u)
 #pragma unroll
-      for (int c = 0; c < 8; ++c) {
-        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(ks + tile_at(32 * kt + lq, 16 * c + 8 * lh));
-        st[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[c], st[kt], 0, 0, 0);
+        for (int kt = 0; kt < 2; ++kt)
+          kf[set][2 * u + kt] =
+              *reinterpret_cast<const bf16x8*>(ks + tile_at(32 * kt + lq, 16 * (2 * cp + u) + 8 * lh));
+    };
+    kread(0, 0);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int cp = 0; cp < 4; ++cp) {
+      const int set = cp & 1;
+      if (cp + 1 < 4) kread(cp + 1, set ^ 1);
+#pragma unroll
+      for (int u = 0; u < 2; ++u)
+#pragma unroll
+        for (int kt = 0; kt < 2; ++kt)
+          st[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[set][2 * u + kt], qf[2 * cp + u], st[kt], 0, 0, 0);
+      if (cp + 1 < 4) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
       }
+      __builtin_amdgcn_sched_barrier(0);
     }
+    // V^T fragments of key steps 0 and 1, read while the softmax runs
+    bf16x8 vf[2][4];   // [key step parity][dt]
+#pragma unroll
+    for (int s = 0; s < 2; ++s)
+#pragma unroll
+      for (int dt = 0; dt < 4; ++dt) vf[s][dt] = tile_t_frag(vs, s, dt, lane);
     if (k0 + FK - 1 > a.pos0 + qw) {   // the block crosses this wave's diagonal
       const int kq = int(qpos - k0);   // keys of the block past this one are masked
 #pragma unroll
@@ -373,12 +446,15 @@ __global__ void __launch_bounds__(64 * FW, 2) attn_prefill_d128(AttnArgs a, int6
         for (int e = 0; e < 16; ++e)
           if (32 * kt + 8 * (e >> 2) + 4 * lh + (e & 3) > kq) st[kt][e] = -INFINITY;
     }
-    float mx = -INFINITY;
+    // the block's maximum: a tree over the lane's 32 scores, then the partner lane's
+    float t8[8];
 #pragma unroll
-    for (int kt = 0; kt < 2; ++kt)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, st[kt][e]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    for (int i = 0; i < 8; ++i) {
+      const int kt = i >> 2, e = 4 * (i & 3);
+      t8[i] = fmaxf(fmaxf(st[kt][e], st[kt][e + 1]), fmaxf(st[kt][e + 2], st[kt][e + 3]));
+    }
+    float mx = fmaxf(fmaxf(fmaxf(t8[0], t8[1]), fmaxf(t8[2], t8[3])), fmaxf(fmaxf(t8[4], t8[5]), fmaxf(t8[6], t8[7])));
+    mx = swap_max(mx);
     // m is the score the exponentials are taken against.  It moves (and the
     // running sum and output are rescaled) only when a block's maximum
     // exceeds it by more than kGrow raw-score units, so p stays below 2^8;
@@ -394,44 +470,25 @@ __global__ void __launch_bounds__(64 * FW, 2) attn_prefill_d128(AttnArgs a, int6
     }
     // a query with no visible key yet keeps m = -inf and contributes nothing
     const float off = m == -INFINITY ? 0.f : m * c2;
-    float sum = 0.f;
+    float ps[4] = {0.f, 0.f, 0.f, 0.f};   // four partial sums: short dependency chains
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
         const float p = __builtin_amdgcn_exp2f(fmaf(st[kt][e], c2, -off));
         st[kt][e] = p;
-        sum += p;
+        ps[e & 3] += p;
       }
-    sum += __shfl_xor(sum, 32, 64);
-    l += sum;
-    // key step s covers keys 16s..16s+15 of the block: lane lh = 0 needs
-    // 16s..+7, lh = 1 needs 16s+8..+15.  In tile kt = s/2 a lane holds
-    // groups g of 4 keys (8g + 4*lh ..); group g0 = 2*(s%2) and g0+1 are
-    // split between the two lanes, which trade one group each.
+    l += swap_sum((ps[0] + ps[1]) + (ps[2] + ps[3]));
+    // O^T += V^T P^T over key steps s (keys 16s..16s+15 of the block); the
+    // V^T fragments of step s+2 are read into the slots step s frees
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
-      const int kt = s >> 1, g0 = 2 * (s & 1);
-      const uint32_t a0 = pack_bf16(st[kt][4 * g0 + 0], st[kt][4 * g0 + 1]);
-      const uint32_t a1 = pack_bf16(st[kt][4 * g0 + 2], st[kt][4 * g0 + 3]);
-      const uint32_t b0 = pack_bf16(st[kt][4 * g0 + 4], st[kt][4 * g0 + 5]);
-      const uint32_t b1 = pack_bf16(st[kt][4 * g0 + 6], st[kt][4 * g0 + 7]);
-      const uint32_t s0 = lh ? a0 : b0, s1 = lh ? a1 : b1;
-      const uint32_t r0 = uint32_t(__shfl_xor(int(s0), 32, 64)), r1 = uint32_t(__shfl_xor(int(s1), 32, 64));
-      const u32x4v pf = lh ? u32x4v{r0, r1, b0, b1} : u32x4v{a0, a1, r0, r1};
-      const bf16x8 pb = __builtin_bit_cast(bf16x8, pf);
+      const bf16x8 pb = c_to_b(st, s);
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt) {
-        // V^T fragment: dim 32*dt + lq, keys 16s + 8*lh + 0..7, as two transpose reads
-        const int row = 16 * s + 8 * (tg >> 1) + (tj >> 2);
-        const int dim = 32 * dt + 16 * (tg & 1) + 4 * (tj & 3);
-        typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
-        const i16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vs + tile_at(row, dim)));
-        const i16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vs + tile_at(row + 4, dim)));
-        typedef short i16x8 __attribute__((ext_vector_type(8)));
-        const i16x8 vv = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
-        const bf16x8 vf = __builtin_bit_cast(bf16x8, vv);
-        ot[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb, ot[dt], 0, 0, 0);
+        ot[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[s & 1][dt], pb, ot[dt], 0, 0, 0);
+        if (s + 2 < 4) vf[s & 1][dt] = tile_t_frag(vs, s + 2, dt, lane);
       }
     }
   }
@@ -460,35 +517,6 @@ __global__ void __launch_bounds__(64 * FW, 2) attn_prefill_d128(AttnArgs a, int6
 //     registers), then dV^T += dO^T P and dK^T += Q^T dS.
 // A lane owns one query (dQ pass) or one key (dK, dV pass), so the 32 x 32
 // accumulator tiles map to one row of the output each.
-
-// the B-operand fragment (16 rows of k, this lane's column) of k-step s from
-// a pair of 32 x 32 C tiles t[0..1] (rows 0..31, 32..63): rows 16s.. of the
-// pair; the lane and its partner (lane ^ 32) trade one 4-row group each
-__device__ __forceinline__ bf16x8 c_to_b(const f32x16* t, int s, int lh) {
-  const int kt = s >> 1, g0 = 2 * (s & 1);
-  const uint32_t a0 = pack_bf16(t[kt][4 * g0 + 0], t[kt][4 * g0 + 1]);
-  const uint32_t a1 = pack_bf16(t[kt][4 * g0 + 2], t[kt][4 * g0 + 3]);
-  const uint32_t b0 = pack_bf16(t[kt][4 * g0 + 4], t[kt][4 * g0 + 5]);
-  const uint32_t b1 = pack_bf16(t[kt][4 * g0 + 6], t[kt][4 * g0 + 7]);
-  const uint32_t s0 = lh ? a0 : b0, s1 = lh ? a1 : b1;
-  const uint32_t r0 = uint32_t(__shfl_xor(int(s0), 32, 64)), r1 = uint32_t(__shfl_xor(int(s1), 32, 64));
-  const u32x4v pf = lh ? u32x4v{r0, r1, b0, b1} : u32x4v{a0, a1, r0, r1};
-  return __builtin_bit_cast(bf16x8, pf);
-}
-
-// the A-operand fragment of the transposed tile (dims 32 dt.., rows 16 s..)
-// from a row-major swizzled 64 x 128 tile, by two LDS transpose reads
-__device__ __forceinline__ bf16x8 tile_t_frag(const bf16_t* tile, int s, int dt, int lane) {
-  const int tg = lane >> 4, tj = lane & 15;
-  const int row = 16 * s + 8 * (tg >> 1) + (tj >> 2);
-  const int dim = 32 * dt + 16 * (tg & 1) + 4 * (tj & 3);
-  typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
-  const i16x4 v0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(tile + tile_at(row, dim)));
-  const i16x4 v1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(tile + tile_at(row + 4, dim)));
-  typedef short i16x8 __attribute__((ext_vector_type(8)));
-  const i16x8 vv = {v0[0], v0[1], v0[2], v0[3], v1[0], v1[1], v1[2], v1[3]};
-  return __builtin_bit_cast(bf16x8, vv);
-}
 
 constexpr float kBwdScale = 0.08838834764831845f;   // 1 / sqrt(128)
 constexpr float kLog2eF = 1.4426950408889634f;
@@ -560,7 +588,7 @@ __global__ void __launch_bounds__(64 * FW, 1) attn_bwd_dq_d128(AttnBwdArgs a, in
       }
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
-      const bf16x8 dsb = c_to_b(st, s, lh);
+      const bf16x8 dsb = c_to_b(st, s);
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt)
         dqt[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tile_t_frag(ks, s, dt, lane), dsb, dqt[dt], 0, 0, 0);
@@ -653,7 +681,7 @@ __global__ void __launch_bounds__(64 * FW, 1) attn_bwd_dkv_d128(AttnBwdArgs a, i
       }
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
-      const bf16x8 pb = c_to_b(sc, s, lh), dsb = c_to_b(dp, s, lh);
+      const bf16x8 pb = c_to_b(sc, s), dsb = c_to_b(dp, s);
 #pragma unroll
       for (int dt = 0; dt < 4; ++dt) {
         dvt[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tile_t_frag(os, s, dt, lane), pb, dvt[dt], 0, 0, 0);
