@@ -193,6 +193,39 @@ def test_training_step_does_not_depend_on_the_budget():
         assert np.array_equal(out[0][k], out[1][k]), k
 
 
+@pytest.mark.parametrize("name", ["gpt-small", "llama-small", "moe-small", "train-small"])
+def test_timed_launches_compute_the_same(name):
+    # under the timing policy every kernel is launched with its timing events
+    # (hipExtLaunchKernelGGL, arguments marshalled by the runtime instead of
+    # the kernel call): outputs bit-identical to the untimed run, every
+    # kernel timed, durations positive and the timeline's kernels in order
+    from paper_2609_06172_amd.capi import TL_KERNEL
+    from paper_2609_06172_amd.session import Session
+    from workloads import configs as C
+    cfg = {"gpt-small": C.GPT_SMALL, "llama-small": C.LLAMA_SMALL, "moe-small": C.MOE_SMALL,
+           "train-small": C.TRAIN_SMALL}[name]
+    w = trace.build(cfg, keep_grads=True) if name == "train-small" else trace.build(cfg)
+    names = [t.name for t in w.tensors if t.flags & 2 or t.name in ("logits", "gen", "losses", "x")]
+    out = []
+    for timing in (0, 1):
+        print(f"{name}: timing={timing}", flush=True)
+        s = Session(w, device=0, timing=timing)
+        s.run_all()
+        out.append({n: s.read(n).copy() for n in names})
+        if timing:
+            dur, _ = s.ctx.get_kernel_times()
+            tl = [e for e in s.ctx.get_timeline() if e[0] == TL_KERNEL]
+            assert len(dur) == len(w.kernels) and min(dur) >= 0 and np.median(dur) > 0
+            assert [e[2] for e in tl] == list(range(len(w.kernels)))
+            for a, b in zip(tl, tl[1:]):
+                if a[1] == b[1]:
+                    assert b[5] >= a[6] - 0.02      # in order on the compute stream (ms)
+        s.close()
+    assert names
+    for k in out[0]:
+        assert np.array_equal(out[0][k], out[1][k]), k
+
+
 def test_replanning_from_measured_kernel_times():
     # runtime monitor: a timed run, classes again from the measured
     # durations, a new plan (the oracle's, bit for bit), the same outputs
