@@ -256,6 +256,23 @@ const char* auvm_last_error(const auvm_ctx* ctx);
  * arena_bytes long, and outlive the context.  Once per context. */
 auvm_status auvm_arena_init(auvm_ctx* ctx, uint64_t arena_bytes, void* host_pinned);
 
+/* A host backing store larger than the host lets the process pin.  Offsets
+ * [0, pinned_bytes) are pinned host memory and [pinned_bytes, arena_bytes)
+ * pageable memory, both allocated by the context (plan-only contexts
+ * allocate nothing).  Fetches of tensors in the pageable tier pass through a
+ * pinned staging ring of 4 x 64 MiB: host threads copy a piece into a free
+ * slot, then the slot goes to the device on the copy stream; the tensors and
+ * the schedule are the same as in a pinned arena.  A tensor window must lie
+ * wholly in one tier, only parameter tensors may lie in the pageable tier,
+ * and no kernel may write one (auvm_register_tensor and auvm_add_kernel
+ * return AUVM_E_INVAL), so nothing is ever written back there.
+ * pinned_bytes: a multiple of 256, at most arena_bytes (equal: as
+ * auvm_arena_init with NULL).  Once per context; AUVM_E_NOMEM when either
+ * allocation fails.  The pageable tier extends the host side of the pooled
+ * arena beyond pinned memory (Sec. II-A: the CPU's memory as the backing
+ * store of an oversubscribed device). */
+auvm_status auvm_arena_init_tiered(auvm_ctx* ctx, uint64_t arena_bytes, uint64_t pinned_bytes);
+
 /* Register a tensor as the sub-allocation [arena_off, arena_off+bytes) of the
  * arena; ids are dense in registration order.  arena_off must be 256-aligned;
  * windows must not overlap and must lie inside the arena.  PARAM and

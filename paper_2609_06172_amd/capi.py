@@ -14,7 +14,7 @@ OK, E_INVAL, E_STATE, E_BUDGET, E_FRAG, E_HIP, E_NOMEM, E_RANGE = 0, -1, -2, -3,
 
 # every symbol the header declares
 SYMBOLS = [
-    "auvm_create", "auvm_destroy", "auvm_last_error", "auvm_arena_init",
+    "auvm_create", "auvm_destroy", "auvm_last_error", "auvm_arena_init", "auvm_arena_init_tiered",
     "auvm_register_tensor", "auvm_tensor_host_ptr", "auvm_add_kernel", "auvm_set_budget",
     "auvm_set_roofs", "auvm_set_policy", "auvm_set_kernel_times", "auvm_clear_kernels", "auvm_plan", "auvm_bind_streams", "auvm_run", "auvm_run_noalloc",
     "auvm_reset", "auvm_read_tensor", "auvm_get_counters", "auvm_get_schedule",
@@ -127,6 +127,7 @@ def bind_library(L):
         "auvm_destroy": (None, [P]),
         "auvm_last_error": (C.c_char_p, [P]),
         "auvm_arena_init": (st, [P, C.c_uint64, P]),
+        "auvm_arena_init_tiered": (st, [P, C.c_uint64, C.c_uint64]),
         "auvm_register_tensor": (st, [P, C.c_uint64, C.c_uint64, C.c_uint32, C.c_uint32,
                                       C.c_uint32, C.POINTER(C.c_int32)]),
         "auvm_tensor_host_ptr": (st, [P, C.c_int32, C.POINTER(P)]),
@@ -192,6 +193,9 @@ class Context:
 
     def arena_init(self, arena_bytes, host_pinned=None):
         self._check(self._L.auvm_arena_init(self._h, int(arena_bytes), host_pinned))
+
+    def arena_init_tiered(self, arena_bytes, pinned_bytes):
+        self._check(self._L.auvm_arena_init_tiered(self._h, int(arena_bytes), int(pinned_bytes)))
 
     def register_tensor(self, arena_off, nbytes, dtype, kind, flags=0):
         out = C.c_int32()

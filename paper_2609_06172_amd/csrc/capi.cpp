@@ -63,11 +63,35 @@ auvm_status auvm_arena_init(auvm_ctx* x, uint64_t arena_bytes, void* host_pinned
   if (c.arena_set) return fail(x, AUVM_E_STATE, "arena already initialised");
   if (arena_bytes == 0) return fail(x, AUVM_E_INVAL, "empty arena");
   c.arena_bytes = arena_bytes;
+  c.pinned_bytes = arena_bytes;
   if (host_pinned) {
     c.host = static_cast<uint8_t*>(host_pinned);
   } else if (c.device >= 0) {
     auvm_status s = host_alloc_pinned(c, arena_bytes);
     if (s != AUVM_OK) return s;
+  }
+  c.arena_set = true;
+  return AUVM_OK;
+}
+
+auvm_status auvm_arena_init_tiered(auvm_ctx* x, uint64_t arena_bytes, uint64_t pinned_bytes) {
+  if (!x) return AUVM_E_INVAL;
+  Ctx& c = x->c;
+  if (c.arena_set) return fail(x, AUVM_E_STATE, "arena already initialised");
+  if (arena_bytes == 0) return fail(x, AUVM_E_INVAL, "empty arena");
+  if (pinned_bytes > arena_bytes || pinned_bytes % kAlign)
+    return fail(x, AUVM_E_INVAL, "pinned_bytes must be a multiple of 256 no larger than the arena");
+  c.arena_bytes = arena_bytes;
+  c.pinned_bytes = pinned_bytes;
+  if (c.device >= 0) {
+    if (pinned_bytes) {
+      auvm_status s = host_alloc_pinned(c, pinned_bytes);
+      if (s != AUVM_OK) return s;
+    }
+    if (pinned_bytes < arena_bytes) {
+      auvm_status s = host_alloc_pageable(c);
+      if (s != AUVM_OK) return s;
+    }
   }
   c.arena_set = true;
   return AUVM_OK;
@@ -85,6 +109,10 @@ auvm_status auvm_register_tensor(auvm_ctx* x, uint64_t arena_off, uint64_t bytes
   uint64_t sz = align_up(bytes);
   if (arena_off > c.arena_bytes || c.arena_bytes - arena_off < sz)
     return fail(x, AUVM_E_INVAL, "tensor window outside the arena");
+  if (arena_off < c.pinned_bytes && arena_off + sz > c.pinned_bytes)
+    return fail(x, AUVM_E_INVAL, "tensor window straddles the pinned and pageable tiers");
+  if (arena_off >= c.pinned_bytes && kind != AUVM_PARAM)
+    return fail(x, AUVM_E_INVAL, "only parameter tensors may live in the pageable tier");
   for (const Tensor& t : c.tensors)  // registration-order overlap check
     if (arena_off < t.arena_off + t.size && t.arena_off < arena_off + sz)
       return fail(x, AUVM_E_INVAL, "tensor windows overlap");
@@ -104,8 +132,9 @@ auvm_status auvm_tensor_host_ptr(auvm_ctx* x, int32_t id, void** out) {
   if (!x || !out) return AUVM_E_INVAL;
   Ctx& c = x->c;
   if (id < 0 || size_t(id) >= c.tensors.size()) return fail(x, AUVM_E_INVAL, "unknown tensor id");
-  if (!c.host) return fail(x, AUVM_E_STATE, "no host arena in this context");
-  *out = c.host + c.tensors[id].arena_off;
+  const Tensor& t = c.tensors[id];
+  if (!(c.pageable(t) ? c.host_pageable : c.host)) return fail(x, AUVM_E_STATE, "no host arena in this context");
+  *out = c.host_at(t.arena_off);
   return AUVM_OK;
 }
 
@@ -122,6 +151,8 @@ auvm_status auvm_add_kernel(auvm_ctx* x, const auvm_kernel_desc* d, int32_t* out
   for (uint32_t i = 0; i < d->n; ++i) {
     int32_t id = d->ids[i];
     if (id < 0 || size_t(id) >= c.tensors.size()) return fail(x, AUVM_E_INVAL, "unknown tensor id in kernel");
+    if ((d->modes[i] & AUVM_W) && c.pageable(c.tensors[id]))
+      return fail(x, AUVM_E_INVAL, "kernel writes tensor " + std::to_string(id) + ", which lives in the pageable tier");
     k.ids.push_back(id);
     k.modes.push_back(d->modes[i]);
     bool merged = false;

@@ -26,12 +26,17 @@
 // they keep float precision over long runs.
 #include <hip/hip_runtime_api.h>
 
+#include <sys/mman.h>
+
 #include <algorithm>
 #include <chrono>
 #include <cmath>
-#include <vector>
+#include <condition_variable>
 #include <cstring>
 #include <map>
+#include <mutex>
+#include <thread>
+#include <vector>
 
 #include "ctx.h"
 #include "kernels.h"
@@ -41,6 +46,69 @@ namespace auvm {
 namespace {
 constexpr int64_t kRing = 8192;    // events per ring
 constexpr int64_t kTimeRing = 4096;
+constexpr int kCopyThreads = 8;    // host threads of a staging copy
+
+// One host memcpy split over worker threads (pageable tier to a staging slot):
+// a single thread copies about 10 GB/s, well below the host link.
+class CopyPool {
+ public:
+  explicit CopyPool(int n) : n_threads_(n) {
+    th_.reserve(size_t(n));
+    for (int i = 0; i < n; ++i) th_.emplace_back([this, i] { work(i); });
+  }
+  ~CopyPool() {
+    {
+      std::lock_guard<std::mutex> g(m_);
+      stop_ = true;
+    }
+    cv_.notify_all();
+    for (auto& t : th_) t.join();
+  }
+  void copy(uint8_t* dst, const uint8_t* src, uint64_t n) {
+    std::unique_lock<std::mutex> g(m_);
+    dst_ = dst;
+    src_ = src;
+    n_ = n;
+    left_ = n_threads_;
+    ++gen_;
+    cv_.notify_all();
+    done_.wait(g, [this] { return left_ == 0; });
+  }
+
+ private:
+  void work(int i) {
+    uint64_t seen = 0;
+    for (;;) {
+      uint8_t* d;
+      const uint8_t* s;
+      uint64_t n;
+      {
+        std::unique_lock<std::mutex> g(m_);
+        cv_.wait(g, [&] { return stop_ || gen_ != seen; });
+        if (stop_) return;
+        seen = gen_;
+        d = dst_;
+        s = src_;
+        n = n_;
+      }
+      // thread i copies the i-th of n_threads_ page-aligned parts (at least a page)
+      const uint64_t per = ((n + uint64_t(n_threads_) - 1) / uint64_t(n_threads_) + 4095) / 4096 * 4096;
+      const uint64_t a = std::min(n, per * uint64_t(i)), b = std::min(n, a + per);
+      if (b > a) std::memcpy(d + a, s + a, b - a);
+      std::lock_guard<std::mutex> g(m_);
+      if (--left_ == 0) done_.notify_one();
+    }
+  }
+  const int n_threads_;
+  std::vector<std::thread> th_;
+  std::mutex m_;
+  std::condition_variable cv_, done_;
+  uint8_t* dst_ = nullptr;
+  const uint8_t* src_ = nullptr;
+  uint64_t n_ = 0, gen_ = 0;
+  int left_ = 0;
+  bool stop_ = false;
+};
 }  // namespace
 
 class Executor {
@@ -89,6 +157,9 @@ class Executor {
     for (auto* ring : {&kev_, &hev_[0], &hev_[1], &dev_, &bases_})
       for (auto& e : *ring)
         if (e) (void)hipEventDestroy(e);
+    for (auto& e : stage_ev_)
+      if (e) (void)hipEventDestroy(e);
+    copy_pool_.reset();
     for (Track* tr : {&ktr_, &htr_[0], &htr_[1], &dtr_})
       for (auto* ring : {&tr->s, &tr->e})
         for (auto& e : *ring)
@@ -115,6 +186,13 @@ class Executor {
   auvm_status reset() {
     if (!ok(hipSetDevice(c_.device), "hipSetDevice")) return AUVM_E_HIP;
     if (!sync_all()) return AUVM_E_HIP;
+    // a tiered arena's staging events and copy threads (the arena comes after
+    // the executor; every plan resets it before a run)
+    if (!c_.stage.empty() && !copy_pool_) {
+      for (auto& e : stage_ev_)
+        if (!ok(hipEventCreateWithFlags(&e, hipEventDisableTiming), "hipEventCreate")) return AUVM_E_HIP;
+      copy_pool_.reset(new CopyPool(kCopyThreads));
+    }
     const size_t nT = c_.tensors.size(), K = c_.kernels.size();
     cursor_ = 0;
     next_k_ = 0;
@@ -223,7 +301,7 @@ class Executor {
       if (!ok(hipMemcpy(dst, c_.pool + where_[id], t.bytes, hipMemcpyDeviceToHost), "hipMemcpy D2H"))
         return AUVM_E_HIP;
     } else {
-      std::memcpy(dst, c_.host + t.arena_off, t.bytes);
+      std::memcpy(dst, c_.host_at(t.arena_off), t.bytes);
     }
     return AUVM_OK;
   }
@@ -252,6 +330,27 @@ class Executor {
   // h2d stream of copy number seq (the rings and waits stay per parity: with
   // one stream for both they are only stronger than needed)
   int lane(int64_t seq) const { return two_h2d_ ? par(seq) : 1; }
+
+  // A copy from the pageable tier: pieces of at most kStageBytes go through
+  // the pinned staging ring.  A slot is refilled once the device copy that
+  // read it last has completed (its previous copies were issued earlier, so
+  // the wait ends); the host copy of a piece overlaps the device copies of
+  // the pieces before it.
+  bool staged_copy(uint8_t* dst, const uint8_t* src, uint64_t bytes, hipStream_t st) {
+    if (c_.stage.size() != size_t(kStageSlots) || !copy_pool_) return ok(hipErrorInvalidValue, "staging ring");
+    for (uint64_t done = 0; done < bytes;) {
+      const uint64_t n = std::min(kStageBytes, bytes - done);
+      const int s = int(stage_next_++ % kStageSlots);
+      if (stage_used_[s] && !ok(hipEventSynchronize(stage_ev_[s]), "hipEventSynchronize")) return false;
+      copy_pool_->copy(c_.stage[s], src + done, n);
+      if (!ok(hipMemcpyAsync(dst + done, c_.stage[s], n, hipMemcpyHostToDevice, st), "hipMemcpyAsync H2D"))
+        return false;
+      if (!ok(hipEventRecord(stage_ev_[s], st), "hipEventRecord")) return false;
+      stage_used_[s] = true;
+      done += n;
+    }
+    return true;
+  }
 
   bool ok(hipError_t e, const char* what) {
     if (e == hipSuccess) return true;
@@ -334,7 +433,7 @@ class Executor {
           const Tensor& x = c_.tensors[t];
           if (c_.pol.timing && !begin_item(dtr_, d2h_, AUVM_TL_D2H, int64_t(cursor_), x.bytes))
             return AUVM_E_HIP;
-          if (!ok(hipMemcpyAsync(c_.host + x.arena_off, c_.pool + e.dev_off, x.bytes,
+          if (!ok(hipMemcpyAsync(c_.host_at(x.arena_off), c_.pool + e.dev_off, x.bytes,
                                  hipMemcpyDeviceToHost, d2h_), "hipMemcpyAsync D2H"))
             return AUVM_E_HIP;
           if (c_.pol.timing && !end_item(dtr_, d2h_)) return AUVM_E_HIP;
@@ -380,9 +479,12 @@ class Executor {
         const Tensor& x = c_.tensors[t];
         const int32_t kind = ln == 1 ? AUVM_TL_H2D : AUVM_TL_H2D_B;   // odd copy numbers: the first stream
         if (c_.pol.timing && !begin_item(htr_[ln], st, kind, int64_t(cursor_), x.bytes)) return AUVM_E_HIP;
-        if (!ok(hipMemcpyAsync(c_.pool + e.dev_off, c_.host + x.arena_off, x.bytes,
-                               hipMemcpyHostToDevice, st), "hipMemcpyAsync H2D"))
+        if (c_.pageable(x)) {
+          if (!staged_copy(c_.pool + e.dev_off, c_.host_at(x.arena_off), x.bytes, st)) return AUVM_E_HIP;
+        } else if (!ok(hipMemcpyAsync(c_.pool + e.dev_off, c_.host + x.arena_off, x.bytes,
+                                      hipMemcpyHostToDevice, st), "hipMemcpyAsync H2D")) {
           return AUVM_E_HIP;
+        }
         if (c_.pol.timing && !end_item(htr_[ln], st)) return AUVM_E_HIP;
         h2d_seq_ = seq;
         if (!record(hev_[sp], hown_[sp], seq, st)) return AUVM_E_HIP;
@@ -551,6 +653,10 @@ class Executor {
   }
 
   Ctx& c_;
+  hipEvent_t stage_ev_[kStageSlots] = {};   // last device copy out of each staging slot
+  bool stage_used_[kStageSlots] = {};
+  uint64_t stage_next_ = 0;
+  std::unique_ptr<CopyPool> copy_pool_;
   hipStream_t comp_ = nullptr, h2d_[2] = {nullptr, nullptr}, d2h_ = nullptr;
   bool own_[4] = {false, false, false, false};   // comp_, h2d_[0], h2d_[1], d2h_
   std::vector<hipEvent_t> kev_, hev_[2], dev_, bases_;   // hev_[p]: copies of h2d stream p
@@ -616,6 +722,25 @@ auvm_status host_alloc_pinned(Ctx& c, uint64_t bytes) {
   return AUVM_OK;
 }
 
+auvm_status host_alloc_pageable(Ctx& c) {
+  const uint64_t n = c.arena_bytes - c.pinned_bytes;
+  void* p = mmap(nullptr, n, PROT_READ | PROT_WRITE, MAP_PRIVATE | MAP_ANONYMOUS | MAP_NORESERVE, -1, 0);
+  if (p == MAP_FAILED) {
+    c.err = "mmap of the pageable host tier failed";
+    return AUVM_E_NOMEM;
+  }
+  c.host_pageable = static_cast<uint8_t*>(p);
+  for (int i = 0; i < kStageSlots; ++i) {
+    void* s = nullptr;
+    if (hipHostMalloc(&s, kStageBytes, hipHostMallocDefault) != hipSuccess || !s) {
+      c.err = "hipHostMalloc of the staging ring failed";
+      return AUVM_E_NOMEM;
+    }
+    c.stage.push_back(static_cast<uint8_t*>(s));
+  }
+  return AUVM_OK;
+}
+
 auvm_status device_alloc_pool(Ctx& c, uint64_t bytes) {
   void* p = nullptr;
   if (hipSetDevice(c.device) != hipSuccess || hipMalloc(&p, bytes) != hipSuccess || !p) {
@@ -640,6 +765,10 @@ void free_owned(Ctx& c) {
   if (c.device >= 0) (void)hipSetDevice(c.device);
   if (c.pool_owned && c.pool) (void)hipFree(c.pool);
   if (c.host_owned && c.host) (void)hipHostFree(c.host);
+  if (c.host_pageable) (void)munmap(c.host_pageable, c.arena_bytes - c.pinned_bytes);
+  for (uint8_t* s : c.stage) (void)hipHostFree(s);
+  c.stage.clear();
+  c.host_pageable = nullptr;
   c.pool = nullptr;
   c.host = nullptr;
   c.pool_owned = c.host_owned = false;

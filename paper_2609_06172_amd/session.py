@@ -18,17 +18,51 @@ from .capi import Context
 NP_DTYPE = {DT_F32: np.float32, DT_I32: np.int32, DT_U8: np.uint8, DT_BF16: np.uint16}
 
 
+def host_layout(w, pinned_limit=None):
+    """Arena offsets of the workload's tensors and the pinned tier's size.
+
+    Without a limit, or when the whole arena fits it, the workload's own
+    offsets and a pinned arena (None).  Otherwise a tiered arena: first every
+    tensor that is not a parameter or that some kernel writes (these must be
+    pinned), then the read-only parameters in registration order, the pinned
+    tier ending before the first tensor that would cross the limit."""
+    from workloads.format import MODE_W
+    if pinned_limit is None or w.arena_bytes <= pinned_limit:
+        return [t.off for t in w.tensors], None
+    written = {tid for k in w.kernels for tid, m in k.operands if m & MODE_W}
+    pin = {t.tid for t in w.tensors if t.kind != KIND_PARAM or t.tid in written}
+    must = [t for t in w.tensors if t.tid in pin]
+    rest = [t for t in w.tensors if t.tid not in pin]
+    offs, off, pinned = [0] * len(w.tensors), 0, None
+    for t in must + rest:
+        size = (t.nbytes + 255) // 256 * 256
+        if pinned is None and t.tid not in pin and off + size > pinned_limit:
+            pinned = off
+        offs[t.tid] = off
+        off += size
+    if pinned is None:
+        pinned = off
+    if sum((t.nbytes + 255) // 256 * 256 for t in must) > pinned_limit:
+        raise ValueError("the tensors that must be pinned exceed the pinned limit")
+    return offs, pinned
+
+
 class Session:
     def __init__(self, w, device=-1, M=None, variant=4, lookahead=0, affinity_w=1, placement=0,
                  validate=0, timing=0, roofs=None, fill=True, threads=16, guard=None, bucket=None,
-                 object_bytes=0):
+                 object_bytes=0, pinned_limit=None):
         self.w = w
         self.device = device
         self.ctx = Context(device)
         ctx = self.ctx
-        ctx.arena_init(w.arena_bytes)
+        offs, pinned = host_layout(w, pinned_limit)
+        if pinned is None:
+            ctx.arena_init(w.arena_bytes)
+        else:
+            ctx.arena_init_tiered(w.arena_bytes, pinned)
+        self.pinned_bytes = w.arena_bytes if pinned is None else pinned
         for t in w.tensors:
-            tid = ctx.register_tensor(t.off, t.nbytes, t.dtype, t.kind, t.flags)
+            tid = ctx.register_tensor(offs[t.tid], t.nbytes, t.dtype, t.kind, t.flags)
             assert tid == t.tid
         if device >= 0 and fill:
             winit.fill_host(w, self.host_view, threads=threads)

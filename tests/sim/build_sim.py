@@ -50,7 +50,7 @@ def build(sanitize=None):
         if os.path.exists(out) and os.path.getmtime(out) >= max(os.path.getmtime(d) for d in deps):
             return out
         tmp = f"{out}.{os.getpid()}.tmp"
-        cmd = ["g++", "-O1", "-g", "-fPIC", "-shared", "-std=c++17", "-Wall", "-Wno-unused-function"] + flags + [
+        cmd = ["g++", "-O1", "-g", "-fPIC", "-shared", "-std=c++17", "-pthread", "-Wall", "-Wno-unused-function"] + flags + [
                "-I" + HERE, "-I" + os.path.join(ROOT, "include"), "-I" + CSRC] + SOURCES + ["-o", tmp]
         subprocess.run(cmd, check=True)
         os.replace(tmp, out)

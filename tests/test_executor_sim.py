@@ -55,21 +55,45 @@ def feasible_budget(tensors, kernels, variant, fracs=((1, 2), (2, 3), (3, 4), (5
 
 
 def run_touch_trace(seed, variant, order_seed, cuts=3, read_only=False, bind=None, timing=0, out=None,
-                    object_bytes=0):
+                    object_bytes=0, tiered=False, big=0):
     """Runs a random touch trace on the simulated executor; returns (executed log
-    equals the plan, reads that saw the wrong version)."""
+    equals the plan, reads that saw the wrong version).
+
+    big: that many read-only parameters of 100 MiB + 4 KiB (larger than a
+    staging slot) joined to the trace, each read by every fifth kernel in turn.
+    tiered: a tiered host arena whose pageable tier holds every parameter that
+    no kernel writes (fetched through the staging ring)."""
     from paper_2609_06172_amd.capi import Context
     L = sim_library()
     n_kernels = (60 if read_only else 40) + (seed * 7) % 60
     tensors, kernels = random_trace(seed, touch=True, n_kernels=n_kernels, read_only=read_only)
-    M = feasible_budget(tensors, kernels, variant, object_bytes=object_bytes)
+    for b in range(big):
+        tensors.append(dict(nbytes=(100 << 20) + 4096, dtype=tensors[1]["dtype"] if len(tensors) > 1 else 3,
+                            kind=KIND_PARAM, host_init=True))
+    for k, kd in enumerate(kernels):
+        if big and k % 5 == 0 and len(kd["operands"]) < 7:
+            kd["operands"].append((len(tensors) - big + (k // 5) % big, 1))
+    M = feasible_budget(tensors, kernels, variant, object_bytes=object_bytes,
+                        fracs=((3, 4), (5, 6), (1, 1)) if big else ((1, 2), (2, 3), (3, 4), (5, 6), (1, 1)))
     w = Workload(None)
     for i, t in enumerate(tensors):
         w.tensor(f"t{i}", (t["nbytes"],), t["dtype"], t["kind"], host_init=t["host_init"])
     ctx = Context(0, library=L)
-    ctx.arena_init(w.arena_bytes)
+    offs = [t.off for t in w.tensors]
+    if tiered:
+        written = {u for kd in kernels for u, m in kd["operands"] if m & 2}
+        pin = [t for t in w.tensors if t.kind != KIND_PARAM or t.tid in written]
+        page = [t for t in w.tensors if not (t.kind != KIND_PARAM or t.tid in written)]
+        assert page
+        off = 0
+        for t in pin + page:
+            offs[t.tid] = off
+            off += (t.nbytes + 255) // 256 * 256
+        ctx.arena_init_tiered(w.arena_bytes, offs[page[0].tid])
+    else:
+        ctx.arena_init(w.arena_bytes)
     for t in w.tensors:
-        ctx.register_tensor(t.off, t.nbytes, t.dtype, t.kind, t.flags)
+        ctx.register_tensor(offs[t.tid], t.nbytes, t.dtype, t.kind, t.flags)
     init = {}
     for i, t in enumerate(tensors):
         view = np.ctypeslib.as_array((C.c_uint8 * t["nbytes"]).from_address(ctx.tensor_host_ptr(i)))
@@ -112,6 +136,40 @@ def test_touch_traces_read_latest_versions_in_any_order(seed, variant):
         executed_ok, bad = run_touch_trace(seed, variant, order_seed, cuts=1 + order_seed % 3)
         assert executed_ok
         assert not bad, (seed, variant, order_seed, bad[:4])
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_pageable_tier_through_the_staging_ring(seed):
+    """A tiered host arena: the parameters no kernel writes live in pageable
+    memory and reach the device through the pinned staging ring, two of them
+    larger than a slot (they move in pieces, reusing slots): every kernel
+    still reads the latest version of each operand, in any order of
+    execution the event waits allow, and the executed log equals the plan."""
+    for variant in (1, 4):
+        executed_ok, bad = run_touch_trace(seed, variant, seed, cuts=2, tiered=True, big=2)
+        assert executed_ok
+        assert not bad, (seed, variant, bad[:4])
+
+
+def test_tiered_arena_refuses_what_would_need_a_write_back():
+    """Only parameters may live in the pageable tier, a window may not
+    straddle the tiers, and no kernel may write a pageable tensor."""
+    from paper_2609_06172_amd.capi import AuvmError, Context
+    from workloads.format import DT_U8, KIND_ACT, MODE_R, MODE_RW, OP_TOUCH
+    ctx = Context(0, library=sim_library())
+    with pytest.raises(AuvmError):
+        ctx.arena_init_tiered(4096, 1000)          # not a multiple of 256
+    ctx.arena_init_tiered(4096, 1024)
+    log = ctx.register_tensor(0, 512, DT_U8, KIND_ACT)
+    with pytest.raises(AuvmError):
+        ctx.register_tensor(768, 512, DT_U8, KIND_PARAM)   # straddles 1024
+    with pytest.raises(AuvmError):
+        ctx.register_tensor(1024, 512, DT_U8, KIND_ACT)    # activation in the pageable tier
+    p = ctx.register_tensor(1024, 512, DT_U8, KIND_PARAM)
+    ctx.add_kernel(OP_TOUCH, (0,), [(log, MODE_RW), (p, MODE_R)])
+    with pytest.raises(AuvmError):
+        ctx.add_kernel(OP_TOUCH, (1,), [(log, MODE_RW), (p, MODE_RW)])
+    ctx.destroy()
 
 
 @pytest.mark.parametrize("variant", [1, 2, 3, 4])

@@ -226,6 +226,36 @@ def test_timed_launches_compute_the_same(name):
         assert np.array_equal(out[0][k], out[1][k]), k
 
 
+@pytest.mark.parametrize("name", ["llama-small", "moe-small"])
+def test_pageable_host_tier_computes_the_same(name):
+    # a tiered host arena: half of the read-only weights' bytes in pageable
+    # memory, fetched through the pinned staging ring; outputs bit-identical
+    # to the pinned arena's, the same schedule executed
+    from paper_2609_06172_amd.session import Session, host_layout
+    from workloads import configs as C
+    from workloads.format import KIND_PARAM, MODE_W
+    cfg = {"llama-small": C.LLAMA_SMALL, "moe-small": C.MOE_SMALL}[name]
+    w = trace.build(cfg)
+    written = {t for k in w.kernels for t, m in k.operands if m & MODE_W}
+    ro = sum((t.nbytes + 255) // 256 * 256 for t in w.tensors if t.kind == KIND_PARAM and t.tid not in written)
+    limit = w.arena_bytes - ro // 2
+    offs, pinned = host_layout(w, limit)
+    assert pinned is not None and pinned <= limit < w.arena_bytes
+    out = []
+    for lim in (None, limit):
+        print(f"{name}: pinned limit {lim}", flush=True)
+        s = Session(w, device=0, pinned_limit=lim)
+        s.run_all()
+        out.append({n: s.read(n).copy() for n in ("logits", "gen")})
+        assert s.ctx.get_executed() == s.ctx.get_schedule()
+        if lim is not None:
+            assert s.pinned_bytes == pinned
+            assert any(s.ctx.tensor_host_ptr(t.tid) != 0 for t in w.tensors)
+        s.close()
+    for k in out[0]:
+        assert np.array_equal(out[0][k], out[1][k]), k
+
+
 def test_replanning_from_measured_kernel_times():
     # runtime monitor: a timed run, classes again from the measured
     # durations, a new plan (the oracle's, bit for bit), the same outputs
