@@ -530,18 +530,11 @@ class Executor {
     }
     const bool timing = c_.pol.timing != 0;
     if (timing) {
-      // the op's kernels record the item's events at their own start and end
       if (ktr_.n != k) return internal("timed kernels must run from kernel 0 in order");
-      if (!begin_item(ktr_, comp_, AUVM_TL_KERNEL, k, 0, false)) return AUVM_E_HIP;
-      launch_events_arm(ktr_.s[ktr_.n % kTimeRing], ktr_.e[ktr_.n % kTimeRing]);
+      if (!begin_item(ktr_, comp_, AUVM_TL_KERNEL, k, 0)) return AUVM_E_HIP;
     }
-    const hipError_t le = launch_op(kd, c_.tensors, ptrs, comp_);
-    const bool recorded = timing && launch_events_disarm();
-    if (!ok(le, "kernel launch")) return AUVM_E_HIP;
-    if (timing) {
-      if (!recorded && !ok(hipEventRecord(ktr_.s[ktr_.n % kTimeRing], comp_), "hipEventRecord")) return AUVM_E_HIP;
-      if (!end_item(ktr_, comp_, !recorded)) return AUVM_E_HIP;
-    }
+    if (!ok(launch_op(kd, c_.tensors, ptrs, comp_), "kernel launch")) return AUVM_E_HIP;
+    if (timing && !end_item(ktr_, comp_)) return AUVM_E_HIP;
     if (need_ev_[k] && !record(kev_, kown_, k, comp_)) return AUVM_E_HIP;
     for (auto& a : kd.acc) last_use_[a.first] = k;
     next_k_ = k + 1;
@@ -590,9 +583,7 @@ class Executor {
     return true;
   }
 
-  // record: the start (end) event goes on stream st now; otherwise the
-  // caller has it recorded (a kernel launched with it)
-  bool begin_item(Track& tr, hipStream_t st, int32_t kind, int64_t index, uint64_t bytes, bool record = true) {
+  bool begin_item(Track& tr, hipStream_t st, int32_t kind, int64_t index, uint64_t bytes) {
     while (tr.harvested + kTimeRing <= tr.n)   // free the slot this item reuses
       if (!harvest(tr, tr.harvested++)) return false;
     auvm_timeline_entry x{};
@@ -603,10 +594,10 @@ class Executor {
     x.host_ms = std::chrono::duration<double, std::milli>(std::chrono::steady_clock::now() - host0_).count();
     tr.tl.push_back(int64_t(tl_.size()));
     tl_.push_back(x);
-    return !record || ok(hipEventRecord(tr.s[tr.n % kTimeRing], st), "hipEventRecord");
+    return ok(hipEventRecord(tr.s[tr.n % kTimeRing], st), "hipEventRecord");
   }
-  bool end_item(Track& tr, hipStream_t st, bool record = true) {
-    if (record && !ok(hipEventRecord(tr.e[tr.n % kTimeRing], st), "hipEventRecord")) return false;
+  bool end_item(Track& tr, hipStream_t st) {
+    if (!ok(hipEventRecord(tr.e[tr.n % kTimeRing], st), "hipEventRecord")) return false;
     ++tr.n;
     return true;
   }

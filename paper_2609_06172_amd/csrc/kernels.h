@@ -14,13 +14,6 @@ namespace auvm {
 hipError_t launch_op(const Kernel& k, const std::vector<Tensor>& T, uint8_t* const* ptrs,
                      hipStream_t s);
 
-// Timing of the next launch_op: its first kernel records `start` when it
-// starts on the device and its last kernel `stop` when it ends (an op
-// without a kernel records them on the stream around its work).  Disarm
-// returns whether the op recorded them.  Per host thread.
-void launch_events_arm(hipEvent_t start, hipEvent_t stop);
-bool launch_events_disarm();
-
 // Fill `bytes` at `p` with 0xFF (NaN for f32/bf16) on stream s.
 hipError_t launch_poison(uint8_t* p, uint64_t bytes, hipStream_t s);
 

@@ -707,29 +707,29 @@ __global__ void __launch_bounds__(64 * FW, 1) attn_bwd_dkv_d128(AttnBwdArgs a, i
 
 hipError_t launch_attention_bwd_d128(const AttnBwdArgs& a, hipStream_t s) {
   const int64_t nb = (a.S + FQ - 1) / FQ;
-  launch_kernel(attn_bwd_dkv_d128, dim3(unsigned(a.B * a.nH * nb)), dim3(64 * FW), kFlashLds, s, a, nb);
+  hipLaunchKernelGGL(attn_bwd_dkv_d128, dim3(unsigned(a.B * a.nH * nb)), dim3(64 * FW), kFlashLds, s, a, nb);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  launch_kernel(attn_bwd_dq_d128, dim3(unsigned(a.B * a.nH * nb)), dim3(64 * FW), kFlashLds, s, a, nb);
+  hipLaunchKernelGGL(attn_bwd_dq_d128, dim3(unsigned(a.B * a.nH * nb)), dim3(64 * FW), kFlashLds, s, a, nb);
   return hipGetLastError();
 }
 
 hipError_t launch_attention(const AttnArgs& a, hipStream_t s) {
   const int64_t rows = a.B * a.nH * a.S;
   if (a.bf16 && a.d == 128 && a.S <= 16 && !a.lse) {
-    launch_kernel(attn_decode_d128, dim3(unsigned(rows)), dim3(64 * kDecWaves), 0, s, a);
+    hipLaunchKernelGGL(attn_decode_d128, dim3(unsigned(rows)), dim3(64 * kDecWaves), 0, s, a);
     return hipGetLastError();
   }
   if (a.bf16 && a.d == 128) {
     const int64_t nqb = (a.S + FQ - 1) / FQ;
-    launch_kernel(attn_prefill_d128, dim3(unsigned(a.B * a.nH * nqb)), dim3(64 * FW), kFlashLds, s, a, nqb);
+    hipLaunchKernelGGL(attn_prefill_d128, dim3(unsigned(a.B * a.nH * nqb)), dim3(64 * FW), kFlashLds, s, a, nqb);
     return hipGetLastError();
   }
   dim3 grid(unsigned((rows + 3) / 4));
   if (a.bf16)
-    launch_kernel(attn_rowwave<bf16_t>, grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL(attn_rowwave<bf16_t>, grid, dim3(256), 0, s, a);
   else
-    launch_kernel(attn_rowwave<float>, grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL(attn_rowwave<float>, grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

@@ -1,35 +1,11 @@
 // Device helpers shared by the HIP kernels (gfx950).
 #pragma once
 
-#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
 
 namespace auvm {
-
-// Timing of traced kernels.  Under the executor's timing policy an op's
-// kernels are launched with a pair of events armed (kernels.h): the op's
-// first kernel carries `start` and each of its kernels `stop`, so the last
-// one keeps it.  hipExtLaunchKernelGGL records such events at the kernel's
-// own start and end on the device; events recorded on the stream around the
-// launch would add the dispatch gap in front of the kernel to its time.
-struct LaunchEvents {
-  hipEvent_t start = nullptr, stop = nullptr;
-  bool used = false;
-};
-LaunchEvents& launch_events();   // the calling host thread's (kernels/ops.hip)
-
-template <typename F, typename... Args>
-inline void launch_kernel(F kernel, dim3 grid, dim3 block, size_t lds, hipStream_t s, Args... args) {
-  LaunchEvents& e = launch_events();
-  if (e.stop) {
-    hipExtLaunchKernelGGL(kernel, grid, block, uint32_t(lds), s, e.used ? nullptr : e.start, e.stop, 0u, args...);
-    e.used = true;
-  } else {
-    hipLaunchKernelGGL(kernel, grid, block, lds, s, args...);
-  }
-}
 namespace dev {
 
 typedef uint16_t bf16_t;  // storage of a bfloat16 value

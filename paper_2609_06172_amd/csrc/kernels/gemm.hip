@@ -106,11 +106,11 @@ hipError_t run(const GemmArgs& g, hipStream_t s) {
   TC* C = reinterpret_cast<TC*>(g.c);
   if (g.M <= 16) {
     dim3 grid(unsigned((g.N + 255) / 256), unsigned((g.M + 15) / 16));
-    launch_kernel((gemm_tiled<16, 256, 1, 16, TA, TC, EPI>), grid, dim3(256), 0, s, A, W, W2, C,
+    hipLaunchKernelGGL((gemm_tiled<16, 256, 1, 16, TA, TC, EPI>), grid, dim3(256), 0, s, A, W, W2, C,
                        g.M, g.N, g.K);
   } else {
     dim3 grid(unsigned((g.N + 63) / 64), unsigned((g.M + 63) / 64));
-    launch_kernel((gemm_tiled<64, 64, 4, 4, TA, TC, EPI>), grid, dim3(256), 0, s, A, W, W2, C,
+    hipLaunchKernelGGL((gemm_tiled<64, 64, 4, 4, TA, TC, EPI>), grid, dim3(256), 0, s, A, W, W2, C,
                        g.M, g.N, g.K);
   }
   return hipGetLastError();

@@ -245,7 +245,7 @@ hipError_t go(const GemmArgs& g, hipStream_t s) {
   using S = Shape<EPI>;
   const int tilesM = int((g.M + S::kBM - 1) / S::kBM), tilesN = int((g.N + S::kBN - 1) / S::kBN);
   const size_t lds = size_t(2) * S::kStage * sizeof(bf16_t);
-  launch_kernel((gemm_big<EPI, TC, LIST>), dim3(unsigned(tilesM * tilesN)), dim3(64 * kWaves), lds, s,
+  hipLaunchKernelGGL((gemm_big<EPI, TC, LIST>), dim3(unsigned(tilesM * tilesN)), dim3(64 * kWaves), lds, s,
                      reinterpret_cast<const bf16_t*>(g.a), reinterpret_cast<const bf16_t*>(g.w),
                      reinterpret_cast<const bf16_t*>(g.w2), reinterpret_cast<TC*>(g.c), g.M, g.N, g.K,
                      tilesN, g.list, g.rw, g.topk);

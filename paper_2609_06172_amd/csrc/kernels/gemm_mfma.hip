@@ -164,7 +164,7 @@ template <int EPI, class TC>
 hipError_t go(const GemmArgs& g, hipStream_t s) {
   const int tilesM = int((g.M + BM - 1) / BM), tilesN = int((g.N + BN - 1) / BN);
   const size_t lds = size_t(2) * (BM + BN + (EPI == EPI_SWIGLU ? BN : 0)) * LDK * sizeof(bf16_t);
-  launch_kernel((gemm_mfma<EPI, TC>), dim3(unsigned(tilesM * tilesN)), dim3(256), lds, s,
+  hipLaunchKernelGGL((gemm_mfma<EPI, TC>), dim3(unsigned(tilesM * tilesN)), dim3(256), lds, s,
                      reinterpret_cast<const bf16_t*>(g.a), reinterpret_cast<const bf16_t*>(g.w),
                      reinterpret_cast<const bf16_t*>(g.w2), reinterpret_cast<TC*>(g.c), g.M, g.N, g.K,
                      tilesN);

@@ -193,7 +193,7 @@ hipError_t go(const GemmArgs& g, hipStream_t s) {
   grp.c1 = c[1];
   grp.c2 = c[2];
   dim3 grid(unsigned(ng * ((g.N + 15) / 16)));
-  launch_kernel((gemv_mfma<EPI, TC, LIST>), grid, dim3(64 * kWaves), 0, s, reinterpret_cast<const bf16_t*>(g.a),
+  hipLaunchKernelGGL((gemv_mfma<EPI, TC, LIST>), grid, dim3(64 * kWaves), 0, s, reinterpret_cast<const bf16_t*>(g.a),
                      grp, reinterpret_cast<const bf16_t*>(g.w2), int(g.M), g.N, g.K, g.list, g.rw, g.topk);
   return hipGetLastError();
 }

@@ -141,17 +141,17 @@ hipError_t launch_moe_route(const void* h, const void* wr, int32_t* rte, float* 
                             int K, bool bf16, hipStream_t s) {
   dim3 grid(unsigned((M + 3) / 4));
   if (bf16)
-    launch_kernel(moe_route_kernel<bf16_t>, grid, dim3(256), 0, s, static_cast<const bf16_t*>(h),
+    hipLaunchKernelGGL(moe_route_kernel<bf16_t>, grid, dim3(256), 0, s, static_cast<const bf16_t*>(h),
                        static_cast<const bf16_t*>(wr), rte, rtw, M, H, E, K);
   else
-    launch_kernel(moe_route_kernel<float>, grid, dim3(256), 0, s, static_cast<const float*>(h),
+    hipLaunchKernelGGL(moe_route_kernel<float>, grid, dim3(256), 0, s, static_cast<const float*>(h),
                        static_cast<const float*>(wr), rte, rtw, M, H, E, K);
   return hipGetLastError();
 }
 
 hipError_t launch_moe_dispatch(const int32_t* rte, int32_t* lists, int32_t* log, int64_t M, int K, int E,
                                int64_t log_row, hipStream_t s) {
-  launch_kernel(moe_dispatch_kernel, dim3(unsigned(E)), dim3(1024), 0, s, rte, lists, log, M, K, E, log_row);
+  hipLaunchKernelGGL(moe_dispatch_kernel, dim3(unsigned(E)), dim3(1024), 0, s, rte, lists, log, M, K, E, log_row);
   return hipGetLastError();
 }
 

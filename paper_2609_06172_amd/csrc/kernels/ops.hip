@@ -164,13 +164,13 @@ void launch_norm(const uint8_t* x, const uint8_t* g, const uint8_t* b, uint8_t* 
   const TO *gp = reinterpret_cast<const TO*>(g), *bp = reinterpret_cast<const TO*>(b);
   TO* hp = reinterpret_cast<TO*>(h);
   if (H % 4 == 0 && H <= 4 * 256 * 2)
-    launch_kernel((norm_vec_kernel<TO, LN, 2>), dim3(unsigned(T)), dim3(256), 0, s, xf, gp, bp, hp, H,
+    hipLaunchKernelGGL((norm_vec_kernel<TO, LN, 2>), dim3(unsigned(T)), dim3(256), 0, s, xf, gp, bp, hp, H,
                        sh[2], sh[3], eps);
   else if (H % 4 == 0 && H <= 4 * 256 * 8)
-    launch_kernel((norm_vec_kernel<TO, LN, 8>), dim3(unsigned(T)), dim3(256), 0, s, xf, gp, bp, hp, H,
+    hipLaunchKernelGGL((norm_vec_kernel<TO, LN, 8>), dim3(unsigned(T)), dim3(256), 0, s, xf, gp, bp, hp, H,
                        sh[2], sh[3], eps);
   else
-    launch_kernel((norm_kernel<TO, LN>), dim3(unsigned(T)), dim3(256), 0, s, xf, gp, bp, hp, H, sh[2],
+    hipLaunchKernelGGL((norm_kernel<TO, LN>), dim3(unsigned(T)), dim3(256), 0, s, xf, gp, bp, hp, H, sh[2],
                        sh[3], eps);
 }
 
@@ -241,7 +241,7 @@ template <class T>
 hipError_t rope_kv(uint8_t* const* p, const int64_t* s, hipStream_t st_) {
   const int64_t B = s[0], S = s[1], nH = s[2], d = s[3], Lmax = s[4], pos0 = s[5];
   int threads = int(d / 2 < 64 ? 64 : d / 2);
-  launch_kernel(rope_kv_kernel<T>, dim3(unsigned(B * S * nH)), dim3(threads), 0, st_, (T*)p[0],
+  hipLaunchKernelGGL(rope_kv_kernel<T>, dim3(unsigned(B * S * nH)), dim3(threads), 0, st_, (T*)p[0],
                      (const T*)p[1], (const T*)p[2], (T*)p[3], (T*)p[4], S, nH, d, Lmax, pos0);
   return hipGetLastError();
 }
@@ -250,20 +250,6 @@ hipError_t rope_kv(uint8_t* const* p, const int64_t* s, hipStream_t st_) {
 
 hipError_t launch_poison(uint8_t* p, uint64_t bytes, hipStream_t s) {
   return hipMemsetAsync(p, 0xff, bytes, s);
-}
-
-LaunchEvents& launch_events() {
-  static thread_local LaunchEvents e;
-  return e;
-}
-
-void launch_events_arm(hipEvent_t start, hipEvent_t stop) { launch_events() = LaunchEvents{start, stop, false}; }
-
-bool launch_events_disarm() {
-  LaunchEvents& e = launch_events();
-  const bool used = e.used;
-  e = LaunchEvents{};
-  return used;
 }
 
 hipError_t launch_op(const Kernel& k, const std::vector<Tensor>& T, uint8_t* const* p, hipStream_t s) {
@@ -280,15 +266,15 @@ hipError_t launch_op(const Kernel& k, const std::vector<Tensor>& T, uint8_t* con
         a.words[i] = T[k.ids[i + 1]].bytes / 4;
         a.mode[i] = k.modes[i + 1];
       }
-      launch_kernel(touch_kernel, dim3(a.n), dim3(256), 0, s, a);
+      hipLaunchKernelGGL(touch_kernel, dim3(a.n), dim3(256), 0, s, a);
       return hipGetLastError();
     }
     case AUVM_OP_EMBED:
       if (dt(1) == AUVM_BF16)
-        launch_kernel(embed_kernel<bf16_t>, dim3(unsigned(sh[0])), dim3(256), 0, s,
+        hipLaunchKernelGGL(embed_kernel<bf16_t>, dim3(unsigned(sh[0])), dim3(256), 0, s,
                            (const int32_t*)p[0], (const bf16_t*)p[1], (float*)p[2], sh[1], sh[2]);
       else
-        launch_kernel(embed_kernel<float>, dim3(unsigned(sh[0])), dim3(256), 0, s,
+        hipLaunchKernelGGL(embed_kernel<float>, dim3(unsigned(sh[0])), dim3(256), 0, s,
                            (const int32_t*)p[0], (const float*)p[1], (float*)p[2], sh[1], sh[2]);
       return hipGetLastError();
     case AUVM_OP_LAYERNORM:
@@ -339,18 +325,8 @@ hipError_t launch_op(const Kernel& k, const std::vector<Tensor>& T, uint8_t* con
       }
       return launch_gemm(g, s);
     }
-    case AUVM_OP_COPY: {
-      // no kernel: armed timing events go on the stream around the copy
-      LaunchEvents& e = launch_events();
-      if (e.stop && !e.used) {
-        const hipError_t r = hipEventRecord(e.start, s);
-        if (r != hipSuccess) return r;
-      }
-      const hipError_t r = hipMemcpyAsync(p[1], p[0], size_t(sh[0]), hipMemcpyDeviceToDevice, s);
-      if (r != hipSuccess || !e.stop) return r;
-      e.used = true;
-      return hipEventRecord(e.stop, s);
-    }
+    case AUVM_OP_COPY:
+      return hipMemcpyAsync(p[1], p[0], size_t(sh[0]), hipMemcpyDeviceToDevice, s);
     case AUVM_OP_TRANSPOSE:
       return launch_transpose(p[0], p[1], sh[0], sh[1], dt(0) == AUVM_BF16, s);
     case AUVM_OP_SWIGLU_ACT:
@@ -452,7 +428,7 @@ hipError_t launch_op(const Kernel& k, const std::vector<Tensor>& T, uint8_t* con
     case AUVM_OP_ROPE_KV:
       return dt(0) == AUVM_BF16 ? rope_kv<bf16_t>(p, sh, s) : rope_kv<float>(p, sh, s);
     case AUVM_OP_ARGMAX:
-      launch_kernel(argmax_kernel, dim3(unsigned(sh[0])), dim3(256), 0, s, (const float*)p[0],
+      hipLaunchKernelGGL(argmax_kernel, dim3(unsigned(sh[0])), dim3(256), 0, s, (const float*)p[0],
                          (int32_t*)p[1], k.ids.size() > 2 ? (int32_t*)p[2] : nullptr, sh[1], sh[0],
                          sh[2]);
       return hipGetLastError();

@@ -243,10 +243,10 @@ unsigned grid_for(int64_t n) {
 hipError_t launch_transpose(const void* a, void* b, int64_t R, int64_t C, bool bf16, hipStream_t s) {
   dim3 grid(unsigned((C + 63) / 64), unsigned((R + 63) / 64));
   if (bf16)
-    launch_kernel(transpose_kernel<bf16_t>, grid, dim3(256), 0, s, static_cast<const bf16_t*>(a),
+    hipLaunchKernelGGL(transpose_kernel<bf16_t>, grid, dim3(256), 0, s, static_cast<const bf16_t*>(a),
                        static_cast<bf16_t*>(b), R, C);
   else
-    launch_kernel(transpose_kernel<float>, grid, dim3(256), 0, s, static_cast<const float*>(a),
+    hipLaunchKernelGGL(transpose_kernel<float>, grid, dim3(256), 0, s, static_cast<const float*>(a),
                        static_cast<float*>(b), R, C);
   return hipGetLastError();
 }
@@ -255,17 +255,17 @@ hipError_t launch_swiglu(bool bwd, uint8_t* const* p, int64_t n, bool bf16, hipS
   const unsigned grid = grid_for(n);
   if (bf16) {
     if (bwd)
-      launch_kernel(swiglu_bwd_kernel<bf16_t>, dim3(grid), dim3(256), 0, s, (const bf16_t*)p[0],
+      hipLaunchKernelGGL(swiglu_bwd_kernel<bf16_t>, dim3(grid), dim3(256), 0, s, (const bf16_t*)p[0],
                          (const bf16_t*)p[1], (const bf16_t*)p[2], (bf16_t*)p[3], (bf16_t*)p[4], n);
     else
-      launch_kernel(swiglu_act_kernel<bf16_t>, dim3(grid), dim3(256), 0, s, (const bf16_t*)p[0],
+      hipLaunchKernelGGL(swiglu_act_kernel<bf16_t>, dim3(grid), dim3(256), 0, s, (const bf16_t*)p[0],
                          (const bf16_t*)p[1], (bf16_t*)p[2], n);
   } else {
     if (bwd)
-      launch_kernel(swiglu_bwd_kernel<float>, dim3(grid), dim3(256), 0, s, (const float*)p[0],
+      hipLaunchKernelGGL(swiglu_bwd_kernel<float>, dim3(grid), dim3(256), 0, s, (const float*)p[0],
                          (const float*)p[1], (const float*)p[2], (float*)p[3], (float*)p[4], n);
     else
-      launch_kernel(swiglu_act_kernel<float>, dim3(grid), dim3(256), 0, s, (const float*)p[0],
+      hipLaunchKernelGGL(swiglu_act_kernel<float>, dim3(grid), dim3(256), 0, s, (const float*)p[0],
                          (const float*)p[1], (float*)p[2], n);
   }
   return hipGetLastError();
@@ -277,21 +277,21 @@ hipError_t launch_rmsnorm_bwd(uint8_t* const* p, int64_t T, int64_t H, int acc, 
   float* dx = (float*)p[3];
   float* rstd = (float*)p[6];
   if (g_bf16)
-    launch_kernel(rmsnorm_bwd_rows<bf16_t>, dim3(unsigned(T)), dim3(256), 0, s, x, (const bf16_t*)p[1], dy, dx,
+    hipLaunchKernelGGL(rmsnorm_bwd_rows<bf16_t>, dim3(unsigned(T)), dim3(256), 0, s, x, (const bf16_t*)p[1], dy, dx,
                        (bf16_t*)p[4], rstd, H, acc);
   else
-    launch_kernel(rmsnorm_bwd_rows<float>, dim3(unsigned(T)), dim3(256), 0, s, x, (const float*)p[1], dy, dx,
+    hipLaunchKernelGGL(rmsnorm_bwd_rows<float>, dim3(unsigned(T)), dim3(256), 0, s, x, (const float*)p[1], dy, dx,
                        (bf16_t*)p[4], rstd, H, acc);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  launch_kernel(rmsnorm_bwd_gain, dim3(unsigned((H + kGainCols - 1) / kGainCols)), dim3(256), 0, s, x, dy, rstd,
+  hipLaunchKernelGGL(rmsnorm_bwd_gain, dim3(unsigned((H + kGainCols - 1) / kGainCols)), dim3(256), 0, s, x, dy, rstd,
                      (float*)p[5], T, H);
   return hipGetLastError();
 }
 
 hipError_t launch_attn_bwd(uint8_t* const* p, int64_t B, int64_t S, int64_t nH, hipStream_t s) {
   const int64_t rows = B * S * nH;
-  launch_kernel(attn_bwd_rowsum, dim3(unsigned((rows + 3) / 4)), dim3(256), 0, s, (const bf16_t*)p[3],
+  hipLaunchKernelGGL(attn_bwd_rowsum, dim3(unsigned((rows + 3) / 4)), dim3(256), 0, s, (const bf16_t*)p[3],
                      (const bf16_t*)p[5], (float*)p[9], B * S, S, nH);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -315,36 +315,36 @@ hipError_t launch_attn_bwd(uint8_t* const* p, int64_t B, int64_t S, int64_t nH, 
 hipError_t launch_rope_bwd(uint8_t* const* p, int64_t B, int64_t S, int64_t nH, int64_t d, bool bf16, hipStream_t s) {
   const int threads = d / 2 >= 64 ? 64 : int(d / 2);
   if (bf16)
-    launch_kernel(rope_bwd_kernel<bf16_t>, dim3(unsigned(B * S * nH)), dim3(threads), 0, s, (bf16_t*)p[0],
+    hipLaunchKernelGGL(rope_bwd_kernel<bf16_t>, dim3(unsigned(B * S * nH)), dim3(threads), 0, s, (bf16_t*)p[0],
                        (const bf16_t*)p[1], (const bf16_t*)p[2], (bf16_t*)p[3], (bf16_t*)p[4], S, nH, d);
   else
-    launch_kernel(rope_bwd_kernel<float>, dim3(unsigned(B * S * nH)), dim3(threads), 0, s, (float*)p[0],
+    hipLaunchKernelGGL(rope_bwd_kernel<float>, dim3(unsigned(B * S * nH)), dim3(threads), 0, s, (float*)p[0],
                        (const float*)p[1], (const float*)p[2], (float*)p[3], (float*)p[4], S, nH, d);
   return hipGetLastError();
 }
 
 hipError_t launch_xent(uint8_t* const* p, int64_t T, int64_t V, bool bf16, hipStream_t s) {
   if (bf16)
-    launch_kernel(xent_kernel<bf16_t>, dim3(unsigned(T)), dim3(256), 0, s, (const float*)p[0],
+    hipLaunchKernelGGL(xent_kernel<bf16_t>, dim3(unsigned(T)), dim3(256), 0, s, (const float*)p[0],
                        (const int32_t*)p[1], (float*)p[2], (bf16_t*)p[3], V, 1.f / float(T));
   else
-    launch_kernel(xent_kernel<float>, dim3(unsigned(T)), dim3(256), 0, s, (const float*)p[0],
+    hipLaunchKernelGGL(xent_kernel<float>, dim3(unsigned(T)), dim3(256), 0, s, (const float*)p[0],
                        (const int32_t*)p[1], (float*)p[2], (float*)p[3], V, 1.f / float(T));
   return hipGetLastError();
 }
 
 hipError_t launch_embed_bwd(uint8_t* const* p, int64_t T, int64_t H, int64_t V, hipStream_t s) {
-  launch_kernel(embed_bwd_kernel, dim3(unsigned((V + 31) / 32)), dim3(256), 0, s, (const int32_t*)p[0],
+  hipLaunchKernelGGL(embed_bwd_kernel, dim3(unsigned((V + 31) / 32)), dim3(256), 0, s, (const int32_t*)p[0],
                      (const float*)p[1], (float*)p[2], T, H, V);
   return hipGetLastError();
 }
 
 hipError_t launch_adam(uint8_t* const* p, int64_t n, const AdamArgs& a, bool bf16, hipStream_t s) {
   if (bf16)
-    launch_kernel(adam_kernel<bf16_t>, dim3(grid_for(n)), dim3(256), 0, s, (const float*)p[0], (float*)p[1],
+    hipLaunchKernelGGL(adam_kernel<bf16_t>, dim3(grid_for(n)), dim3(256), 0, s, (const float*)p[0], (float*)p[1],
                        (float*)p[2], (float*)p[3], (bf16_t*)p[4], n, a);
   else
-    launch_kernel(adam_kernel<float>, dim3(grid_for(n)), dim3(256), 0, s, (const float*)p[0], (float*)p[1],
+    hipLaunchKernelGGL(adam_kernel<float>, dim3(grid_for(n)), dim3(256), 0, s, (const float*)p[0], (float*)p[1],
                        (float*)p[2], (float*)p[3], (float*)p[4], n, a);
   return hipGetLastError();
 }

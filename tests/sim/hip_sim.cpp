@@ -195,29 +195,8 @@ hipError_t hipHostFree(void* p) { return hipFree(p); }
 
 namespace auvm {
 
-// armed timing events: recorded around the simulated kernel, as the kernel
-// itself records them on the device
-namespace {
-hipEvent_t armed_start = nullptr, armed_stop = nullptr;
-bool armed_used = false;
-}  // namespace
-
-void launch_events_arm(hipEvent_t start, hipEvent_t stop) {
-  armed_start = start;
-  armed_stop = stop;
-  armed_used = false;
-}
-
-bool launch_events_disarm() {
-  const bool used = armed_used;
-  armed_start = armed_stop = nullptr;
-  armed_used = false;
-  return used;
-}
-
 hipError_t launch_op(const Kernel& k, const std::vector<Tensor>& T, uint8_t* const* ptrs, hipStream_t s) {
   if (k.op != AUVM_OP_TOUCH) return hipErrorInvalidValue;
-  if (armed_stop && hipEventRecord(armed_start, s) != hipSuccess) return hipErrorUnknown;
   const int n = int(k.ids.size()) - 1;
   std::vector<uint32_t*> data(n);
   std::vector<uint64_t> words(n);
@@ -246,10 +225,6 @@ hipError_t launch_op(const Kernel& k, const std::vector<Tensor>& T, uint8_t* con
     }
   };
   push(s, std::move(o));
-  if (armed_stop) {
-    armed_used = true;
-    return hipEventRecord(armed_stop, s);
-  }
   return hipSuccess;
 }
 
