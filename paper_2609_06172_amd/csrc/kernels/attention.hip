@@ -220,6 +220,7 @@ __global__ void __launch_bounds__(64 * kDecWaves, 4) attn_decode_d128(AttnArgs a
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 
@@ -317,14 +318,21 @@ __device__ __forceinline__ float swap_sum(float x) {
 // Workgroup order of the flash kernels (grid = nblk blocks of each of nbh
 // (batch, head) pairs).  Workgroup w runs on XCD w % 8 (round-robin
 // dispatch), and each XCD has its own L2: all blocks of one (b, h) go to the
-// same XCD, so its K and V (or Q and dO) are fetched into one L2 only, and
-// each XCD starts the heaviest blocks (rank 0) of all its heads first.
-// Without eight-way divisible heads the order is rank-major.
-__device__ __forceinline__ void xcd_order(int64_t w, int64_t nbh, int64_t* rank, int64_t* bh) {
+// same XCD, so its K and V (or Q and dO) are fetched into one L2 only.  An
+// XCD with more than eight heads takes them four at a time, all blocks of a
+// group before the next, heaviest blocks (rank 0) of the group first: the
+// blocks resident on the XCD together then share few heads, and the K and V
+// tiles they walk stay in its L2 (one group otherwise).  Without eight-way
+// divisible heads the order is rank-major.
+__device__ __forceinline__ void xcd_order(int64_t w, int64_t nbh, int64_t nblk, int64_t* rank, int64_t* bh) {
   if (nbh % 8 == 0) {
     const int64_t x = w % 8, slot = w / 8, hx = nbh / 8;
-    *rank = slot / hx;
-    *bh = (slot % hx) * 8 + x;
+    const int64_t G = hx <= 8 ? hx : 4;                     // heads per group
+    const int64_t g0 = slot / (G * nblk) * G;               // first head of the group
+    const int64_t gn = hx - g0 < G ? hx - g0 : G;           // heads in it (the last may hold fewer)
+    const int64_t in = slot - g0 * nblk;
+    *rank = in / gn;
+    *bh = (g0 + in % gn) * 8 + x;
   } else {
     *rank = w / nbh;
     *bh = w % nbh;
@@ -338,7 +346,7 @@ __global__ void __launch_bounds__(64 * FW, 2) attn_prefill_d128(AttnArgs a, int6
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int lq = lane & 31, lh = lane >> 5;
   int64_t rank, bh;
-  xcd_order(blockIdx.x, int64_t(gridDim.x) / nqb, &rank, &bh);
+  xcd_order(blockIdx.x, int64_t(gridDim.x) / nqb, nqb, &rank, &bh);
   const int64_t qb = nqb - 1 - rank;
   const int64_t h = bh % a.nH, b = bh / a.nH;
   const int64_t q0 = qb * FQ, qw = q0 + 32 * wv;
@@ -528,7 +536,7 @@ __global__ void __launch_bounds__(64 * FW, 1) attn_bwd_dq_d128(AttnBwdArgs a, in
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int lq = lane & 31, lh = lane >> 5;
   int64_t rank, bh;
-  xcd_order(blockIdx.x, int64_t(gridDim.x) / nqb, &rank, &bh);
+  xcd_order(blockIdx.x, int64_t(gridDim.x) / nqb, nqb, &rank, &bh);
   const int64_t qb = nqb - 1 - rank;
   const int64_t h = bh % a.nH, b = bh / a.nH, S = a.S;
   const int64_t q0 = qb * FQ, qw = q0 + 32 * wv, qr = qw + lq;
@@ -578,12 +586,17 @@ __global__ void __launch_bounds__(64 * FW, 1) attn_bwd_dq_d128(AttnBwdArgs a, in
         dpt[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, df[c], dpt[kt], 0, 0, 0);
       }
     }
+    // P^T, then dS^T.  Only a block that crosses this wave's diagonal or
+    // holds queries past S is masked (a select, not a branch): there a key
+    // counts when its offset in the block is at most kq.
+    const bool edge = k0 + FK - 1 > qw || qw + 31 >= S;
+    const int kq = qr < S ? int(qr - k0) - 4 * lh : -1;
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const int64_t key = k0 + 32 * kt + 8 * (e >> 2) + 4 * lh + (e & 3);
-        const float p = (key <= qr && qr < S) ? __builtin_amdgcn_exp2f(fmaf(st[kt][e], c2, -lse2)) : 0.f;
+        float p = __builtin_amdgcn_exp2f(fmaf(st[kt][e], c2, -lse2));
+        if (edge) p = 32 * kt + 8 * (e >> 2) + (e & 3) <= kq ? p : 0.f;
         st[kt][e] = p * (dpt[kt][e] - Dq);       // dS^T
       }
 #pragma unroll
@@ -608,11 +621,11 @@ __global__ void __launch_bounds__(64 * FW, 1) attn_bwd_dkv_d128(AttnBwdArgs a, i
   extern __shared__ __align__(16) bf16_t fsm[];
   bf16_t* Qs = fsm;                 // [2][FK][FD] query rows
   bf16_t* Os = fsm + 2 * TS;        // [2][FK][FD] dO rows
-  __shared__ float lsS[2][FK], dsS[2][FK];
+  __shared__ __align__(16) float lsS[2][FK], dsS[2][FK];
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int lq = lane & 31, lh = lane >> 5;
   int64_t kb, bh;   // key block 0 sees every query: the heaviest
-  xcd_order(blockIdx.x, int64_t(gridDim.x) / nkb, &kb, &bh);
+  xcd_order(blockIdx.x, int64_t(gridDim.x) / nkb, nkb, &kb, &bh);
   const int64_t h = bh % a.nH, b = bh / a.nH, S = a.S;
   const int64_t kbase = kb * FQ, kw = kbase + 32 * wv, kr = kw + lq;
   const int64_t krc = kr < S ? kr : S - 1;
@@ -668,16 +681,26 @@ __global__ void __launch_bounds__(64 * FW, 1) attn_bwd_dkv_d128(AttnBwdArgs a, i
         dp[qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(oa, vf[c], dp[qt], 0, 0, 0);
       }
     }
+    // P and dS.  Only a block that crosses this wave's diagonal or holds
+    // queries past S is masked (a select, not a branch): there a query counts
+    // when its offset in the block, less 4 lh, lies in [lo, hi).
+    const bool edge = q0 < kw + 31 || q0 + FK > S;
+    const int lo = int(kr - q0) - 4 * lh, hi = int(S - q0) - 4 * lh;
 #pragma unroll
     for (int qt = 0; qt < 2; ++qt)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int qrow = 32 * qt + 8 * (e >> 2) + 4 * lh + (e & 3);
-        const int64_t q = q0 + qrow;
-        const float p =
-            (q < S && kr <= q) ? __builtin_amdgcn_exp2f(fmaf(sc[qt][e], c2, -lsS[buf][qrow])) : 0.f;
-        sc[qt][e] = p;                                   // P
-        dp[qt][e] = p * (dp[qt][e] - dsS[buf][qrow]);    // dS
+      for (int j = 0; j < 4; ++j) {
+        const int qrow = 32 * qt + 8 * j + 4 * lh;
+        const f32x4 ls = *reinterpret_cast<const f32x4*>(&lsS[buf][qrow]);
+        const f32x4 ds = *reinterpret_cast<const f32x4*>(&dsS[buf][qrow]);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int e = 4 * j + i, c = 32 * qt + 8 * j + i;
+          float p = __builtin_amdgcn_exp2f(fmaf(sc[qt][e], c2, -ls[i]));
+          if (edge) p = c >= lo && c < hi ? p : 0.f;
+          sc[qt][e] = p;                          // P
+          dp[qt][e] = p * (dp[qt][e] - ds[i]);    // dS
+        }
       }
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
