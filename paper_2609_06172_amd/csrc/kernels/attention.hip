@@ -273,15 +273,16 @@ __device__ __forceinline__ void load_kv_rows(bf16_t* tile, const char* base, con
                                      16, 0, 0);
 }
 
-// the B-operand fragment (16 rows of k, this lane's column) of k-step s from
-// a pair of 32 x 32 C tiles t[0..1] (rows 0..31, 32..63): rows 16s.. of the
-// pair; the lane and its partner (lane ^ 32) trade one 4-row group each
-__device__ __forceinline__ bf16x8 c_to_b(const f32x16* t, int s) {
-  const int kt = s >> 1, g0 = 2 * (s & 1);
-  const uint32_t a0 = pack_bf16(t[kt][4 * g0 + 0], t[kt][4 * g0 + 1]);
-  const uint32_t a1 = pack_bf16(t[kt][4 * g0 + 2], t[kt][4 * g0 + 3]);
-  const uint32_t b0 = pack_bf16(t[kt][4 * g0 + 4], t[kt][4 * g0 + 5]);
-  const uint32_t b1 = pack_bf16(t[kt][4 * g0 + 6], t[kt][4 * g0 + 7]);
+// the B-operand fragment (16 rows of k, this lane's column) of k-step u
+// (0, 1) from one 32 x 32 C tile t: rows 16u.. of the tile; the lane and its
+// partner (lane ^ 32) trade one 4-row group each.  c_to_b: k-step s of a
+// pair of tiles t[0..1] (rows 0..31, 32..63).
+__device__ __forceinline__ bf16x8 c_to_b1(const f32x16& t, int u) {
+  const int g0 = 2 * u;
+  const uint32_t a0 = pack_bf16(t[4 * g0 + 0], t[4 * g0 + 1]);
+  const uint32_t a1 = pack_bf16(t[4 * g0 + 2], t[4 * g0 + 3]);
+  const uint32_t b0 = pack_bf16(t[4 * g0 + 4], t[4 * g0 + 5]);
+  const uint32_t b1 = pack_bf16(t[4 * g0 + 6], t[4 * g0 + 7]);
   // v_permlane32_swap(x, y) returns x' = (lanes < 32: x, lanes >= 32: y of
   // lane - 32) and y' = (lanes < 32: x of lane + 32, lanes >= 32: y): lane
   // l < 32 gets {its a, its partner's a}, lane l >= 32 {its partner's b, its b}
@@ -290,9 +291,7 @@ __device__ __forceinline__ bf16x8 c_to_b(const f32x16* t, int s) {
   const u32x4v pf = {x0[0], x1[0], x0[1], x1[1]};
   return __builtin_bit_cast(bf16x8, pf);
 }
-
-// the A-operand fragment of the transposed tile (dims 32 dt.., rows 16 s..)
-// from a row-major swizzled 64 x 128 tile, by two LDS transpose reads
+__device__ __forceinline__ bf16x8 c_to_b(const f32x16* t, int s) { return c_to_b1(t[s >> 1], s & 1); }
 __device__ __forceinline__ bf16x8 tile_t_frag(const bf16_t* tile, int s, int dt, int lane) {
   const int tg = lane >> 4, tj = lane & 15;
   const int row = 16 * s + 8 * (tg >> 1) + (tj >> 2);
@@ -524,12 +523,15 @@ __global__ void __launch_bounds__(64 * FW, 2) attn_prefill_d128(AttnArgs a, int6
 //     and dP = dO V^T (Q, dO tiles in LDS, the wave's K, V rows in
 //     registers), then dV^T += dO^T P and dK^T += Q^T dS.
 // A lane owns one query (dQ pass) or one key (dK, dV pass), so the 32 x 32
-// accumulator tiles map to one row of the output each.
+// accumulator tiles map to one row of the output each.  The dQ pass fits in
+// 256 registers a lane (two workgroups per CU); the dK, dV pass, with two
+// accumulator sets, takes one workgroup per CU and software-pipelines its
+// LDS reads instead.
 
 constexpr float kBwdScale = 0.08838834764831845f;   // 1 / sqrt(128)
 constexpr float kLog2eF = 1.4426950408889634f;
 
-__global__ void __launch_bounds__(64 * FW, 1) attn_bwd_dq_d128(AttnBwdArgs a, int64_t nqb) {
+__global__ void __launch_bounds__(64 * FW, 2) attn_bwd_dq_d128(AttnBwdArgs a, int64_t nqb) {
   extern __shared__ __align__(16) bf16_t fsm[];
   bf16_t* Ks = fsm;                 // [2][FK][FD]
   bf16_t* Vs = fsm + 2 * TS;        // [2][FK][FD]
@@ -569,7 +571,8 @@ __global__ void __launch_bounds__(64 * FW, 1) attn_bwd_dq_d128(AttnBwdArgs a, in
       load_kv(Ks + (buf ^ 1) * TS, Kg, FD, k0 + FK, klast, wv, lane);
       load_kv(Vs + (buf ^ 1) * TS, Vg, FD, k0 + FK, klast, wv, lane);
     }
-    if (k0 > wlast) continue;
+    // A wave whose queries all precede the block still runs it, fully
+    // masked: a uniform loop body keeps the dQ accumulators in place.
     const bf16_t* ks = Ks + buf * TS;
     const bf16_t* vs = Vs + buf * TS;
     // S^T and dP^T tiles kt: element e is key k0 + 32 kt + 8 (e/4) + 4 lh + e%4 of query qr
@@ -664,51 +667,86 @@ __global__ void __launch_bounds__(64 * FW, 1) attn_bwd_dkv_d128(AttnBwdArgs a, i
       load_kv(Os + (buf ^ 1) * TS, Og, a.q_rs, q0 + FK, qlast, wv, lane);
       stats(buf ^ 1, q0 + FK);
     }
-    if (q0 + FK - 1 < kw) continue;      // every query of the block precedes this wave's keys
+    // A wave whose keys all follow the block's queries (the first block, for
+    // waves 2 and 3) still runs it, fully masked: a uniform loop body keeps
+    // the dK and dV accumulators in place across iterations.
     const bf16_t* qs = Qs + buf * TS;
     const bf16_t* os = Os + buf * TS;
-    // S and dP tiles qt: element e is query q0 + 32 qt + 8 (e/4) + 4 lh + e%4 against key kr
-    f32x16 sc[2], dp[2];
-#pragma unroll
-    for (int qt = 0; qt < 2; ++qt) {
-      sc[qt] = f32x16{};
-      dp[qt] = f32x16{};
-#pragma unroll
-      for (int c = 0; c < 8; ++c) {
-        const bf16x8 qa = *reinterpret_cast<const bf16x8*>(qs + tile_at(32 * qt + lq, 16 * c + 8 * lh));
-        sc[qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qa, kf[c], sc[qt], 0, 0, 0);
-        const bf16x8 oa = *reinterpret_cast<const bf16x8*>(os + tile_at(32 * qt + lq, 16 * c + 8 * lh));
-        dp[qt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(oa, vf[c], dp[qt], 0, 0, 0);
-      }
-    }
-    // P and dS.  Only a block that crosses this wave's diagonal or holds
-    // queries past S is masked (a select, not a branch): there a query counts
-    // when its offset in the block, less 4 lh, lies in [lo, hi).
+    // Only a block that crosses this wave's diagonal or holds queries past S
+    // is masked (a select, not a branch): there a query counts when its
+    // offset in the block, less 4 lh, lies in [lo, hi).
     const bool edge = q0 < kw + 31 || q0 + FK > S;
     const int lo = int(kr - q0) - 4 * lh, hi = int(S - q0) - 4 * lh;
+    // The block's 64 queries in two halves of 32 (qt), each: S and dP tiles
+    // (element e is query q0 + 32 qt + 8 (e/4) + 4 lh + e%4 against key kr),
+    // P and dS, then their share of dV^T and dK^T.  LDS fragments are read
+    // two steps ahead; each step is one scheduling region whose MFMAs take
+    // fragments read two regions earlier.
 #pragma unroll
-    for (int qt = 0; qt < 2; ++qt)
+    for (int qt = 0; qt < 2; ++qt) {
+      f32x16 sc = f32x16{}, dp = f32x16{};
+      bf16x8 fa[3][2];   // [step % 3][Q, dO] for dim step c
+      auto rda = [&](int c) {
+        fa[c % 3][0] = *reinterpret_cast<const bf16x8*>(qs + tile_at(32 * qt + lq, 16 * c + 8 * lh));
+        fa[c % 3][1] = *reinterpret_cast<const bf16x8*>(os + tile_at(32 * qt + lq, 16 * c + 8 * lh));
+      };
+      f32x4 ls[4], ds[4];   // log-sum-exp (base 2) and D of the lane's 16 queries
+      rda(0);
+      rda(1);
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const int qrow = 32 * qt + 8 * j + 4 * lh;
-        const f32x4 ls = *reinterpret_cast<const f32x4*>(&lsS[buf][qrow]);
-        const f32x4 ds = *reinterpret_cast<const f32x4*>(&dsS[buf][qrow]);
+        ls[j] = *reinterpret_cast<const f32x4*>(&lsS[buf][32 * qt + 8 * j + 4 * lh]);
+        ds[j] = *reinterpret_cast<const f32x4*>(&dsS[buf][32 * qt + 8 * j + 4 * lh]);
+      }
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int c = 0; c < 8; ++c) {
+        if (c + 2 < 8) rda(c + 2);
+        sc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[c % 3][0], kf[c], sc, 0, 0, 0);
+        dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[c % 3][1], vf[c], dp, 0, 0, 0);
+        if (c + 2 < 8) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      // dV and dK: step t takes query step u = t / 4 of the half and dim
+      // tile dt = t % 4; its dO^T and Q^T fragments are read ahead
+      bf16x8 fc[3][2];   // [step % 3][dO^T, Q^T]
+      auto rdc = [&](int t) {
+        const int sq = 2 * qt + (t >> 2), dt = t & 3;
+        fc[t % 3][0] = tile_t_frag(os, sq, dt, lane);
+        fc[t % 3][1] = tile_t_frag(qs, sq, dt, lane);
+      };
+      rdc(0);
+      rdc(1);
+      // P and dS
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int e = 4 * j + i, c = 32 * qt + 8 * j + i;
-          float p = __builtin_amdgcn_exp2f(fmaf(sc[qt][e], c2, -ls[i]));
-          if (edge) p = c >= lo && c < hi ? p : 0.f;
-          sc[qt][e] = p;                          // P
-          dp[qt][e] = p * (dp[qt][e] - ds[i]);    // dS
+          const int e = 4 * j + i, cq = 32 * qt + 8 * j + i;
+          float pv = __builtin_amdgcn_exp2f(fmaf(sc[e], c2, -ls[j][i]));
+          if (edge) pv = cq >= lo && cq < hi ? pv : 0.f;
+          sc[e] = pv;                            // P
+          dp[e] = pv * (dp[e] - ds[j][i]);       // dS
         }
-      }
+      const bf16x8 pb[2] = {c_to_b1(sc, 0), c_to_b1(sc, 1)};
+      const bf16x8 dsb[2] = {c_to_b1(dp, 0), c_to_b1(dp, 1)};
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      const bf16x8 pb = c_to_b(sc, s), dsb = c_to_b(dp, s);
-#pragma unroll
-      for (int dt = 0; dt < 4; ++dt) {
-        dvt[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tile_t_frag(os, s, dt, lane), pb, dvt[dt], 0, 0, 0);
-        dkt[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(tile_t_frag(qs, s, dt, lane), dsb, dkt[dt], 0, 0, 0);
+      for (int t = 0; t < 8; ++t) {
+        if (t + 2 < 8) rdc(t + 2);
+        const int u = t >> 2, dt = t & 3;
+        dvt[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fc[t % 3][0], pb[u], dvt[dt], 0, 0, 0);
+        dkt[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fc[t % 3][1], dsb[u], dkt[dt], 0, 0, 0);
+        if (t + 2 < 8) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
   }
