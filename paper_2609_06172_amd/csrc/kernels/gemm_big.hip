@@ -218,9 +218,44 @@ __global__ void __launch_bounds__(64 * kWaves) gemm_big(const bf16_t* __restrict
     for (int j = 0; j < TN; ++j) {
       const int64_t col = n0 + wn * 32 * TN + 32 * j + lr;
       if (col >= N) continue;
+      const int64_t r0 = m0 + wm * 32 * TM + 32 * i;   // first row of the 32-row tile
+      if constexpr (EPI == EPI_RESID || EPI == EPI_MOE) {
+        // Read-modify-write of fp32 rows.  A tile whose 32 rows all exist
+        // takes straight-line code: every load, then every store, so the lane
+        // waits for memory once per tile rather than once per element (the
+        // compiler does not move a load past a store to the same array).
+        float* x = reinterpret_cast<float*>(C);
+        if (r0 + 32 <= rows) {
+          int64_t at[16];
+          float sc[16], xv[16];
+#pragma clang loop unroll(full)
+          for (int e = 0; e < 16; ++e) {
+            const int64_t row = r0 + 8 * (e >> 2) + 4 * lc + (e & 3);
+            if constexpr (EPI == EPI_MOE) {
+              const int64_t jr = list[1 + row], lim = M * topk;
+              const int64_t jc = jr < 0 ? 0 : (jr < lim ? jr : lim - 1);
+              at[e] = (jc / topk) * N + col;
+              sc[e] = rw[jc];
+            } else {
+              at[e] = row * N + col;
+              sc[e] = 1.f;
+            }
+          }
+#pragma clang loop unroll(full)
+          for (int e = 0; e < 16; ++e) xv[e] = x[at[e]];
+#pragma clang loop unroll(full)
+          for (int e = 0; e < 16; ++e) {
+            if constexpr (EPI == EPI_MOE)
+              x[at[e]] = xv[e] + sc[e] * acc[i][j][e];
+            else
+              x[at[e]] = xv[e] + acc[i][j][e];
+          }
+          continue;
+        }
+      }
 #pragma clang loop unroll(full)
       for (int e = 0; e < 16; ++e) {
-        const int64_t row = m0 + wm * 32 * TM + 32 * i + 8 * (e >> 2) + 4 * lc + (e & 3);
+        const int64_t row = r0 + 8 * (e >> 2) + 4 * lc + (e & 3);
         if (row >= rows) continue;
         float v = acc[i][j][e];
         if constexpr (EPI == EPI_GELU) v = gelu_erf(v);

@@ -14,7 +14,8 @@
 // Work split: one 1024-thread workgroup per 16 output features; its sixteen
 // waves take interleaved 64-wide K chunks (adjacent waves read adjacent 128 B
 // of every row), two chunks in flight per wave, keep fp32 partial tiles in
-// registers and reduce them through LDS in a fixed order (deterministic).
+// registers and reduce them through LDS in a fixed order (deterministic);
+// four waves then write one output each per lane.
 //
 // Loads: the MFMA operand layout gives each row only four lanes (64 B) per
 // load instruction, which spends a cache-line request on half a line.  Each
@@ -142,35 +143,34 @@ __global__ void __launch_bounds__(64 * kWaves) gemv_mfma(const bf16_t* __restric
   part[wv][0][lane] = acc;
   if constexpr (DUAL) part[wv][1][lane] = acc2;
   __syncthreads();
-  if (wv != 0) return;
-  f32x4 s = part[0][0][lane], s2 = {0.f, 0.f, 0.f, 0.f};
-  if constexpr (DUAL) s2 = part[0][1][lane];
+  // Waves 0..3 finish element i = wv of every lane's tile, the partials summed
+  // in wave order: one output per lane, so a read-modify-write epilogue waits
+  // for memory once.  Accumulator layout: element i of lane l is row
+  // 4*(l/16)+i, column l%16.
+  if (wv >= 4) return;
+  const int i = wv;
+  float v = part[0][0][lane][i], v2 = 0.f;
+  if constexpr (DUAL) v2 = part[0][1][lane][i];
 #pragma unroll
   for (int w = 1; w < kWaves; ++w) {
-    s += part[w][0][lane];
-    if constexpr (DUAL) s2 += part[w][1][lane];
+    v += part[w][0][lane][i];
+    if constexpr (DUAL) v2 += part[w][1][lane][i];
   }
-  // accumulator layout: element i of lane l is row 4*(l/16)+i, column l%16
   const int64_t col = n0 + (lane & 15);
-  if (col >= N) return;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int row = 4 * (lane >> 4) + i;
-    if (row >= rows) continue;
-    float v = s[i];
-    if constexpr (EPI == EPI_GELU) v = gelu_erf(v);
-    if constexpr (EPI == EPI_SWIGLU) v = silu(v) * s2[i];
-    if constexpr (EPI == EPI_MOE) {
-      const int64_t j = list[1 + row], lim = int64_t(M) * topk;
-      const int64_t jc = j < 0 ? 0 : (j < lim ? j : lim - 1);
-      float* x = reinterpret_cast<float*>(C);
-      x[(jc / topk) * N + col] += rw[jc] * v;
-    } else if constexpr (EPI == EPI_RESID) {
-      float* x = reinterpret_cast<float*>(C);
-      x[int64_t(row) * N + col] += v;
-    } else {
-      st(C, int64_t(row) * N + col, v);
-    }
+  const int row = 4 * (lane >> 4) + i;
+  if (col >= N || row >= rows) return;
+  if constexpr (EPI == EPI_GELU) v = gelu_erf(v);
+  if constexpr (EPI == EPI_SWIGLU) v = silu(v) * v2;
+  if constexpr (EPI == EPI_MOE) {
+    const int64_t j = list[1 + row], lim = int64_t(M) * topk;
+    const int64_t jc = j < 0 ? 0 : (j < lim ? j : lim - 1);
+    float* x = reinterpret_cast<float*>(C);
+    x[(jc / topk) * N + col] += rw[jc] * v;
+  } else if constexpr (EPI == EPI_RESID) {
+    float* x = reinterpret_cast<float*>(C);
+    x[int64_t(row) * N + col] += v;
+  } else {
+    st(C, int64_t(row) * N + col, v);
   }
 }
 
