@@ -143,9 +143,23 @@ __global__ void __launch_bounds__(256) gemm_mfma(const bf16_t* __restrict__ A, c
     for (int j = 0; j < 2; ++j) {
       const int64_t col = n0 + wn * 64 + j * 32 + (lane & 31);
       if (col >= N) continue;
+      const int64_t r0 = m0 + wm * 64 + i * 32;   // first row of the 32-row tile
+      if constexpr (EPI == EPI_RESID) {
+        // every residual load of a full tile before its stores: one wait for
+        // memory per tile rather than one per element
+        if (r0 + 32 <= M) {
+          float* x = reinterpret_cast<float*>(C) + (r0 + 4 * (lane >> 5)) * N + col;
+          float xv[16];
+#pragma unroll
+          for (int e = 0; e < 16; ++e) xv[e] = x[(8 * (e >> 2) + (e & 3)) * N];
+#pragma unroll
+          for (int e = 0; e < 16; ++e) x[(8 * (e >> 2) + (e & 3)) * N] = xv[e] + acc[i][j][e];
+          continue;
+        }
+      }
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const int64_t row = m0 + wm * 64 + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+        const int64_t row = r0 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
         if (row >= M) continue;
         float v = acc[i][j][e];
         if constexpr (EPI == EPI_GELU) v = gelu_erf(v);
