@@ -106,7 +106,26 @@ __global__ void __launch_bounds__(256) norm_kernel(const float* x, const TO* g, 
   }
 }
 
-// Row in registers: H % 4 == 0 and H <= 4 * 256 * NV; float4 loads, one read.
+// Four consecutive elements (index a multiple of 4) in one load or store.
+__device__ __forceinline__ void ld4(const float* p, int64_t i, float* o) {
+  const float4 v = *reinterpret_cast<const float4*>(p + i);
+  o[0] = v.x; o[1] = v.y; o[2] = v.z; o[3] = v.w;
+}
+__device__ __forceinline__ void ld4(const bf16_t* p, int64_t i, float* o) {
+  const uint2 v = *reinterpret_cast<const uint2*>(p + i);
+  o[0] = bf2f(bf16_t(v.x & 0xffffu)); o[1] = bf2f(bf16_t(v.x >> 16));
+  o[2] = bf2f(bf16_t(v.y & 0xffffu)); o[3] = bf2f(bf16_t(v.y >> 16));
+}
+__device__ __forceinline__ void st4(float* p, int64_t i, const float* y) {
+  *reinterpret_cast<float4*>(p + i) = float4{y[0], y[1], y[2], y[3]};
+}
+__device__ __forceinline__ void st4(bf16_t* p, int64_t i, const float* y) {
+  const uint2 v = {uint32_t(f2bf(y[0])) | (uint32_t(f2bf(y[1])) << 16), uint32_t(f2bf(y[2])) | (uint32_t(f2bf(y[3])) << 16)};
+  *reinterpret_cast<uint2*>(p + i) = v;
+}
+
+// Row in registers: H % 4 == 0 and H <= 4 * 256 * NV; float4 loads, one read;
+// gains, biases and outputs four elements at a time.
 template <class TO, bool LN, int NV>
 __global__ void __launch_bounds__(256) norm_vec_kernel(const float* x, const TO* g, const TO* b, TO* h,
                                                        int64_t H, int64_t stride, int64_t offset,
@@ -146,13 +165,16 @@ __global__ void __launch_bounds__(256) norm_vec_kernel(const float* x, const TO*
     const int j = threadIdx.x + 256 * u;
     if (j >= n4) continue;
     const float e[4] = {v[u].x, v[u].y, v[u].z, v[u].w};
+    const int64_t col = 4 * int64_t(j);
+    float gv[4], bv[4] = {0.f, 0.f, 0.f, 0.f}, y[4];
+    ld4(g, col, gv);
+    if (LN) ld4(b, col, bv);
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
-      const int64_t col = 4 * int64_t(j) + c;
-      float y = (e[c] - mean) * rs * ld(g, col);
-      if (LN) y += ld(b, col);
-      st(h, r * H + col, y);
+      y[c] = (e[c] - mean) * rs * gv[c];
+      if (LN) y[c] += bv[c];
     }
+    st4(h, r * H + col, y);
   }
 }
 
