@@ -45,6 +45,10 @@ PREFILL_GUARD = 16
 # planned H2D per 7B step at 1.5x, guard 4 / 5 / 6 -> 7.579 / 7.528 / 7.528 GB
 # (the separate projections at guard 4: 7.527 GB)
 DECODE_GUARD = 5
+# 13B-shape training step at 2x (5 layers), two timed steps, same box:
+# guard 0 / 1 / 2 / 3 / 4 / 5 -> 697 / 672.3-672.7 / 699 / 1064 / 689-691 / 699
+# ms per step (34.9 / 35.5 / 37.0 / 37.6 / 37.9 / 39.4 GB over the link)
+TRAIN_GUARD = 1
 POLICY_NAMES = {0: "DEMAND_LRU", 1: "DEMAND_BELADY", 2: "T", 3: "T+A", 4: "T+A+P"}
 
 
@@ -80,7 +84,7 @@ def parse():
                     help="MoE and training configs: layers to run (default: MoE all of them, on a tiered host "
                          "arena past the pinned limit; training as many as fit the pinned limit)")
     ap.add_argument("--guard", type=int, default=None,
-                    help="victim guard of the T+A+P plan (default: 5 for LLaMA-style decode and the sweep, 16 for prefill configs, the library's 4 otherwise)")
+                    help="victim guard of the T+A+P plan (default: 5 for LLaMA-style decode and the sweep, 16 for prefill configs, 1 for the training step, the library's 4 for MoE)")
     ap.add_argument("--separate-qkv", action="store_true",
                     help="LLaMA-style traces: q, k and v projections as three LINEAR kernels "
                          "instead of one LINEAR_QKV")
@@ -1078,7 +1082,8 @@ def train_main(args, cfg):
         f"{len(w.kernels)} kernels ({W + K} steps), footprint {w.footprint} B, budget {M} B")
     bl_meas = link_bandwidth()
     t = time.perf_counter()
-    s = Session(w, device=0, M=M, variant=4, timing=1, guard=args.guard)
+    guard = TRAIN_GUARD if args.guard is None else args.guard
+    s = Session(w, device=0, M=M, variant=4, timing=1, guard=guard)
     log(f"session ready in {time.perf_counter() - t:.1f} s")
 
     def run(sess):
@@ -1121,7 +1126,8 @@ def train_main(args, cfg):
                                f"SwiGLU {cfg.ffn}, vocab {cfg.vocab}, {cfg.batch} x {cfg.prompt_len} tokens, bf16 "
                                f"weights with fp32 master weights and AdamW moments, budget = footprint*{den}/{num}",
                    "tokens_per_step": cfg.tokens, "layers": layers, "model_layers": n_layers,
-                   "factor": f"{num}/{den}", "footprint_bytes": w.footprint, "budget_bytes": M, "policy": "T+A+P"},
+                   "factor": f"{num}/{den}", "footprint_bytes": w.footprint, "budget_bytes": M,
+                   "policy": f"T+A+P (guard {guard})"},
         "path_roofline": pr,
         "roofline": {"kernel": "GEMMs of the step (forward, data and weight gradients; bf16 matrix cores)",
                      "bound": "mfma", "achieved": round(g_flops / g_time / 1e12, 1), "peak": 2500.0,
