@@ -253,6 +253,37 @@ __global__ void __launch_bounds__(64 * kWaves) gemm_big(const bf16_t* __restrict
           continue;
         }
       }
+      if constexpr ((EPI == EPI_STORE || EPI == EPI_GELU || EPI == EPI_SWIGLU) && sizeof(TC) == 2) {
+        // bf16 outputs of a full tile: each lane trades half of its 16
+        // values with its neighbour (lane ^ 1, the next column) and stores
+        // column pairs, 4 bytes a lane, so the tile takes half the store
+        // instructions.  The even lane of a pair stores the rows of elements
+        // 0..7, the odd lane those of elements 8..15.
+        const int64_t c0 = n0 + wn * 32 * TN + 32 * j;   // first column of the tile
+        if (r0 + 32 <= rows && c0 + 32 <= N && (N & 1) == 0) {
+          float v[16];
+#pragma clang loop unroll(full)
+          for (int e = 0; e < 16; ++e) {
+            v[e] = acc[i][j][e];
+            if constexpr (EPI == EPI_GELU) v[e] = gelu_erf(v[e]);
+            if constexpr (EPI == EPI_SWIGLU) v[e] = silu(v[e]) * acc2[i][j][e];
+          }
+          const bool odd = lr & 1;
+          const int64_t cp = col - (odd ? 1 : 0);   // the pair's even column
+#pragma clang loop unroll(full)
+          for (int e = 0; e < 8; ++e) {
+            const float send = odd ? v[e] : v[e + 8];
+            // quad_perm [1, 0, 3, 2]: the value of lane ^ 1
+            const float got = __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(send), 0xB1, 0xF, 0xF, false));
+            const float lo = odd ? got : v[e], hi = odd ? v[e + 8] : got;
+            const int ee = odd ? e + 8 : e;
+            const int64_t row = r0 + 8 * (ee >> 2) + 4 * lc + (ee & 3);
+            *reinterpret_cast<uint32_t*>(reinterpret_cast<bf16_t*>(C) + row * N + cp) =
+                uint32_t(f2bf(lo)) | (uint32_t(f2bf(hi)) << 16);
+          }
+          continue;
+        }
+      }
 #pragma clang loop unroll(full)
       for (int e = 0; e < 16; ++e) {
         const int64_t row = r0 + 8 * (e >> 2) + 4 * lc + (e & 3);
