@@ -54,7 +54,7 @@ def rnd(*shape, scale=1.0):
 # otherwise the 128 x 128 GEMM (including M >= 512 with K % 64 != 0)
 LIN_SHAPES = [(1, 64, 32), (5, 100, 64), (7, 130, 160), (16, 33, 96), (16, 4096 + 16, 256), (17, 96, 96), (100, 130, 160),
               (257, 300, 512), (512, 256, 64), (600, 300, 128), (1030, 520, 192), (777, 1000, 256),
-              (520, 130, 96)]
+              (520, 130, 96), (640, 333, 128)]   # the last: odd N, so no column pairs in the 256 x 256 epilogue
 
 
 @pytest.mark.parametrize("dt", [DT_F32, DT_BF16])
@@ -457,7 +457,9 @@ def _attn_fwd_bwd_ref(q, K, V, dO, B, S, nH):
     return o.reshape(B * S, nH * d), lse, dq.reshape(B * S, nH * d), dK, dV
 
 
-@pytest.mark.parametrize("B,S,nH", [(1, 1, 1), (1, 70, 2), (2, 160, 2), (1, 300, 1)])
+# (1, 160, 80) and (2, 130, 40): 80 (batch, head) pairs, ten per XCD, taken in
+# groups of four, the last group of two (the flash kernels' workgroup order)
+@pytest.mark.parametrize("B,S,nH", [(1, 1, 1), (1, 70, 2), (2, 160, 2), (1, 300, 1), (1, 160, 80), (2, 130, 40)])
 def test_attention_lse_and_backward(B, S, nH):
     d = 128
     q, K, V, dO = rnd(B * S, nH * d), rnd(B, nH, S, d), rnd(B, nH, S, d), rnd(B * S, nH * d)
