@@ -255,10 +255,11 @@ __global__ void __launch_bounds__(64 * kWaves) gemm_big(const bf16_t* __restrict
       }
       if constexpr ((EPI == EPI_STORE || EPI == EPI_GELU || EPI == EPI_SWIGLU) && sizeof(TC) == 2) {
         // bf16 outputs of a full tile: each lane trades half of its 16
-        // values with its neighbour (lane ^ 1, the next column) and stores
-        // column pairs, 4 bytes a lane, so the tile takes half the store
-        // instructions.  The even lane of a pair stores the rows of elements
-        // 0..7, the odd lane those of elements 8..15.
+        // values with its neighbour (lane ^ 1, the next column), so that the
+        // even lane of a pair holds column pairs for the rows of elements
+        // 0..7 and the odd lane for those of 8..15; with N % 4 == 0 a second
+        // trade with lane ^ 2 gives four columns, 8 bytes a store: a quarter
+        // of the store instructions.
         const int64_t c0 = n0 + wn * 32 * TN + 32 * j;   // first column of the tile
         if (r0 + 32 <= rows && c0 + 32 <= N && (N & 1) == 0) {
           float v[16];
@@ -269,17 +270,39 @@ __global__ void __launch_bounds__(64 * kWaves) gemm_big(const bf16_t* __restrict
             if constexpr (EPI == EPI_SWIGLU) v[e] = silu(v[e]) * acc2[i][j][e];
           }
           const bool odd = lr & 1;
-          const int64_t cp = col - (odd ? 1 : 0);   // the pair's even column
+          uint32_t pk[8];   // column pair (2m, 2m+1) of the rows of element e (odd lane: e + 8)
 #pragma clang loop unroll(full)
           for (int e = 0; e < 8; ++e) {
             const float send = odd ? v[e] : v[e + 8];
             // quad_perm [1, 0, 3, 2]: the value of lane ^ 1
             const float got = __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(send), 0xB1, 0xF, 0xF, false));
             const float lo = odd ? got : v[e], hi = odd ? v[e + 8] : got;
-            const int ee = odd ? e + 8 : e;
-            const int64_t row = r0 + 8 * (ee >> 2) + 4 * lc + (ee & 3);
-            *reinterpret_cast<uint32_t*>(reinterpret_cast<bf16_t*>(C) + row * N + cp) =
-                uint32_t(f2bf(lo)) | (uint32_t(f2bf(hi)) << 16);
+            pk[e] = uint32_t(f2bf(lo)) | (uint32_t(f2bf(hi)) << 16);
+          }
+          if ((N & 3) == 0) {
+            // a second trade with lane ^ 2 (the next column pair): four
+            // columns, 8 bytes a lane; the lower pair's lane keeps elements
+            // 0..3 of its eight, the upper pair's lane elements 4..7
+            const bool up = (lr >> 1) & 1;
+            const int64_t c4 = col - (lr & 3);   // first of the four columns
+#pragma clang loop unroll(full)
+            for (int r = 0; r < 4; ++r) {
+              const uint32_t send = up ? pk[r] : pk[r + 4];
+              // quad_perm [2, 3, 0, 1]: the value of lane ^ 2
+              const uint32_t got = uint32_t(__builtin_amdgcn_mov_dpp(int(send), 0x4E, 0xF, 0xF, false));
+              const int i8 = up ? r + 4 : r, ee = odd ? i8 + 8 : i8;
+              const int64_t row = r0 + 8 * (ee >> 2) + 4 * lc + (ee & 3);
+              const uint2 w = up ? uint2{got, pk[r + 4]} : uint2{pk[r], got};
+              *reinterpret_cast<uint2*>(reinterpret_cast<bf16_t*>(C) + row * N + c4) = w;
+            }
+          } else {
+            const int64_t cp = col - (odd ? 1 : 0);   // the pair's even column
+#pragma clang loop unroll(full)
+            for (int e = 0; e < 8; ++e) {
+              const int ee = odd ? e + 8 : e;
+              const int64_t row = r0 + 8 * (ee >> 2) + 4 * lc + (ee & 3);
+              *reinterpret_cast<uint32_t*>(reinterpret_cast<bf16_t*>(C) + row * N + cp) = pk[e];
+            }
           }
           continue;
         }
