@@ -54,7 +54,9 @@ def rnd(*shape, scale=1.0):
 # otherwise the 128 x 128 GEMM (including M >= 512 with K % 64 != 0)
 LIN_SHAPES = [(1, 64, 32), (5, 100, 64), (7, 130, 160), (16, 33, 96), (16, 4096 + 16, 256), (17, 96, 96), (100, 130, 160),
               (257, 300, 512), (512, 256, 64), (600, 300, 128), (1030, 520, 192), (777, 1000, 256),
-              (520, 130, 96), (640, 333, 128)]   # the last: odd N, so no column pairs in the 256 x 256 epilogue
+              (520, 130, 96), (640, 333, 128), (544, 130, 128)]
+# the last two in the 256 x 256 epilogue: odd N (single columns) and N % 4 == 2
+# (column pairs, no four-column stores); the other 256 x 256 cases have N % 4 == 0
 
 
 @pytest.mark.parametrize("dt", [DT_F32, DT_BF16])
